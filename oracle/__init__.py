@@ -1,0 +1,377 @@
+"""CPU oracle for the W8A8 SmoothQuant path of arxiv 2608.28003.
+
+TEST INFRASTRUCTURE ONLY.  This package is the slow, plain reference the GPU
+library is checked against.  Only ``tests/``, ``__graft_entry__.smoke()`` and
+the ``cpu_baseline`` leg of ``bench.py`` may import it; the product package
+never does, and the two share no code.
+
+The arithmetic lives in ``w8a8_oracle.c`` (plain C loops, one function per
+definition of the paper); this module only marshals numpy arrays and composes
+those functions in the order the paper states:
+
+* calibration, eq. ``delta-attn`` / ``delta-lmhead`` (Sec. 4 and Sec. 6);
+* smoothing, eq. ``xhat-lmhead`` / ``what-lmhead`` (Sec. 6);
+* per-output-channel weight quantisation, eq. ``si`` / ``what-ffn`` (Sec. 3);
+* dynamic per-token activation quantisation, eq. ``stx`` / ``xint8`` (Sec. 6);
+* the INT8 product and its two-scale dequantisation, eq. ``gemm-final``;
+* the gated FFN between the projections (Sec. 3, Tab. 1 ``fused_fc``/``proj``);
+* the FFN layer subsets, eq. ``ffn55`` / ``ffn1010`` / ``ffnall26``.
+
+bf16 tensors are passed as ``numpy.uint16`` bit patterns.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "w8a8_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liborc.so")
+
+MODE_DIV = 0  # activations: x / delta
+MODE_MUL = 1  # weights:     W * delta
+
+# GELU's tanh form, RMSNorm epsilon and the calibration floor are readings of
+# a paper that leaves them implicit; see the module docstring of the C file.
+RMS_EPS = 1e-6
+CAL_EPS = 1e-5
+ALPHA = 0.5  # SmoothQuant migration strength used throughout the paper
+
+
+def build(force: bool = False) -> str:
+    """Compile ``w8a8_oracle.c`` into ``liborc.so`` with gcc."""
+    if force or not os.path.exists(_LIB_PATH) or (
+            os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC)):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
+               "-ffp-contract=off", "-fno-fast-math", "-Wall", "-Wextra",
+               "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+_lib = None
+
+
+def _L():
+    global _lib
+    if _lib is None:
+        build()
+        lib = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.c_void_p
+        I64 = ctypes.c_int64
+        D = ctypes.c_double
+        sigs = {
+            "orc_bf16_to_f32": [P, I64, P],
+            "orc_f32_to_bf16": [P, I64, P],
+            "orc_f64_to_bf16": [P, I64, P],
+            "orc_col_absmax": [P, I64, I64, P],
+            "orc_smooth_delta": [P, P, I64, D, D, P],
+            "orc_quant_rows": [P, I64, I64, P, ctypes.c_int, P, P, P],
+            "orc_gemm_i32": [P, P, I64, I64, I64, P],
+            "orc_dequant": [P, P, P, I64, I64, P],
+            "orc_geglu": [P, P, I64, P],
+            "orc_geglu_f64": [P, P, I64, P],
+            "orc_linear_f64": [P, P, I64, I64, I64, P],
+            "orc_rmsnorm_f64": [P, I64, I64, D, P],
+        }
+        for name, args in sigs.items():
+            fn = getattr(lib, name)
+            fn.argtypes = args
+            fn.restype = None
+        lib.orc_gemm_i32.restype = ctypes.c_int64
+        _lib = lib
+    return _lib
+
+
+def _p(a):
+    return a.ctypes.data_as(ctypes.c_void_p) if a is not None else None
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+# ---------------------------------------------------------------- formats
+
+def bf16_to_f32(b: np.ndarray) -> np.ndarray:
+    b = _c(b, np.uint16)
+    out = np.empty(b.shape, np.float32)
+    _L().orc_bf16_to_f32(_p(b), b.size, _p(out))
+    return out
+
+
+def f32_to_bf16(x: np.ndarray) -> np.ndarray:
+    x = _c(x, np.float32)
+    out = np.empty(x.shape, np.uint16)
+    _L().orc_f32_to_bf16(_p(x), x.size, _p(out))
+    return out
+
+
+def f64_to_bf16(x: np.ndarray) -> np.ndarray:
+    x = _c(x, np.float64)
+    out = np.empty(x.shape, np.uint16)
+    _L().orc_f64_to_bf16(_p(x), x.size, _p(out))
+    return out
+
+
+def as_f32(x: np.ndarray) -> np.ndarray:
+    """Exact binary32 view of an input given as float32 or bf16 bits."""
+    if x.dtype == np.uint16:
+        return bf16_to_f32(x)
+    return _c(x, np.float32)
+
+
+# ---------------------------------------------------------------- a1
+
+def col_absmax(x: np.ndarray, amax: np.ndarray | None = None) -> np.ndarray:
+    """Running max_t |X_tj| (eq. delta-attn numerator statistic)."""
+    xf = as_f32(x)
+    rows, k = xf.shape
+    out = np.zeros(k, np.float32) if amax is None else _c(amax, np.float32).copy()
+    _L().orc_col_absmax(_p(xf), rows, k, _p(out))
+    return out
+
+
+def smooth_delta(act_amax, w_amax, alpha: float = ALPHA, eps: float = CAL_EPS):
+    """delta_j = a_j^alpha / w_j^(1-alpha)  (eq. delta-attn, eq. delta-lmhead)."""
+    a = _c(act_amax, np.float32)
+    w = _c(w_amax, np.float32)
+    out = np.empty(a.shape[0], np.float32)
+    _L().orc_smooth_delta(_p(a), _p(w), a.shape[0], float(alpha), float(eps), _p(out))
+    return out
+
+
+def smooth_calibrate(x_cal, weights, alpha: float = ALPHA):
+    """delta from calibration activations and every weight that consumes them.
+
+    The weight statistic max_i |W_ij| runs over the rows of all matrices fed by
+    this input (gate and up for the FFN input), stacked."""
+    a = col_absmax(x_cal)
+    w = None
+    for wm in weights:
+        w = col_absmax(wm, w)
+    return smooth_delta(a, w, alpha)
+
+
+# ---------------------------------------------------------------- a2 / a3
+
+def quant_rows(x, delta=None, mode=MODE_DIV, want_vhat=False):
+    """Symmetric per-row int8 codes and scales (eq. si/what-ffn, stx/xint8)."""
+    xf = as_f32(x)
+    rows, k = xf.shape
+    q = np.empty((rows, k), np.int8)
+    s = np.empty(rows, np.float32)
+    d = None if delta is None else _c(delta, np.float32)
+    vhat = np.empty((rows, k), np.float32) if want_vhat else None
+    _L().orc_quant_rows(_p(xf), rows, k, _p(d), mode, _p(q), _p(s), _p(vhat))
+    return (q, s, vhat) if want_vhat else (q, s)
+
+
+def quantize_weights(w, delta=None):
+    """W_hat = W diag(delta), then per-output-channel codes (a2)."""
+    return quant_rows(w, delta, MODE_MUL)
+
+
+def quantize_act(x, delta=None):
+    """x_hat = x / delta, then per-token codes (a3)."""
+    return quant_rows(x, delta, MODE_DIV)
+
+
+# ---------------------------------------------------------------- a4 / a5
+
+def gemm_i32(qa: np.ndarray, qb: np.ndarray) -> np.ndarray:
+    qa = _c(qa, np.int8)
+    qb = _c(qb, np.int8)
+    m, k = qa.shape
+    n, k2 = qb.shape
+    assert k == k2
+    acc = np.empty((m, n), np.int32)
+    ovf = _L().orc_gemm_i32(_p(qa), _p(qb), m, n, k, _p(acc))
+    if ovf:
+        raise OverflowError("int32 accumulator overflow in %d sums" % ovf)
+    return acc
+
+
+def dequant(acc, s_tok, s_ch) -> np.ndarray:
+    acc = _c(acc, np.int32)
+    m, n = acc.shape
+    y = np.empty((m, n), np.float32)
+    _L().orc_dequant(_p(acc), _p(_c(s_tok, np.float32)), _p(_c(s_ch, np.float32)),
+                     m, n, _p(y))
+    return y
+
+
+def w8a8_linear(x, wq, s_w, delta, out_dtype="f32"):
+    """y = s_t s_i sum_j q_x q_w  with x quantised per token after x / delta."""
+    qx, sx = quantize_act(x, delta)
+    acc = gemm_i32(qx, wq)
+    y = dequant(acc, sx, s_w)
+    return y if out_dtype == "f32" else f32_to_bf16(y)
+
+
+# ---------------------------------------------------------------- a6
+
+def geglu(g, u) -> np.ndarray:
+    """h = gelu_tanh(g) * u in binary32 (tanh from binary64 libm)."""
+    g = _c(g, np.float32)
+    u = _c(u, np.float32)
+    h = np.empty(g.shape, np.float32)
+    _L().orc_geglu(_p(g), _p(u), g.size, _p(h))
+    return h
+
+
+def geglu_f64(g, u) -> np.ndarray:
+    g = _c(g, np.float64)
+    u = _c(u, np.float64)
+    h = np.empty(g.shape, np.float64)
+    _L().orc_geglu_f64(_p(g), _p(u), g.size, _p(h))
+    return h
+
+
+def w8a8_ffn(x_bf16, q, stages=False):
+    """INT8 FFN block: quantise x, gate/up INT8 products, GeGLU, bf16 h,
+    requantise h / delta_down per token, down INT8 product, bf16 y.
+
+    ``q`` holds the oracle's quantised weights: wq_gate, s_gate, wq_up, s_up,
+    delta_gu, wq_down, s_down, delta_down."""
+    qx, sx = quantize_act(x_bf16, q["delta_gu"])
+    acc_g = gemm_i32(qx, q["wq_gate"])
+    acc_u = gemm_i32(qx, q["wq_up"])
+    g = dequant(acc_g, sx, q["s_gate"])
+    u = dequant(acc_u, sx, q["s_up"])
+    h = f32_to_bf16(geglu(g, u))
+    qh, sh = quantize_act(h, q["delta_down"])
+    acc_d = gemm_i32(qh, q["wq_down"])
+    y = f32_to_bf16(dequant(acc_d, sh, q["s_down"]))
+    if stages:
+        return y, dict(qx=qx, sx=sx, acc_g=acc_g, acc_u=acc_u, g=g, u=u, h=h,
+                       qh=qh, sh=sh, acc_d=acc_d)
+    return y
+
+
+def quantize_ffn(w_gate, w_up, w_down, x_cal, alpha=ALPHA):
+    """Offline preparation of one INT8 FFN (a1 + a2): delta for the FFN input
+    from the calibration tokens and the stacked gate/up rows; delta for the
+    down input from the GeGLU output of the same tokens through the
+    unquantised gate/up projections."""
+    d_gu = smooth_calibrate(x_cal, [w_gate, w_up], alpha)
+    g = linear_f64(x_cal, w_gate)
+    u = linear_f64(x_cal, w_up)
+    h_cal = f32_to_bf16(geglu(g.astype(np.float32), u.astype(np.float32)))
+    d_dn = smooth_calibrate(h_cal, [w_down], alpha)
+    wq_g, s_g = quantize_weights(w_gate, d_gu)
+    wq_u, s_u = quantize_weights(w_up, d_gu)
+    wq_d, s_d = quantize_weights(w_down, d_dn)
+    return dict(wq_gate=wq_g, s_gate=s_g, wq_up=wq_u, s_up=s_u, delta_gu=d_gu,
+                wq_down=wq_d, s_down=s_d, delta_down=d_dn)
+
+
+# ---------------------------------------------------------------- bf16 path
+
+def linear_f64(x, w) -> np.ndarray:
+    xf = as_f32(x)
+    wf = as_f32(w)
+    m, k = xf.shape
+    n = wf.shape[0]
+    y = np.empty((m, n), np.float64)
+    _L().orc_linear_f64(_p(xf), _p(wf), m, n, k, _p(y))
+    return y
+
+
+def bf16_linear(x, w) -> np.ndarray:
+    """bf16 reference projection: exact products summed in binary64, one
+    rounding to bf16."""
+    return f64_to_bf16(linear_f64(x, w))
+
+
+def bf16_ffn(x_bf16, w_gate, w_up, w_down) -> np.ndarray:
+    """bf16 FFN block (layers the precision map keeps in bf16): g, u kept
+    unrounded, h = bf16(gelu_tanh(g) u), y = bf16(h W_down^T)."""
+    g = linear_f64(x_bf16, w_gate).astype(np.float32)
+    u = linear_f64(x_bf16, w_up).astype(np.float32)
+    h = f32_to_bf16(geglu(g, u))
+    return bf16_linear(h, w_down)
+
+
+def rmsnorm(x) -> np.ndarray:
+    """RMSNorm with unit gain, binary64, rounded once to bf16."""
+    xf = as_f32(x)
+    m, d = xf.shape
+    y = np.empty((m, d), np.float64)
+    _L().orc_rmsnorm_f64(_p(xf), m, d, RMS_EPS, _p(y))
+    return f64_to_bf16(y)
+
+
+# ---------------------------------------------------------------- a7
+
+def w8a8_lm_head(x_bf16, wq, s_w, delta) -> np.ndarray:
+    """Logits in bf16 from the INT8 lm_head (Sec. 6, eq. gemm-final)."""
+    return w8a8_linear(x_bf16, wq, s_w, delta, out_dtype="bf16")
+
+
+# ---------------------------------------------------------------- a8 / a9
+
+N_LAYERS = 26
+
+
+def precision_map(name: str, n_layers: int = N_LAYERS) -> np.ndarray:
+    """Q_FFN of eq. ffn55 / ffn1010 / ffnall26 as a 0/1 vector (1 = INT8)."""
+    p = np.zeros(n_layers, np.uint8)
+    if name == "bf16":
+        pass
+    elif name == "5+5":
+        p[0:5] = 1
+        p[21:26] = 1
+    elif name == "10+10":
+        p[0:10] = 1
+        p[16:26] = 1
+    elif name == "all26":
+        p[:] = 1
+    else:
+        raise ValueError(name)
+    return p
+
+
+def residual_add(x, y) -> np.ndarray:
+    return f64_to_bf16(as_f32(x).astype(np.float64) + as_f32(y).astype(np.float64))
+
+
+def stack(x_bf16, layers, prec, lm_head, lm_head_int8, return_hidden=False):
+    """FFN stack under a precision map (config glue, Sec. 3):
+    x <- bf16(x + RMSNorm(FFN_l(RMSNorm(x)))) for every layer, where FFN_l is
+    the INT8 block for layers in Q_FFN and the bf16 block otherwise; then the
+    final RMSNorm and the lm_head (INT8 or bf16)."""
+    x = _c(x_bf16, np.uint16)
+    hidden = []
+    for l, L in enumerate(layers):
+        a = rmsnorm(x)
+        if prec[l]:
+            f = w8a8_ffn(a, L["int8"])
+        else:
+            f = bf16_ffn(a, L["w_gate"], L["w_up"], L["w_down"])
+        b = rmsnorm(f)
+        x = residual_add(x, b)
+        hidden.append(x)
+    xf = rmsnorm(x)
+    if lm_head_int8:
+        logits = w8a8_lm_head(xf, lm_head["wq"], lm_head["s_w"], lm_head["delta"])
+    else:
+        logits = bf16_linear(xf, lm_head["w"])
+    return (logits, hidden) if return_hidden else logits
+
+
+# ---------------------------------------------------------------- metrics
+
+def sqnr_db(clean, dirty) -> float:
+    """10 log10(||y_clean||^2 / ||y_clean - y_dirty||^2)  (eq. sqnr-ffn)."""
+    c = np.asarray(clean, np.float64)
+    d = np.asarray(dirty, np.float64)
+    num = float(np.sum(c * c))
+    den = float(np.sum((c - d) ** 2))
+    return float("inf") if den == 0.0 else 10.0 * np.log10(num / den)

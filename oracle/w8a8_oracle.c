@@ -1,0 +1,267 @@
+/*
+ * CPU oracle for the W8A8 SmoothQuant path of arxiv 2608.28003 (Gemma-3-1B
+ * layer-wise INT8/bf16 allocation).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the plain, slow reference that the
+ * GPU library is checked against.  Only the test-suite, the smoke check and
+ * the CPU-baseline leg of the benchmark may load it; the product library never
+ * links, includes or calls it, and it shares no code with the HIP sources.
+ *
+ * Every function is a direct loop over the definition it cites: no blocking,
+ * no fusion, no reordering of the arithmetic the definition states.  OpenMP
+ * only distributes independent output rows.
+ *
+ * Precision (readings of a paper that does not fix it):
+ *   - values that decide an integer code (smoothed inputs, scales, the ratio
+ *     that is rounded) are formed in IEEE binary32, one rounding per
+ *     operation, no contraction -- the precision the GPU kernels decide them in;
+ *   - integer products are summed exactly (int64, then range-checked to int32);
+ *   - the dequantised value y = s_t * s_i * acc is formed in binary32 with the
+ *     token scale applied first (its result feeds the codes of the next
+ *     projection inside the FFN);
+ *   - tanh inside GELU is libm's binary64 tanh rounded once to binary32;
+ *   - the bf16 reference path (layers the precision map keeps in bf16) and the
+ *     RMSNorm glue are evaluated in binary64 and rounded once.
+ *
+ * Build: gcc -O2 -std=c11 -fPIC -shared -fopenmp -ffp-contract=off
+ *        -fno-fast-math   (contraction would fuse a*b+c and change results)
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#define ORC_MODE_DIV 0 /* activations: x_hat = x / delta   (eq. xhat-lmhead) */
+#define ORC_MODE_MUL 1 /* weights:     W_hat = W * delta   (eq. what-lmhead) */
+
+/* ------------------------------------------------------------------ */
+/* Number formats                                                       */
+/* ------------------------------------------------------------------ */
+
+/* bf16 -> fp32 is exact: the bf16 pattern is the top half of the fp32 one. */
+void orc_bf16_to_f32(const uint16_t* src, int64_t n, float* dst) {
+    for (int64_t i = 0; i < n; ++i) {
+        uint32_t u = ((uint32_t)src[i]) << 16;
+        memcpy(&dst[i], &u, 4);
+    }
+}
+
+/* fp32 -> bf16, round to nearest, ties to even (IEEE default rounding). */
+static uint16_t f32_to_bf16_rne(float f) {
+    uint32_t u;
+    memcpy(&u, &f, 4);
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return 0x7fc0; /* NaN */
+    uint32_t keep = u >> 16;
+    uint32_t rest = u & 0xffffu;
+    if (rest > 0x8000u || (rest == 0x8000u && (keep & 1u))) keep += 1u;
+    return (uint16_t)keep;
+}
+
+void orc_f32_to_bf16(const float* src, int64_t n, uint16_t* dst) {
+    for (int64_t i = 0; i < n; ++i) dst[i] = f32_to_bf16_rne(src[i]);
+}
+
+/* binary64 -> bf16 rounded once (not through binary32, which would round
+   twice): scale |v| onto the grid of 8 significant bits (the bf16 spacing,
+   never finer than the subnormal step 2^-133), round half to even there and
+   scale back; the result has at most 8 significant bits, so it converts to
+   binary32 exactly (or overflows to inf, as round-to-nearest requires). */
+static uint16_t f64_to_bf16_rne(double v) {
+    if (v != v) return 0x7fc0;
+    if (v == 0.0) return signbit(v) ? 0x8000 : 0x0000;
+    int e;
+    (void)frexp(v, &e);  /* |v| in [2^(e-1), 2^e) */
+    int q = e - 8;       /* spacing of 8 significant bits */
+    if (q < -133) q = -133;
+    double r = rint(ldexp(v, -q));
+    float f = (float)ldexp(r, q);
+    uint32_t u;
+    memcpy(&u, &f, 4);
+    return (uint16_t)(u >> 16);
+}
+
+void orc_f64_to_bf16(const double* src, int64_t n, uint16_t* dst) {
+    for (int64_t i = 0; i < n; ++i) dst[i] = f64_to_bf16_rne(src[i]);
+}
+
+/* round half to even, in binary32 (the default IEEE rounding mode) */
+static float rne_f32(float r) { return rintf(r); }
+
+/* ------------------------------------------------------------------ */
+/* a1  Calibration (eq. delta-attn, eq. delta-lmhead)                   */
+/* ------------------------------------------------------------------ */
+
+/* Running column maximum of |X[t][j]| over rows t: the activation statistic
+   max_t |X_tj| gathered over calibration tokens, and, applied to a weight
+   matrix, max_i |W_ij| over its output rows.  amax is read and updated. */
+void orc_col_absmax(const float* x, int64_t rows, int64_t k, float* amax) {
+    for (int64_t j = 0; j < k; ++j) {
+        float m = amax[j];
+        for (int64_t t = 0; t < rows; ++t) {
+            float v = fabsf(x[t * k + j]);
+            if (v > m) m = v;
+        }
+        amax[j] = m;
+    }
+}
+
+/* delta_j = (max_t |X_tj|)^alpha / (max_i |W_ij|)^(1-alpha), both maxima
+   floored at eps so a dead channel yields a finite factor.  Evaluated in
+   binary64 and rounded once; at alpha = 1/2 the powers are square roots. */
+void orc_smooth_delta(const float* act_amax, const float* w_amax, int64_t k,
+                      double alpha, double eps, float* delta) {
+    for (int64_t j = 0; j < k; ++j) {
+        double a = (double)act_amax[j], w = (double)w_amax[j];
+        if (a < eps) a = eps;
+        if (w < eps) w = eps;
+        double d;
+        if (alpha == 0.5)
+            d = sqrt(a) / sqrt(w);
+        else
+            d = pow(a, alpha) / pow(w, 1.0 - alpha);
+        delta[j] = (float)d;
+    }
+}
+
+/* ------------------------------------------------------------------ */
+/* a2/a3  Symmetric per-row int8 quantisation                           */
+/*   eq. si / what-ffn (per output channel of W_hat = W diag(delta))    */
+/*   eq. stx / xint8   (per token of x_hat = x / delta)                 */
+/* ------------------------------------------------------------------ */
+
+/* For each row r:  v_j = x_rj / delta_j (DIV) or x_rj * delta_j (MUL), or x_rj
+   when delta is NULL;  amax = max_j |v_j|;  s_r = amax / 127;
+   q_rj = clamp(rne(v_j / s_r), -127, 127);  an all-zero row gives s = 0, q = 0.
+   If vhat is not NULL the smoothed binary32 values v are also stored. */
+void orc_quant_rows(const float* x, int64_t rows, int64_t k, const float* delta,
+                    int mode, int8_t* q, float* s, float* vhat) {
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < rows; ++r) {
+        const float* xr = x + r * k;
+        float amax = 0.0f;
+        for (int64_t j = 0; j < k; ++j) {
+            float v = xr[j];
+            if (delta) v = (mode == ORC_MODE_DIV) ? v / delta[j] : v * delta[j];
+            if (vhat) vhat[r * k + j] = v;
+            float a = fabsf(v);
+            if (a > amax) amax = a;
+        }
+        float sr = amax / 127.0f;
+        s[r] = sr;
+        for (int64_t j = 0; j < k; ++j) {
+            float v = xr[j];
+            if (delta) v = (mode == ORC_MODE_DIV) ? v / delta[j] : v * delta[j];
+            int8_t code = 0;
+            if (sr != 0.0f) {
+                float c = rne_f32(v / sr);
+                if (c > 127.0f) c = 127.0f;
+                if (c < -127.0f) c = -127.0f;
+                code = (int8_t)c;
+            }
+            q[r * k + j] = code;
+        }
+    }
+}
+
+/* ------------------------------------------------------------------ */
+/* a4  INT8 x INT8 -> INT32 product (the sum of eq. gemm-final)         */
+/* ------------------------------------------------------------------ */
+
+/* acc[t][i] = sum_j a[t][j] * b[i][j], summed exactly in int64.  Returns the
+   number of sums outside the int32 range (0 for every K <= 133144). */
+int64_t orc_gemm_i32(const int8_t* a, const int8_t* b, int64_t m, int64_t n,
+                     int64_t k, int32_t* acc) {
+    int64_t overflow = 0;
+#pragma omp parallel for schedule(static) reduction(+ : overflow)
+    for (int64_t t = 0; t < m; ++t) {
+        for (int64_t i = 0; i < n; ++i) {
+            int64_t sum = 0;
+            for (int64_t j = 0; j < k; ++j)
+                sum += (int64_t)a[t * k + j] * (int64_t)b[i * k + j];
+            if (sum > INT32_MAX || sum < INT32_MIN) overflow += 1;
+            acc[t * n + i] = (int32_t)sum;
+        }
+    }
+    return overflow;
+}
+
+/* ------------------------------------------------------------------ */
+/* a5  Dequantisation (eq. gemm-final)                                  */
+/* ------------------------------------------------------------------ */
+
+/* y[t][i] = (float(acc[t][i]) * s_t) * s_i, binary32, token scale first. */
+void orc_dequant(const int32_t* acc, const float* s_tok, const float* s_ch,
+                 int64_t m, int64_t n, float* y) {
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < m; ++t)
+        for (int64_t i = 0; i < n; ++i) {
+            float a = (float)acc[t * n + i];
+            float p = a * s_tok[t];
+            y[t * n + i] = p * s_ch[i];
+        }
+}
+
+/* ------------------------------------------------------------------ */
+/* a6  GeGLU with the tanh form of GELU (gate branch), times up         */
+/* ------------------------------------------------------------------ */
+
+/* gelu(g) = 0.5 g (1 + tanh( sqrt(2/pi) (g + 0.044715 g^3) ));  h = gelu(g) u.
+   Binary32 operations in the order written, tanh taken from binary64 libm and
+   rounded once.  The caller rounds h to bf16 (the FFN intermediate format). */
+void orc_geglu(const float* g, const float* u, int64_t n, float* h) {
+    const float c = (float)0.79788456080286535588; /* sqrt(2/pi) */
+    const float k3 = 0.044715f;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+        float x = g[i];
+        float x2 = x * x;
+        float x3 = x2 * x;
+        float inner = x + k3 * x3;
+        float z = c * inner;
+        float t = (float)tanh((double)z);
+        float half = 0.5f * x;
+        float one_t = 1.0f + t;
+        float ge = half * one_t;
+        h[i] = ge * u[i];
+    }
+}
+
+/* Same GELU-tanh in binary64 throughout (used by the pins and by the bf16
+   reference path through orc_geglu_f64). */
+void orc_geglu_f64(const double* g, const double* u, int64_t n, double* h) {
+    const double c = 0.79788456080286535588;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+        double x = g[i];
+        double ge = 0.5 * x * (1.0 + tanh(c * (x + 0.044715 * x * x * x)));
+        h[i] = ge * u[i];
+    }
+}
+
+/* ------------------------------------------------------------------ */
+/* bf16 reference path and stack glue (binary64)                       */
+/* ------------------------------------------------------------------ */
+
+/* y[t][i] = sum_j x[t][j] * w[i][j] in binary64 (x, w given exactly as
+   binary32 values widened from bf16). */
+void orc_linear_f64(const float* x, const float* w, int64_t m, int64_t n,
+                    int64_t k, double* y) {
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < m; ++t)
+        for (int64_t i = 0; i < n; ++i) {
+            double sum = 0.0;
+            for (int64_t j = 0; j < k; ++j)
+                sum += (double)x[t * k + j] * (double)w[i * k + j];
+            y[t * n + i] = sum;
+        }
+}
+
+/* RMSNorm with unit gain: y = x / sqrt(mean_j x_j^2 + eps), binary64. */
+void orc_rmsnorm_f64(const float* x, int64_t m, int64_t d, double eps, double* y) {
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < m; ++t) {
+        double ss = 0.0;
+        for (int64_t j = 0; j < d; ++j) ss += (double)x[t * d + j] * (double)x[t * d + j];
+        double inv = 1.0 / sqrt(ss / (double)d + eps);
+        for (int64_t j = 0; j < d; ++j) y[t * d + j] = (double)x[t * d + j] * inv;
+    }
+}

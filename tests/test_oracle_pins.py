@@ -1,0 +1,398 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+None of these tests re-types the oracle's formula: each checks it against a
+value derived by hand, a closed form, an invariant that a plausible mistake
+(dropped term, wrong sign, wrong divisor, transposed operand, wrong smoothing
+direction, truncation instead of rounding) would break, brute force in exact
+integer arithmetic, or an independent library routine.
+"""
+
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_28003_amd import synth
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _gold(name):
+    with open(os.path.join(GOLD, name)) as f:
+        return json.load(f)
+
+
+# ------------------------------------------------------------------ formats
+
+def test_bf16_from_f32_matches_torch():
+    rng = np.random.default_rng(7)
+    x = np.concatenate([
+        rng.standard_normal(20000).astype(np.float32) * np.float32(30),
+        (rng.standard_normal(2000) * 1e-39).astype(np.float32),
+        np.array([0.0, -0.0, 1.0, -1.0, 3.0e38, -3.0e38, 1e-45], np.float32),
+        # exact bf16 midpoints
+        np.array([1.00390625, 1.01171875, -1.00390625], np.float32),
+    ])
+    got = oracle.f32_to_bf16(x)
+    want = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(got, want)
+
+
+def test_bf16_from_f64_fixture():
+    for c in _gold("quant_rounding.json")["bf16_from_f64"]["cases"]:
+        got = oracle.f64_to_bf16(np.array([c["v"]], np.float64))[0]
+        assert got == int(c["bits"], 16), (c, hex(got))
+
+
+def test_bf16_from_f64_is_nearest():
+    # Exact rational check: the result is a nearest bf16 value of v.
+    rng = np.random.default_rng(11)
+    v = rng.standard_normal(3000) * np.exp(rng.uniform(-30, 30, 3000))
+    bits = oracle.f64_to_bf16(v)
+    vals = oracle.bf16_to_f32(bits).astype(np.float64)
+    for vi, bi, ri in zip(v, bits, vals):
+        # neighbours one bf16 step up and down
+        up = oracle.bf16_to_f32(np.array([bi + 1], np.uint16))[0]
+        dn = oracle.bf16_to_f32(np.array([bi - 1], np.uint16))[0]
+        e = abs(Fraction(vi) - Fraction(float(ri)))
+        assert e <= abs(Fraction(vi) - Fraction(float(up)))
+        assert e <= abs(Fraction(vi) - Fraction(float(dn)))
+
+
+def test_bf16_widening_exact():
+    b = np.arange(0, 65536, 7, dtype=np.uint16)
+    b = b[(b & 0x7F80) != 0x7F80]  # finite only
+    got = oracle.bf16_to_f32(b)
+    want = torch.from_numpy(b.view(np.int16)).view(torch.bfloat16).float().numpy()
+    np.testing.assert_array_equal(got, want)
+
+
+# ------------------------------------------------------------------ a2 / a3
+
+def test_quant_hand_derived_cases():
+    for c in _gold("quant_rounding.json")["cases"]:
+        x = np.array([c["x"]], np.float32)
+        d = None if c["delta"] is None else np.array(c["delta"], np.float32)
+        mode = oracle.MODE_DIV if c["mode"] == "act" else oracle.MODE_MUL
+        q, s = oracle.quant_rows(x, d, mode)
+        assert list(q[0]) == c["q"], c["name"]
+        assert float(s[0]) == pytest.approx(c["s"], rel=0, abs=0), c["name"]
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+@pytest.mark.parametrize("mode", [oracle.MODE_DIV, oracle.MODE_MUL])
+def test_quant_invariants(seed, mode):
+    rng = np.random.default_rng(seed)
+    rows, k = 37, 301
+    x = (rng.standard_normal((rows, k)) * np.exp(rng.uniform(-8, 8, (rows, 1)))).astype(np.float32)
+    x[5] = 0.0  # an all-zero row
+    delta = np.exp(rng.uniform(-3, 3, k)).astype(np.float32)
+    q, s, v = oracle.quant_rows(x, delta, mode, want_vhat=True)
+    # smoothing direction: v is x / delta (act) or x * delta (weights), to 1 ulp
+    ref = x.astype(np.float64) / delta if mode == oracle.MODE_DIV else x.astype(np.float64) * delta
+    np.testing.assert_allclose(v, ref, rtol=2 ** -23, atol=0)
+    for r in range(rows):
+        if r == 5:
+            assert s[r] == 0 and not q[r].any()
+            continue
+        # every nonzero row reaches the full code range (divisor 127, not 128/255)
+        assert np.abs(q[r]).max() == 127
+        # scale is amax / 127 to one rounding
+        amax = np.abs(v[r]).max().astype(np.float64)
+        assert abs(float(s[r]) - amax / 127) <= amax / 127 * 2 ** -24
+        # reconstruction error within half a step (round-to-nearest, not truncation)
+        err = np.abs(v[r].astype(np.float64) - s[r].astype(np.float64) * q[r])
+        assert err.max() <= 0.5 * float(s[r]) * (1 + 2 ** -20)
+        # sign of the code follows the sign of the smoothed value
+        assert np.all((np.sign(q[r]) == np.sign(v[r])) | (q[r] == 0))
+
+
+def test_quant_power_of_two_row_scaling():
+    rng = np.random.default_rng(4)
+    x = rng.standard_normal((8, 64)).astype(np.float32)
+    q1, s1 = oracle.quantize_act(x)
+    for e in (-20, -3, 5, 40):
+        q2, s2 = oracle.quantize_act(x * np.float32(2.0 ** e))
+        np.testing.assert_array_equal(q1, q2)
+        np.testing.assert_array_equal(s2, s1 * np.float32(2.0 ** e))
+
+
+def test_quant_rows_independent():
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((16, 96)).astype(np.float32)
+    q1, s1 = oracle.quantize_act(x)
+    x2 = x.copy()
+    x2[3] *= 1000.0
+    x2[9] = 0.0
+    q2, s2 = oracle.quantize_act(x2)
+    keep = [i for i in range(16) if i not in (3, 9)]
+    np.testing.assert_array_equal(q1[keep], q2[keep])
+    np.testing.assert_array_equal(s1[keep], s2[keep])
+
+
+# ------------------------------------------------------------------ a4
+
+@pytest.mark.parametrize("m,n,k", [(1, 1, 1), (2, 3, 7), (3, 17, 16), (7, 16, 64), (16, 2, 17)])
+def test_gemm_brute_force_python_ints(m, n, k):
+    rng = np.random.default_rng(m * 100 + n * 10 + k)
+    a = rng.integers(-127, 128, (m, k), dtype=np.int8)
+    b = rng.integers(-127, 128, (n, k), dtype=np.int8)
+    acc = oracle.gemm_i32(a, b)
+    al, bl = a.tolist(), b.tolist()
+    for t in range(m):
+        for i in range(n):
+            assert acc[t, i] == sum(al[t][j] * bl[i][j] for j in range(k))
+
+
+def test_gemm_matches_float64_blas_exactly():
+    # every partial sum is an integer below 2^53, so binary64 BLAS is exact
+    rng = np.random.default_rng(8)
+    a = rng.integers(-127, 128, (33, 1152), dtype=np.int8)
+    b = rng.integers(-127, 128, (71, 1152), dtype=np.int8)
+    acc = oracle.gemm_i32(a, b)
+    ref = a.astype(np.float64) @ b.astype(np.float64).T
+    np.testing.assert_array_equal(acc.astype(np.float64), ref)
+
+
+def test_gemm_row_split_and_k_permutation_invariance():
+    # the lm_head was run as 4 row blocks and concatenated (Sec. 6)
+    rng = np.random.default_rng(9)
+    a = rng.integers(-127, 128, (5, 256), dtype=np.int8)
+    b = rng.integers(-127, 128, (64, 256), dtype=np.int8)
+    full = oracle.gemm_i32(a, b)
+    parts = np.concatenate([oracle.gemm_i32(a, b[i:i + 16]) for i in range(0, 64, 16)], 1)
+    np.testing.assert_array_equal(full, parts)
+    perm = rng.permutation(256)
+    np.testing.assert_array_equal(full, oracle.gemm_i32(a[:, perm], b[:, perm]))
+
+
+def test_gemm_int32_range_bound():
+    # K * 127^2 <= 2^31 - 1  <=>  K <= 133144
+    k = 133144
+    a = np.full((1, k), 127, np.int8)
+    assert oracle.gemm_i32(a, a)[0, 0] == k * 127 * 127
+    a2 = np.full((1, k + 1), 127, np.int8)
+    with pytest.raises(OverflowError):
+        oracle.gemm_i32(a2, a2)
+
+
+# ------------------------------------------------------------------ a1
+
+def test_calibration_closed_form_alpha_half():
+    rng = np.random.default_rng(10)
+    k = 200
+    x = (rng.standard_normal((64, k)) * np.exp(rng.uniform(-2, 4, k))).astype(np.float32)
+    w = (rng.standard_normal((50, k)) * 0.02).astype(np.float32)
+    delta = oracle.smooth_calibrate(x, [w], 0.5)
+    a = np.abs(x).max(0).astype(np.float64)
+    wm = np.abs(w).max(0).astype(np.float64)
+    # after smoothing both channel maxima equal sqrt(a_j w_j)
+    np.testing.assert_allclose(np.abs(x / delta.astype(np.float64)).max(0), np.sqrt(a * wm), rtol=1e-6)
+    np.testing.assert_allclose(np.abs(w * delta.astype(np.float64)).max(0), np.sqrt(a * wm), rtol=1e-6)
+
+
+def test_calibration_alpha_extremes():
+    rng = np.random.default_rng(12)
+    k = 64
+    x = (rng.standard_normal((32, k)) * np.exp(rng.uniform(-2, 4, k))).astype(np.float32)
+    w = (rng.standard_normal((40, k)) * 0.02).astype(np.float32)
+    d1 = oracle.smooth_calibrate(x, [w], 1.0)   # all difficulty moved to the weights
+    np.testing.assert_allclose(np.abs(x / d1.astype(np.float64)).max(0), 1.0, rtol=1e-6)
+    d0 = oracle.smooth_calibrate(x, [w], 0.0)   # all difficulty left in the activations
+    np.testing.assert_allclose(np.abs(w * d0.astype(np.float64)).max(0), 1.0, rtol=1e-6)
+
+
+def test_calibration_stacks_every_consumer_and_floors_dead_channels():
+    x = np.ones((4, 3), np.float32)
+    x[:, 2] = 0.0                      # dead channel
+    w1 = np.array([[0.25, 0.01, 0.5]], np.float32)
+    w2 = np.array([[0.04, 0.64, 0.5]], np.float32)
+    d = oracle.smooth_calibrate(x, [w1, w2], 0.5)
+    # w_j = max over the rows of both matrices: 0.25, 0.64, 0.5
+    np.testing.assert_allclose(d[:2], [1 / 0.5, 1 / 0.8], rtol=1e-7)
+    assert np.isfinite(d[2]) and d[2] > 0
+    np.testing.assert_allclose(d[2], math.sqrt(oracle.CAL_EPS) / math.sqrt(0.5), rtol=1e-6)
+
+
+# ------------------------------------------------------------------ smoothing identity
+
+def test_smoothing_identity_fp64():
+    # X diag(delta)^-1 (diag(delta) W)^T = X W^T, on the oracle's own smoothed values
+    cfg = synth.linear_config(m=16, n=96)
+    x, w = cfg["x"], cfg["w"]
+    delta = oracle.smooth_calibrate(cfg["x_cal"], [w])
+    _, _, xh = oracle.quant_rows(x, delta, oracle.MODE_DIV, want_vhat=True)
+    _, _, wh = oracle.quant_rows(w, delta, oracle.MODE_MUL, want_vhat=True)
+    lhs = xh.astype(np.float64) @ wh.astype(np.float64).T
+    rhs = x.astype(np.float64) @ w.astype(np.float64).T
+    assert np.linalg.norm(lhs - rhs) / np.linalg.norm(rhs) < 1e-5
+
+
+# ------------------------------------------------------------------ a5
+
+def test_dequant_error_bound_against_exact_product():
+    cfg = synth.linear_config(m=16, n=128)
+    x, w = cfg["x"], cfg["w"]
+    delta = oracle.smooth_calibrate(cfg["x_cal"], [w])
+    wq, sw, wh = oracle.quant_rows(w, delta, oracle.MODE_MUL, want_vhat=True)
+    qx, sx, xh = oracle.quant_rows(x, delta, oracle.MODE_DIV, want_vhat=True)
+    y = oracle.dequant(oracle.gemm_i32(qx, wq), sx, sw).astype(np.float64)
+    exact = x.astype(np.float64) @ w.astype(np.float64).T
+    st = sx.astype(np.float64)[:, None]
+    si = sw.astype(np.float64)[None, :]
+    bound = (0.5 * st * (np.abs(wh).astype(np.float64).sum(1)[None, :])
+             + 0.5 * si * (np.abs(xh).astype(np.float64).sum(1)[:, None])
+             + 0.25 * st * si * x.shape[1])
+    slack = 4 * 2 ** -24 * np.abs(y) + 1e-6 * np.abs(exact)
+    assert np.all(np.abs(y - exact) <= bound + slack)
+
+
+def test_dequant_unit_scales_is_exact():
+    rng = np.random.default_rng(13)
+    qa = rng.integers(-127, 128, (4, 64), dtype=np.int8)
+    qb = rng.integers(-127, 128, (6, 64), dtype=np.int8)
+    acc = oracle.gemm_i32(qa, qb)
+    y = oracle.dequant(acc, np.ones(4, np.float32), np.ones(6, np.float32))
+    np.testing.assert_array_equal(y, acc.astype(np.float32))
+    # token scale applied per row, channel scale per column (not transposed)
+    st = np.array([1, 2, 4, 8], np.float32)
+    si = np.array([1, 0.5, 0.25, 2, 4, 16], np.float32)
+    y2 = oracle.dequant(acc, st, si)
+    np.testing.assert_array_equal(y2, acc.astype(np.float64) * st[:, None] * si[None, :])
+
+
+# ------------------------------------------------------------------ a6
+
+def test_gelu_tanh_matches_torch_library():
+    g = np.linspace(-12, 12, 20001).astype(np.float32)
+    ones = np.ones_like(g)
+    h32 = oracle.geglu(g, ones)
+    h64 = oracle.geglu_f64(g.astype(np.float64), ones.astype(np.float64))
+    ref = torch.nn.functional.gelu(torch.from_numpy(g.astype(np.float64)), approximate="tanh").numpy()
+    np.testing.assert_allclose(h64, ref, rtol=1e-13, atol=1e-15)
+    # binary32 evaluation: a few roundings, plus the cancellation in 1 + tanh
+    # for negative g, where the result is tiny
+    np.testing.assert_allclose(h32, ref, rtol=2e-6, atol=2e-7)
+
+
+def test_gelu_tanh_identities():
+    g = np.linspace(-9, 9, 1801)
+    z = np.zeros_like(g)
+    h = oracle.geglu_f64(g, np.ones_like(g))
+    hm = oracle.geglu_f64(-g, np.ones_like(g))
+    np.testing.assert_allclose(h - hm, g, atol=1e-12)   # tanh is odd
+    assert oracle.geglu_f64(np.array([0.0]), np.array([1.0]))[0] == 0.0
+    assert abs(oracle.geglu_f64(np.array([30.0]), np.array([1.0]))[0] - 30.0) < 1e-12
+    assert abs(oracle.geglu_f64(np.array([-30.0]), np.array([1.0]))[0]) < 1e-12
+    # the up branch multiplies
+    np.testing.assert_allclose(oracle.geglu_f64(g, 3 * np.ones_like(g)), 3 * h, rtol=1e-15)
+    np.testing.assert_array_equal(oracle.geglu_f64(g, z), 0 * h)
+
+
+def test_rmsnorm_matches_torch():
+    rng = np.random.default_rng(14)
+    x = synth.to_bf16_bits(rng.standard_normal((9, 1152)).astype(np.float32) * 3)
+    got = oracle.bf16_to_f32(oracle.rmsnorm(x)).astype(np.float64)
+    xt = torch.from_numpy(oracle.bf16_to_f32(x).astype(np.float64))
+    ref = torch.nn.functional.rms_norm(xt, (1152,), eps=oracle.RMS_EPS).numpy()
+    # one bf16 rounding of the exact value
+    np.testing.assert_allclose(got, ref, rtol=2 ** -8, atol=0)
+    # small activations, where the epsilon inside the root is not negligible
+    xs = synth.to_bf16_bits(rng.standard_normal((5, 1152)).astype(np.float32) * 1e-3)
+    got = oracle.bf16_to_f32(oracle.rmsnorm(xs)).astype(np.float64)
+    xt = torch.from_numpy(oracle.bf16_to_f32(xs).astype(np.float64))
+    ref = torch.nn.functional.rms_norm(xt, (1152,), eps=oracle.RMS_EPS).numpy()
+    np.testing.assert_allclose(got, ref, rtol=2 ** -8, atol=0)
+    assert np.abs(got).max() < 0.8 * np.abs(xt.numpy() / np.sqrt((xt.numpy() ** 2).mean(1, keepdims=True))).max()
+
+
+# ------------------------------------------------------------------ a8 and paper tables
+
+def test_precision_maps_match_paper():
+    t = _gold("paper_tables.json")
+    for name, ranges in t["q_ffn"].items():
+        want = set()
+        for lo, hi in ranges:
+            want |= set(range(lo, hi + 1))
+        p = oracle.precision_map(name, t["layers"])
+        assert set(np.nonzero(p)[0].tolist()) == want
+        assert int(p.sum()) == t["tab3_int8_layers"][name]
+    assert int(oracle.precision_map("bf16").sum()) == t["tab3_int8_layers"]["bf16"]
+
+
+def test_shapes_reproduce_tab1_weight_sizes():
+    t = _gold("paper_tables.json")
+    d, f, v = synth.D_MODEL, synth.D_FF, synth.VOCAB
+    assert (d, f, v, synth.N_LAYERS) == (t["hidden"], t["ffn_intermediate"], t["vocab"], t["layers"])
+    head_dim = 256  # 3.37 MB of fp16 QKV = (4 + 1 + 1) heads * head_dim * 1152 * 2 B
+    mib = lambda n: n * 2 / 2 ** 20
+    sizes = {"attention/qkv": mib((t["q_heads"] + 2 * t["kv_heads"]) * head_dim * d),
+             "attention/dense": mib(t["q_heads"] * head_dim * d),
+             "fnn/fused_fc": mib(2 * f * d), "fnn/proj": mib(f * d), "lm_head": mib(v * d)}
+    for key, mb in t["tab1_weights_MB"].items():
+        assert abs(sizes[key] - mb) < 0.006, key
+    assert t["lm_head_split"]["plugin_rows_per_call"] * t["lm_head_split"]["calls"] == v
+
+
+# ------------------------------------------------------------------ method-level claims
+
+def test_smoothing_improves_sqnr_on_outlier_channels():
+    # Sec. 6: without delta the W8A8 lm_head breaks; on channel-outlier inputs the
+    # smoothed path must be clearly better than the unsmoothed one
+    cfg = synth.linear_config(m=16, n=512)
+    x, w = cfg["x"], cfg["w"]
+    exact = x.astype(np.float64) @ w.astype(np.float64).T
+    delta = oracle.smooth_calibrate(cfg["x_cal"], [w])
+    wq, sw = oracle.quantize_weights(w, delta)
+    y_s = oracle.w8a8_linear(x, wq, sw, delta)
+    wq0, sw0 = oracle.quantize_weights(w, None)
+    y_0 = oracle.w8a8_linear(x, wq0, sw0, None)
+    s_smooth = oracle.sqnr_db(exact, y_s)
+    s_plain = oracle.sqnr_db(exact, y_0)
+    assert s_smooth > s_plain + 6.0, (s_smooth, s_plain)
+    assert s_smooth > 30.0
+
+
+def test_int8_ffn_tracks_exact_ffn():
+    cfg = synth.ffn_config(m=8, d=256, f=512)
+    q = oracle.quantize_ffn(cfg["w_gate"], cfg["w_up"], cfg["w_down"], cfg["x_cal"])
+    y = oracle.bf16_to_f32(oracle.w8a8_ffn(cfg["x"], q))
+    xf = oracle.bf16_to_f32(cfg["x"]).astype(np.float64)
+    g = xf @ oracle.bf16_to_f32(cfg["w_gate"]).astype(np.float64).T
+    u = xf @ oracle.bf16_to_f32(cfg["w_up"]).astype(np.float64).T
+    h = torch.nn.functional.gelu(torch.from_numpy(g), approximate="tanh").numpy() * u
+    exact = h @ oracle.bf16_to_f32(cfg["w_down"]).astype(np.float64).T
+    assert oracle.sqnr_db(exact, y) > 25.0
+
+
+def test_lm_head_row_split_invariance():
+    cfg = synth.lm_head_config(m=4, d=128, vocab=256)
+    delta = oracle.smooth_calibrate(cfg["x_cal"], [cfg["w"]])
+    wq, sw = oracle.quantize_weights(cfg["w"], delta)
+    full = oracle.w8a8_lm_head(cfg["x"], wq, sw, delta)
+    parts = []
+    for i in range(0, 256, 64):
+        wqi, swi = oracle.quantize_weights(cfg["w"][i:i + 64], delta)
+        parts.append(oracle.w8a8_lm_head(cfg["x"], wqi, swi, delta))
+    np.testing.assert_array_equal(full, np.concatenate(parts, 1))
+
+
+def test_stack_all_bf16_and_int8_maps_differ_only_on_int8_layers():
+    cfg = synth.stack_config(m=4, n_layers=3, d=128, f=256, vocab=64)
+    layers = []
+    for L in cfg["layers"]:
+        layers.append(dict(L, int8=oracle.quantize_ffn(L["w_gate"], L["w_up"], L["w_down"], cfg["x_cal"])))
+    lm = dict(w=cfg["w_lm"])
+    p0 = np.zeros(3, np.uint8)
+    p1 = np.array([0, 1, 0], np.uint8)
+    l0, h0 = oracle.stack(cfg["x"], layers, p0, lm, False, return_hidden=True)
+    l1, h1 = oracle.stack(cfg["x"], layers, p1, lm, False, return_hidden=True)
+    np.testing.assert_array_equal(h0[0], h1[0])     # layer 0 is bf16 in both maps
+    assert not np.array_equal(h0[1], h1[1])          # layer 1 switched to INT8
+    # the INT8 layer stays close to its bf16 counterpart
+    assert oracle.sqnr_db(oracle.bf16_to_f32(h0[1]), oracle.bf16_to_f32(h1[1])) > 20.0
