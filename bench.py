@@ -1,0 +1,353 @@
+#!/usr/bin/env python3
+"""Benchmark of the W8A8 SmoothQuant hot path on one MI355X.
+
+Step: one forward pass of Gemma-3-1B's FFN path over a batch of synthetic
+tokens -- 26 FFN blocks (d = 1152, f = 6912) under a precision map, RMSNorm
+glue, final RMSNorm and the lm_head (V = 262144) -- launched through the C ABI
+(``w8a8_ffn_stack``) and replayed as a captured graph.  Default: M = 128
+prefill tokens, every FFN block INT8 (the paper's all26 map) and INT8 lm_head,
+so every product of the step runs on the INT8 path.
+
+Printed (one JSON line): INT8 TOPS of the step, the roofline of its dominant
+kernel (INT8 gate/up GEMM with the fused GeGLU epilogue), the oracle timed on
+the host, and per layer group the INT8-vs-bf16 speedup, decode GB/s and prefill
+TOPS.  Inputs are seeded synthetic tensors (``paper_2608_28003_amd.synth``).
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--m 128] [--map all26]
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
+INT8_PEAK_TOPS = 5000.0     # dense INT8 MFMA (published figure without sparsity)
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--m", type=int, default=128)
+    ap.add_argument("--map", default="all26")
+    ap.add_argument("--no-extras", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: this path has no multi-GPU mode "
+              "(data parallelism needs no collective in the forward pass; see DESIGN.md)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_28003_amd import synth, w8a8
+
+    w8a8.lib()  # fails loudly without the HIP library
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    dev = torch.device("cuda:0")
+    M, D, F, V, NL = args.m, synth.D_MODEL, synth.D_FF, synth.VOCAB, synth.N_LAYERS
+
+    def dbf(u16):
+        return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    # ------------------------------------------------------------ inputs
+    t0 = time.time()
+    cfg = synth.stack_config(m=max(M, 64), n_layers=NL)
+    log("synthetic weights drawn in %.1f s" % (time.time() - t0))
+    x_all = dbf(cfg["x"])
+    x = x_all[:M].contiguous()
+    x_cal = dbf(cfg["x_cal"])
+    w_layers = [{k: dbf(v) for k, v in L.items()} for L in cfg["layers"]]
+    w_lm = dbf(cfg["w_lm"])
+    del cfg
+
+    # ------------------------------------------------------------ offline: a1 + a2 on the GPU
+    t0 = time.time()
+    bf16_layers = [w8a8.FfnBF16.from_weights(L["w_gate"], L["w_up"], L["w_down"]) for L in w_layers]
+    int8_layers = []
+    a = torch.empty_like(x_cal)
+    xc = x_cal.clone()
+    ws_cal = torch.empty(w8a8.bf16_ffn_workspace_bytes(x_cal.shape[0], D, F), dtype=torch.uint8, device=dev)
+    fo = torch.empty_like(x_cal)
+    for l, L in enumerate(w_layers):
+        w8a8.rmsnorm(xc, out=a)
+        a_amax = w8a8.col_absmax(a)
+        w_amax = w8a8.col_absmax(L["w_up"], w8a8.col_absmax(L["w_gate"]))
+        d_gu = w8a8.smooth_calibrate(a_amax, w_amax)
+        h = w8a8.bf16_ffn_gate_up(bf16_layers[l], a)
+        d_dn = w8a8.smooth_calibrate(w8a8.col_absmax(h), w8a8.col_absmax(L["w_down"]))
+        int8_layers.append(w8a8.FfnW8A8.from_weights(L["w_gate"], L["w_up"], L["w_down"], d_gu, d_dn))
+        w8a8.bf16_ffn(bf16_layers[l], a, out=fo, ws=ws_cal)
+        w8a8.rmsnorm_residual(xc, fo, out=xc)
+    w8a8.rmsnorm(xc, out=a)
+    d_lm = w8a8.smooth_calibrate(w8a8.col_absmax(a), w8a8.col_absmax(w_lm))
+    lm_int8 = w8a8.LinearW8A8.from_weight(w_lm, d_lm)
+    lm_bf16 = w8a8.pack_bf16(w_lm)
+    torch.cuda.synchronize()
+    del w_layers, ws_cal
+    log("calibration + quantisation on the GPU in %.1f s" % (time.time() - t0))
+
+    stack = w8a8.Stack(int8_layers, bf16_layers, lm_int8, lm_bf16, V)
+
+    def ops_int8(prec, lm8, m):
+        n8 = int(np.sum(prec))
+        return n8 * 6.0 * m * D * F + (2.0 * m * D * V if lm8 else 0.0)
+
+    def ops_all(m):
+        return NL * 6.0 * m * D * F + 2.0 * m * D * V
+
+    def make_graph(fn):
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            fn()
+            fn()
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn()
+        torch.cuda.synchronize()
+        return g
+
+    def time_graph(g, reps, warm=3):
+        for _ in range(warm):
+            g.replay()
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for _ in range(reps):
+            g.replay()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t) / reps
+
+    def time_eager(fn, reps, warm=3):
+        for _ in range(warm):
+            fn()
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t) / reps
+
+    # ------------------------------------------------------------ the step
+    prec = w8a8.precision_map(args.map)
+    lm8 = True
+    out = torch.empty((M, V), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(w8a8.stack_workspace_bytes(M, D, F, V), dtype=torch.uint8, device=dev)
+
+    def step():
+        stack.run(x, prec, lm8, out=out, ws=ws)
+
+    g = make_graph(step)
+    for _ in range(args.warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    for _ in range(args.steps):
+        g.replay()
+    torch.cuda.synchronize()
+    sec = (time.perf_counter() - t) / args.steps
+    value = ops_int8(prec, lm8, M) / sec / 1e12
+    eager_sec = time_eager(step, max(3, args.steps // 4), warm=1)
+    log("step %.3f ms (graph), %.3f ms (eager launches): %.1f INT8 TOPS" % (sec * 1e3, eager_sec * 1e3, value))
+
+    # ------------------------------------------------------------ dominant kernel roofline
+    # INT8 gate/up GEMM with the fused GeGLU epilogue, same shapes and launch
+    # configuration as inside the step, timed per launch with HIP events on the
+    # stream the library launches on (torch's current stream).
+    qx, sx = w8a8.quantize_act(x, int8_layers[0].gate.delta)
+    h = torch.empty((M, F), dtype=torch.bfloat16, device=dev)
+    reps = 4
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(NL * reps)]
+    for L in int8_layers:
+        w8a8.ffn_gate_up(L, qx, sx, M, out=h)
+    torch.cuda.synchronize()
+    for i, (e0, e1) in enumerate(evs):
+        e0.record()
+        w8a8.ffn_gate_up(int8_layers[i % NL], qx, sx, M, out=h)
+        e1.record()
+    torch.cuda.synchronize()
+    gu_us = float(np.mean([e0.elapsed_time(e1) for e0, e1 in evs])) * 1e3
+    gu_bytes = 2 * F * D + 2 * F * 4 + M * D + M * 4 + M * F * 2
+    gu_ops = 2.0 * M * D * 2 * F
+    achieved = gu_bytes / (gu_us * 1e-6) / 1e9
+    roofline = {"kernel": "gemm_tile_kernel<int8, GeGLU epilogue> (FFN gate/up)",
+                "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "avg_launch_us": round(gu_us, 3), "bytes_per_launch": gu_bytes,
+                "int8_tops": round(gu_ops / (gu_us * 1e-6) / 1e12, 1)}
+    log("gate/up kernel %.2f us: %.0f GB/s" % (gu_us, achieved))
+
+    result = {
+        "metric": "W8A8 linear INT8 TOPS (% MFMA peak) + decode GB/s; INT8-vs-bf16 speedup",
+        "value": round(value, 2), "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(sec * 1e3, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "int8", "data": "synthetic",
+        "config": {"workload": "Gemma-3-1B FFN stack: 26 gated FFN blocks (1152 -> 6912 -> 1152) "
+                               "under the %s precision map + RMSNorm glue + INT8 lm_head "
+                               "(1152 -> 262144), M=%d prefill tokens" % (args.map, M),
+                   "m": M, "layers": NL, "map": args.map, "lm_head": "int8",
+                   "launch": "captured graph", "int8_mfma_frac": round(value / INT8_PEAK_TOPS, 4),
+                   "eager_ms_per_step": round(eager_sec * 1e3, 4)},
+        "roofline": roofline,
+    }
+
+    # ------------------------------------------------------------ per layer group
+    if not args.no_extras:
+        result["groups"] = extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16,
+                                  x_all, w_lm, M, D, F, V, NL, make_graph, time_graph, ops_int8,
+                                  ops_all, sec)
+
+    # ------------------------------------------------------------ oracle on the host
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(M)
+
+    print(json.dumps(result), flush=True)
+
+
+def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all, w_lm, M, D, F,
+           V, NL, make_graph, time_graph, ops_int8, ops_all, step_sec):
+    dev = x_all.device
+    groups = {}
+
+    # --- FFN block, decode and prefill, 26 distinct layers per timed pass
+    for m in (1, 128, 2048):
+        xm = (x_all[:m] if m <= x_all.shape[0] else
+              x_all.repeat((m + x_all.shape[0] - 1) // x_all.shape[0], 1)[:m]).contiguous()
+        y = torch.empty((m, D), dtype=torch.bfloat16, device=dev)
+        ws8 = torch.empty(w8a8.ffn_workspace_bytes(m, D, F), dtype=torch.uint8, device=dev)
+        wsb = torch.empty(w8a8.bf16_ffn_workspace_bytes(m, D, F), dtype=torch.uint8, device=dev)
+        g8 = make_graph(lambda: [w8a8.ffn(L, xm, out=y, ws=ws8) for L in int8_layers])
+        gb = make_graph(lambda: [w8a8.bf16_ffn(L, xm, out=y, ws=wsb) for L in bf16_layers])
+        t8 = time_graph(g8, 10) / NL
+        tb = time_graph(gb, 10) / NL
+        bytes8 = 3 * F * D + 2 * F * 4 + D * 4 + F * 4 + D * 4 + m * D * 2 * 2
+        bytesb = 3 * F * D * 2 + m * D * 2 * 2
+        ops = 6.0 * m * D * F
+        groups["ffn_m%d" % m] = {
+            "int8_us": round(t8 * 1e6, 2), "bf16_us": round(tb * 1e6, 2),
+            "speedup": round(tb / t8, 3),
+            "int8_GBs": round(bytes8 / t8 / 1e9, 1), "int8_hbm_frac": round(bytes8 / t8 / 1e9 / HBM_PEAK_GBS, 3),
+            "bf16_GBs": round(bytesb / tb / 1e9, 1),
+            "int8_tops": round(ops / t8 / 1e12, 1), "int8_mfma_frac": round(ops / t8 / 1e12 / INT8_PEAK_TOPS, 4),
+            "note": "per FFN block incl. activation quant, GeGLU and requant; graph of 26 distinct layers"}
+        del g8, gb
+        log("ffn m=%d: int8 %.2f us, bf16 %.2f us" % (m, t8 * 1e6, tb * 1e6))
+
+    # --- FFN GEMMs alone at M = 2048 (prefill), INT8 TOPS against the MFMA peak
+    m = 2048
+    xm = x_all.repeat((m + x_all.shape[0] - 1) // x_all.shape[0], 1)[:m].contiguous()
+    qx, sx = w8a8.quantize_act(xm, int8_layers[0].gate.delta)
+    h = torch.empty((m, F), dtype=torch.bfloat16, device=dev)
+    qh, sh = w8a8.quantize_act(h.normal_(), int8_layers[0].down.delta)
+    y = torch.empty((m, D), dtype=torch.bfloat16, device=dev)
+    wsl = torch.empty(w8a8.linear_workspace_bytes(m, D, F), dtype=torch.uint8, device=dev)
+    acc = torch.empty((m, D), dtype=torch.int32, device=dev)
+    g_gu = make_graph(lambda: [w8a8.ffn_gate_up(L, qx, sx, m, out=h) for L in int8_layers])
+    g_dn = make_graph(lambda: [w8a8.gemm_i8_i32(qh, m, L.down.wq, D, F, ws=wsl) for L in int8_layers])
+    t_gu = time_graph(g_gu, 10) / NL
+    t_dn = time_graph(g_dn, 10) / NL
+    groups["prefill_gemm_m2048"] = {
+        "gate_up_us": round(t_gu * 1e6, 2), "gate_up_tops": round(4.0 * m * D * F / t_gu / 1e12, 1),
+        "gate_up_mfma_frac": round(4.0 * m * D * F / t_gu / 1e12 / INT8_PEAK_TOPS, 4),
+        "down_us": round(t_dn * 1e6, 2), "down_tops": round(2.0 * m * D * F / t_dn / 1e12, 1),
+        "down_mfma_frac": round(2.0 * m * D * F / t_dn / 1e12 / INT8_PEAK_TOPS, 4)}
+    del g_gu, g_dn
+    log("prefill gemms m=2048: gate/up %.2f us, down %.2f us" % (t_gu * 1e6, t_dn * 1e6))
+
+    # --- lm_head decode: INT8 vs our bf16 kernel vs torch.mm (hipBLASLt) bf16
+    w_lm_t = w_lm.t().contiguous()           # d x V, a plain (non-transposed) right operand
+    for m in (1, 8, 64):
+        xm = x_all[:m].contiguous()
+        lg = torch.empty((m, V), dtype=torch.bfloat16, device=dev)
+        ws8 = torch.empty(w8a8.lm_head_workspace_bytes(m, V, D), dtype=torch.uint8, device=dev)
+        wsb_n = w8a8.bf16_linear_workspace_bytes(m, V, D)
+        wsb = torch.empty(max(wsb_n, 1), dtype=torch.uint8, device=dev)
+        g8 = make_graph(lambda: w8a8.lm_head(lm_int8, xm, out=lg, ws=ws8))
+        gb = make_graph(lambda: w8a8.bf16_linear(xm, lm_bf16, V, D, out=lg, ws=wsb if wsb_n else None))
+        gt = make_graph(lambda: torch.mm(xm, w_lm_t, out=lg))
+        t8 = time_graph(g8, 20)
+        tb = time_graph(gb, 20)
+        tt = time_graph(gt, 20)
+        b8 = V * D + V * 4 + D * 4 + m * D * 2 + m * V * 2
+        bb = V * D * 2 + m * D * 2 + m * V * 2
+        groups["lm_head_m%d" % m] = {
+            "int8_us": round(t8 * 1e6, 2), "bf16_ours_us": round(tb * 1e6, 2),
+            "bf16_torch_us": round(tt * 1e6, 2), "speedup": round(min(tb, tt) / t8, 3),
+            "int8_GBs": round(b8 / t8 / 1e9, 1), "int8_hbm_frac": round(b8 / t8 / 1e9 / HBM_PEAK_GBS, 3),
+            "bf16_best_GBs": round(bb / min(tb, tt) / 1e9, 1)}
+        del g8, gb, gt
+        log("lm_head m=%d: int8 %.2f us, bf16 ours %.2f us, torch %.2f us" % (m, t8 * 1e6, tb * 1e6, tt * 1e6))
+    del w_lm_t
+
+    # --- the paper's precision maps on the whole step (same M as the step)
+    xm = x_all[:M].contiguous()
+    out = torch.empty((M, V), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(w8a8.stack_workspace_bytes(M, D, F, V), dtype=torch.uint8, device=dev)
+    maps = {}
+    base = None
+    for name, mp, lm8 in [("bf16", "bf16", False), ("lm_head only", "bf16", True),
+                          ("FFN 5+5", "5+5", False), ("FFN 5+5 + lm_head", "5+5", True),
+                          ("FFN 10+10 + lm_head", "10+10", True), ("FFN all26", "all26", False),
+                          ("FFN all26 + lm_head", "all26", True)]:
+        prec = w8a8.precision_map(mp)
+        gs = make_graph(lambda: stack.run(xm, prec, lm8, out=out, ws=ws))
+        ts = time_graph(gs, 10)
+        del gs
+        if base is None:
+            base = ts
+        maps[name] = {"ms": round(ts * 1e3, 4), "speedup_vs_bf16": round(base / ts, 3)}
+    groups["stack_maps_m%d" % M] = maps
+    groups["paper_context"] = {"note": "RTX 5090 + TensorRT-LLM, end-to-end decode tok/s at batch 1; not a target",
+                               "FFN 5+5 + lm_head": 1.110, "FFN all26 + lm_head": 1.191}
+    return groups
+
+
+def cpu_baseline(M):
+    """The oracle, untouched, on a bounded sample of the workload: INT8 FFN
+    blocks at the step's M on the first layers, until ~10 s of CPU work."""
+    import oracle
+    from paper_2608_28003_amd import synth
+    oracle.build()
+    cfg = synth.ffn_config(m=M)
+    x = cfg["x"]
+    d_gu = oracle.smooth_calibrate(cfg["x_cal"], [cfg["w_gate"], cfg["w_up"]])
+    q = dict(delta_gu=d_gu, delta_down=np.ones(synth.D_FF, np.float32))
+    q["wq_gate"], q["s_gate"] = oracle.quantize_weights(cfg["w_gate"], d_gu)
+    q["wq_up"], q["s_up"] = oracle.quantize_weights(cfg["w_up"], d_gu)
+    q["wq_down"], q["s_down"] = oracle.quantize_weights(cfg["w_down"], q["delta_down"])
+    ops = 6.0 * M * synth.D_MODEL * synth.D_FF
+    n, t = 0, 0.0
+    while t < 10.0 and n < 26:
+        t0 = time.perf_counter()
+        oracle.w8a8_ffn(x, q)
+        t += time.perf_counter() - t0
+        n += 1
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": round(ops * n / t / 1e12, 5), "unit": "TOPS", "cores": threads,
+            "kind": "oracle",
+            "sample": "%d INT8 FFN block(s) (1152 -> 6912 -> 1152, M=%d) of the step's 26 + lm_head, "
+                      "oracle C loops with OpenMP, %.1f s" % (n, M, t)}
+
+
+if __name__ == "__main__":
+    main()

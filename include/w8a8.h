@@ -1,0 +1,274 @@
+/*
+ * w8a8.h -- C ABI of the MI355X (gfx950) W8A8 SmoothQuant library.
+ *
+ * The operations follow arxiv 2608.28003 ("layer bit-width allocation ... under
+ * a quality-degradation constraint", Gemma-3-1B):
+ *   Sec. 3  eq. si, what-ffn    symmetric per-output-channel int8 weights, b = 8
+ *   Sec. 4  eq. delta-attn      SmoothQuant migration factor, alpha = 0.5
+ *   Sec. 6  eq. delta-lmhead, xhat-lmhead, what-lmhead   smoothing x/delta, W*delta
+ *           eq. stx, xint8      dynamic per-token activation quantisation
+ *           eq. gemm-final      y = s_t * s_i * sum_j q_x q_w
+ *   Sec. 3  eq. ffn55, ffn1010, ffnall26   which FFN layers run in INT8
+ *
+ * Conventions for every entry point
+ *   - Tensor pointers are DEVICE pointers allocated by the caller; the library
+ *     allocates nothing, keeps no pointer after returning and holds no state
+ *     beyond a cache of device properties.  Work is enqueued on `stream`
+ *     (a hipStream_t; NULL is the default stream) and is asynchronous: results
+ *     are ready after the caller synchronises that stream.
+ *   - All matrices are row-major unless stated otherwise.  bf16 tensors are
+ *     16-bit bfloat16 bit patterns.
+ *   - Arguments are validated on the host before any HIP call:
+ *       W8A8_EINVAL       NULL pointer, a size < 1, a pointer not 16-byte aligned
+ *       W8A8_EUNSUPPORTED a dtype the call does not take, K > 133144 (the int32
+ *                         accumulator bound K * 127^2 <= 2^31 - 1), or a shape
+ *                         constraint stated at the call
+ *       W8A8_EWORKSPACE   ws_bytes below the size the *_workspace_bytes query returns
+ *       W8A8_EHIP         a HIP launch error (text in w8a8_last_error())
+ *   - Numerical readings (the paper leaves them implicit): round() is round-half-
+ *     to-even; codes are clamped to [-127, 127]; an all-zero row has scale 0 and
+ *     codes 0; a smoothed value, its scale and the ratio that is rounded are IEEE
+ *     binary32 with one rounding per operation; the dequantised value is
+ *     (float(acc) * s_t) * s_i in binary32; bf16 outputs round to nearest even.
+ *   - No exception crosses the ABI.  Non-finite inputs are outside the contract.
+ *
+ * Packed int8 layout ("fragment layout", used for weights and for quantised
+ * activations).  A logical R x K int8 matrix is stored as Rp = ceil(R/16)*16 rows
+ * by Kp = ceil(K/64)*64 columns, zero padded, cut into 16 x 64 fragments of
+ * 1024 bytes.  Fragment (rb, kb) starts at byte (rb * Kp/64 + kb) * 1024; inside
+ * it, lane l = 0..63 owns bytes [16 l, 16 l + 16), which hold row rb*16 + (l % 16),
+ * columns kb*64 + (l / 16)*16 + 0..15.  One wavefront load of 16 bytes per lane
+ * therefore reads one whole fragment, and a 16-row block is one contiguous run
+ * of Kp*16 bytes.
+ *
+ * Packed bf16 layout: the same with 16 x 32 fragments of bf16 (1024 bytes):
+ * Kp = ceil(K/32)*32; lane l holds row rb*16 + (l % 16), columns
+ * kb*32 + (l / 16)*8 + 0..7.
+ */
+#ifndef W8A8_H
+#define W8A8_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef void* w8a8_stream_t; /* a hipStream_t */
+
+typedef enum {
+    W8A8_OK = 0,
+    W8A8_EINVAL = 1,
+    W8A8_EUNSUPPORTED = 2,
+    W8A8_EHIP = 3,
+    W8A8_EWORKSPACE = 4
+} w8a8_status;
+
+typedef enum { W8A8_F32 = 0, W8A8_BF16 = 1 } w8a8_dtype;
+
+#define W8A8_MAX_K 133144
+
+/* One INT8 linear layer y = x W^T (Sec. 6): packed codes of W_hat = W diag(delta)
+   (n x k, fragment layout), their per-output-channel scales s_w[n], and the
+   smoothing factors delta[k] the activations are divided by (NULL: none). */
+typedef struct {
+    int64_t n, k;
+    const void* wq;
+    const float* s_w;
+    const float* delta;
+} w8a8_linear_desc;
+
+/* One INT8 gated FFN block (Sec. 3): gate and up are d -> f and share the input
+   and its smoothing delta_gu[d]; down is f -> d with its own delta_down[f]. */
+typedef struct {
+    int64_t d, f;
+    const void* wq_gate; const float* s_gate;   /* f x d packed, [f] */
+    const void* wq_up;   const float* s_up;     /* f x d packed, [f] */
+    const float* delta_gu;                      /* [d] or NULL */
+    const void* wq_down; const float* s_down;   /* d x f packed, [d] */
+    const float* delta_down;                    /* [f] or NULL */
+} w8a8_ffn_desc;
+
+/* One bf16 gated FFN block (the layers a precision map keeps in bf16):
+   weights in the packed bf16 layout. */
+typedef struct {
+    int64_t d, f;
+    const void* wp_gate;  /* f x d */
+    const void* wp_up;    /* f x d */
+    const void* wp_down;  /* d x f */
+} w8a8_bf16_ffn_desc;
+
+/* A stack of FFN blocks with RMSNorm glue and an lm_head (used with a
+   precision map).  int8_ffn[l] is read for layers the map sets to INT8,
+   bf16_ffn[l] for the others; both arrays live in HOST memory. */
+typedef struct {
+    int64_t n_layers, d, f, vocab;
+    const w8a8_ffn_desc* int8_ffn;
+    const w8a8_bf16_ffn_desc* bf16_ffn;
+    w8a8_linear_desc lm_head_int8;   /* n = vocab, k = d */
+    const void* lm_head_bf16;        /* vocab x d, packed bf16 layout */
+} w8a8_stack_desc;
+
+/* ---------------------------------------------------------------- sizes */
+
+/* Bytes of the packed int8 layout for a logical n x k matrix. */
+size_t w8a8_packed_bytes(int64_t n, int64_t k);
+/* Bytes of the packed bf16 layout for a logical n x k matrix. */
+size_t w8a8_packed_bf16_bytes(int64_t n, int64_t k);
+/* Workspace the calls below need (bytes, 256-byte aligned sub-buffers). */
+size_t w8a8_linear_workspace_bytes(int64_t m, int64_t n, int64_t k);
+size_t w8a8_ffn_workspace_bytes(int64_t m, int64_t d, int64_t f);
+size_t w8a8_bf16_ffn_workspace_bytes(int64_t m, int64_t d, int64_t f);
+size_t w8a8_lm_head_workspace_bytes(int64_t m, int64_t n, int64_t k);
+size_t w8a8_bf16_linear_workspace_bytes(int64_t m, int64_t n, int64_t k);
+size_t w8a8_stack_workspace_bytes(int64_t m, int64_t d, int64_t f, int64_t vocab);
+
+/* ---------------------------------------------------------------- a1: calibration */
+
+/* Running column maximum (Sec. 4 eq. delta-attn, Sec. 6 eq. delta-lmhead):
+   amax[j] <- max(amax[j], max_t |x[t][j]|) over the rows x[rows][k].  Applied to
+   calibration activations it gives max_t |X_tj|; applied to each weight matrix
+   that consumes an input (gate and up for the FFN input) it gives max_i |W_ij|.
+   x: f32 or bf16; amax: device float[k], read and written (start from zeros). */
+w8a8_status w8a8_col_absmax(const void* x, w8a8_dtype x_dtype, int64_t rows, int64_t k,
+                            float* amax, w8a8_stream_t stream);
+
+/* SmoothQuant factor (Sec. 4 eq. delta-attn, Sec. 6 eq. delta-lmhead):
+   delta[j] = a_j^alpha / w_j^(1 - alpha) with a_j = max(act_amax[j], 1e-5) and
+   w_j = max(w_amax[j], 1e-5), evaluated in binary64 and rounded once to float
+   (square roots at alpha = 0.5).  All three arrays are device float[k].
+   EUNSUPPORTED if alpha is outside [0, 1]. */
+w8a8_status w8a8_smooth_calibrate(const float* act_amax, const float* w_amax, int64_t k,
+                                  float alpha, float* delta, w8a8_stream_t stream);
+
+/* ---------------------------------------------------------------- a2: weights */
+
+/* Offline weight quantisation (Sec. 3 eq. si, what-ffn; Sec. 6 eq. what-lmhead):
+   W_hat = W diag(delta) (delta NULL: W), s_w[i] = max_j |W_hat_ij| / 127,
+   q_ij = clamp(rne(W_hat_ij / s_w[i]), -127, 127).
+   w: n x k, f32 or bf16.  wq: w8a8_packed_bytes(n, k) bytes, fragment layout
+   (padding written as zeros).  s_w: float[n]. */
+w8a8_status w8a8_quantize_weights(const void* w, w8a8_dtype w_dtype, int64_t n, int64_t k,
+                                  const float* delta, void* wq, float* s_w,
+                                  w8a8_stream_t stream);
+
+/* Copy the packed int8 layout back to a row-major int8 n x k matrix (checks). */
+w8a8_status w8a8_unpack_weights(const void* wq, int64_t n, int64_t k, int8_t* q,
+                                w8a8_stream_t stream);
+
+/* Repack a bf16 n x k weight into the packed bf16 layout
+   (w8a8_packed_bf16_bytes(n, k) bytes) for the bf16 path.  k % 8 == 0. */
+w8a8_status w8a8_pack_bf16(const void* w, int64_t n, int64_t k, void* wp,
+                           w8a8_stream_t stream);
+
+/* ---------------------------------------------------------------- a3: activations */
+
+/* Dynamic per-token quantisation (Sec. 6 eq. xhat-lmhead, stx, xint8):
+   x_hat = x / delta (delta NULL: x), s_x[t] = max_j |x_hat_tj| / 127,
+   q = clamp(rne(x_hat / s_x[t]), -127, 127).
+   x: m x k, f32 or bf16.  qx: w8a8_packed_bytes(m, k) bytes in the fragment
+   layout (zero padded).  s_x: float[m]. */
+w8a8_status w8a8_quantize_act(const void* x, w8a8_dtype x_dtype, int64_t m, int64_t k,
+                              const float* delta, void* qx, float* s_x,
+                              w8a8_stream_t stream);
+
+/* ---------------------------------------------------------------- a4, a5: INT8 GEMM */
+
+/* The integer product of eq. gemm-final: acc[t][i] = sum_j qx[t][j] * wq[i][j]
+   in int32, exact.  qx: packed m x k codes, wq: packed n x k codes, acc: int32
+   m x n row-major.  Uses the same GEMM kernels as w8a8_linear with an identity
+   epilogue.  ws: w8a8_linear_workspace_bytes(m, n, k) bytes. */
+w8a8_status w8a8_gemm_i8_i32(const void* qx, int64_t m, const void* wq, int64_t n,
+                             int64_t k, int32_t* acc, void* ws, size_t ws_bytes,
+                             w8a8_stream_t stream);
+
+/* W8A8 linear layer (Sec. 6): quantise x per token after x / delta, INT8 GEMM,
+   dequantise y = (float(acc) * s_x[t]) * s_w[i] to y_dtype (f32 or bf16).
+   x: m x k (f32 or bf16), y: m x n.  ws: w8a8_linear_workspace_bytes(m, n, k). */
+w8a8_status w8a8_linear(const w8a8_linear_desc* desc, const void* x, w8a8_dtype x_dtype,
+                        int64_t m, void* y, w8a8_dtype y_dtype, void* ws, size_t ws_bytes,
+                        w8a8_stream_t stream);
+
+/* ---------------------------------------------------------------- a6: FFN */
+
+/* Gate/up stage of the INT8 FFN with the gated activation fused in its epilogue:
+   g = dequant(qx . gate), u = dequant(qx . up) (binary32, never stored),
+   h = bf16(gelu_tanh(g) * u), gelu_tanh(g) = 0.5 g (1 + tanh(sqrt(2/pi)(g + 0.044715 g^3))).
+   qx: packed m x d codes, s_x: float[m], h: bf16 m x f row-major. */
+w8a8_status w8a8_ffn_gate_up(const w8a8_ffn_desc* desc, const void* qx, const float* s_x,
+                             int64_t m, void* h, w8a8_stream_t stream);
+
+/* Whole INT8 FFN block (Sec. 3, Tab. 1 fused_fc + proj): quantise x / delta_gu,
+   gate/up + GeGLU (above), requantise h / delta_down per token, down INT8 GEMM,
+   dequantise to bf16.  x, y: bf16 m x d.  ws: w8a8_ffn_workspace_bytes(m, d, f). */
+w8a8_status w8a8_ffn(const w8a8_ffn_desc* desc, const void* x, int64_t m, void* y,
+                     void* ws, size_t ws_bytes, w8a8_stream_t stream);
+
+/* ---------------------------------------------------------------- a7: lm_head */
+
+/* INT8 lm_head (Sec. 6, eq. gemm-final, all 262144 rows in one launch): logits
+   bf16 m x n from x bf16 m x k.  Tuned for m <= 64.
+   ws: w8a8_lm_head_workspace_bytes(m, n, k). */
+w8a8_status w8a8_lm_head(const w8a8_linear_desc* desc, const void* x, int64_t m,
+                         void* logits, void* ws, size_t ws_bytes, w8a8_stream_t stream);
+
+/* ---------------------------------------------------------------- bf16 path */
+
+/* bf16 projection y = bf16(x W^T), fp32 accumulation.  x: bf16 m x k
+   (k % 32 == 0), wp: packed bf16 n x k, y: bf16 m x n.
+   ws: w8a8_bf16_linear_workspace_bytes(m, n, k) bytes (may be 0, then ws may be NULL). */
+w8a8_status w8a8_bf16_linear(const void* x, int64_t m, const void* wp, int64_t n,
+                             int64_t k, void* y, void* ws, size_t ws_bytes,
+                             w8a8_stream_t stream);
+
+/* Gate/up stage of the bf16 FFN: h = bf16(gelu_tanh(g) * u), g and u the fp32
+   accumulators of x W_gate^T and x W_up^T.  x: bf16 m x d, h: bf16 m x f.  Used
+   for the bf16 layers and to gather the calibration statistic of the down
+   projection's input (Sec. 6, eq. delta-lmhead applied to that input). */
+w8a8_status w8a8_bf16_ffn_gate_up(const w8a8_bf16_ffn_desc* desc, const void* x, int64_t m,
+                                  void* h, w8a8_stream_t stream);
+
+/* bf16 FFN block: h = bf16(gelu_tanh(g) * u) with g, u the fp32 accumulators,
+   y = bf16(h W_down^T).  ws: w8a8_bf16_ffn_workspace_bytes(m, d, f). */
+w8a8_status w8a8_bf16_ffn(const w8a8_bf16_ffn_desc* desc, const void* x, int64_t m,
+                          void* y, void* ws, size_t ws_bytes, w8a8_stream_t stream);
+
+/* ---------------------------------------------------------------- a8, a9: stack */
+
+/* RMSNorm with unit gain: y = bf16(x / sqrt(mean_j x_j^2 + 1e-6)), bf16 m x d;
+   d % 8 == 0 and d <= 8192 (EUNSUPPORTED otherwise). */
+w8a8_status w8a8_rmsnorm(const void* x, int64_t m, int64_t d, void* y,
+                         w8a8_stream_t stream);
+
+/* Post-FFN norm and residual: x_out = bf16(x + bf16(RMSNorm(f))), bf16 m x d.
+   x_out may alias x. */
+w8a8_status w8a8_rmsnorm_residual(const void* x, const void* f, int64_t m, int64_t d,
+                                  void* x_out, w8a8_stream_t stream);
+
+/* FFN layer subsets of Sec. 3 eq. ffn55 / ffn1010 / ffnall26 as a host array:
+   prec[l] = 1 when layer l runs in INT8.  name: "bf16", "5+5", "10+10", "all26".
+   Returns the number of INT8 layers, or -1 for an unknown name or n_layers < 26
+   (the subsets index a 26-layer model). */
+int w8a8_precision_map(const char* name, uint8_t* prec, int n_layers);
+
+/* The FFN stack under a precision map (host prec[n_layers], 0 = bf16, 1 = INT8):
+   for each layer x <- bf16(x + RMSNorm(FFN_l(RMSNorm(x)))), FFN_l INT8 or bf16 by
+   prec[l]; then the final RMSNorm and the lm_head, INT8 if lm_head_int8 != 0.
+   x: bf16 m x d (not modified), logits: bf16 m x vocab.
+   ws: w8a8_stack_workspace_bytes(m, d, f, vocab). */
+w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec,
+                           int lm_head_int8, const void* x, int64_t m, void* logits,
+                           void* ws, size_t ws_bytes, w8a8_stream_t stream);
+
+/* ---------------------------------------------------------------- errors */
+
+const char* w8a8_status_str(w8a8_status s);
+/* Detail of the last error on the calling thread ("" if none). */
+const char* w8a8_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* W8A8_H */

@@ -1,0 +1,711 @@
+// Host side of the C ABI declared in include/w8a8.h: argument validation (done
+// before any HIP call), the GEMM planner, workspace carving and the pipelines
+// (linear, FFN block, lm_head, bf16 path, precision-map stack).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+
+#include "../../include/w8a8.h"
+#include "kernels.h"
+
+using namespace w8a8;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+w8a8_status fail(w8a8_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+w8a8_status hip_check(hipError_t e, const char* what) {
+  if (e == hipSuccess) return W8A8_OK;
+  return fail(W8A8_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+hipStream_t S(w8a8_stream_t s) { return reinterpret_cast<hipStream_t>(s); }
+
+// ------------------------------------------------------------------ planner
+
+struct Plan {
+  bool skinny = false;
+  int tile = TILE_128x128;
+  int mb = 1;       // skinny: 16-row blocks of A
+  int kc = 18;      // skinny: LDS fragment columns
+  int splits = 1;
+  int kchunk = 0;
+  int nbpb = 4;     // skinny: column blocks per workgroup
+};
+
+int env_int(const char* name, int dflt) {
+  const char* v = std::getenv(name);
+  return v && *v ? std::atoi(v) : dflt;
+}
+
+void tile_shape(int tile, int* bm, int* bn) {
+  switch (tile) {
+    case TILE_128x128: *bm = 128; *bn = 128; break;
+    case TILE_128x64: *bm = 128; *bn = 64; break;
+    case TILE_64x64: *bm = 64; *bn = 64; break;
+    case TILE_256x128: *bm = 256; *bn = 128; break;
+    case TILE_GLU_128x32: *bm = 128; *bn = 32; break;
+    case TILE_GLU_64x64: *bm = 64; *bn = 64; break;
+    case TILE_GLU_128x64: *bm = 128; *bn = 64; break;
+    default: *bm = 128; *bn = 128;
+  }
+}
+
+int64_t tiles_of(int tile, int64_t m, int64_t n) {
+  int bm, bn;
+  tile_shape(tile, &bm, &bn);
+  return ceil_div(m, bm) * ceil_div(n, bn);
+}
+
+// Deterministic in (m, n, k, path); the workspace queries use the same plan.
+// W8A8_GEMM_TILE / W8A8_GEMM_SPLITS override the tiled path (tuning hook).
+Plan plan_gemm(int64_t m, int64_t n, int64_t k, bool bf16, bool glu) {
+  Plan p;
+  const int64_t kb = bf16 ? ceil_div(k, kFragK16) : ceil_div(k, kFragK8);
+  const int64_t nbc = ceil_div(n, 16);
+  if (m <= 64) {
+    p.skinny = true;
+    p.mb = m <= 16 ? 1 : (m <= 32 ? 2 : 4);
+    const int kcs[3] = {9, 18, 36};
+    int kc_fit = 0;
+    for (int c : kcs)
+      if (kb <= c) { kc_fit = c; break; }
+    const bool fits_lds = kc_fit && (int64_t)p.mb * kc_fit <= 144;
+    if (glu || (fits_lds && nbc >= 512)) {
+      if (!fits_lds) {
+        p.skinny = false;  // falls through to the tiled plan
+      } else {
+        p.kc = kc_fit;
+        p.splits = 1;
+        p.kchunk = (int)kb;
+      }
+    } else {
+      p.kc = 9;
+      p.kchunk = 9;
+      p.splits = (int)ceil_div(kb, 9);
+    }
+    if (p.skinny) {
+      int64_t nbpb = p.mb == 1 ? std::max<int64_t>(1, ceil_div(nbc, 2048))
+                               : round_up(std::max<int64_t>(4, ceil_div(nbc, 512)), 4);
+      p.nbpb = env_int("W8A8_SKINNY_NBPB", (int)nbpb);
+      return p;
+    }
+  }
+  p.skinny = false;
+  if (glu) {
+    if (m <= 128)
+      p.tile = TILE_GLU_128x32;
+    else
+      p.tile = tiles_of(TILE_GLU_128x64, m, n) >= 256 ? TILE_GLU_128x64 : TILE_GLU_64x64;
+  } else {
+    if (tiles_of(TILE_128x128, m, n) >= 256)
+      p.tile = TILE_128x128;
+    else if (tiles_of(TILE_128x64, m, n) >= 256)
+      p.tile = TILE_128x64;
+    else
+      p.tile = TILE_64x64;
+  }
+  p.tile = env_int("W8A8_GEMM_TILE", p.tile);
+  const int64_t tiles = tiles_of(p.tile, m, n);
+  int splits = 1;
+  if (!glu && tiles < 200)
+    splits = (int)std::min<int64_t>(ceil_div(256, tiles), std::max<int64_t>(1, kb / 4));
+  splits = env_int("W8A8_GEMM_SPLITS", splits);
+  if (glu || splits < 1) splits = 1;
+  p.kchunk = (int)ceil_div(kb, splits);
+  p.splits = (int)ceil_div(kb, p.kchunk);
+  return p;
+}
+
+size_t plan_ws_bytes(const Plan& p, int64_t m, int64_t n) {
+  if (p.splits <= 1) return 0;
+  return align256((size_t)p.splits * m * n * 4);
+}
+
+// Run one GEMM with a plan.  A: packed codes (int8) or row-major bf16;
+// B (and B2 for the gated epilogue): packed weights.  A K-split plan writes
+// partial sums to gemm_ws and a second launch reduces them into `out`.
+w8a8_status run_gemm(const Plan& pl, bool bf16, int epi, const void* A, int64_t lda, int64_t m,
+                     const void* B, const void* B2, int64_t n, int64_t k, const float* s_a,
+                     const float* s_b, const float* s_b2, void* out, int64_t ldo, void* gemm_ws,
+                     hipStream_t st) {
+  GemmParams p{};
+  p.A = A;
+  p.B = B;
+  p.B2 = B2;
+  p.lda = lda;
+  p.M = (int)m;
+  p.N = (int)n;
+  p.rb_a = (int)ceil_div(m, 16);
+  p.rb_b = (int)ceil_div(n, 16);
+  p.kb_count = (int)(bf16 ? ceil_div(k, kFragK16) : ceil_div(k, kFragK8));
+  p.kchunk = pl.kchunk;
+  p.splits = pl.splits;
+  p.s_a = s_a;
+  p.s_b = s_b;
+  p.s_b2 = s_b2;
+  p.out = out;
+  p.ldo = ldo;
+  p.part = pl.splits > 1 ? gemm_ws : nullptr;
+  hipError_t e = pl.skinny ? launch_gemm_skinny(bf16, epi, pl.mb, pl.kc, p, pl.nbpb, st)
+                           : launch_gemm_tile(bf16, epi, pl.tile, p, st);
+  w8a8_status s = hip_check(e, pl.skinny ? "gemm_skinny" : "gemm_tile");
+  if (s != W8A8_OK || pl.splits <= 1) return s;
+  return hip_check(launch_splitk_reduce(bf16, epi, p, st), "splitk_reduce");
+}
+
+// ------------------------------------------------------------------ validation
+
+#define REQUIRE(cond, code, msg) \
+  do {                           \
+    if (!(cond)) return fail(code, msg); \
+  } while (0)
+
+w8a8_status check_ptr(const void* p, const char* name) {
+  if (!p) return fail(W8A8_EINVAL, std::string(name) + " is NULL");
+  if (!aligned16(p)) return fail(W8A8_EINVAL, std::string(name) + " is not 16-byte aligned");
+  return W8A8_OK;
+}
+
+#define CHECK_PTR(p)                                \
+  do {                                              \
+    w8a8_status _s = check_ptr((p), #p);            \
+    if (_s != W8A8_OK) return _s;                   \
+  } while (0)
+
+w8a8_status check_k(int64_t k) {
+  REQUIRE(k >= 1, W8A8_EINVAL, "k < 1");
+  REQUIRE(k % 16 == 0, W8A8_EUNSUPPORTED, "k must be a multiple of 16");
+  REQUIRE(k <= W8A8_MAX_K, W8A8_EUNSUPPORTED, "k > 133144 would overflow the int32 accumulator");
+  return W8A8_OK;
+}
+
+#define CHECK(expr)                      \
+  do {                                   \
+    w8a8_status _s = (expr);             \
+    if (_s != W8A8_OK) return _s;        \
+  } while (0)
+
+w8a8_status check_desc(const w8a8_linear_desc* d) {
+  REQUIRE(d, W8A8_EINVAL, "desc is NULL");
+  REQUIRE(d->n >= 1, W8A8_EINVAL, "desc->n < 1");
+  CHECK(check_k(d->k));
+  CHECK(check_ptr(d->wq, "desc->wq"));
+  CHECK(check_ptr(d->s_w, "desc->s_w"));
+  if (d->delta) CHECK(check_ptr(d->delta, "desc->delta"));
+  REQUIRE(d->n <= (int64_t)1 << 30, W8A8_EUNSUPPORTED, "n too large");
+  return W8A8_OK;
+}
+
+// ------------------------------------------------------------------ workspace layouts
+
+struct LinearWs {
+  size_t qx, sx, gemm, total;
+};
+LinearWs linear_ws(int64_t m, int64_t n, int64_t k) {
+  LinearWs w;
+  Plan pl = plan_gemm(m, n, k, false, false);
+  w.qx = 0;
+  w.sx = align256(w8a8_packed_bytes(m, k));
+  w.gemm = w.sx + align256((size_t)m * 4);
+  w.total = w.gemm + plan_ws_bytes(pl, m, n);
+  return w;
+}
+
+struct FfnWs {
+  size_t qx, sx, h, qh, sh, gemm, total;
+};
+FfnWs ffn_ws(int64_t m, int64_t d, int64_t f) {
+  FfnWs w;
+  Plan pd = plan_gemm(m, d, f, false, false);
+  w.qx = 0;
+  w.sx = align256(w8a8_packed_bytes(m, d));
+  w.h = w.sx + align256((size_t)m * 4);
+  w.qh = w.h + align256((size_t)m * f * 2);
+  w.sh = w.qh + align256(w8a8_packed_bytes(m, f));
+  w.gemm = w.sh + align256((size_t)m * 4);
+  w.total = w.gemm + plan_ws_bytes(pd, m, d);
+  return w;
+}
+
+struct Bf16FfnWs {
+  size_t h, gemm_gu, gemm_dn, total;
+};
+Bf16FfnWs bf16_ffn_ws(int64_t m, int64_t d, int64_t f) {
+  Bf16FfnWs w;
+  Plan pd = plan_gemm(m, d, f, true, false);
+  w.h = 0;
+  w.gemm_dn = align256((size_t)m * f * 2);
+  w.total = w.gemm_dn + plan_ws_bytes(pd, m, d);
+  w.gemm_gu = 0;
+  return w;
+}
+
+size_t bf16_linear_ws(int64_t m, int64_t n, int64_t k) {
+  return plan_ws_bytes(plan_gemm(m, n, k, true, false), m, n);
+}
+
+// ------------------------------------------------------------------ pipelines
+
+w8a8_status quant_act_impl(const void* x, bool bf16, int64_t m, int64_t k, const float* delta,
+                           void* qx, float* sx, hipStream_t st) {
+  return hip_check(launch_quant_rows(x, bf16, false, m, k, delta, (int8_t*)qx, sx, st),
+                   "quant_rows");
+}
+
+w8a8_status linear_impl(const w8a8_linear_desc* d, const void* x, bool x_bf16, int64_t m, void* y,
+                        int epi, void* ws, hipStream_t st) {
+  LinearWs w = linear_ws(m, d->n, d->k);
+  char* base = (char*)ws;
+  Plan pl = plan_gemm(m, d->n, d->k, false, false);
+  CHECK(quant_act_impl(x, x_bf16, m, d->k, d->delta, base + w.qx, (float*)(base + w.sx), st));
+  return run_gemm(pl, false, epi, base + w.qx, 0, m, d->wq, nullptr, d->n, d->k,
+                  (const float*)(base + w.sx), d->s_w, nullptr, y, d->n, base + w.gemm, st);
+}
+
+w8a8_status ffn_impl(const w8a8_ffn_desc* d, const void* x, int64_t m, void* y, void* ws,
+                     hipStream_t st) {
+  FfnWs w = ffn_ws(m, d->d, d->f);
+  char* base = (char*)ws;
+  CHECK(quant_act_impl(x, true, m, d->d, d->delta_gu, base + w.qx, (float*)(base + w.sx), st));
+  Plan pg = plan_gemm(m, d->f, d->d, false, true);
+  CHECK(run_gemm(pg, false, EPI_GLU, base + w.qx, 0, m, d->wq_gate, d->wq_up, d->f, d->d,
+                 (const float*)(base + w.sx), d->s_gate, d->s_up, base + w.h, d->f, nullptr, st));
+  Plan pd = plan_gemm(m, d->d, d->f, false, false);
+  CHECK(quant_act_impl(base + w.h, true, m, d->f, d->delta_down, base + w.qh,
+                       (float*)(base + w.sh), st));
+  return run_gemm(pd, false, EPI_BF16, base + w.qh, 0, m, d->wq_down, nullptr, d->d, d->f,
+                  (const float*)(base + w.sh), d->s_down, nullptr, y, d->d, base + w.gemm, st);
+}
+
+w8a8_status bf16_linear_impl(const void* x, int64_t m, const void* wp, int64_t n, int64_t k,
+                             void* y, void* ws, hipStream_t st) {
+  Plan pl = plan_gemm(m, n, k, true, false);
+  return run_gemm(pl, true, EPI_BF16, x, k, m, wp, nullptr, n, k, nullptr, nullptr, nullptr, y, n,
+                  ws, st);
+}
+
+w8a8_status bf16_ffn_impl(const w8a8_bf16_ffn_desc* d, const void* x, int64_t m, void* y,
+                          void* ws, hipStream_t st) {
+  Bf16FfnWs w = bf16_ffn_ws(m, d->d, d->f);
+  char* base = (char*)ws;
+  Plan pg = plan_gemm(m, d->f, d->d, true, true);
+  CHECK(run_gemm(pg, true, EPI_GLU, x, d->d, m, d->wp_gate, d->wp_up, d->f, d->d, nullptr, nullptr,
+                 nullptr, base + w.h, d->f, nullptr, st));
+  Plan pd = plan_gemm(m, d->d, d->f, true, false);
+  return run_gemm(pd, true, EPI_BF16, base + w.h, d->f, m, d->wp_down, nullptr, d->d, d->f,
+                  nullptr, nullptr, nullptr, y, d->d, base + w.gemm_dn, st);
+}
+
+}  // namespace
+
+// ====================================================================== C ABI
+
+extern "C" {
+
+size_t w8a8_packed_bytes(int64_t n, int64_t k) {
+  if (n < 1 || k < 1) return 0;
+  return (size_t)round_up(n, 16) * (size_t)round_up(k, 64);
+}
+
+size_t w8a8_packed_bf16_bytes(int64_t n, int64_t k) {
+  if (n < 1 || k < 1) return 0;
+  return (size_t)round_up(n, 16) * (size_t)round_up(k, 32) * 2;
+}
+
+size_t w8a8_linear_workspace_bytes(int64_t m, int64_t n, int64_t k) {
+  if (m < 1 || n < 1 || k < 1) return 0;
+  return linear_ws(m, n, k).total;
+}
+
+size_t w8a8_ffn_workspace_bytes(int64_t m, int64_t d, int64_t f) {
+  if (m < 1 || d < 1 || f < 1) return 0;
+  return ffn_ws(m, d, f).total;
+}
+
+size_t w8a8_bf16_ffn_workspace_bytes(int64_t m, int64_t d, int64_t f) {
+  if (m < 1 || d < 1 || f < 1) return 0;
+  return bf16_ffn_ws(m, d, f).total;
+}
+
+size_t w8a8_bf16_linear_workspace_bytes(int64_t m, int64_t n, int64_t k) {
+  if (m < 1 || n < 1 || k < 1) return 0;
+  return bf16_linear_ws(m, n, k);
+}
+
+size_t w8a8_lm_head_workspace_bytes(int64_t m, int64_t n, int64_t k) {
+  return w8a8_linear_workspace_bytes(m, n, k);
+}
+
+size_t w8a8_stack_workspace_bytes(int64_t m, int64_t d, int64_t f, int64_t vocab) {
+  if (m < 1 || d < 1 || f < 1 || vocab < 1) return 0;
+  size_t act = 3 * align256((size_t)m * d * 2);
+  size_t inner = std::max(std::max(ffn_ws(m, d, f).total, bf16_ffn_ws(m, d, f).total),
+                          std::max(linear_ws(m, vocab, d).total, bf16_linear_ws(m, vocab, d)));
+  return act + align256(inner);
+}
+
+const char* w8a8_status_str(w8a8_status s) {
+  switch (s) {
+    case W8A8_OK: return "ok";
+    case W8A8_EINVAL: return "invalid argument";
+    case W8A8_EUNSUPPORTED: return "unsupported shape or dtype";
+    case W8A8_EHIP: return "HIP error";
+    case W8A8_EWORKSPACE: return "workspace too small";
+  }
+  return "unknown status";
+}
+
+const char* w8a8_last_error(void) { return g_last_error.c_str(); }
+
+// ---------------------------------------------------------------- a1
+
+w8a8_status w8a8_col_absmax(const void* x, w8a8_dtype xt, int64_t rows, int64_t k, float* amax,
+                            w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(x);
+  CHECK_PTR(amax);
+  REQUIRE(rows >= 1 && k >= 1, W8A8_EINVAL, "rows or k < 1");
+  REQUIRE(xt == W8A8_F32 || xt == W8A8_BF16, W8A8_EUNSUPPORTED, "x dtype");
+  return hip_check(launch_col_absmax(x, xt == W8A8_BF16, rows, k, amax, S(stream)), "col_absmax");
+}
+
+w8a8_status w8a8_smooth_calibrate(const float* act_amax, const float* w_amax, int64_t k,
+                                  float alpha, float* delta, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(act_amax);
+  CHECK_PTR(w_amax);
+  CHECK_PTR(delta);
+  REQUIRE(k >= 1, W8A8_EINVAL, "k < 1");
+  REQUIRE(alpha >= 0.0f && alpha <= 1.0f, W8A8_EUNSUPPORTED, "alpha outside [0, 1]");
+  return hip_check(launch_smooth_delta(act_amax, w_amax, k, (double)alpha, delta, S(stream)),
+                   "smooth_delta");
+}
+
+// ---------------------------------------------------------------- a2
+
+w8a8_status w8a8_quantize_weights(const void* w, w8a8_dtype wt, int64_t n, int64_t k,
+                                  const float* delta, void* wq, float* s_w, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(w);
+  CHECK_PTR(wq);
+  CHECK_PTR(s_w);
+  if (delta) CHECK_PTR(delta);
+  REQUIRE(n >= 1, W8A8_EINVAL, "n < 1");
+  CHECK(check_k(k));
+  REQUIRE(wt == W8A8_F32 || wt == W8A8_BF16, W8A8_EUNSUPPORTED, "w dtype");
+  return hip_check(launch_quant_rows(w, wt == W8A8_BF16, true, n, k, delta, (int8_t*)wq, s_w,
+                                     S(stream)),
+                   "quant_rows");
+}
+
+w8a8_status w8a8_unpack_weights(const void* wq, int64_t n, int64_t k, int8_t* q,
+                                w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(wq);
+  REQUIRE(q, W8A8_EINVAL, "q is NULL");
+  REQUIRE(n >= 1, W8A8_EINVAL, "n < 1");
+  CHECK(check_k(k));
+  return hip_check(launch_unpack(wq, n, k, q, S(stream)), "unpack");
+}
+
+w8a8_status w8a8_pack_bf16(const void* w, int64_t n, int64_t k, void* wp, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(w);
+  CHECK_PTR(wp);
+  REQUIRE(n >= 1 && k >= 1, W8A8_EINVAL, "n or k < 1");
+  REQUIRE(k % 32 == 0, W8A8_EUNSUPPORTED, "k must be a multiple of 32 on the bf16 path");
+  return hip_check(launch_pack_bf16(w, n, k, wp, S(stream)), "pack_bf16");
+}
+
+// ---------------------------------------------------------------- a3
+
+w8a8_status w8a8_quantize_act(const void* x, w8a8_dtype xt, int64_t m, int64_t k,
+                              const float* delta, void* qx, float* s_x, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(x);
+  CHECK_PTR(qx);
+  CHECK_PTR(s_x);
+  if (delta) CHECK_PTR(delta);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  CHECK(check_k(k));
+  REQUIRE(xt == W8A8_F32 || xt == W8A8_BF16, W8A8_EUNSUPPORTED, "x dtype");
+  return quant_act_impl(x, xt == W8A8_BF16, m, k, delta, qx, s_x, S(stream));
+}
+
+// ---------------------------------------------------------------- a4 / a5
+
+w8a8_status w8a8_gemm_i8_i32(const void* qx, int64_t m, const void* wq, int64_t n, int64_t k,
+                             int32_t* acc, void* ws, size_t ws_bytes, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(qx);
+  CHECK_PTR(wq);
+  CHECK_PTR(acc);
+  REQUIRE(m >= 1 && n >= 1, W8A8_EINVAL, "m or n < 1");
+  CHECK(check_k(k));
+  Plan pl = plan_gemm(m, n, k, false, false);
+  size_t need = plan_ws_bytes(pl, m, n);
+  if (need) {
+    CHECK_PTR(ws);
+    REQUIRE(ws_bytes >= need, W8A8_EWORKSPACE, "workspace too small");
+  }
+  return run_gemm(pl, false, EPI_I32, qx, 0, m, wq, nullptr, n, k, nullptr, nullptr, nullptr, acc,
+                  n, ws, S(stream));
+}
+
+w8a8_status w8a8_linear(const w8a8_linear_desc* desc, const void* x, w8a8_dtype xt, int64_t m,
+                        void* y, w8a8_dtype yt, void* ws, size_t ws_bytes, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK(check_desc(desc));
+  CHECK_PTR(x);
+  CHECK_PTR(y);
+  CHECK_PTR(ws);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  REQUIRE(xt == W8A8_F32 || xt == W8A8_BF16, W8A8_EUNSUPPORTED, "x dtype");
+  REQUIRE(yt == W8A8_F32 || yt == W8A8_BF16, W8A8_EUNSUPPORTED, "y dtype");
+  REQUIRE(ws_bytes >= w8a8_linear_workspace_bytes(m, desc->n, desc->k), W8A8_EWORKSPACE,
+          "workspace too small");
+  return linear_impl(desc, x, xt == W8A8_BF16, m, y, yt == W8A8_BF16 ? EPI_BF16 : EPI_F32, ws,
+                     S(stream));
+}
+
+// ---------------------------------------------------------------- a6
+
+static w8a8_status check_ffn_desc(const w8a8_ffn_desc* d) {
+  REQUIRE(d, W8A8_EINVAL, "desc is NULL");
+  REQUIRE(d->d >= 1 && d->f >= 1, W8A8_EINVAL, "d or f < 1");
+  CHECK(check_k(d->d));
+  CHECK(check_k(d->f));
+  CHECK(check_ptr(d->wq_gate, "desc->wq_gate"));
+  CHECK(check_ptr(d->s_gate, "desc->s_gate"));
+  CHECK(check_ptr(d->wq_up, "desc->wq_up"));
+  CHECK(check_ptr(d->s_up, "desc->s_up"));
+  CHECK(check_ptr(d->wq_down, "desc->wq_down"));
+  CHECK(check_ptr(d->s_down, "desc->s_down"));
+  if (d->delta_gu) CHECK(check_ptr(d->delta_gu, "desc->delta_gu"));
+  if (d->delta_down) CHECK(check_ptr(d->delta_down, "desc->delta_down"));
+  return W8A8_OK;
+}
+
+w8a8_status w8a8_ffn_gate_up(const w8a8_ffn_desc* desc, const void* qx, const float* s_x,
+                             int64_t m, void* h, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK(check_ffn_desc(desc));
+  CHECK_PTR(qx);
+  CHECK_PTR(s_x);
+  CHECK_PTR(h);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  Plan pg = plan_gemm(m, desc->f, desc->d, false, true);
+  return run_gemm(pg, false, EPI_GLU, qx, 0, m, desc->wq_gate, desc->wq_up, desc->f, desc->d, s_x,
+                  desc->s_gate, desc->s_up, h, desc->f, nullptr, S(stream));
+}
+
+w8a8_status w8a8_ffn(const w8a8_ffn_desc* desc, const void* x, int64_t m, void* y, void* ws,
+                     size_t ws_bytes, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK(check_ffn_desc(desc));
+  CHECK_PTR(x);
+  CHECK_PTR(y);
+  CHECK_PTR(ws);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  REQUIRE(ws_bytes >= w8a8_ffn_workspace_bytes(m, desc->d, desc->f), W8A8_EWORKSPACE,
+          "workspace too small");
+  return ffn_impl(desc, x, m, y, ws, S(stream));
+}
+
+// ---------------------------------------------------------------- a7
+
+w8a8_status w8a8_lm_head(const w8a8_linear_desc* desc, const void* x, int64_t m, void* logits,
+                         void* ws, size_t ws_bytes, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK(check_desc(desc));
+  CHECK_PTR(x);
+  CHECK_PTR(logits);
+  CHECK_PTR(ws);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  REQUIRE(ws_bytes >= w8a8_lm_head_workspace_bytes(m, desc->n, desc->k), W8A8_EWORKSPACE,
+          "workspace too small");
+  return linear_impl(desc, x, true, m, logits, EPI_BF16, ws, S(stream));
+}
+
+// ---------------------------------------------------------------- bf16 path
+
+w8a8_status w8a8_bf16_linear(const void* x, int64_t m, const void* wp, int64_t n, int64_t k,
+                             void* y, void* ws, size_t ws_bytes, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(x);
+  CHECK_PTR(wp);
+  CHECK_PTR(y);
+  REQUIRE(m >= 1 && n >= 1 && k >= 1, W8A8_EINVAL, "m, n or k < 1");
+  REQUIRE(k % 32 == 0, W8A8_EUNSUPPORTED, "k must be a multiple of 32 on the bf16 path");
+  size_t need = bf16_linear_ws(m, n, k);
+  if (need) {
+    CHECK_PTR(ws);
+    REQUIRE(ws_bytes >= need, W8A8_EWORKSPACE, "workspace too small");
+  }
+  return bf16_linear_impl(x, m, wp, n, k, y, ws, S(stream));
+}
+
+static w8a8_status check_bf16_ffn_desc(const w8a8_bf16_ffn_desc* d) {
+  REQUIRE(d, W8A8_EINVAL, "desc is NULL");
+  REQUIRE(d->d >= 1 && d->f >= 1, W8A8_EINVAL, "d or f < 1");
+  REQUIRE(d->d % 32 == 0 && d->f % 32 == 0, W8A8_EUNSUPPORTED,
+          "d and f must be multiples of 32 on the bf16 path");
+  CHECK(check_ptr(d->wp_gate, "desc->wp_gate"));
+  CHECK(check_ptr(d->wp_up, "desc->wp_up"));
+  CHECK(check_ptr(d->wp_down, "desc->wp_down"));
+  return W8A8_OK;
+}
+
+w8a8_status w8a8_bf16_ffn_gate_up(const w8a8_bf16_ffn_desc* desc, const void* x, int64_t m,
+                                  void* h, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK(check_bf16_ffn_desc(desc));
+  CHECK_PTR(x);
+  CHECK_PTR(h);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  Plan pg = plan_gemm(m, desc->f, desc->d, true, true);
+  return run_gemm(pg, true, EPI_GLU, x, desc->d, m, desc->wp_gate, desc->wp_up, desc->f, desc->d,
+                  nullptr, nullptr, nullptr, h, desc->f, nullptr, S(stream));
+}
+
+w8a8_status w8a8_bf16_ffn(const w8a8_bf16_ffn_desc* desc, const void* x, int64_t m, void* y,
+                          void* ws, size_t ws_bytes, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK(check_bf16_ffn_desc(desc));
+  CHECK_PTR(x);
+  CHECK_PTR(y);
+  CHECK_PTR(ws);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  REQUIRE(ws_bytes >= w8a8_bf16_ffn_workspace_bytes(m, desc->d, desc->f), W8A8_EWORKSPACE,
+          "workspace too small");
+  return bf16_ffn_impl(desc, x, m, y, ws, S(stream));
+}
+
+// ---------------------------------------------------------------- a8 / a9
+
+static w8a8_status check_norm_d(int64_t d) {
+  REQUIRE(d >= 1, W8A8_EINVAL, "d < 1");
+  REQUIRE(d % 8 == 0 && d <= 8192, W8A8_EUNSUPPORTED, "RMSNorm needs d % 8 == 0 and d <= 8192");
+  return W8A8_OK;
+}
+
+w8a8_status w8a8_rmsnorm(const void* x, int64_t m, int64_t d, void* y, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(x);
+  CHECK_PTR(y);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  CHECK(check_norm_d(d));
+  return hip_check(launch_rmsnorm(nullptr, (const uint16_t*)x, m, d, (uint16_t*)y, S(stream)),
+                   "rmsnorm");
+}
+
+w8a8_status w8a8_rmsnorm_residual(const void* x, const void* f, int64_t m, int64_t d, void* x_out,
+                                  w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(x);
+  CHECK_PTR(f);
+  CHECK_PTR(x_out);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  CHECK(check_norm_d(d));
+  return hip_check(launch_rmsnorm((const uint16_t*)x, (const uint16_t*)f, m, d,
+                                  (uint16_t*)x_out, S(stream)),
+                   "rmsnorm_residual");
+}
+
+int w8a8_precision_map(const char* name, uint8_t* prec, int n_layers) {
+  if (!name || !prec || n_layers < 26) return -1;
+  int lo1 = 0, hi1 = -1, lo2 = 0, hi2 = -1;
+  if (std::strcmp(name, "bf16") == 0) {
+  } else if (std::strcmp(name, "5+5") == 0) {
+    lo1 = 0; hi1 = 4; lo2 = 21; hi2 = 25;      // eq. ffn55
+  } else if (std::strcmp(name, "10+10") == 0) {
+    lo1 = 0; hi1 = 9; lo2 = 16; hi2 = 25;      // eq. ffn1010
+  } else if (std::strcmp(name, "all26") == 0) {
+    lo1 = 0; hi1 = 25;                         // eq. ffnall26
+  } else {
+    return -1;
+  }
+  int count = 0;
+  for (int l = 0; l < n_layers; ++l) {
+    bool q = (l >= lo1 && l <= hi1) || (l >= lo2 && l <= hi2);
+    prec[l] = q ? 1 : 0;
+    count += q;
+  }
+  return count;
+}
+
+w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec, int lm_head_int8,
+                           const void* x, int64_t m, void* logits, void* ws, size_t ws_bytes,
+                           w8a8_stream_t stream) {
+  g_last_error.clear();
+  REQUIRE(desc, W8A8_EINVAL, "desc is NULL");
+  REQUIRE(prec, W8A8_EINVAL, "prec is NULL");
+  CHECK_PTR(x);
+  CHECK_PTR(logits);
+  CHECK_PTR(ws);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  REQUIRE(desc->n_layers >= 1 && desc->d >= 1 && desc->f >= 1 && desc->vocab >= 1, W8A8_EINVAL,
+          "stack sizes < 1");
+  REQUIRE(ws_bytes >= w8a8_stack_workspace_bytes(m, desc->d, desc->f, desc->vocab),
+          W8A8_EWORKSPACE, "workspace too small");
+  const int64_t d = desc->d, f = desc->f;
+  CHECK(check_norm_d(d));
+  for (int64_t l = 0; l < desc->n_layers; ++l) {
+    if (prec[l]) {
+      REQUIRE(desc->int8_ffn, W8A8_EINVAL, "int8_ffn is NULL");
+      CHECK(check_ffn_desc(&desc->int8_ffn[l]));
+      REQUIRE(desc->int8_ffn[l].d == d && desc->int8_ffn[l].f == f, W8A8_EINVAL, "layer shape");
+    } else {
+      REQUIRE(desc->bf16_ffn, W8A8_EINVAL, "bf16_ffn is NULL");
+      CHECK(check_bf16_ffn_desc(&desc->bf16_ffn[l]));
+      REQUIRE(desc->bf16_ffn[l].d == d && desc->bf16_ffn[l].f == f, W8A8_EINVAL, "layer shape");
+    }
+  }
+  if (lm_head_int8) {
+    CHECK(check_desc(&desc->lm_head_int8));
+    REQUIRE(desc->lm_head_int8.n == desc->vocab && desc->lm_head_int8.k == d, W8A8_EINVAL,
+            "lm_head shape");
+  } else {
+    CHECK_PTR(desc->lm_head_bf16);
+    REQUIRE(d % 32 == 0, W8A8_EUNSUPPORTED, "d must be a multiple of 32 on the bf16 path");
+  }
+
+  hipStream_t st = S(stream);
+  char* base = (char*)ws;
+  const size_t act = align256((size_t)m * d * 2);
+  uint16_t* xcur = (uint16_t*)base;
+  uint16_t* a = (uint16_t*)(base + act);
+  uint16_t* fo = (uint16_t*)(base + 2 * act);
+  void* inner = base + 3 * act;
+  CHECK(hip_check(hipMemcpyAsync(xcur, x, (size_t)m * d * 2, hipMemcpyDeviceToDevice, st),
+                  "copy x"));
+  for (int64_t l = 0; l < desc->n_layers; ++l) {
+    CHECK(hip_check(launch_rmsnorm(nullptr, xcur, m, d, a, st), "rmsnorm"));
+    if (prec[l])
+      CHECK(ffn_impl(&desc->int8_ffn[l], a, m, fo, inner, st));
+    else
+      CHECK(bf16_ffn_impl(&desc->bf16_ffn[l], a, m, fo, inner, st));
+    CHECK(hip_check(launch_rmsnorm(xcur, fo, m, d, xcur, st), "rmsnorm_residual"));
+  }
+  CHECK(hip_check(launch_rmsnorm(nullptr, xcur, m, d, a, st), "rmsnorm"));
+  if (lm_head_int8)
+    return linear_impl(&desc->lm_head_int8, a, true, m, logits, EPI_BF16, inner, st);
+  return bf16_linear_impl(a, m, desc->lm_head_bf16, desc->vocab, d, logits, inner, st);
+}
+
+}  // extern "C"

@@ -1,0 +1,75 @@
+// Device-side helpers shared by the gfx950 kernels of the W8A8 library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace w8a8 {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+
+constexpr int kWave = 64;        // CDNA wavefront
+constexpr int kFragBytes = 1024; // one 16 x 64 int8 (or 16 x 32 bf16) fragment
+
+__device__ __forceinline__ float bf16_bits_to_float(uint32_t b) {
+  return __uint_as_float(b << 16);
+}
+
+// binary32 -> bf16, round to nearest even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint16_t float_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return 0x7fc0;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, kWave));
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (kWave - 1)); }
+
+// Byte offset of fragment (rb, kb) in a packed matrix with kb_count fragment columns.
+__device__ __forceinline__ int64_t frag_offset(int64_t rb, int64_t kb, int64_t kb_count) {
+  return (rb * kb_count + kb) * (int64_t)kFragBytes;
+}
+
+// 16x16x64 int8 MFMA: C[i][j] += sum_k A[i][k] B[j][k]; lane l supplies row
+// (l % 16) of A and of B with the same 16 k values, so any fixed assignment of
+// k to (lane group, byte) used by both operands gives the same sum.  The
+// accumulator element r of lane l is C[4 (l / 16) + r][l % 16].
+__device__ __forceinline__ v4i mma_i8(v4i a, v4i b, v4i c) {
+  return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ v4f mma_bf16(v4i a, v4i b, v4f c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, a),
+                                                 __builtin_bit_cast(v8bf, b), c, 0, 0, 0);
+}
+
+// GELU with the tanh form, binary32 operations in a fixed order (the library
+// is compiled without floating-point contraction).
+__device__ __forceinline__ float gelu_tanh(float x) {
+  const float c = 0.7978845608028654f;  // sqrt(2/pi)
+  const float k3 = 0.044715f;
+  float x2 = x * x;
+  float x3 = x2 * x;
+  float inner = x + k3 * x3;
+  float z = c * inner;
+  float t = tanhf(z);
+  float half = 0.5f * x;
+  float one_t = 1.0f + t;
+  return half * one_t;
+}
+
+}  // namespace w8a8

@@ -1,0 +1,64 @@
+// Host-side launch functions of the gfx950 kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace w8a8 {
+
+constexpr int kFragK8 = 64;   // int8 columns per 1 KiB fragment
+constexpr int kFragK16 = 32;  // bf16 columns per 1 KiB fragment
+
+enum Epi { EPI_I32 = 0, EPI_F32 = 1, EPI_BF16 = 2, EPI_GLU = 3 };
+
+// Arguments of one GEMM launch C = A B^T.
+struct GemmParams {
+  const void* A;          // int8 path: packed codes (fragment layout); bf16 path: row-major bf16
+  const void* B;          // packed weights (gate weights for the gated epilogue)
+  const void* B2;         // packed up weights (gated epilogue only)
+  int64_t lda;            // bf16 path: row stride of A in elements
+  int M, N;               // logical rows of A and of B (output columns)
+  int rb_a, rb_b;         // 16-row blocks stored in A and B
+  int kb_count;           // fragment columns (Kp / 64 for int8, Kp / 32 for bf16)
+  int kchunk;             // fragment columns per K split
+  int splits;             // number of K splits (1: no split)
+  const float* s_a;       // int8 path: per-token scales [M]
+  const float* s_b;       // int8 path: per-channel scales [N] (gate)
+  const float* s_b2;      // int8 path: per-channel scales [N] (up)
+  void* out;              // int32 / f32 / bf16 output
+  int64_t ldo;            // row stride of out in elements
+  void* part;             // K-split partial sums: splits x M x N (int32 or f32)
+};
+
+// tile shapes selectable at run time
+enum TileCfg {
+  TILE_128x128 = 0,   // 4 waves of 64 x 64
+  TILE_128x64 = 1,    // 4 waves of 64 x 32
+  TILE_64x64 = 2,     // 4 waves of 32 x 32
+  TILE_256x128 = 3,   // 4 waves of 128 x 64
+  TILE_GLU_128x32 = 4,
+  TILE_GLU_64x64 = 5,
+  TILE_GLU_128x64 = 6,
+};
+
+hipError_t launch_col_absmax(const void* x, bool bf16, int64_t rows, int64_t k, float* amax,
+                             hipStream_t st);
+hipError_t launch_smooth_delta(const float* a, const float* w, int64_t k, double alpha,
+                               float* delta, hipStream_t st);
+hipError_t launch_quant_rows(const void* x, bool bf16, bool mul, int64_t rows, int64_t k,
+                             const float* delta, int8_t* qpacked, float* s, hipStream_t st);
+hipError_t launch_unpack(const void* qp, int64_t n, int64_t k, int8_t* q, hipStream_t st);
+hipError_t launch_pack_bf16(const void* w, int64_t n, int64_t k, void* wp, hipStream_t st);
+
+// tiled MFMA GEMM (any M); `tile` picks the block shape
+hipError_t launch_gemm_tile(bool bf16, int epi, int tile, const GemmParams& p, hipStream_t st);
+// skinny MFMA GEMM for M <= 64: weights streamed from HBM, A held in LDS
+hipError_t launch_gemm_skinny(bool bf16, int epi, int mb, int kc, const GemmParams& p,
+                              int nb_per_block, hipStream_t st);
+// sum of K-split partials (in split order) followed by the epilogue
+hipError_t launch_splitk_reduce(bool bf16, int epi, const GemmParams& p, hipStream_t st);
+
+hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* f, int64_t m, int64_t d,
+                          uint16_t* y, hipStream_t st);
+
+}  // namespace w8a8

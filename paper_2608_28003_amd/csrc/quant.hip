@@ -1,0 +1,294 @@
+// Calibration, smoothing and symmetric int8 quantisation kernels (gfx950).
+//
+//   col_absmax      running max_t |X_tj|, the statistic of Sec. 4 eq. delta-attn
+//   smooth_delta    delta_j = a_j^alpha / w_j^(1-alpha)          (eq. delta-lmhead)
+//   quant_rows      per-row symmetric int8 codes of x / delta (eq. xhat-lmhead,
+//                   stx, xint8) or W * delta (eq. what-lmhead, si, what-ffn),
+//                   written straight into the packed fragment layout the GEMMs read
+//   unpack          packed layout -> row-major int8 (checks only)
+//   pack_bf16       row-major bf16 -> packed bf16 layout (bf16 path weights)
+//
+// Quantisation runs one workgroup per row: each thread owns a 16-column chunk
+// held in registers, a butterfly + LDS max gives the row absmax, and each chunk
+// becomes one 16-byte store into its fragment slot.  All arithmetic is IEEE binary32 (correctly rounded
+// division, v_rndne_f32 for round-half-to-even, no contraction).
+#include "device.h"
+#include "kernels.h"
+
+namespace w8a8 {
+
+// ------------------------------------------------------------------ loads
+
+template <typename T>
+__device__ __forceinline__ void load16(const T* p, float (&v)[16]);
+
+template <>
+__device__ __forceinline__ void load16<float>(const float* p, float (&v)[16]) {
+  const float4* q = reinterpret_cast<const float4*>(p);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float4 t = q[i];
+    v[4 * i + 0] = t.x; v[4 * i + 1] = t.y; v[4 * i + 2] = t.z; v[4 * i + 3] = t.w;
+  }
+}
+
+template <>
+__device__ __forceinline__ void load16<uint16_t>(const uint16_t* p, float (&v)[16]) {
+  const uint4* q = reinterpret_cast<const uint4*>(p);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    uint4 t = q[i];
+    uint32_t w[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[8 * i + 2 * j + 0] = bf16_bits_to_float(w[j] & 0xffffu);
+      v[8 * i + 2 * j + 1] = bf16_bits_to_float(w[j] >> 16);
+    }
+  }
+}
+
+// ------------------------------------------------------------------ a1
+
+template <typename T>
+__global__ __launch_bounds__(256) void col_absmax_kernel(const T* __restrict__ x, int64_t rows,
+                                                         int64_t k, int rows_per_block,
+                                                         float* __restrict__ amax) {
+  int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (j >= k) return;
+  int64_t r0 = (int64_t)blockIdx.y * rows_per_block;
+  int64_t r1 = r0 + rows_per_block < rows ? r0 + rows_per_block : rows;
+  float m = 0.0f;
+  for (int64_t r = r0; r < r1; ++r) {
+    float v;
+    if constexpr (sizeof(T) == 2)
+      v = bf16_bits_to_float(x[r * k + j]);
+    else
+      v = x[r * k + j];
+    m = fmaxf(m, fabsf(v));
+  }
+  // non-negative binary32 values order like their unsigned bit patterns
+  atomicMax(reinterpret_cast<unsigned int*>(amax) + j, __float_as_uint(m));
+}
+
+__global__ void smooth_delta_kernel(const float* __restrict__ a, const float* __restrict__ w,
+                                    int64_t k, double alpha, float* __restrict__ delta) {
+  int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= k) return;
+  const double eps = 1e-5;
+  double aj = (double)a[j], wj = (double)w[j];
+  if (aj < eps) aj = eps;
+  if (wj < eps) wj = eps;
+  double d = (alpha == 0.5) ? sqrt(aj) / sqrt(wj) : pow(aj, alpha) / pow(wj, 1.0 - alpha);
+  delta[j] = (float)d;
+}
+
+// ------------------------------------------------------------------ a2 / a3
+
+// Workgroup-wide maximum (blockDim.x a multiple of 64, at most 1024).
+__device__ __forceinline__ float block_max(float v) {
+  __shared__ float red[16];
+  v = wave_max(v);
+  const int w = threadIdx.x >> 6;
+  if (lane_id() == 0) red[w] = v;
+  __syncthreads();
+  float m = red[0];
+  for (int i = 1; i < (int)(blockDim.x >> 6); ++i) m = fmaxf(m, red[i]);
+  return m;
+}
+
+// q = rne(v / s) clamped to [-127, 127], with v / s the correctly rounded
+// binary32 quotient.  Fast path: v * inv with inv = 1/s differs from v / s by at
+// most 2.3e-5 for |v / s| <= 127.5 (two roundings of 2^-24 each plus the one of
+// the quotient), so whenever v * inv is more than 2^-10 away from a half-integer
+// both round to the same integer; otherwise (or when inv is not finite) the
+// exact quotient is formed.
+__device__ __forceinline__ int8_t code_of(float v, float s, float inv, bool fast) {
+  float c;
+  if (fast) {
+    float q = v * inv;
+    float fr = fabsf(q - truncf(q));
+    if (fabsf(fr - 0.5f) > 0.0009765625f)
+      c = rintf(q);
+    else
+      c = rintf(v / s);
+  } else {
+    c = rintf(v / s);
+  }
+  c = fminf(fmaxf(c, -127.0f), 127.0f);
+  return (int8_t)(int)c;
+}
+
+template <typename T, bool MUL>
+__device__ __forceinline__ void smooth16(const T* __restrict__ xr, const float* __restrict__ delta,
+                                         int64_t c, float (&v)[16]) {
+  load16<T>(xr + c * 16, v);
+  if (delta) {
+    float d[16];
+    load16<float>(delta + c * 16, d);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) v[e] = MUL ? v[e] * d[e] : v[e] / d[e];
+  }
+}
+
+__device__ __forceinline__ void store_codes(int8_t* __restrict__ q, int64_t r, int64_t c,
+                                            int64_t kb_count, const int32_t (&packed)[4]) {
+  const int64_t kb = c >> 2;
+  const int g = (int)(c & 3);
+  const int64_t off = frag_offset(r >> 4, kb, kb_count) + (int64_t)((r & 15) + 16 * g) * 16;
+  *reinterpret_cast<int4*>(q + off) = make_int4(packed[0], packed[1], packed[2], packed[3]);
+}
+
+// One workgroup per row r of a rows x k matrix (k % 16 == 0); thread t owns the
+// 16-column chunk t (and t + blockDim, ... for very long rows), keeping its
+// smoothed values in registers between the absmax and the rounding pass.
+// Rows in [rows, rows_pad) and columns in [k, kp) of the packed output are
+// written as zeros.  MUL: v = x * delta (weights); else v = x / delta.
+template <typename T, bool MUL>
+__global__ __launch_bounds__(1024) void quant_rows_kernel(const T* __restrict__ x, int64_t rows,
+                                                          int64_t k, const float* __restrict__ delta,
+                                                          int64_t rows_pad, int64_t kp,
+                                                          int8_t* __restrict__ q,
+                                                          float* __restrict__ s) {
+  const int64_t r = blockIdx.x;
+  const int t = threadIdx.x;
+  const int nt = blockDim.x;
+  const int64_t kb_count = kp / kFragK8;
+  const int64_t chunks_pad = kp / 16;
+  const int64_t chunks = k / 16;
+  const int32_t zeros[4] = {0, 0, 0, 0};
+
+  if (r >= rows) {  // padding row: zeros
+    for (int64_t c = t; c < chunks_pad; c += nt) store_codes(q, r, c, kb_count, zeros);
+    return;
+  }
+
+  const T* xr = x + r * k;
+  float v[16];
+  float amax = 0.0f;
+  if (t < chunks) {
+    smooth16<T, MUL>(xr, delta, t, v);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) amax = fmaxf(amax, fabsf(v[e]));
+  }
+  for (int64_t c = t + nt; c < chunks; c += nt) {  // rows longer than 16 * blockDim
+    float w[16];
+    smooth16<T, MUL>(xr, delta, c, w);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) amax = fmaxf(amax, fabsf(w[e]));
+  }
+  amax = block_max(amax);
+  const float sr = amax / 127.0f;
+  if (t == 0) s[r] = sr;
+  const float inv = 1.0f / sr;
+  const bool fast = isfinite(inv);
+
+  for (int64_t c = t; c < chunks_pad; c += nt) {
+    int32_t packed[4] = {0, 0, 0, 0};
+    if (c < chunks && sr != 0.0f) {
+      float w[16];
+      if (c == t) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) w[e] = v[e];
+      } else {
+        smooth16<T, MUL>(xr, delta, c, w);
+      }
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        int32_t iv = (int32_t)code_of(w[e], sr, inv, fast) & 0xff;
+        packed[e >> 2] |= iv << (8 * (e & 3));
+      }
+    }
+    store_codes(q, r, c, kb_count, packed);
+  }
+}
+
+// packed int8 -> row-major int8 (n x k)
+__global__ void unpack_kernel(const int8_t* __restrict__ qp, int64_t n, int64_t k, int64_t kp,
+                              int8_t* __restrict__ q) {
+  int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= n * k) return;
+  int64_t r = idx / k, c = idx % k;
+  int64_t kb = c / kFragK8;
+  int g = (int)((c % kFragK8) / 16);
+  int e = (int)(c % 16);
+  int64_t off = frag_offset(r >> 4, kb, kp / kFragK8) + (int64_t)((r & 15) + 16 * g) * 16 + e;
+  q[idx] = qp[off];
+}
+
+// row-major bf16 (n x k, k % 8 == 0) -> packed bf16 layout; one thread per
+// 8-element (16-byte) chunk of the padded matrix.
+__global__ void pack_bf16_kernel(const uint16_t* __restrict__ w, int64_t n, int64_t k,
+                                 int64_t n_pad, int64_t kp, uint16_t* __restrict__ wp) {
+  int64_t chunk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t chunks_row = kp / 8;
+  if (chunk >= n_pad * chunks_row) return;
+  int64_t r = chunk / chunks_row, c = chunk % chunks_row;
+  uint4 val = make_uint4(0, 0, 0, 0);
+  if (r < n && c * 8 < k) val = *reinterpret_cast<const uint4*>(w + r * k + c * 8);
+  int64_t kb = c >> 2;
+  int g = (int)(c & 3);
+  int64_t off = frag_offset(r >> 4, kb, kp / kFragK16) + (int64_t)((r & 15) + 16 * g) * 16;
+  *reinterpret_cast<uint4*>(reinterpret_cast<int8_t*>(wp) + off) = val;
+}
+
+// ------------------------------------------------------------------ launchers
+
+hipError_t launch_col_absmax(const void* x, bool bf16, int64_t rows, int64_t k, float* amax,
+                             hipStream_t st) {
+  const int rpb = 64;
+  dim3 grid((unsigned)((k + 255) / 256), (unsigned)((rows + rpb - 1) / rpb));
+  if (bf16)
+    col_absmax_kernel<uint16_t><<<grid, 256, 0, st>>>((const uint16_t*)x, rows, k, rpb, amax);
+  else
+    col_absmax_kernel<float><<<grid, 256, 0, st>>>((const float*)x, rows, k, rpb, amax);
+  return hipGetLastError();
+}
+
+hipError_t launch_smooth_delta(const float* a, const float* w, int64_t k, double alpha,
+                               float* delta, hipStream_t st) {
+  smooth_delta_kernel<<<(unsigned)((k + 255) / 256), 256, 0, st>>>(a, w, k, alpha, delta);
+  return hipGetLastError();
+}
+
+hipError_t launch_quant_rows(const void* x, bool bf16, bool mul, int64_t rows, int64_t k,
+                             const float* delta, int8_t* qpacked, float* s, hipStream_t st) {
+  const int64_t rows_pad = (rows + 15) / 16 * 16;
+  const int64_t kp = (k + kFragK8 - 1) / kFragK8 * kFragK8;
+  int64_t threads = (kp / 16 + 63) / 64 * 64;
+  if (threads > 1024) threads = 1024;
+  dim3 grid((unsigned)rows_pad), block((unsigned)threads);
+  if (bf16) {
+    if (mul)
+      quant_rows_kernel<uint16_t, true><<<grid, block, 0, st>>>((const uint16_t*)x, rows, k, delta,
+                                                               rows_pad, kp, qpacked, s);
+    else
+      quant_rows_kernel<uint16_t, false><<<grid, block, 0, st>>>((const uint16_t*)x, rows, k, delta,
+                                                                rows_pad, kp, qpacked, s);
+  } else {
+    if (mul)
+      quant_rows_kernel<float, true><<<grid, block, 0, st>>>((const float*)x, rows, k, delta,
+                                                            rows_pad, kp, qpacked, s);
+    else
+      quant_rows_kernel<float, false><<<grid, block, 0, st>>>((const float*)x, rows, k, delta,
+                                                             rows_pad, kp, qpacked, s);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_unpack(const void* qp, int64_t n, int64_t k, int8_t* q, hipStream_t st) {
+  const int64_t kp = (k + kFragK8 - 1) / kFragK8 * kFragK8;
+  int64_t total = n * k;
+  unpack_kernel<<<(unsigned)((total + 255) / 256), 256, 0, st>>>((const int8_t*)qp, n, k, kp, q);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_bf16(const void* w, int64_t n, int64_t k, void* wp, hipStream_t st) {
+  const int64_t n_pad = (n + 15) / 16 * 16;
+  const int64_t kp = (k + kFragK16 - 1) / kFragK16 * kFragK16;
+  int64_t total = n_pad * (kp / 8);
+  pack_bf16_kernel<<<(unsigned)((total + 255) / 256), 256, 0, st>>>(
+      (const uint16_t*)w, n, k, n_pad, kp, (uint16_t*)wp);
+  return hipGetLastError();
+}
+
+}  // namespace w8a8

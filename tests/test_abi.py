@@ -1,0 +1,151 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, and rejects bad arguments on the host before any HIP call.
+Every call below fails validation, so no kernel is ever launched."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2608_28003_amd import w8a8
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "w8a8.h")
+
+P = ctypes.c_void_p
+FAKE = P(0x1000)          # aligned, never dereferenced: validation fails first
+MISALIGNED = P(0x1004)
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(w8a8_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = w8a8.lib()
+    names = _declared()
+    assert len(names) >= 25
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(w8a8.exported_names())
+
+
+def test_status_strings():
+    L = w8a8.lib()
+    for code in range(5):
+        assert L.w8a8_status_str(code)
+    assert L.w8a8_status_str(99) == b"unknown status"
+
+
+def test_packed_sizes():
+    assert w8a8.packed_bytes(6912, 1152) == 6912 * 1152
+    assert w8a8.packed_bytes(262144, 1152) == 301989888
+    assert w8a8.packed_bytes(1, 16) == 16 * 64          # padded to a 16 x 64 fragment
+    assert w8a8.packed_bytes(17, 65) == 32 * 128
+    assert w8a8.packed_bytes(0, 16) == 0
+    assert w8a8.packed_bf16_bytes(6912, 1152) == 6912 * 1152 * 2
+    assert w8a8.packed_bf16_bytes(3, 40) == 16 * 64 * 2
+
+
+def test_workspace_queries_cover_buffers():
+    m, d, f = 128, 1152, 6912
+    ws = w8a8.ffn_workspace_bytes(m, d, f)
+    assert ws >= w8a8.packed_bytes(m, d) + m * 4 + m * f * 2 + w8a8.packed_bytes(m, f) + m * 4
+    assert w8a8.linear_workspace_bytes(1, 262144, 1152) >= w8a8.packed_bytes(1, 1152) + 4
+    assert w8a8.stack_workspace_bytes(512, d, f, 262144) > w8a8.ffn_workspace_bytes(512, d, f)
+    assert w8a8.linear_workspace_bytes(0, 1, 1) == 0
+
+
+def test_precision_maps_from_library_match_oracle():
+    for name in ("bf16", "5+5", "10+10", "all26"):
+        np.testing.assert_array_equal(w8a8.precision_map(name), oracle.precision_map(name))
+    with pytest.raises(ValueError):
+        w8a8.precision_map("3+3")
+    with pytest.raises(ValueError):
+        w8a8.precision_map("5+5", 20)
+
+
+def _status(fn, *args):
+    return fn(*args)
+
+
+def test_quantize_act_validation():
+    L = w8a8.lib()
+    q = L.w8a8_quantize_act
+    assert q(None, w8a8.BF16, 4, 1152, None, FAKE, FAKE, None) == w8a8.EINVAL
+    assert q(FAKE, w8a8.BF16, 0, 1152, None, FAKE, FAKE, None) == w8a8.EINVAL
+    assert q(FAKE, w8a8.BF16, 4, 1000, None, FAKE, FAKE, None) == w8a8.EUNSUPPORTED
+    assert q(FAKE, w8a8.BF16, 4, w8a8.MAX_K + 16, None, FAKE, FAKE, None) == w8a8.EUNSUPPORTED
+    assert q(FAKE, 7, 4, 1152, None, FAKE, FAKE, None) == w8a8.EUNSUPPORTED
+    assert q(MISALIGNED, w8a8.BF16, 4, 1152, None, FAKE, FAKE, None) == w8a8.EINVAL
+    assert b"aligned" in L.w8a8_last_error()
+
+
+def test_quantize_weights_and_calibration_validation():
+    L = w8a8.lib()
+    assert L.w8a8_quantize_weights(FAKE, w8a8.F32, 16, 24, None, FAKE, FAKE, None) == w8a8.EUNSUPPORTED
+    assert L.w8a8_quantize_weights(FAKE, w8a8.F32, 0, 64, None, FAKE, FAKE, None) == w8a8.EINVAL
+    assert L.w8a8_quantize_weights(FAKE, w8a8.F32, 16, 64, MISALIGNED, FAKE, FAKE, None) == w8a8.EINVAL
+    assert L.w8a8_smooth_calibrate(FAKE, FAKE, 64, 1.5, FAKE, None) == w8a8.EUNSUPPORTED
+    assert L.w8a8_smooth_calibrate(FAKE, None, 64, 0.5, FAKE, None) == w8a8.EINVAL
+    assert L.w8a8_col_absmax(FAKE, w8a8.BF16, 0, 64, FAKE, None) == w8a8.EINVAL
+    assert L.w8a8_pack_bf16(FAKE, 16, 48, FAKE, None) == w8a8.EUNSUPPORTED
+
+
+def test_linear_and_ffn_validation():
+    L = w8a8.lib()
+    d = w8a8.LinearDesc(6912, 1152, FAKE, FAKE, None)
+    need = w8a8.linear_workspace_bytes(16, 6912, 1152)
+    assert L.w8a8_linear(ctypes.byref(d), FAKE, w8a8.F32, 16, FAKE, w8a8.F32, FAKE, need - 1, None) == w8a8.EWORKSPACE
+    assert L.w8a8_linear(None, FAKE, w8a8.F32, 16, FAKE, w8a8.F32, FAKE, need, None) == w8a8.EINVAL
+    assert L.w8a8_linear(ctypes.byref(d), FAKE, w8a8.F32, 16, FAKE, 5, FAKE, need, None) == w8a8.EUNSUPPORTED
+    bad = w8a8.LinearDesc(6912, 1100, FAKE, FAKE, None)
+    assert L.w8a8_linear(ctypes.byref(bad), FAKE, w8a8.F32, 16, FAKE, w8a8.F32, FAKE, need, None) == w8a8.EUNSUPPORTED
+    nul = w8a8.LinearDesc(6912, 1152, None, FAKE, None)
+    assert L.w8a8_linear(ctypes.byref(nul), FAKE, w8a8.F32, 16, FAKE, w8a8.F32, FAKE, need, None) == w8a8.EINVAL
+    f = w8a8.FfnDesc(1152, 6912, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
+    need = w8a8.ffn_workspace_bytes(8, 1152, 6912)
+    assert L.w8a8_ffn(ctypes.byref(f), FAKE, 8, FAKE, FAKE, need - 1, None) == w8a8.EWORKSPACE
+    f2 = w8a8.FfnDesc(1152, 6912, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE)
+    assert L.w8a8_ffn(ctypes.byref(f2), FAKE, 8, FAKE, FAKE, need, None) == w8a8.EINVAL
+    assert L.w8a8_lm_head(ctypes.byref(d), FAKE, 0, FAKE, FAKE, 1 << 30, None) == w8a8.EINVAL
+    assert L.w8a8_gemm_i8_i32(FAKE, 4, FAKE, 16, 1000, FAKE, FAKE, 1 << 20, None) == w8a8.EUNSUPPORTED
+    assert L.w8a8_bf16_linear(FAKE, 4, FAKE, 16, 48, FAKE, None, 0, None) == w8a8.EUNSUPPORTED
+
+
+def test_stack_validation():
+    L = w8a8.lib()
+    i8 = (w8a8.FfnDesc * 2)()
+    bf = (w8a8.Bf16FfnDesc * 2)(w8a8.Bf16FfnDesc(1152, 6912, FAKE, FAKE, FAKE),
+                                w8a8.Bf16FfnDesc(1152, 6912, FAKE, FAKE, FAKE))
+    sd = w8a8.StackDesc(2, 1152, 6912, 4096, i8, bf, w8a8.LinearDesc(), FAKE)
+    need = w8a8.stack_workspace_bytes(4, 1152, 6912, 4096)
+    prec = np.array([1, 0], np.uint8)   # layer 0 asks for INT8 but has no descriptor
+    assert L.w8a8_ffn_stack(ctypes.byref(sd), prec.ctypes.data_as(P), 0, FAKE, 4, FAKE, FAKE,
+                            need, None) == w8a8.EINVAL
+    prec = np.array([0, 0], np.uint8)
+    assert L.w8a8_ffn_stack(ctypes.byref(sd), prec.ctypes.data_as(P), 1, FAKE, 4, FAKE, FAKE,
+                            need, None) == w8a8.EINVAL   # lm_head INT8 requested, desc empty
+    assert L.w8a8_ffn_stack(ctypes.byref(sd), prec.ctypes.data_as(P), 0, FAKE, 4, FAKE, FAKE,
+                            need - 1, None) == w8a8.EWORKSPACE
+
+
+def test_fragment_layout_helpers_roundtrip():
+    rng = np.random.default_rng(3)
+    for rows, k in [(1, 16), (17, 80), (48, 1152), (5, 64)]:
+        q = rng.integers(-127, 128, (rows, k), dtype=np.int8)
+        packed = w8a8.rowmajor_to_frag(q)
+        assert packed.size == w8a8.packed_bytes(rows, k)
+        np.testing.assert_array_equal(w8a8.frag_to_rowmajor(packed, rows, k), q)
+    # lane l of fragment (0, 0) holds row l % 16, columns (l // 16) * 16 .. +15
+    q = np.arange(16 * 64, dtype=np.int64).reshape(16, 64)
+    qq = (q % 251 - 125).astype(np.int8)
+    packed = w8a8.rowmajor_to_frag(qq).view(np.int8)
+    for lane in (0, 5, 16, 37, 63):
+        r, g = lane % 16, lane // 16
+        np.testing.assert_array_equal(packed[16 * lane:16 * lane + 16], qq[r, 16 * g:16 * g + 16])

@@ -1,0 +1,490 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bar (see the oracle's readings):
+* int8 codes, scales, int32 accumulators and delta at alpha = 0.5: bit-exact;
+* dequantised outputs of the linear layer and the lm_head: bit-exact (same
+  binary32 formula on both sides), which is stricter than rel-L2 <= 1e-3;
+* the GeGLU intermediate h: within one bf16 ulp, and the share of elements
+  that differ bounded (device tanhf vs correctly rounded tanh);
+* FFN block output: rel-L2 <= 1e-3 against the oracle;
+* bf16 path and stack glue: rel-L2 bounds derived from bf16 rounding.
+
+Every oracle input is drawn by ``synth`` or computed by the oracle; nothing
+the GPU produced is fed to the oracle.
+"""
+
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_28003_amd import synth, w8a8
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+DEV = "cuda:0"
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def dev_bf16(u16):
+    return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).view(torch.bfloat16).to(DEV)
+
+
+def dev_f32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV)
+
+
+def host_bf16(t):
+    return t.detach().cpu().view(torch.int16).numpy().view(np.uint16)
+
+
+def host(t):
+    return t.detach().cpu().numpy()
+
+
+def packed_full(t, rows, k):
+    """The whole padded packed matrix, row-major (to check zero padding)."""
+    rp, kp = -(-rows // 16) * 16, -(-k // 64) * 64
+    return w8a8.frag_to_rowmajor(host(t), rp, kp)
+
+
+def rel_l2(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def bf16_ulp_diff(a_bits, b_bits):
+    """|difference| in units of bf16 ulps (same-sign finite values)."""
+    a = a_bits.astype(np.int32)
+    b = b_bits.astype(np.int32)
+    sa = np.where(a & 0x8000, -(a & 0x7FFF), a & 0x7FFF)
+    sb = np.where(b & 0x8000, -(b & 0x7FFF), b & 0x7FFF)
+    return np.abs(sa - sb)
+
+
+def act_input(m, k, seed, n_out=None, factor=30.0, dtype="bf16"):
+    ch = synth.outlier_channels(seed + 1, k, n_out if n_out is not None else max(1, k // 100))
+    x = synth.activations(seed, m, k, ch, factor)
+    return synth.to_bf16_bits(x) if dtype == "bf16" else x
+
+
+def to_dev(x):
+    return dev_bf16(x) if x.dtype == np.uint16 else dev_f32(x)
+
+
+# ------------------------------------------------------------------ a3
+
+@pytest.mark.parametrize("m,k,dtype,smooth", [
+    (1, 1152, "bf16", True), (16, 1152, "f32", True), (37, 1152, "bf16", False),
+    (128, 6912, "bf16", True), (3, 16, "f32", False), (5, 80, "bf16", True),
+    (2048, 1152, "bf16", True), (64, 1040, "f32", True)])
+def test_quantize_act_bit_exact(m, k, dtype, smooth):
+    say("quantize_act", m, k, dtype, smooth)
+    x = act_input(m, k, 100 + m + k, dtype=dtype)
+    if m > 2:
+        xf = oracle.as_f32(x).copy()
+        xf[1] = 0.0                                             # all-zero token
+        xf[2, : min(k, 8)] = [127, 2.5, -3.5, 0.5, 63.5, -127, 1.5, 64.5][: min(k, 8)]
+        xf[2, 8:] = 0.0                                         # exact ties at s = 1
+        x = synth.to_bf16_bits(xf) if dtype == "bf16" else xf
+    delta = None
+    if smooth:
+        delta = np.exp(np.random.default_rng(k).uniform(-2, 2, k)).astype(np.float32)
+    q_o, s_o = oracle.quantize_act(x, delta)
+    qx, sx = w8a8.quantize_act(to_dev(x), None if delta is None else dev_f32(delta))
+    torch.cuda.synchronize()
+    full = packed_full(qx, m, k)
+    np.testing.assert_array_equal(full[:m, :k], q_o)
+    assert not full[m:].any() and not full[:, k:].any(), "padding must be zero"
+    np.testing.assert_array_equal(host(sx), s_o)
+
+
+# ------------------------------------------------------------------ a1 / a2
+
+@pytest.mark.parametrize("alpha", [0.5, 0.3])
+def test_calibration_matches_oracle(alpha):
+    say("calibration", alpha)
+    cfg = synth.ffn_config(m=4)
+    x_cal = cfg["x_cal"]
+    a_o = oracle.col_absmax(x_cal)
+    w_o = oracle.col_absmax(cfg["w_up"], oracle.col_absmax(cfg["w_gate"]))
+    d_o = oracle.smooth_delta(a_o, w_o, alpha)
+    a_g = w8a8.col_absmax(dev_bf16(x_cal))
+    w_g = w8a8.col_absmax(dev_bf16(cfg["w_gate"]))
+    w_g = w8a8.col_absmax(dev_bf16(cfg["w_up"]), w_g)
+    d_g = w8a8.smooth_calibrate(a_g, w_g, alpha)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(a_g), a_o)
+    np.testing.assert_array_equal(host(w_g), w_o)
+    if alpha == 0.5:
+        np.testing.assert_array_equal(host(d_g), d_o)
+    else:   # pow in binary64 on both sides, then one rounding to binary32
+        ulps = np.abs(host(d_g).view(np.int32) - d_o.view(np.int32))
+        assert ulps.max() <= 1
+
+
+@pytest.mark.parametrize("n,k,dtype", [(6912, 1152, "f32"), (1152, 6912, "bf16"),
+                                       (33, 80, "bf16"), (7, 16, "f32")])
+def test_quantize_weights_bit_exact(n, k, dtype):
+    say("quantize_weights", n, k, dtype)
+    w = synth.normal(7 + n, (n, k), 0.02)
+    w[0, :] = 0.0
+    if dtype == "bf16":
+        w = synth.to_bf16_bits(w)
+    delta = np.exp(np.random.default_rng(n).uniform(-2, 2, k)).astype(np.float32)
+    q_o, s_o = oracle.quantize_weights(w, delta)
+    wq, s_w = w8a8.quantize_weights(to_dev(w), dev_f32(delta))
+    q_g = w8a8.unpack_weights(wq, n, k)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(q_g), q_o)
+    np.testing.assert_array_equal(host(s_w), s_o)
+    full = packed_full(wq, n, k)
+    np.testing.assert_array_equal(full[:n, :k], q_o)
+    assert not full[n:].any() and not full[:, k:].any()
+
+
+def test_quantize_weights_lm_head_full_size():
+    say("quantize_weights lm_head 262144 x 1152")
+    cfg = synth.lm_head_config(m=1)
+    delta = oracle.smooth_calibrate(cfg["x_cal"], [cfg["w"]])
+    q_o, s_o = oracle.quantize_weights(cfg["w"], delta)
+    wq, s_w = w8a8.quantize_weights(dev_bf16(cfg["w"]), dev_f32(delta))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(w8a8.frag_to_rowmajor(host(wq), 262144, 1152), q_o)
+    np.testing.assert_array_equal(host(s_w), s_o)
+
+
+# ------------------------------------------------------------------ a4
+
+GEMM_SHAPES = [(1, 16, 64), (5, 48, 80), (16, 6912, 1152), (1, 1152, 6912), (17, 1152, 6912),
+               (64, 4096, 1152), (65, 1152, 6912), (128, 6912, 1152), (300, 1000, 1152),
+               (512, 1152, 6912), (129, 13824, 1152), (40, 4112, 1152)]
+
+
+@pytest.mark.parametrize("m,n,k", GEMM_SHAPES)
+def test_gemm_i32_bit_exact(m, n, k):
+    say("gemm_i8_i32", m, n, k)
+    rng = np.random.default_rng(m * 7 + n * 3 + k)
+    qa = rng.integers(-127, 128, (m, k), dtype=np.int8)
+    qb = rng.integers(-127, 128, (n, k), dtype=np.int8)
+    qa[0, :] = 127
+    qb[0, :] = -127           # extreme accumulator magnitude
+    acc_o = oracle.gemm_i32(qa, qb)
+    A = torch.from_numpy(w8a8.rowmajor_to_frag(qa)).to(DEV)
+    B = torch.from_numpy(w8a8.rowmajor_to_frag(qb)).to(DEV)
+    acc = w8a8.gemm_i8_i32(A, m, B, n, k)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(acc), acc_o)
+
+
+@pytest.mark.parametrize("m,n,k,splits", [(128, 1152, 6912, 1), (128, 1152, 6912, 3),
+                                          (300, 640, 1152, 7), (96, 2048, 6912, 2)])
+def test_gemm_split_k_is_bit_identical(m, n, k, splits, monkeypatch):
+    say("split-K", m, n, k, splits)
+    rng = np.random.default_rng(99 + splits)
+    qa = rng.integers(-127, 128, (m, k), dtype=np.int8)
+    qb = rng.integers(-127, 128, (n, k), dtype=np.int8)
+    acc_o = oracle.gemm_i32(qa, qb)
+    A = torch.from_numpy(w8a8.rowmajor_to_frag(qa)).to(DEV)
+    B = torch.from_numpy(w8a8.rowmajor_to_frag(qb)).to(DEV)
+    monkeypatch.setenv("W8A8_GEMM_SPLITS", str(splits))
+    for tile in (0, 1, 2, 3):
+        monkeypatch.setenv("W8A8_GEMM_TILE", str(tile))
+        acc = w8a8.gemm_i8_i32(A, m, B, n, k)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(host(acc), acc_o, err_msg="tile %d" % tile)
+
+
+# ------------------------------------------------------------------ a5: linear
+
+@pytest.mark.parametrize("out_dtype", ["f32", "bf16"])
+def test_linear_config1_bit_exact(out_dtype):
+    say("linear cfg1", out_dtype)
+    cfg = synth.linear_config()                       # X fp32 16 x 1152, W 6912 x 1152
+    delta = oracle.smooth_calibrate(cfg["x_cal"], [cfg["w"]])
+    wq_o, sw_o = oracle.quantize_weights(cfg["w"], delta)
+    y_o = oracle.w8a8_linear(cfg["x"], wq_o, sw_o, delta, out_dtype)
+    layer = w8a8.LinearW8A8.from_weight(dev_f32(cfg["w"]), dev_f32(delta))
+    y = w8a8.linear(layer, dev_f32(cfg["x"]),
+                    torch.float32 if out_dtype == "f32" else torch.bfloat16)
+    torch.cuda.synchronize()
+    got = host(y) if out_dtype == "f32" else host_bf16(y)
+    np.testing.assert_array_equal(got, y_o)
+    ref = oracle.bf16_to_f32(y_o) if out_dtype == "bf16" else y_o
+    assert rel_l2(oracle.bf16_to_f32(got) if out_dtype == "bf16" else got, ref) <= 1e-3
+
+
+@pytest.mark.parametrize("m,n,k", [(1, 1536, 1152), (32, 1536, 1152), (256, 1536, 1152),
+                                   (1, 1152, 1024), (256, 1152, 1024), (77, 300, 208)])
+def test_linear_attention_shapes_bit_exact(m, n, k):
+    say("linear attention shape", m, n, k)
+    x = act_input(m, k, 500 + m)
+    w = synth.to_bf16_bits(synth.normal(600 + n, (n, k), 0.02))
+    x_cal = act_input(512, k, 500 + m)
+    delta = oracle.smooth_calibrate(x_cal, [w])
+    wq_o, sw_o = oracle.quantize_weights(w, delta)
+    y_o = oracle.w8a8_linear(x, wq_o, sw_o, delta, "bf16")
+    layer = w8a8.LinearW8A8.from_weight(dev_bf16(w), dev_f32(delta))
+    y = w8a8.linear(layer, dev_bf16(x), torch.bfloat16)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host_bf16(y), y_o)
+
+
+# ------------------------------------------------------------------ a6: FFN
+
+def _ffn_setup(m, d=1152, f=6912, seed_base=2000):
+    cfg = synth.ffn_config(m=m, d=d, f=f, seed_base=seed_base)
+    q = oracle.quantize_ffn(cfg["w_gate"], cfg["w_up"], cfg["w_down"], cfg["x_cal"])
+    layer = w8a8.FfnW8A8.from_weights(dev_bf16(cfg["w_gate"]), dev_bf16(cfg["w_up"]),
+                                      dev_bf16(cfg["w_down"]), dev_f32(q["delta_gu"]),
+                                      dev_f32(q["delta_down"]))
+    return cfg, q, layer
+
+
+@pytest.mark.parametrize("m", [1, 5, 64, 128, 300])
+def test_ffn_gate_up_geglu_stage(m):
+    say("ffn gate/up + GeGLU", m)
+    cfg, q, layer = _ffn_setup(m)
+    _, st = oracle.w8a8_ffn(cfg["x"], q, stages=True)
+    qx = torch.from_numpy(w8a8.rowmajor_to_frag(st["qx"])).to(DEV)
+    h = w8a8.ffn_gate_up(layer, qx, dev_f32(st["sx"]), m)
+    torch.cuda.synchronize()
+    hg = host_bf16(h)
+    ulps = bf16_ulp_diff(hg, st["h"])
+    assert ulps.max() <= 1, ulps.max()
+    frac = float((ulps > 0).mean())
+    say("  h mismatch fraction", frac)
+    assert frac <= 1e-3
+
+
+@pytest.mark.parametrize("m", [1, 8, 64, 128, 512])
+def test_ffn_block_matches_oracle(m):
+    say("ffn block", m)
+    cfg, q, layer = _ffn_setup(m)
+    y_o, st = oracle.w8a8_ffn(cfg["x"], q, stages=True)
+    y = w8a8.ffn(layer, dev_bf16(cfg["x"]))
+    torch.cuda.synchronize()
+    yg = host_bf16(y)
+    err = rel_l2(oracle.bf16_to_f32(yg), oracle.bf16_to_f32(y_o))
+    same = float((yg == y_o).mean())
+    say("  rel-L2 %.3g, bit-identical fraction %.6f" % (err, same))
+    assert err <= 1e-3
+    assert same >= 0.99
+
+
+def test_ffn_requant_of_oracle_h_bit_exact():
+    # the requantisation of h uses the activation quantiser; on the oracle's h
+    # it must reproduce the oracle's codes and scales exactly
+    say("ffn requant stage")
+    cfg, q, layer = _ffn_setup(128)
+    _, st = oracle.w8a8_ffn(cfg["x"], q, stages=True)
+    qh, sh = w8a8.quantize_act(dev_bf16(st["h"]), dev_f32(q["delta_down"]))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(w8a8.frag_to_rowmajor(host(qh), 128, 6912), st["qh"])
+    np.testing.assert_array_equal(host(sh), st["sh"])
+
+
+def test_ffn_weights_quantised_on_gpu_equal_oracle_codes():
+    cfg, q, layer = _ffn_setup(1)
+    for name, lin, n, k in [("gate", layer.gate, 6912, 1152), ("up", layer.up, 6912, 1152),
+                            ("down", layer.down, 1152, 6912)]:
+        np.testing.assert_array_equal(host(w8a8.unpack_weights(lin.wq, n, k)), q["wq_" + name])
+        np.testing.assert_array_equal(host(lin.s_w), q["s_" + name])
+
+
+def test_ffn_deterministic():
+    cfg, q, layer = _ffn_setup(128)
+    x = dev_bf16(cfg["x"])
+    y1 = host_bf16(w8a8.ffn(layer, x))
+    for _ in range(5):
+        np.testing.assert_array_equal(host_bf16(w8a8.ffn(layer, x)), y1)
+
+
+# ------------------------------------------------------------------ a7: lm_head
+
+@pytest.mark.parametrize("m", [1, 8, 64])
+def test_lm_head_reduced_vocab_bit_exact(m):
+    say("lm_head vocab 4096", m)
+    cfg = synth.lm_head_config(m=m, vocab=4096)
+    delta = oracle.smooth_calibrate(cfg["x_cal"], [cfg["w"]])
+    wq_o, sw_o = oracle.quantize_weights(cfg["w"], delta)
+    y_o = oracle.w8a8_lm_head(cfg["x"], wq_o, sw_o, delta)
+    layer = w8a8.LinearW8A8.from_weight(dev_bf16(cfg["w"]), dev_f32(delta))
+    y = w8a8.lm_head(layer, dev_bf16(cfg["x"]))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host_bf16(y), y_o)
+
+
+@pytest.fixture(scope="module")
+def lm_full():
+    cfg = synth.lm_head_config(m=64)
+    delta = oracle.smooth_calibrate(cfg["x_cal"], [cfg["w"]])
+    layer = w8a8.LinearW8A8.from_weight(dev_bf16(cfg["w"]), dev_f32(delta))
+    return cfg, delta, layer
+
+
+@pytest.mark.parametrize("m", [1, 8, 64])
+def test_lm_head_full_vocab_sampled_columns(m, lm_full):
+    say("lm_head full vocab, sampled columns", m)
+    cfg, delta, layer = lm_full
+    x = np.ascontiguousarray(cfg["x"][:m])
+    y = w8a8.lm_head(layer, dev_bf16(x))
+    torch.cuda.synchronize()
+    yg = host_bf16(y)
+    cols = np.sort(np.random.default_rng(m).choice(262144, 3000, replace=False))
+    cols = np.unique(np.concatenate([cols, [0, 1, 65535, 65536, 131071, 262143]]))
+    wq_o, sw_o = oracle.quantize_weights(cfg["w"][cols], delta)   # rows are independent
+    y_o = oracle.w8a8_lm_head(x, wq_o, sw_o, delta)
+    np.testing.assert_array_equal(yg[:, cols], y_o)
+    assert np.isfinite(oracle.bf16_to_f32(yg)).all()
+
+
+# ------------------------------------------------------------------ bf16 path and glue
+
+@pytest.mark.parametrize("m,n,k", [(1, 6912, 1152), (128, 1152, 6912), (64, 4096, 1152),
+                                   (300, 1000, 1152), (2048, 1152, 1152)])
+def test_bf16_linear_matches_oracle(m, n, k):
+    say("bf16 linear", m, n, k)
+    x = act_input(m, k, 800 + m, factor=4.0)
+    w = synth.to_bf16_bits(synth.normal(900 + n, (n, k), 0.02))
+    y_o = oracle.bf16_linear(x, w)
+    wp = w8a8.pack_bf16(dev_bf16(w))
+    y = w8a8.bf16_linear(dev_bf16(x), wp, n, k)
+    torch.cuda.synchronize()
+    yg = host_bf16(y)
+    # fp32 accumulation in any order is within gamma_K * sum_j |x_j w_j| of the
+    # exact sum; each side then rounds once to bf16 (half an ulp each)
+    xf = oracle.bf16_to_f32(x).astype(np.float64)
+    wf = oracle.bf16_to_f32(w).astype(np.float64)
+    gamma = k * 2.0 ** -24 / (1 - k * 2.0 ** -24)
+    bound = gamma * (np.abs(xf) @ np.abs(wf).T)
+    a = oracle.bf16_to_f32(yg).astype(np.float64)
+    b = oracle.bf16_to_f32(y_o).astype(np.float64)
+    big = np.maximum(np.abs(a), np.abs(b))
+    ulp = np.exp2(np.floor(np.log2(np.maximum(big, 2.0 ** -126))) - 7)
+    assert np.all(np.abs(a - b) <= bound + ulp)
+    assert rel_l2(a, b) <= 1e-3
+    assert float((yg == y_o).mean()) >= 0.99
+
+
+@pytest.mark.parametrize("m", [1, 128])
+def test_bf16_ffn_matches_oracle(m):
+    say("bf16 ffn", m)
+    cfg = synth.ffn_config(m=m)
+    y_o = oracle.bf16_ffn(cfg["x"], cfg["w_gate"], cfg["w_up"], cfg["w_down"])
+    layer = w8a8.FfnBF16.from_weights(dev_bf16(cfg["w_gate"]), dev_bf16(cfg["w_up"]),
+                                      dev_bf16(cfg["w_down"]))
+    y = w8a8.bf16_ffn(layer, dev_bf16(cfg["x"]))
+    torch.cuda.synchronize()
+    err = rel_l2(oracle.bf16_to_f32(host_bf16(y)), oracle.bf16_to_f32(y_o))
+    say("  rel-L2", err)
+    assert err <= 2e-3
+
+
+def test_rmsnorm_and_residual():
+    say("rmsnorm")
+    x = act_input(33, 1152, 77, factor=10.0)
+    f = act_input(33, 1152, 78, factor=3.0)
+    a_o = oracle.rmsnorm(x)
+    r_o = oracle.residual_add(x, oracle.rmsnorm(f))
+    a = w8a8.rmsnorm(dev_bf16(x))
+    r = w8a8.rmsnorm_residual(dev_bf16(x), dev_bf16(f))
+    torch.cuda.synchronize()
+    assert bf16_ulp_diff(host_bf16(a), a_o).max() <= 1
+    assert bf16_ulp_diff(host_bf16(r), r_o).max() <= 1
+    assert float((host_bf16(a) != a_o).mean()) < 1e-2
+
+
+# ------------------------------------------------------------------ a8 / a9: stack
+
+def test_stack_precision_map_matches_oracle():
+    say("stack 4 layers")
+    n_layers, m, vocab = 4, 16, 4096
+    cfg = synth.stack_config(m=m, n_layers=n_layers, vocab=vocab)
+    layers_o, i8, bf = [], [], []
+    for L in cfg["layers"]:
+        qL = oracle.quantize_ffn(L["w_gate"], L["w_up"], L["w_down"], cfg["x_cal"])
+        layers_o.append(dict(L, int8=qL))
+        i8.append(w8a8.FfnW8A8.from_weights(dev_bf16(L["w_gate"]), dev_bf16(L["w_up"]),
+                                            dev_bf16(L["w_down"]), dev_f32(qL["delta_gu"]),
+                                            dev_f32(qL["delta_down"])))
+        bf.append(w8a8.FfnBF16.from_weights(dev_bf16(L["w_gate"]), dev_bf16(L["w_up"]),
+                                            dev_bf16(L["w_down"])))
+    d_lm = oracle.smooth_calibrate(cfg["x_cal"], [cfg["w_lm"]])
+    wq_lm, sw_lm = oracle.quantize_weights(cfg["w_lm"], d_lm)
+    lm_o = dict(w=cfg["w_lm"], wq=wq_lm, s_w=sw_lm, delta=d_lm)
+    stack = w8a8.Stack(i8, bf, w8a8.LinearW8A8.from_weight(dev_bf16(cfg["w_lm"]), dev_f32(d_lm)),
+                       w8a8.pack_bf16(dev_bf16(cfg["w_lm"])), vocab)
+    x = dev_bf16(cfg["x"])
+    for prec, lm8 in [([0, 0, 0, 0], False), ([1, 0, 0, 1], True), ([1, 1, 1, 1], True)]:
+        prec = np.array(prec, np.uint8)
+        y_o = oracle.stack(cfg["x"], layers_o, prec, lm_o, lm8)
+        y = stack.run(x, prec, lm8)
+        torch.cuda.synchronize()
+        err = rel_l2(oracle.bf16_to_f32(host_bf16(y)), oracle.bf16_to_f32(y_o))
+        say("  map", prec, "lm_head int8", lm8, "rel-L2 %.3g" % err)
+        assert err <= 1e-2
+
+
+# ------------------------------------------------------------------ graph replay
+
+def test_graph_replay_matches_eager():
+    """The benchmark replays the step as a captured graph: every replay, with
+    eager work and synchronisation in between, must equal the eager result."""
+    say("graph replay")
+    cfg, q, layer = _ffn_setup(128)
+    x = dev_bf16(cfg["x"])
+    lm_cfg = synth.lm_head_config(m=8, vocab=4096)
+    d_lm = oracle.smooth_calibrate(lm_cfg["x_cal"], [lm_cfg["w"]])
+    lm = w8a8.LinearW8A8.from_weight(dev_bf16(lm_cfg["w"]), dev_f32(d_lm))
+    xl = dev_bf16(lm_cfg["x"])
+    ws = torch.empty(w8a8.ffn_workspace_bytes(128, 1152, 6912), dtype=torch.uint8, device=DEV)
+    wsl = torch.empty(w8a8.lm_head_workspace_bytes(8, 4096, 1152), dtype=torch.uint8, device=DEV)
+    y = torch.empty((128, 1152), dtype=torch.bfloat16, device=DEV)
+    logits = torch.empty((8, 4096), dtype=torch.bfloat16, device=DEV)
+    w8a8.ffn(layer, x, out=y, ws=ws)
+    w8a8.lm_head(lm, xl, out=logits, ws=wsl)
+    torch.cuda.synchronize()
+    y_eager, l_eager = host_bf16(y), host_bf16(logits)
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            w8a8.ffn(layer, x, out=y, ws=ws)
+            w8a8.lm_head(lm, xl, out=logits, ws=wsl)
+    torch.cuda.current_stream().wait_stream(s)
+    for i in range(4):
+        y.zero_()
+        logits.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(host_bf16(y), y_eager, err_msg="replay %d" % i)
+        np.testing.assert_array_equal(host_bf16(logits), l_eager, err_msg="replay %d" % i)
+        w8a8.ffn(layer, x, out=torch.empty_like(y))   # eager work between replays
+
+
+def test_bf16_gate_up_stage_matches_oracle():
+    say("bf16 gate/up stage")
+    cfg = synth.ffn_config(m=64)
+    g = oracle.linear_f64(cfg["x"], cfg["w_gate"]).astype(np.float32)
+    u = oracle.linear_f64(cfg["x"], cfg["w_up"]).astype(np.float32)
+    h_o = oracle.f32_to_bf16(oracle.geglu(g, u))
+    layer = w8a8.FfnBF16.from_weights(dev_bf16(cfg["w_gate"]), dev_bf16(cfg["w_up"]),
+                                      dev_bf16(cfg["w_down"]))
+    h = w8a8.bf16_ffn_gate_up(layer, dev_bf16(cfg["x"]))
+    torch.cuda.synchronize()
+    hg = host_bf16(h)
+    err = rel_l2(oracle.bf16_to_f32(hg), oracle.bf16_to_f32(h_o))
+    say("  rel-L2", err)
+    assert err <= 2e-3
+    assert float((hg == h_o).mean()) >= 0.95
