@@ -52,7 +52,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on one GPU only: this path has no multi-GPU mode "
-              "(data parallelism needs no collective in the forward pass; see DESIGN.md)",
+              "(each GPU would run its own batch shard; the forward pass needs no collective)",
               file=sys.stderr)
         sys.exit(2)
 

@@ -38,13 +38,13 @@ hipStream_t S(w8a8_stream_t s) { return reinterpret_cast<hipStream_t>(s); }
 // ------------------------------------------------------------------ planner
 
 struct Plan {
-  bool skinny = false;
+  bool stream = false;  // streaming kernel (M <= 128) or tiled kernel
   int tile = TILE_128x128;
-  int mb = 1;       // skinny: 16-row blocks of A
-  int kc = 18;      // skinny: LDS fragment columns
+  int mb = 1;           // streaming: 16-row blocks of A
+  int nw = 1, wk = 1;   // streaming: waves per workgroup, waves splitting K
   int splits = 1;
   int kchunk = 0;
-  int nbpb = 4;     // skinny: column blocks per workgroup
+  int nbpb = 1;         // streaming: column blocks per workgroup
 };
 
 int env_int(const char* name, int dflt) {
@@ -61,6 +61,8 @@ void tile_shape(int tile, int* bm, int* bn) {
     case TILE_GLU_128x32: *bm = 128; *bn = 32; break;
     case TILE_GLU_64x64: *bm = 64; *bn = 64; break;
     case TILE_GLU_128x64: *bm = 128; *bn = 64; break;
+    case TILE_256x256: *bm = 256; *bn = 256; break;
+    case TILE_GLU_256x128: *bm = 256; *bn = 128; break;
     default: *bm = 128; *bn = 128;
   }
 }
@@ -71,41 +73,81 @@ int64_t tiles_of(int tile, int64_t m, int64_t n) {
   return ceil_div(m, bm) * ceil_div(n, bn);
 }
 
+// Streaming plan for M <= 128, or false if the A panel cannot fit in LDS.
+bool plan_stream(Plan& p, int64_t m, int64_t n, int64_t kb, bool glu) {
+  const int64_t nbc = ceil_div(n, 16);
+  const int64_t lds_kb = 160;  // LDS per workgroup, KiB (one fragment = 1 KiB)
+  p.mb = m <= 16 ? 1 : (m <= 32 ? 2 : (m <= 64 ? 4 : 8));
+  auto lds = [&](int64_t kchunk, int wk) { return p.mb * kchunk + (wk - 1) * (glu ? 2 : 1) * p.mb; };
+  if (glu) {  // gate/up pair: no K split across workgroups (the epilogue needs full sums)
+    for (int wk : {4, 2, 1}) {
+      if (wk == 4 && p.mb > 4) continue;  // 4-wave K split spills at MB = 8
+      if (lds(kb, wk) <= lds_kb) {
+        p.nw = p.wk = wk;
+        p.splits = 1;
+        p.kchunk = (int)kb;
+        p.nbpb = 1;
+        return true;
+      }
+    }
+    return false;
+  }
+  if (nbc >= 1024) {  // wide output (lm_head): every wave owns its column blocks
+    if (p.mb * kb > 144) return false;
+    p.wk = 1;
+    p.nw = p.mb == 1 ? 1 : 4;
+    p.splits = 1;
+    p.kchunk = (int)kb;
+    p.nbpb = p.nw == 1 ? (int)std::max<int64_t>(1, ceil_div(nbc, 2048))
+                       : (int)round_up(std::max<int64_t>(4, ceil_div(nbc, 512)), 4);
+    return true;
+  }
+  // narrow output, long K (down projection): waves of a workgroup split one
+  // column block's K range; pick the split with the most work per wave among
+  // those that keep >= 768 waves busy
+  bool found = false;
+  int64_t best_pw = -1, best_waves = -1;
+  for (int wk : {16, 4, 2}) {
+    if (wk == 16 && p.mb > 1) continue;  // 16-wave workgroups only for MB = 1
+    int64_t max_kc = (lds_kb - (wk - 1) * p.mb) / p.mb;
+    if (max_kc < wk) continue;
+    int64_t splits = ceil_div(kb, max_kc);
+    int64_t kchunk = ceil_div(kb, splits);
+    splits = ceil_div(kb, kchunk);
+    int64_t pw = ceil_div(kchunk, wk), waves = nbc * splits * wk;
+    bool better;
+    if (!found) better = true;
+    else if ((waves >= 768) != (best_waves >= 768)) better = waves >= 768;
+    else if (waves >= 768) better = pw > best_pw;
+    else better = waves > best_waves;
+    if (better) {
+      found = true;
+      best_pw = pw;
+      best_waves = waves;
+      p.nw = p.wk = wk;
+      p.splits = (int)splits;
+      p.kchunk = (int)kchunk;
+      p.nbpb = 1;
+    }
+  }
+  return found;
+}
+
 // Deterministic in (m, n, k, path); the workspace queries use the same plan.
-// W8A8_GEMM_TILE / W8A8_GEMM_SPLITS override the tiled path (tuning hook).
+// Tuning hooks for the tiled path: W8A8_GEMM_TILE / W8A8_GEMM_SPLITS (plain
+// epilogues) and W8A8_GLU_TILE (gated epilogue).
 Plan plan_gemm(int64_t m, int64_t n, int64_t k, bool bf16, bool glu) {
   Plan p;
   const int64_t kb = bf16 ? ceil_div(k, kFragK16) : ceil_div(k, kFragK8);
-  const int64_t nbc = ceil_div(n, 16);
-  if (m <= 64) {
-    p.skinny = true;
-    p.mb = m <= 16 ? 1 : (m <= 32 ? 2 : 4);
-    const int kcs[3] = {9, 18, 36};
-    int kc_fit = 0;
-    for (int c : kcs)
-      if (kb <= c) { kc_fit = c; break; }
-    const bool fits_lds = kc_fit && (int64_t)p.mb * kc_fit <= 144;
-    if (glu || (fits_lds && nbc >= 512)) {
-      if (!fits_lds) {
-        p.skinny = false;  // falls through to the tiled plan
-      } else {
-        p.kc = kc_fit;
-        p.splits = 1;
-        p.kchunk = (int)kb;
-      }
-    } else {
-      p.kc = 9;
-      p.kchunk = 9;
-      p.splits = (int)ceil_div(kb, 9);
-    }
-    if (p.skinny) {
-      int64_t nbpb = p.mb == 1 ? std::max<int64_t>(1, ceil_div(nbc, 2048))
-                               : round_up(std::max<int64_t>(4, ceil_div(nbc, 512)), 4);
-      p.nbpb = env_int("W8A8_SKINNY_NBPB", (int)nbpb);
-      return p;
-    }
+  // The streaming kernel wins while the weights dominate the traffic: up to
+  // 32 rows, and up to 64 rows for the very wide lm_head; the tiled kernel
+  // reuses operands better beyond that.
+  const bool wide = ceil_div(n, 16) >= 1024;
+  if ((m <= 32 || (m <= 64 && wide && !glu)) && plan_stream(p, m, n, kb, glu)) {
+    p.stream = true;
+    return p;
   }
-  p.skinny = false;
+  p = Plan();
   if (glu) {
     if (m <= 128)
       p.tile = TILE_GLU_128x32;
@@ -119,7 +161,7 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, bool bf16, bool glu) {
     else
       p.tile = TILE_64x64;
   }
-  p.tile = env_int("W8A8_GEMM_TILE", p.tile);
+  p.tile = glu ? env_int("W8A8_GLU_TILE", p.tile) : env_int("W8A8_GEMM_TILE", p.tile);
   const int64_t tiles = tiles_of(p.tile, m, n);
   int splits = 1;
   if (!glu && tiles < 200)
@@ -161,9 +203,9 @@ w8a8_status run_gemm(const Plan& pl, bool bf16, int epi, const void* A, int64_t 
   p.out = out;
   p.ldo = ldo;
   p.part = pl.splits > 1 ? gemm_ws : nullptr;
-  hipError_t e = pl.skinny ? launch_gemm_skinny(bf16, epi, pl.mb, pl.kc, p, pl.nbpb, st)
+  hipError_t e = pl.stream ? launch_gemm_stream(bf16, epi, pl.mb, pl.nw, pl.wk, p, pl.nbpb, st)
                            : launch_gemm_tile(bf16, epi, pl.tile, p, st);
-  w8a8_status s = hip_check(e, pl.skinny ? "gemm_skinny" : "gemm_tile");
+  w8a8_status s = hip_check(e, pl.stream ? "gemm_stream" : "gemm_tile");
   if (s != W8A8_OK || pl.splits <= 1) return s;
   return hip_check(launch_splitk_reduce(bf16, epi, p, st), "splitk_reduce");
 }

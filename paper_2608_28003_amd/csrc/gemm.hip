@@ -126,36 +126,41 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int PF, int S>
-__device__ __forceinline__ void wait_stage(int remaining_after) {
-  // stages issued after the one we need: min(S - 2, remaining_after)
-  if (remaining_after >= S - 2) {
-    wait_vmcnt<PF * (S - 2)>();
-  } else if constexpr (S >= 4) {
-    if (remaining_after == 1) wait_vmcnt<PF>(); else wait_vmcnt<0>();
-  } else {
+// Wait until at most PF * min(n, N) of this wave's loads are outstanding.
+template <int PF, int N>
+__device__ __forceinline__ void wait_outstanding(int n) {
+  if constexpr (N <= 0) {
     wait_vmcnt<0>();
+  } else {
+    if (n >= N)
+      wait_vmcnt<PF * N>();
+    else
+      wait_outstanding<PF, N - 1>(n);
   }
 }
 
 // ------------------------------------------------------------------ tiled kernel
 
-// BM x BN output tile per workgroup of 4 waves arranged WAVES_M x (4 / WAVES_M).
+// BM x BN output tile per workgroup of NW waves arranged WAVES_M x (NW / WAVES_M).
 // The K loop runs over an S-stage LDS ring: each stage holds BM/16 A and
 // BN/16 (x2 gated) B fragments, filled by LDS-DMA loads issued S-1 steps ahead,
 // so S-2 stages of HBM/L2 traffic stay in flight while the MFMAs of the
 // current stage run.  One barrier per K step.
-template <bool BF16, int BM, int BN, int WAVES_M, int EPI, int S>
-__global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
+//
+// Workgroups are dealt to the 8 XCDs round-robin by ID; the tile order gives
+// every XCD a contiguous range of tiles (M tile fastest), so the A and B
+// panels a range touches stay in that XCD's L2.
+template <bool BF16, int BM, int BN, int WAVES_M, int NW, int EPI, int S>
+__global__ __launch_bounds__(64 * NW) void gemm_tile_kernel(GemmParams p) {
   constexpr bool GLU = (EPI == EPI_GLU);
-  constexpr int WAVES_N = 4 / WAVES_M;
+  constexpr int WAVES_N = NW / WAVES_M;
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int TM = WM / 16, TN = WN / 16;
   constexpr int NA = BM / 16;
   constexpr int NB = (BN / 16) * (GLU ? 2 : 1);
   constexpr int NF = NA + NB;
-  static_assert(NF % 4 == 0, "fragments per stage must split over 4 waves");
-  constexpr int PF = NF / 4;  // fragments each wave fetches per stage
+  static_assert(NF % NW == 0, "fragments per stage must split over the waves");
+  constexpr int PF = NF / NW;  // fragments each wave fetches per stage
   typedef typename Acc<BF16>::T AccT;
 
   __shared__ v4i lds[S][NF * 64];
@@ -165,8 +170,13 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
 
   const int m_tiles = (p.M + BM - 1) / BM;
-  const int mt = blockIdx.x % m_tiles;
-  const int nt = blockIdx.x / m_tiles;
+  const int n_tiles = (p.N + BN - 1) / BN;
+  const int n_total = m_tiles * n_tiles;
+  const int per_xcd = (n_total + 7) / 8;
+  const int t = (int)(blockIdx.x % 8) * per_xcd + (int)(blockIdx.x / 8);
+  if (t >= n_total) return;  // whole workgroup, before any barrier
+  const int mt = t % m_tiles;
+  const int nt = t / m_tiles;
   const int z = blockIdx.y;
   const int kb0 = z * p.kchunk;
   const int kb1 = min(p.kb_count, kb0 + p.kchunk);
@@ -177,7 +187,7 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
   int64_t src_step[PF];
 #pragma unroll
   for (int i = 0; i < PF; ++i) {
-    const int f = wave + 4 * i;
+    const int f = wave + NW * i;
     if (f < NA) {
       int rb = min(mt * (BM / 16) + f, p.rb_a - 1);
       if constexpr (BF16) {
@@ -201,11 +211,17 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
       src_step[i] = kFragBytes;
     }
   }
+  // Each workgroup walks its K range from a different starting point, so the
+  // operand panels shared by many workgroups (A by every N tile, B by every
+  // M tile) are not all requested from the same L2 lines at the same time.
+  const int rot = nk > 0 ? (int)((blockIdx.x * 5u) % (unsigned)nk) : 0;
   auto issue = [&](int j) {  // stage j (relative to kb0) into slot j % S
-    const int kb = kb0 + j;
+    int jj = j + rot;
+    if (jj >= nk) jj -= nk;
+    const int kb = kb0 + jj;
 #pragma unroll
     for (int i = 0; i < PF; ++i)
-      to_lds_async(src[i] + (int64_t)kb * src_step[i], &lds[j % S][(wave + 4 * i) * 64]);
+      to_lds_async(src[i] + (int64_t)kb * src_step[i], &lds[j % S][(wave + NW * i) * 64]);
   };
 
   AccT acc[TM][TN];
@@ -218,144 +234,250 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
       if constexpr (GLU) accu[i][j] = Acc<BF16>::zero();
     }
 
-#pragma unroll
-  for (int j = 0; j < S - 1; ++j)
-    if (j < nk) issue(j);
-  for (int j = 0; j < nk; ++j) {
-    wait_stage<PF, S>(nk - 1 - j);
-    lds_barrier();
-    if (j + S - 1 < nk) issue(j + S - 1);
+  // Fragments of one stage held in registers: the LDS reads of stage j+1 are
+  // issued right after the barrier and complete while the MFMAs of stage j
+  // (already in registers) run.
+  struct Frags {
+    v4i a[TM];
+    v4i b[TN];
+    v4i bu[GLU ? TN : 1];
+  };
+  auto read_frags = [&](int j, Frags& F) {
     const v4i* St = lds[j % S];
-    v4i a[TM], b[TN];
 #pragma unroll
-    for (int i = 0; i < TM; ++i) a[i] = St[(wm * TM + i) * 64 + lane];
+    for (int i = 0; i < TM; ++i) F.a[i] = St[(wm * TM + i) * 64 + lane];
 #pragma unroll
-    for (int t = 0; t < TN; ++t) b[t] = St[(NA + wn * TN + t) * 64 + lane];
+    for (int t = 0; t < TN; ++t) F.b[t] = St[(NA + wn * TN + t) * 64 + lane];
+    if constexpr (GLU) {
+#pragma unroll
+      for (int t = 0; t < TN; ++t) F.bu[t] = St[(NA + BN / 16 + wn * TN + t) * 64 + lane];
+    }
+  };
+  auto mma_frags = [&](const Frags& F) {
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int t = 0; t < TN; ++t) acc[i][t] = Acc<BF16>::mma(a[i], b[t], acc[i][t]);
+      for (int t = 0; t < TN; ++t) acc[i][t] = Acc<BF16>::mma(F.a[i], F.b[t], acc[i][t]);
     if constexpr (GLU) {
-      v4i bu[TN];
-#pragma unroll
-      for (int t = 0; t < TN; ++t) bu[t] = St[(NA + BN / 16 + wn * TN + t) * 64 + lane];
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int t = 0; t < TN; ++t) accu[i][t] = Acc<BF16>::mma(a[i], bu[t], accu[i][t]);
+        for (int t = 0; t < TN; ++t) accu[i][t] = Acc<BF16>::mma(F.a[i], F.bu[t], accu[i][t]);
     }
+  };
+
+  int issued = -1;  // last stage handed to the LDS-DMA
+#pragma unroll
+  for (int j = 0; j < S - 1; ++j)
+    if (j < nk) {
+      issue(j);
+      issued = j;
+    }
+  Frags F0, F1;
+  if (nk > 0) {
+    wait_outstanding<PF, S - 2>(issued);
+    lds_barrier();
+    read_frags(0, F0);
+  }
+  // One step: stage j+1 must have landed (own loads, then the barrier for the
+  // other waves'); the slot of stage j-1 is free (its fragments were read one
+  // step earlier), so stage j+S-1 goes into it.
+  auto step = [&](int j, Frags& Fc, Frags& Fn) {
+    if (j + 1 < nk) wait_outstanding<PF, S - 2>(issued - (j + 1));
+    lds_barrier();
+    if (j + S - 1 < nk) {
+      issue(j + S - 1);
+      issued = j + S - 1;
+    }
+    if (j + 1 < nk) read_frags(j + 1, Fn);
+    mma_frags(Fc);
+  };
+  for (int j = 0; j < nk; j += 2) {
+    step(j, F0, F1);
+    if (j + 1 < nk) step(j + 1, F1, F0);
   }
 
   // ---------------- epilogue
-  const int row0 = mt * BM + wm * WM + (lane >> 4) * 4;
-  const int col0 = nt * BN + wn * WN + (lane & 15);
+  // Scales are read once into registers; each wave then stages one 16-row
+  // block of its output at a time in a private LDS area (the K-loop ring is
+  // free by now) and writes it back as 16-byte row segments.
+  lds_barrier();
+  const int row_w = mt * BM + wm * WM;  // first row of this wave
+  const int col_w = nt * BN + wn * WN;  // first column of this wave
+  const int row0 = row_w + (lane >> 4) * 4;
+  const int col0 = col_w + (lane & 15);
+  float sa[TM][4], sb[TN], sb2[GLU ? TN : 1];
+  if constexpr (!BF16) {
+    if (EPI != EPI_I32 && !(EPI != EPI_GLU && p.splits > 1)) {
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = row0 + i * 16 + r;
+          sa[i][r] = row < p.M ? p.s_a[row] : 0.f;
+        }
+#pragma unroll
+      for (int t = 0; t < TN; ++t) {
+        const int col = col0 + t * 16;
+        sb[t] = col < p.N ? p.s_b[col] : 0.f;
+        if constexpr (GLU) sb2[t] = col < p.N ? p.s_b2[col] : 0.f;
+      }
+    }
+  }
+  // output element type and destination of this launch
+  const bool partial = (EPI != EPI_GLU) && p.splits > 1;
+  constexpr int OB = (EPI == EPI_GLU || EPI == EPI_BF16) ? 2 : 4;  // bytes per element
+  const int esz = partial ? 4 : OB;
+  char* dst = partial ? reinterpret_cast<char*>(p.part) + (int64_t)z * p.M * p.N * 4
+                      : reinterpret_cast<char*>(p.out);
+  const int64_t ld = partial ? p.N : p.ldo;
+  static_assert(NW * 16 * WN * 4 <= S * NF * 64 * 16, "epilogue staging must fit in the ring");
+  char* stage = reinterpret_cast<char*>(&lds[0][0]) + wave * (16 * WN * 4);
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
 #pragma unroll
     for (int t = 0; t < TN; ++t)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int row = row0 + i * 16 + r, col = col0 + t * 16;
-        if (row >= p.M || col >= p.N) continue;
+        const int rr = (lane >> 4) * 4 + r;           // row within the 16-row block
+        const int cc = t * 16 + (lane & 15);          // column within the wave's WN
+        char* slot = stage + (rr * WN + cc) * esz;
         if constexpr (GLU) {
-          store_glu<BF16>(p, row, col, (float)acc[i][t][r], (float)accu[i][t][r]);
-        } else if (p.splits > 1) {
-          write_partial<BF16>(p, z, row, col, BF16 ? 0 : (int32_t)acc[i][t][r], (float)acc[i][t][r]);
+          float g, u;
+          if constexpr (BF16) {
+            g = (float)acc[i][t][r];
+            u = (float)accu[i][t][r];
+          } else {
+            g = ((float)acc[i][t][r] * sa[i][r]) * sb[t];
+            u = ((float)accu[i][t][r] * sa[i][r]) * sb2[t];
+          }
+          *reinterpret_cast<uint16_t*>(slot) = float_to_bf16_bits(gelu_tanh(g) * u);
+        } else if (partial || EPI == EPI_I32) {
+          if constexpr (BF16)
+            *reinterpret_cast<float*>(slot) = (float)acc[i][t][r];
+          else
+            *reinterpret_cast<int32_t*>(slot) = (int32_t)acc[i][t][r];
         } else {
-          store_elem<BF16, EPI>(p, row, col, BF16 ? 0 : (int32_t)acc[i][t][r], (float)acc[i][t][r]);
+          float y;
+          if constexpr (BF16)
+            y = (float)acc[i][t][r];
+          else
+            y = ((float)acc[i][t][r] * sa[i][r]) * sb[t];
+          if constexpr (EPI == EPI_F32)
+            *reinterpret_cast<float*>(slot) = y;
+          else
+            *reinterpret_cast<uint16_t*>(slot) = float_to_bf16_bits(y);
         }
       }
+    // this wave's own LDS writes are complete before its reads (in-order LDS)
+    const int row_bytes = WN * esz;
+    const int chunks = 16 * row_bytes / 16;
+    for (int c = lane; c < chunks; c += 64) {
+      const int rr = c / (row_bytes / 16);
+      const int cb = (c % (row_bytes / 16)) * 16;     // byte offset within the row
+      const int row = row_w + i * 16 + rr;
+      const int col = col_w + cb / esz;
+      if (row >= p.M) continue;
+      const char* srcp = stage + rr * row_bytes + cb;
+      char* gp = dst + ((int64_t)row * ld + col) * esz;
+      const int n_in = min(16 / esz, p.N - col);
+      if (n_in == 16 / esz && ((reinterpret_cast<uintptr_t>(gp) & 15) == 0)) {
+        *reinterpret_cast<uint4*>(gp) = *reinterpret_cast<const uint4*>(srcp);
+      } else {
+        for (int e = 0; e < n_in; ++e)
+          for (int bb = 0; bb < esz; ++bb) gp[e * esz + bb] = srcp[e * esz + bb];
+      }
+    }
+  }
 }
 
-// ------------------------------------------------------------------ skinny kernel
+// ------------------------------------------------------------------ streaming kernel
 
-// M <= 16 * MB rows (MB <= 4).  The workgroup stages the A fragments of its K
-// range (MB x KC fragments) in LDS with LDS-DMA loads; each wave then walks its
-// own output column blocks of 16, streaming the weight fragments of a block
-// (one contiguous run) from HBM in batches of KU fragments, double buffered in
-// registers: the loads of batch i+1 are in flight while the MFMAs (MB per
-// fragment) and, at the end of a block, the epilogue of batch i run.  For
-// MB == 1 a workgroup is a single wave, so the work spreads over every CU.
-// K splits (a grid dimension) write partial sums.
-template <bool BF16, int MB, int KC, int EPI>
-__global__ __launch_bounds__(MB == 1 ? 64 : 256) void gemm_skinny_kernel(GemmParams p,
-                                                                        int nb_per_block) {
+// Skinny GEMM, M <= 16 * MB rows (MB <= 8), for decode and small prefill
+// batches where the weights dominate the traffic.  The workgroup has NW waves.
+// With WK == 1 every wave walks its own output column blocks of 16 (the wide
+// lm_head); with WK == NW all waves share one column block and split its K
+// range, reducing through LDS (long-K, narrow-N projections such as the FFN
+// down projection, or the gated gate/up pair).  A wave stages the A fragments
+// of its own K slice in LDS once (LDS-DMA), then streams the weight fragments
+// of a column block -- one contiguous run -- from HBM in batches of KU,
+// double buffered in registers, so the loads of batch i+1 are in flight while
+// the MFMAs (MB per fragment) and the epilogue of batch i run.  Cross-workgroup
+// K splits (a grid dimension) write partial sums for the reduction kernel.
+template <bool BF16, int MB, int EPI, int NW, int WK>
+__global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int nb_per_block) {
+  static_assert(WK == 1 || WK == NW, "either every wave owns its column blocks or all share one");
   constexpr bool GLU = (EPI == EPI_GLU);
   constexpr int KU = 9;  // weight fragments per batch and operand
   constexpr int KG = GLU ? KU : 1;
-  constexpr int NW = MB == 1 ? 1 : 4;
+  constexpr int NC = GLU ? 2 : 1;
+  constexpr int GROUPS = NW / WK;
   typedef typename Acc<BF16>::T AccT;
-  __shared__ v4i lds_a[MB * KC * 64];
+  extern __shared__ v4i lds_dyn[];
 
   const int lane = lane_id();
   const int wave = threadIdx.x >> 6;
+  const int grp = wave / WK, wk = wave % WK;
   const int z = blockIdx.y;
   const int kb0 = z * p.kchunk;
-  const int kb1 = min(p.kb_count, kb0 + p.kchunk);
-  const int kc = kb1 - kb0;  // <= KC
+  const int kc = min(p.kb_count, kb0 + p.kchunk) - kb0;
+  v4i* lds_a = lds_dyn;                                       // MB x kchunk fragments
+  AccT* red = reinterpret_cast<AccT*>(lds_dyn + (int64_t)MB * p.kchunk * 64);  // (WK-1) x NC x MB
+
+  // this wave's K slice [ks0, ks1) of the workgroup's range
+  const int kpw = (kc + WK - 1) / WK;
+  const int ks0 = min(kc, wk * kpw), ks1 = min(kc, ks0 + kpw);
+  const int my_k = ks1 - ks0;
+  const int bpn = (kpw + KU - 1) / KU;  // batches per column block (uniform over the waves)
+
   const int nb_begin = blockIdx.x * nb_per_block;
   const int nb_end = min(p.rb_b, nb_begin + nb_per_block);
-  const int my_first = nb_begin + wave;
-  const int my_count = my_first < nb_end ? (nb_end - my_first + NW - 1) / NW : 0;
-  const int bpn = (kc + KU - 1) / KU;  // batches per column block
+  const int my_first = nb_begin + grp;
+  const int my_count = my_first < nb_end ? (nb_end - my_first + GROUPS - 1) / GROUPS : 0;
   const int total = my_count * bpn;
 
-  for (int f = wave; f < MB * kc; f += NW) {
-    const int mb = f / kc, kk = f % kc;
-    const int8_t* src;
+  // stage the A fragments: with WK > 1 each wave its own K slice (read only
+  // by itself); with WK == 1 the waves share the whole panel
+  auto a_src = [&](int mb, int kk) -> const int8_t* {
     if constexpr (BF16) {
       int64_t row = min((int64_t)mb * 16 + (lane & 15), (int64_t)p.M - 1);
-      src = reinterpret_cast<const int8_t*>(reinterpret_cast<const uint16_t*>(p.A) + row * p.lda +
-                                            (int64_t)(kb0 + kk) * kFragK16 + (lane >> 4) * 8);
+      return reinterpret_cast<const int8_t*>(reinterpret_cast<const uint16_t*>(p.A) + row * p.lda +
+                                             (int64_t)(kb0 + kk) * kFragK16 + (lane >> 4) * 8);
     } else {
-      src = reinterpret_cast<const int8_t*>(p.A) +
-            frag_offset(min(mb, p.rb_a - 1), kb0 + kk, p.kb_count) + lane * 16;
+      return reinterpret_cast<const int8_t*>(p.A) +
+             frag_offset(min(mb, p.rb_a - 1), kb0 + kk, p.kb_count) + lane * 16;
     }
-    to_lds_async(src, &lds_a[(mb * KC + kk) * 64]);
+  };
+  if constexpr (WK > 1) {
+    for (int f = 0; f < MB * my_k; ++f) {
+      const int mb = f / my_k, kk = ks0 + f % my_k;
+      to_lds_async(a_src(mb, kk), &lds_a[(mb * p.kchunk + kk) * 64]);
+    }
+  } else {
+    for (int f = wave; f < MB * kc; f += NW) {
+      const int mb = f / kc, kk = f % kc;
+      to_lds_async(a_src(mb, kk), &lds_a[(mb * p.kchunk + kk) * 64]);
+    }
   }
 
   v4i b0[KU], b1[KU], u0[KG], u1[KG];
   auto load_batch = [&](int idx, v4i (&b)[KU], v4i (&bu)[KG]) {
-    const int nb = my_first + NW * (idx / bpn);
+    const int nb = my_first + GROUPS * (idx / bpn);
     const int k0 = (idx % bpn) * KU;
 #pragma unroll
     for (int u = 0; u < KU; ++u) {
-      if (k0 + u < kc) {
-        b[u] = load_frag_packed(p.B, nb, kb0 + k0 + u, p.kb_count, lane);
-        if constexpr (GLU) bu[u] = load_frag_packed(p.B2, nb, kb0 + k0 + u, p.kb_count, lane);
+      if (k0 + u < my_k) {
+        b[u] = load_frag_packed(p.B, nb, kb0 + ks0 + k0 + u, p.kb_count, lane);
+        if constexpr (GLU) bu[u] = load_frag_packed(p.B2, nb, kb0 + ks0 + k0 + u, p.kb_count, lane);
       }
     }
   };
   if (total > 0) load_batch(0, b0, u0);  // first weights go out with the A fragments
   wait_vmcnt<0>();
-  lds_barrier();
+  if (WK == 1 && NW > 1) lds_barrier();  // the shared panel is read by every wave
 
   AccT acc[MB], accu[GLU ? MB : 1];
-  auto compute = [&](int idx, const v4i (&b)[KU], const v4i (&bu)[KG]) {
-    const int nb = my_first + NW * (idx / bpn);
-    const int bi = idx % bpn;
-    const int k0 = bi * KU;
-    if (bi == 0) {
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        acc[mb] = Acc<BF16>::zero();
-        if constexpr (GLU) accu[mb] = Acc<BF16>::zero();
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < KU; ++u) {
-      if (k0 + u < kc) {
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-          const v4i a = lds_a[(mb * KC + k0 + u) * 64 + lane];
-          acc[mb] = Acc<BF16>::mma(a, b[u], acc[mb]);
-          if constexpr (GLU) accu[mb] = Acc<BF16>::mma(a, bu[u], accu[mb]);
-        }
-      }
-    }
-    if (bi != bpn - 1) return;
-
-    // ---- epilogue of column block nb
+  auto epilogue = [&](int nb) {
     const int col = nb * 16 + (lane & 15);
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
@@ -371,6 +493,55 @@ __global__ __launch_bounds__(MB == 1 ? 64 : 256) void gemm_skinny_kernel(GemmPar
           store_elem<BF16, EPI>(p, row, col, BF16 ? 0 : (int32_t)acc[mb][r], (float)acc[mb][r]);
         }
       }
+  };
+  auto compute = [&](int idx, const v4i (&b)[KU], const v4i (&bu)[KG]) {
+    const int nb = my_first + GROUPS * (idx / bpn);
+    const int bi = idx % bpn;
+    const int k0 = bi * KU;
+    if (bi == 0) {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        acc[mb] = Acc<BF16>::zero();
+        if constexpr (GLU) accu[mb] = Acc<BF16>::zero();
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < KU; ++u) {
+      if (k0 + u < my_k) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const v4i a = lds_a[(mb * p.kchunk + ks0 + k0 + u) * 64 + lane];
+          acc[mb] = Acc<BF16>::mma(a, b[u], acc[mb]);
+          if constexpr (GLU) accu[mb] = Acc<BF16>::mma(a, bu[u], accu[mb]);
+        }
+      }
+    }
+    if (bi != bpn - 1) return;
+    if constexpr (WK == 1) {
+      epilogue(nb);
+    } else {
+      // in-workgroup K reduction: waves 1..WK-1 hand their sums to wave 0,
+      // which adds them in wave order and runs the epilogue
+      if (wk > 0) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          red[(((wk - 1) * NC + 0) * MB + mb) * 64 + lane] = acc[mb];
+          if constexpr (GLU) red[(((wk - 1) * NC + 1) * MB + mb) * 64 + lane] = accu[mb];
+        }
+      }
+      lds_barrier();
+      if (wk == 0) {
+        for (int w = 1; w < WK; ++w) {
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) {
+            acc[mb] += red[(((w - 1) * NC + 0) * MB + mb) * 64 + lane];
+            if constexpr (GLU) accu[mb] += red[(((w - 1) * NC + 1) * MB + mb) * 64 + lane];
+          }
+        }
+        epilogue(nb);
+      }
+      lds_barrier();
+    }
   };
 
   for (int idx = 0; idx < total; idx += 2) {
@@ -398,6 +569,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmParams p) {
   const int ncol = min(4, p.N - col0);
   int32_t isum[4] = {0, 0, 0, 0};
   float fsum[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
   for (int zz = 0; zz < p.splits; ++zz) {
     const int64_t base = zz * plane + (int64_t)row * p.N + col0;
 #pragma unroll
@@ -422,18 +594,22 @@ static hipError_t tile_dispatch(int tile, const GemmParams& p, hipStream_t st) {
   auto grid_for = [&](int bm, int bn) {
     int mt = (p.M + bm - 1) / bm;
     int nt = (p.N + bn - 1) / bn;
-    return dim3((unsigned)(mt * nt), (unsigned)p.splits);
+    int per_xcd = (mt * nt + 7) / 8;
+    return dim3((unsigned)(8 * per_xcd), (unsigned)p.splits);
   };
   if constexpr (EPI == EPI_GLU) {
     switch (tile) {
       case TILE_GLU_128x32:
-        gemm_tile_kernel<BF16, 128, 32, 4, EPI, 6><<<grid_for(128, 32), 256, 0, st>>>(p);
+        gemm_tile_kernel<BF16, 128, 32, 4, 4, EPI, 12><<<grid_for(128, 32), 256, 0, st>>>(p);
         break;
       case TILE_GLU_64x64:
-        gemm_tile_kernel<BF16, 64, 64, 2, EPI, 6><<<grid_for(64, 64), 256, 0, st>>>(p);
+        gemm_tile_kernel<BF16, 64, 64, 2, 4, EPI, 6><<<grid_for(64, 64), 256, 0, st>>>(p);
         break;
       case TILE_GLU_128x64:
-        gemm_tile_kernel<BF16, 128, 64, 2, EPI, 4><<<grid_for(128, 64), 256, 0, st>>>(p);
+        gemm_tile_kernel<BF16, 128, 64, 2, 4, EPI, 5><<<grid_for(128, 64), 256, 0, st>>>(p);
+        break;
+      case TILE_GLU_256x128:
+        gemm_tile_kernel<BF16, 256, 128, 2, 8, EPI, 5><<<grid_for(256, 128), 512, 0, st>>>(p);
         break;
       default:
         return hipErrorInvalidValue;
@@ -441,16 +617,19 @@ static hipError_t tile_dispatch(int tile, const GemmParams& p, hipStream_t st) {
   } else {
     switch (tile) {
       case TILE_128x128:
-        gemm_tile_kernel<BF16, 128, 128, 2, EPI, 4><<<grid_for(128, 128), 256, 0, st>>>(p);
+        gemm_tile_kernel<BF16, 128, 128, 2, 4, EPI, 5><<<grid_for(128, 128), 256, 0, st>>>(p);
         break;
       case TILE_128x64:
-        gemm_tile_kernel<BF16, 128, 64, 2, EPI, 6><<<grid_for(128, 64), 256, 0, st>>>(p);
+        gemm_tile_kernel<BF16, 128, 64, 2, 4, EPI, 6><<<grid_for(128, 64), 256, 0, st>>>(p);
         break;
       case TILE_64x64:
-        gemm_tile_kernel<BF16, 64, 64, 2, EPI, 6><<<grid_for(64, 64), 256, 0, st>>>(p);
+        gemm_tile_kernel<BF16, 64, 64, 2, 4, EPI, 6><<<grid_for(64, 64), 256, 0, st>>>(p);
         break;
       case TILE_256x128:
-        gemm_tile_kernel<BF16, 256, 128, 2, EPI, 3><<<grid_for(256, 128), 256, 0, st>>>(p);
+        gemm_tile_kernel<BF16, 256, 128, 2, 8, EPI, 5><<<grid_for(256, 128), 512, 0, st>>>(p);
+        break;
+      case TILE_256x256:
+        gemm_tile_kernel<BF16, 256, 256, 2, 8, EPI, 5><<<grid_for(256, 256), 512, 0, st>>>(p);
         break;
       default:
         return hipErrorInvalidValue;
@@ -477,45 +656,78 @@ hipError_t launch_gemm_tile(bool bf16, int epi, int tile, const GemmParams& p, h
   }
 }
 
-template <bool BF16, int EPI, int KC>
-static hipError_t skinny_mb(int mb, const GemmParams& p, int nbpb, hipStream_t st) {
-  dim3 grid((unsigned)((p.rb_b + nbpb - 1) / nbpb), (unsigned)p.splits);
-  switch (mb) {
-    case 1: gemm_skinny_kernel<BF16, 1, KC, EPI><<<grid, 64, 0, st>>>(p, nbpb); break;
-    case 2: gemm_skinny_kernel<BF16, 2, KC, EPI><<<grid, 256, 0, st>>>(p, nbpb); break;
-    case 4: gemm_skinny_kernel<BF16, 4, KC, EPI><<<grid, 256, 0, st>>>(p, nbpb); break;
-    default: return hipErrorInvalidValue;
+// dynamic LDS of a streaming launch: A panel + reduction scratch
+static size_t stream_lds_bytes(int mb, int kchunk, int wk, bool glu) {
+  return (size_t)mb * kchunk * kFragBytes + (size_t)(wk - 1) * (glu ? 2 : 1) * mb * kFragBytes;
+}
+
+template <bool BF16, int MB, int EPI, int NW, int WK>
+static hipError_t stream_launch(const GemmParams& p, int nbpb, hipStream_t st) {
+  auto kern = gemm_stream_kernel<BF16, MB, EPI, NW, WK>;
+  static bool attr_set = false;  // benign race: every caller sets the same value
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    attr_set = true;
   }
+  const size_t lds = stream_lds_bytes(MB, p.kchunk, WK, EPI == EPI_GLU);
+  if (lds > 160 * 1024) return hipErrorInvalidValue;
+  const int groups = NW / WK;
+  dim3 grid((unsigned)((p.rb_b + nbpb - 1) / nbpb), (unsigned)p.splits);
+  (void)groups;
+  kern<<<grid, 64 * NW, lds, st>>>(p, nbpb);
   return hipGetLastError();
 }
 
+// Instantiated wave layouts: 16-wave workgroups only for MB == 1 (at 16 waves a
+// wave has 128 registers, too few for larger MB), 4 waves sharing K only where
+// the accumulators still fit without spilling.
+template <bool BF16, int MB, int EPI>
+static hipError_t stream_waves(int nw, int wk, const GemmParams& p, int nbpb, hipStream_t st) {
+  if (nw == 1 && wk == 1) return stream_launch<BF16, MB, EPI, 1, 1>(p, nbpb, st);
+  if (nw == 4 && wk == 1) return stream_launch<BF16, MB, EPI, 4, 1>(p, nbpb, st);
+  if (nw == 2 && wk == 2) return stream_launch<BF16, MB, EPI, 2, 2>(p, nbpb, st);
+  if constexpr (MB <= 4 || EPI != EPI_GLU) {
+    if (nw == 4 && wk == 4) return stream_launch<BF16, MB, EPI, 4, 4>(p, nbpb, st);
+  }
+  if constexpr (MB == 1) {
+    if (nw == 16 && wk == 16) return stream_launch<BF16, MB, EPI, 16, 16>(p, nbpb, st);
+  }
+  return hipErrorInvalidValue;
+}
+
 template <bool BF16, int EPI>
-static hipError_t skinny_kc(int mb, int kc, const GemmParams& p, int nbpb, hipStream_t st) {
-  switch (kc) {
-    case 9: return skinny_mb<BF16, EPI, 9>(mb, p, nbpb, st);
-    case 18: return skinny_mb<BF16, EPI, 18>(mb, p, nbpb, st);
-    case 36: return skinny_mb<BF16, EPI, 36>(mb, p, nbpb, st);
+static hipError_t stream_mb(int mb, int nw, int wk, const GemmParams& p, int nbpb, hipStream_t st) {
+  switch (mb) {
+    case 1: return stream_waves<BF16, 1, EPI>(nw, wk, p, nbpb, st);
+    case 2: return stream_waves<BF16, 2, EPI>(nw, wk, p, nbpb, st);
+    case 4: return stream_waves<BF16, 4, EPI>(nw, wk, p, nbpb, st);
+    case 8: return stream_waves<BF16, 8, EPI>(nw, wk, p, nbpb, st);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_gemm_skinny(bool bf16, int epi, int mb, int kc, const GemmParams& p,
+hipError_t launch_gemm_stream(bool bf16, int epi, int mb, int nw, int wk, const GemmParams& p,
                               int nb_per_block, hipStream_t st) {
   if (bf16) {
     switch (epi) {
-      case EPI_F32: return skinny_kc<true, EPI_F32>(mb, kc, p, nb_per_block, st);
-      case EPI_BF16: return skinny_kc<true, EPI_BF16>(mb, kc, p, nb_per_block, st);
-      case EPI_GLU: return skinny_kc<true, EPI_GLU>(mb, kc, p, nb_per_block, st);
+      case EPI_BF16: return stream_mb<true, EPI_BF16>(mb, nw, wk, p, nb_per_block, st);
+      case EPI_GLU: return stream_mb<true, EPI_GLU>(mb, nw, wk, p, nb_per_block, st);
       default: return hipErrorInvalidValue;
     }
   }
   switch (epi) {
-    case EPI_I32: return skinny_kc<false, EPI_I32>(mb, kc, p, nb_per_block, st);
-    case EPI_F32: return skinny_kc<false, EPI_F32>(mb, kc, p, nb_per_block, st);
-    case EPI_BF16: return skinny_kc<false, EPI_BF16>(mb, kc, p, nb_per_block, st);
-    case EPI_GLU: return skinny_kc<false, EPI_GLU>(mb, kc, p, nb_per_block, st);
+    case EPI_I32: return stream_mb<false, EPI_I32>(mb, nw, wk, p, nb_per_block, st);
+    case EPI_F32: return stream_mb<false, EPI_F32>(mb, nw, wk, p, nb_per_block, st);
+    case EPI_BF16: return stream_mb<false, EPI_BF16>(mb, nw, wk, p, nb_per_block, st);
+    case EPI_GLU: return stream_mb<false, EPI_GLU>(mb, nw, wk, p, nb_per_block, st);
     default: return hipErrorInvalidValue;
   }
+}
+
+size_t gemm_stream_lds_bytes(int mb, int kchunk, int wk, bool glu) {
+  return stream_lds_bytes(mb, kchunk, wk, glu);
 }
 
 template <bool BF16>

@@ -32,13 +32,15 @@ struct GemmParams {
 
 // tile shapes selectable at run time
 enum TileCfg {
-  TILE_128x128 = 0,   // 4 waves of 64 x 64
-  TILE_128x64 = 1,    // 4 waves of 64 x 32
-  TILE_64x64 = 2,     // 4 waves of 32 x 32
-  TILE_256x128 = 3,   // 4 waves of 128 x 64
-  TILE_GLU_128x32 = 4,
-  TILE_GLU_64x64 = 5,
-  TILE_GLU_128x64 = 6,
+  TILE_128x128 = 0,     // 4 waves of 64 x 64
+  TILE_128x64 = 1,      // 4 waves of 64 x 32
+  TILE_64x64 = 2,       // 4 waves of 32 x 32
+  TILE_256x128 = 3,     // 8 waves of 128 x 32
+  TILE_GLU_128x32 = 4,  // gated: 4 waves of 32 x (32 gate + 32 up)
+  TILE_GLU_64x64 = 5,   // gated: 4 waves of 32 x (32 + 32)
+  TILE_GLU_128x64 = 6,  // gated: 4 waves of 64 x (32 + 32)
+  TILE_256x256 = 7,     // 8 waves of 128 x 64
+  TILE_GLU_256x128 = 8, // gated: 8 waves of 128 x (32 + 32)
 };
 
 hipError_t launch_col_absmax(const void* x, bool bf16, int64_t rows, int64_t k, float* amax,
@@ -52,9 +54,11 @@ hipError_t launch_pack_bf16(const void* w, int64_t n, int64_t k, void* wp, hipSt
 
 // tiled MFMA GEMM (any M); `tile` picks the block shape
 hipError_t launch_gemm_tile(bool bf16, int epi, int tile, const GemmParams& p, hipStream_t st);
-// skinny MFMA GEMM for M <= 64: weights streamed from HBM, A held in LDS
-hipError_t launch_gemm_skinny(bool bf16, int epi, int mb, int kc, const GemmParams& p,
+// streaming MFMA GEMM for M <= 128: weights streamed from HBM, A staged in
+// LDS; nw waves per workgroup, wk of them splitting one column block's K range
+hipError_t launch_gemm_stream(bool bf16, int epi, int mb, int nw, int wk, const GemmParams& p,
                               int nb_per_block, hipStream_t st);
+size_t gemm_stream_lds_bytes(int mb, int kchunk, int wk, bool glu);
 // sum of K-split partials (in split order) followed by the epilogue
 hipError_t launch_splitk_reduce(bool bf16, int epi, const GemmParams& p, hipStream_t st);
 

@@ -196,7 +196,7 @@ def test_gemm_split_k_is_bit_identical(m, n, k, splits, monkeypatch):
     A = torch.from_numpy(w8a8.rowmajor_to_frag(qa)).to(DEV)
     B = torch.from_numpy(w8a8.rowmajor_to_frag(qb)).to(DEV)
     monkeypatch.setenv("W8A8_GEMM_SPLITS", str(splits))
-    for tile in (0, 1, 2, 3):
+    for tile in (0, 1, 2, 3, 7):
         monkeypatch.setenv("W8A8_GEMM_TILE", str(tile))
         acc = w8a8.gemm_i8_i32(A, m, B, n, k)
         torch.cuda.synchronize()
@@ -263,6 +263,30 @@ def test_ffn_gate_up_geglu_stage(m):
     frac = float((ulps > 0).mean())
     say("  h mismatch fraction", frac)
     assert frac <= 1e-3
+
+
+@pytest.mark.parametrize("m", [300, 2048])
+def test_gate_up_tiles_bit_identical(m, monkeypatch):
+    """Every gated tile shape yields the same h: the int32 sums are exact and
+    the epilogue is the same binary32 sequence."""
+    say("gate/up tiles", m)
+    cfg, q, layer = _ffn_setup(m)
+    qx_o, sx_o = oracle.quantize_act(cfg["x"], q["delta_gu"])
+    qx = torch.from_numpy(w8a8.rowmajor_to_frag(qx_o)).to(DEV)
+    sx = dev_f32(sx_o)
+    ref = None
+    for tile in (4, 5, 6, 8):
+        monkeypatch.setenv("W8A8_GLU_TILE", str(tile))
+        h = host_bf16(w8a8.ffn_gate_up(layer, qx, sx, m))
+        if ref is None:
+            ref = h
+        else:
+            np.testing.assert_array_equal(h, ref, err_msg="tile %d" % tile)
+    if m == 300:   # small enough for the oracle's gate/up stage
+        g = oracle.dequant(oracle.gemm_i32(qx_o, q["wq_gate"]), sx_o, q["s_gate"])
+        u = oracle.dequant(oracle.gemm_i32(qx_o, q["wq_up"]), sx_o, q["s_up"])
+        ulps = bf16_ulp_diff(ref, oracle.f32_to_bf16(oracle.geglu(g, u)))
+        assert ulps.max() <= 1 and float((ulps > 0).mean()) <= 1e-3
 
 
 @pytest.mark.parametrize("m", [1, 8, 64, 128, 512])
