@@ -204,35 +204,19 @@ void orc_dequant(const int32_t* acc, const float* s_tok, const float* s_ch,
 /* a6  GeGLU with the tanh form of GELU (gate branch), times up         */
 /* ------------------------------------------------------------------ */
 
-/* gelu(g) = 0.5 g (1 + tanh( sqrt(2/pi) (g + 0.044715 g^3) ));  h = gelu(g) u.
-   Binary32 operations in the order written, tanh taken from binary64 libm and
-   rounded once.  The caller rounds h to bf16 (the FFN intermediate format). */
-void orc_geglu(const float* g, const float* u, int64_t n, float* h) {
-    const float c = (float)0.79788456080286535588; /* sqrt(2/pi) */
-    const float k3 = 0.044715f;
-#pragma omp parallel for schedule(static)
-    for (int64_t i = 0; i < n; ++i) {
-        float x = g[i];
-        float x2 = x * x;
-        float x3 = x2 * x;
-        float inner = x + k3 * x3;
-        float z = c * inner;
-        float t = (float)tanh((double)z);
-        float half = 0.5f * x;
-        float one_t = 1.0f + t;
-        float ge = half * one_t;
-        h[i] = ge * u[i];
-    }
-}
-
-/* Same GELU-tanh in binary64 throughout (used by the pins and by the bf16
-   reference path through orc_geglu_f64). */
+/* gelu(g) = 0.5 g (1 + tanh(z)),  z = sqrt(2/pi) (g + 0.044715 g^3);  h = gelu(g) u.
+   Binary64 throughout; the caller rounds h once to bf16 (the FFN intermediate
+   format).  The factor 1 + tanh(z) is taken as 2 / (1 + exp(-2z)), the same
+   number: written as 1 + tanh(z) it cancels for negative z and keeps no
+   correct digit below z of about -18 in binary64. */
 void orc_geglu_f64(const double* g, const double* u, int64_t n, double* h) {
     const double c = 0.79788456080286535588;
 #pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < n; ++i) {
         double x = g[i];
-        double ge = 0.5 * x * (1.0 + tanh(c * (x + 0.044715 * x * x * x)));
+        double z = c * (x + 0.044715 * x * x * x);
+        double one_plus_tanh = 2.0 / (1.0 + exp(-2.0 * z));
+        double ge = 0.5 * x * one_plus_tanh;
         h[i] = ge * u[i];
     }
 }

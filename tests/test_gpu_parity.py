@@ -285,7 +285,7 @@ def test_gate_up_tiles_bit_identical(m, monkeypatch):
     if m == 300:   # small enough for the oracle's gate/up stage
         g = oracle.dequant(oracle.gemm_i32(qx_o, q["wq_gate"]), sx_o, q["s_gate"])
         u = oracle.dequant(oracle.gemm_i32(qx_o, q["wq_up"]), sx_o, q["s_up"])
-        ulps = bf16_ulp_diff(ref, oracle.f32_to_bf16(oracle.geglu(g, u)))
+        ulps = bf16_ulp_diff(ref, oracle.f64_to_bf16(oracle.geglu(g, u)))
         assert ulps.max() <= 1 and float((ulps > 0).mean()) <= 1e-3
 
 
@@ -502,7 +502,7 @@ def test_bf16_gate_up_stage_matches_oracle():
     cfg = synth.ffn_config(m=64)
     g = oracle.linear_f64(cfg["x"], cfg["w_gate"]).astype(np.float32)
     u = oracle.linear_f64(cfg["x"], cfg["w_up"]).astype(np.float32)
-    h_o = oracle.f32_to_bf16(oracle.geglu(g, u))
+    h_o = oracle.f64_to_bf16(oracle.geglu(g, u))
     layer = w8a8.FfnBF16.from_weights(dev_bf16(cfg["w_gate"]), dev_bf16(cfg["w_up"]),
                                       dev_bf16(cfg["w_down"]))
     h = w8a8.bf16_ffn_gate_up(layer, dev_bf16(cfg["x"]))
