@@ -18,11 +18,9 @@ __device__ __forceinline__ float bf16_bits_to_float(uint32_t b) {
 }
 
 // binary32 -> bf16, round to nearest even; NaN stays a quiet NaN.
+// binary32 -> bfloat16, round to nearest even (one v_cvt_pk_bf16_f32 on gfx950)
 __device__ __forceinline__ uint16_t float_to_bf16_bits(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return 0x7fc0;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
 }
 
 __device__ __forceinline__ float wave_max(float v) {
@@ -60,16 +58,17 @@ __device__ __forceinline__ v4f mma_bf16(v4i a, v4i b, v4f c) {
 // GELU with the tanh form, binary32 operations in a fixed order (the library
 // is compiled without floating-point contraction).
 __device__ __forceinline__ float gelu_tanh(float x) {
-  const float c = 0.7978845608028654f;  // sqrt(2/pi)
+  // 0.5 x (1 + tanh(z)) equals x / (1 + 2^a) with a = -2 z log2(e): no
+  // cancellation for z < 0, one exp2 and one reciprocal, no branch.
+  // z = sqrt(2/pi) (x + 0.044715 x^3); kE = -2 sqrt(2/pi) log2(e).
+  // For a above 126 the reciprocal leaves the normal binary32 range and the
+  // result (below 2^-126 |x| in magnitude) may come out as zero.
   const float k3 = 0.044715f;
+  const float kE = -2.3022082f;
   float x2 = x * x;
-  float x3 = x2 * x;
-  float inner = x + k3 * x3;
-  float z = c * inner;
-  float t = tanhf(z);
-  float half = 0.5f * x;
-  float one_t = 1.0f + t;
-  return half * one_t;
+  float inner = x + (k3 * x2) * x;
+  float a = inner * kE;
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(a));
 }
 
 }  // namespace w8a8

@@ -309,18 +309,17 @@ __global__ __launch_bounds__(64 * NW) void gemm_tile_kernel(GemmParams p) {
   float sa[TM][4], sb[TN], sb2[GLU ? TN : 1];
   if constexpr (!BF16) {
     if (EPI != EPI_I32 && !(EPI != EPI_GLU && p.splits > 1)) {
+      // indexes clamped into range: rows and columns past the edge are
+      // computed but never stored
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = row0 + i * 16 + r;
-          sa[i][r] = row < p.M ? p.s_a[row] : 0.f;
-        }
+        for (int r = 0; r < 4; ++r) sa[i][r] = p.s_a[min(row0 + i * 16 + r, p.M - 1)];
 #pragma unroll
       for (int t = 0; t < TN; ++t) {
-        const int col = col0 + t * 16;
-        sb[t] = col < p.N ? p.s_b[col] : 0.f;
-        if constexpr (GLU) sb2[t] = col < p.N ? p.s_b2[col] : 0.f;
+        const int col = min(col0 + t * 16, p.N - 1);
+        sb[t] = p.s_b[col];
+        if constexpr (GLU) sb2[t] = p.s_b2[col];
       }
     }
   }
