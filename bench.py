@@ -48,6 +48,8 @@ def main():
     ap.add_argument("--map", default="all26")
     ap.add_argument("--no-extras", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a plain 256 MiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -58,6 +60,18 @@ def main():
 
     import torch
     from paper_2608_28003_amd import synth, w8a8
+
+    if args.copy_probe:
+        # A copy of known size: its FETCH_SIZE / WRITE_SIZE readings per
+        # dispatch convert the counters of the other kernels into bytes.
+        n = 256 << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(4):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n, "dispatches": 4}), flush=True)
+        return
 
     w8a8.lib()  # fails loudly without the HIP library
     assert torch.cuda.is_available(), "bench.py needs the GPU"
@@ -192,7 +206,8 @@ def main():
     achieved = gu_bytes / (gu_us * 1e-6) / 1e9
     roofline = {"kernel": "gemm_tile_kernel<int8, GeGLU epilogue> (FFN gate/up)",
                 "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": measured_traffic(M),
                 "avg_launch_us": round(gu_us, 3), "bytes_per_launch": gu_bytes,
                 "int8_tops": round(gu_ops / (gu_us * 1e-6) / 1e12, 1)}
     log("gate/up kernel %.2f us: %.0f GB/s" % (gu_us, achieved))
@@ -222,6 +237,27 @@ def main():
         result["cpu_baseline"] = cpu_baseline(M)
 
     print(json.dumps(result), flush=True)
+
+
+def measured_traffic(m):
+    """HBM bytes per launch of the gate/up kernel from the committed counter
+    summary, or None when it was taken at another M or on other kernel
+    sources than the ones built here."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", "gate_up_geglu_m128_hbm_traffic.md")
+    try:
+        text = open(path).read()
+        rec = json.loads(re.search(r"```json\n(.*?)\n```", text, re.S).group(1))
+    except (OSError, AttributeError, ValueError):
+        return None
+    h = hashlib.sha256()
+    for f in ("gemm.hip", "device.h", "kernels.h"):
+        with open(os.path.join(ROOT, "paper_2608_28003_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    if rec.get("m") != m or rec.get("source_sha256") != h.hexdigest():
+        return None
+    return rec["traffic_bytes"]
 
 
 def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all, w_lm, M, D, F,
