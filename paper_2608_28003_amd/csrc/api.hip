@@ -210,6 +210,32 @@ w8a8_status run_gemm(const Plan& pl, bool bf16, int epi, const void* A, int64_t 
   return hip_check(launch_splitk_reduce(bf16, epi, p, st), "splitk_reduce");
 }
 
+// The same GEMM without any reduction or dequantisation: raw sums (int32 for
+// INT8 operands, fp32 for bf16) in the plan's split-K layout
+// part[split][m][n] (one split: a plain m x n matrix), for a consumer that
+// reduces them itself.
+w8a8_status run_gemm_raw(const Plan& pl, bool bf16, const void* A, int64_t lda, int64_t m,
+                         const void* B, int64_t n, int64_t k, void* part, hipStream_t st) {
+  GemmParams p{};
+  p.A = A;
+  p.B = B;
+  p.lda = lda;
+  p.M = (int)m;
+  p.N = (int)n;
+  p.rb_a = (int)ceil_div(m, 16);
+  p.rb_b = (int)ceil_div(n, 16);
+  p.kb_count = (int)(bf16 ? ceil_div(k, kFragK16) : ceil_div(k, kFragK8));
+  p.kchunk = pl.kchunk;
+  p.splits = pl.splits;
+  p.out = part;
+  p.ldo = n;
+  p.part = pl.splits > 1 ? part : nullptr;
+  const int epi = bf16 ? EPI_F32 : EPI_I32;
+  hipError_t e = pl.stream ? launch_gemm_stream(bf16, epi, pl.mb, pl.nw, pl.wk, p, pl.nbpb, st)
+                           : launch_gemm_tile(bf16, epi, pl.tile, p, st);
+  return hip_check(e, pl.stream ? "gemm_stream" : "gemm_tile");
+}
+
 // ------------------------------------------------------------------ validation
 
 #define REQUIRE(cond, code, msg) \
@@ -299,6 +325,31 @@ Bf16FfnWs bf16_ffn_ws(int64_t m, int64_t d, int64_t f) {
 
 size_t bf16_linear_ws(int64_t m, int64_t n, int64_t k) {
   return plan_ws_bytes(plan_gemm(m, n, k, true, false), m, n);
+}
+
+// Stack workspace: token stream, next-consumer input (bf16 and codes), FFN
+// intermediates, the down projection's raw partial sums, the lm_head's GEMM
+// workspace.
+struct StackWs {
+  size_t x, a, q, s, h, qh, sh, part, lm, total;
+};
+StackWs stack_ws(int64_t m, int64_t d, int64_t f, int64_t vocab) {
+  StackWs w;
+  const Plan p8 = plan_gemm(m, d, f, false, false), p16 = plan_gemm(m, d, f, true, false);
+  const size_t part = (size_t)std::max(p8.splits, p16.splits) * m * d * 4;
+  const size_t lm = std::max(plan_ws_bytes(plan_gemm(m, vocab, d, false, false), m, vocab),
+                             bf16_linear_ws(m, vocab, d));
+  w.x = 0;
+  w.a = w.x + align256((size_t)m * d * 2);
+  w.q = w.a + align256((size_t)m * d * 2);
+  w.s = w.q + align256(w8a8_packed_bytes(m, d));
+  w.h = w.s + align256((size_t)m * 4);
+  w.qh = w.h + align256((size_t)m * f * 2);
+  w.sh = w.qh + align256(w8a8_packed_bytes(m, f));
+  w.part = w.sh + align256((size_t)m * 4);
+  w.lm = w.part + align256(part);
+  w.total = w.lm + align256(lm);
+  return w;
 }
 
 // ------------------------------------------------------------------ pipelines
@@ -395,10 +446,7 @@ size_t w8a8_lm_head_workspace_bytes(int64_t m, int64_t n, int64_t k) {
 
 size_t w8a8_stack_workspace_bytes(int64_t m, int64_t d, int64_t f, int64_t vocab) {
   if (m < 1 || d < 1 || f < 1 || vocab < 1) return 0;
-  size_t act = 3 * align256((size_t)m * d * 2);
-  size_t inner = std::max(std::max(ffn_ws(m, d, f).total, bf16_ffn_ws(m, d, f).total),
-                          std::max(linear_ws(m, vocab, d).total, bf16_linear_ws(m, vocab, d)));
-  return act + align256(inner);
+  return stack_ws(m, d, f, vocab).total;
 }
 
 const char* w8a8_status_str(w8a8_status s) {
@@ -729,25 +777,74 @@ w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec, int
 
   hipStream_t st = S(stream);
   char* base = (char*)ws;
-  const size_t act = align256((size_t)m * d * 2);
-  uint16_t* xcur = (uint16_t*)base;
-  uint16_t* a = (uint16_t*)(base + act);
-  uint16_t* fo = (uint16_t*)(base + 2 * act);
-  void* inner = base + 3 * act;
-  CHECK(hip_check(hipMemcpyAsync(xcur, x, (size_t)m * d * 2, hipMemcpyDeviceToDevice, st),
-                  "copy x"));
+  const StackWs w = stack_ws(m, d, f, desc->vocab);
+  uint16_t* xcur = (uint16_t*)(base + w.x);
+  uint16_t* a = (uint16_t*)(base + w.a);
+  int8_t* q = (int8_t*)(base + w.q);
+  float* s = (float*)(base + w.s);
+  uint16_t* h = (uint16_t*)(base + w.h);
+  int8_t* qh = (int8_t*)(base + w.qh);
+  float* sh = (float*)(base + w.sh);
+  void* part = base + w.part;
+  const Plan p8 = plan_gemm(m, d, f, false, false), p16 = plan_gemm(m, d, f, true, false);
+  const Plan pg8 = plan_gemm(m, f, d, false, true), pg16 = plan_gemm(m, f, d, true, true);
+
+  // Glue launch l (0..n_layers): FFN output of layer l-1 into the token
+  // stream (none for l = 0, which copies x in), then the pre-norm input of
+  // layer l (or of the lm_head for l = n_layers), as codes for an INT8
+  // consumer and as bf16 for a bf16 one.
+  auto glue = [&](int64_t l) -> w8a8_status {
+    GlueParams g;
+    g.m = m;
+    g.d = d;
+    g.rows_pad = round_up(m, 16);
+    g.kp = round_up(d, 64);
+    g.x_in = l == 0 ? (const uint16_t*)x : xcur;
+    g.x_out = xcur;
+    if (l > 0) {
+      const bool i8 = prec[l - 1] != 0;
+      g.part = part;
+      g.splits = i8 ? p8.splits : p16.splits;
+      g.part_f32 = !i8;
+      if (i8) {
+        g.s_t = sh;
+        g.s_i = desc->int8_ffn[l - 1].s_down;
+      }
+    }
+    const bool next_i8 = l < desc->n_layers ? prec[l] != 0 : lm_head_int8 != 0;
+    if (next_i8) {
+      g.q = q;
+      g.s = s;
+      g.delta = l < desc->n_layers ? desc->int8_ffn[l].delta_gu : desc->lm_head_int8.delta;
+    } else {
+      g.a = a;
+    }
+    return hip_check(launch_glue(g, st), "glue");
+  };
+
   for (int64_t l = 0; l < desc->n_layers; ++l) {
-    CHECK(hip_check(launch_rmsnorm(nullptr, xcur, m, d, a, st), "rmsnorm"));
-    if (prec[l])
-      CHECK(ffn_impl(&desc->int8_ffn[l], a, m, fo, inner, st));
-    else
-      CHECK(bf16_ffn_impl(&desc->bf16_ffn[l], a, m, fo, inner, st));
-    CHECK(hip_check(launch_rmsnorm(xcur, fo, m, d, xcur, st), "rmsnorm_residual"));
+    CHECK(glue(l));
+    if (prec[l]) {
+      const w8a8_ffn_desc* L = &desc->int8_ffn[l];
+      CHECK(run_gemm(pg8, false, EPI_GLU, q, 0, m, L->wq_gate, L->wq_up, f, d, s, L->s_gate,
+                     L->s_up, h, f, nullptr, st));
+      CHECK(quant_act_impl(h, true, m, f, L->delta_down, qh, sh, st));
+      CHECK(run_gemm_raw(p8, false, qh, 0, m, L->wq_down, d, f, part, st));
+    } else {
+      const w8a8_bf16_ffn_desc* L = &desc->bf16_ffn[l];
+      CHECK(run_gemm(pg16, true, EPI_GLU, a, d, m, L->wp_gate, L->wp_up, f, d, nullptr, nullptr,
+                     nullptr, h, f, nullptr, st));
+      CHECK(run_gemm_raw(p16, true, h, f, m, L->wp_down, d, f, part, st));
+    }
   }
-  CHECK(hip_check(launch_rmsnorm(nullptr, xcur, m, d, a, st), "rmsnorm"));
-  if (lm_head_int8)
-    return linear_impl(&desc->lm_head_int8, a, true, m, logits, EPI_BF16, inner, st);
-  return bf16_linear_impl(a, m, desc->lm_head_bf16, desc->vocab, d, logits, inner, st);
+  CHECK(glue(desc->n_layers));
+  const int64_t V = desc->vocab;
+  if (lm_head_int8) {
+    const Plan pl = plan_gemm(m, V, d, false, false);
+    return run_gemm(pl, false, EPI_BF16, q, 0, m, desc->lm_head_int8.wq, nullptr, V, d, s,
+                    desc->lm_head_int8.s_w, nullptr, logits, V, base + w.lm, st);
+  }
+  return bf16_linear_impl(a, m, desc->lm_head_bf16, V, d, logits, base + w.lm, st);
 }
 
 }  // extern "C"

@@ -711,6 +711,7 @@ hipError_t launch_gemm_stream(bool bf16, int epi, int mb, int nw, int wk, const 
                               int nb_per_block, hipStream_t st) {
   if (bf16) {
     switch (epi) {
+      case EPI_F32: return stream_mb<true, EPI_F32>(mb, nw, wk, p, nb_per_block, st);
       case EPI_BF16: return stream_mb<true, EPI_BF16>(mb, nw, wk, p, nb_per_block, st);
       case EPI_GLU: return stream_mb<true, EPI_GLU>(mb, nw, wk, p, nb_per_block, st);
       default: return hipErrorInvalidValue;

@@ -3,6 +3,8 @@
 //   post-norm residual x_out = bf16(x + bf16(RMSNorm(f))).
 // One workgroup per row; each thread owns an 8-element (16-byte) chunk kept in
 // registers; the sum of squares is a binary32 butterfly + LDS reduction.
+#include <algorithm>
+
 #include "device.h"
 #include "kernels.h"
 
@@ -63,6 +65,177 @@ __global__ __launch_bounds__(1024) void rmsnorm_kernel(const uint16_t* x,
   o.z = (uint32_t)b[4] | ((uint32_t)b[5] << 16);
   o.w = (uint32_t)b[6] | ((uint32_t)b[7] << 16);
   *reinterpret_cast<uint4*>(y + r * d + t * 8) = o;
+}
+
+// ------------------------------------------------------------------ fused row glue
+
+// Workgroup reductions over the per-thread values of one row; each call site
+// passes its own LDS array, so consecutive reductions need no extra barrier.
+__device__ __forceinline__ float block_sum_in(float v, float* red) {
+  v = wave_sum(v);
+  if (lane_id() == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  float s = 0.0f;
+  for (int i = 0; i < (int)(blockDim.x >> 6); ++i) s += red[i];
+  return s;
+}
+
+__device__ __forceinline__ float block_max_in(float v, float* red) {
+  v = wave_max(v);
+  if (lane_id() == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  float m = red[0];
+  for (int i = 1; i < (int)(blockDim.x >> 6); ++i) m = fmaxf(m, red[i]);
+  return m;
+}
+
+// One row r per workgroup, thread t owns columns [8t, 8t + 8).  Steps, each
+// optional and in this order (the arithmetic of every step is the one of the
+// standalone kernels: split-K reduction + dequant epilogue, rmsnorm_kernel,
+// quant_rows_kernel):
+//   1. y = FFN output from split-K partial sums (int32 with two scales, or
+//      fp32), rounded to bf16;  x_out = bf16(x_in + bf16(RMSNorm(y)));
+//      without partial sums x_out = x_in.
+//   2. a = bf16(RMSNorm(x_out)), written as bf16 and/or
+//   3. smoothed by delta and quantised per row into the fragment layout
+//      (codes q, scale s); rows in [m, rows_pad) and columns in [d, kp) of
+//      the packed output are zero.
+__global__ __launch_bounds__(1024) void glue_kernel(GlueParams g) {
+  __shared__ float red_y[16], red_x[16], red_q[16];
+  const int64_t r = blockIdx.x;
+  const int t = threadIdx.x;
+  const int64_t d = g.d;
+  const int64_t chunks = d / 8;
+  const int64_t kb_count = g.kp / kFragK8;
+  auto store_codes8 = [&](int64_t c, uint2 v) {  // 8 codes of columns [8c, 8c + 8)
+    const int64_t col = c * 8;
+    const int64_t off = frag_offset(r >> 4, col / kFragK8, kb_count) +
+                        (int64_t)((r & 15) + 16 * ((col % kFragK8) / 16)) * 16 + (col % 16);
+    *reinterpret_cast<uint2*>(g.q + off) = v;
+  };
+  if (r >= g.m) {  // padding row of the packed codes
+    for (int64_t c = t; c < g.kp / 8; c += blockDim.x) store_codes8(c, make_uint2(0, 0));
+    return;
+  }
+  const bool own = t < chunks;
+  const int64_t col0 = (int64_t)t * 8;
+  float xv[8];
+  if (own) {
+    uint4 raw = *reinterpret_cast<const uint4*>(g.x_in + r * d + col0);
+    uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      xv[2 * j] = bf16_bits_to_float(w[j] & 0xffffu);
+      xv[2 * j + 1] = bf16_bits_to_float(w[j] >> 16);
+    }
+  }
+  if (g.part) {
+    float y[8];
+    float ss = 0.0f;
+    if (own) {
+      const int64_t plane = g.m * d;
+      if (g.part_f32) {
+        const float* pp = reinterpret_cast<const float*>(g.part) + r * d + col0;
+        float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        for (int z = 0; z < g.splits; ++z) {
+          float4 a0 = *reinterpret_cast<const float4*>(pp + z * plane);
+          float4 a1 = *reinterpret_cast<const float4*>(pp + z * plane + 4);
+          acc[0] += a0.x; acc[1] += a0.y; acc[2] += a0.z; acc[3] += a0.w;
+          acc[4] += a1.x; acc[5] += a1.y; acc[6] += a1.z; acc[7] += a1.w;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) y[e] = bf16_bits_to_float(float_to_bf16_bits(acc[e]));
+      } else {
+        const int32_t* pp = reinterpret_cast<const int32_t*>(g.part) + r * d + col0;
+        int32_t acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (int z = 0; z < g.splits; ++z) {
+          int4 a0 = *reinterpret_cast<const int4*>(pp + z * plane);
+          int4 a1 = *reinterpret_cast<const int4*>(pp + z * plane + 4);
+          acc[0] += a0.x; acc[1] += a0.y; acc[2] += a0.z; acc[3] += a0.w;
+          acc[4] += a1.x; acc[5] += a1.y; acc[6] += a1.z; acc[7] += a1.w;
+        }
+        const float st = g.s_t[r];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          float v = ((float)acc[e] * st) * g.s_i[col0 + e];
+          y[e] = bf16_bits_to_float(float_to_bf16_bits(v));
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss += y[e] * y[e];
+    }
+    ss = block_sum_in(ss, red_y);
+    const float inv = 1.0f / sqrtf(ss / (float)d + 1e-6f);
+    if (own) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float b = bf16_bits_to_float(float_to_bf16_bits(y[e] * inv));
+        xv[e] = bf16_bits_to_float(float_to_bf16_bits(xv[e] + b));
+      }
+    }
+  }
+  if (own && g.x_out && (g.part || g.x_out != g.x_in)) {
+    uint4 o;
+    o.x = (uint32_t)float_to_bf16_bits(xv[0]) | ((uint32_t)float_to_bf16_bits(xv[1]) << 16);
+    o.y = (uint32_t)float_to_bf16_bits(xv[2]) | ((uint32_t)float_to_bf16_bits(xv[3]) << 16);
+    o.z = (uint32_t)float_to_bf16_bits(xv[4]) | ((uint32_t)float_to_bf16_bits(xv[5]) << 16);
+    o.w = (uint32_t)float_to_bf16_bits(xv[6]) | ((uint32_t)float_to_bf16_bits(xv[7]) << 16);
+    *reinterpret_cast<uint4*>(g.x_out + r * d + col0) = o;
+  }
+  if (!g.a && !g.q) return;  // uniform over the workgroup
+  float ss = 0.0f;
+  if (own) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss += xv[e] * xv[e];
+  }
+  ss = block_sum_in(ss, red_x);
+  const float inv = 1.0f / sqrtf(ss / (float)d + 1e-6f);
+  float a[8];
+  if (own) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) a[e] = bf16_bits_to_float(float_to_bf16_bits(xv[e] * inv));
+    if (g.a) {
+      uint4 o;
+      o.x = (uint32_t)float_to_bf16_bits(a[0]) | ((uint32_t)float_to_bf16_bits(a[1]) << 16);
+      o.y = (uint32_t)float_to_bf16_bits(a[2]) | ((uint32_t)float_to_bf16_bits(a[3]) << 16);
+      o.z = (uint32_t)float_to_bf16_bits(a[4]) | ((uint32_t)float_to_bf16_bits(a[5]) << 16);
+      o.w = (uint32_t)float_to_bf16_bits(a[6]) | ((uint32_t)float_to_bf16_bits(a[7]) << 16);
+      *reinterpret_cast<uint4*>(g.a + r * d + col0) = o;
+    }
+  }
+  if (!g.q) return;
+  float amax = 0.0f;
+  if (own) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      if (g.delta) a[e] = a[e] / g.delta[col0 + e];
+      amax = fmaxf(amax, fabsf(a[e]));
+    }
+  }
+  amax = block_max_in(amax, red_q);
+  const float sr = amax / 127.0f;
+  if (t == 0) g.s[r] = sr;
+  const float sinv = 1.0f / sr;
+  const bool fast = isfinite(sinv);
+  for (int64_t c = t; c < g.kp / 8; c += blockDim.x) {
+    uint32_t lo = 0, hi = 0;
+    if (c == t && own && sr != 0.0f) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        lo |= ((uint32_t)code_of(a[e], sr, sinv, fast) & 0xffu) << (8 * e);
+        hi |= ((uint32_t)code_of(a[e + 4], sr, sinv, fast) & 0xffu) << (8 * e);
+      }
+    }
+    store_codes8(c, make_uint2(lo, hi));
+  }
+}
+
+hipError_t launch_glue(const GlueParams& g, hipStream_t st) {
+  const int64_t rows = g.q ? g.rows_pad : g.m;
+  const int64_t per_row = std::max(g.d / 8, g.q ? g.kp / 8 : 0);
+  const int64_t threads = std::min<int64_t>((per_row + 63) / 64 * 64, 1024);
+  glue_kernel<<<(unsigned)rows, (unsigned)threads, 0, st>>>(g);
+  return hipGetLastError();
 }
 
 hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* f, int64_t m, int64_t d,

@@ -65,4 +65,24 @@ hipError_t launch_splitk_reduce(bool bf16, int epi, const GemmParams& p, hipStre
 hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* f, int64_t m, int64_t d,
                           uint16_t* y, hipStream_t st);
 
+// Row glue between FFN blocks of the stack (one launch per layer boundary):
+// FFN output from split-K partial sums -> post-norm residual update of the
+// token stream -> pre-norm of the next consumer, as bf16 and/or INT8 codes.
+struct GlueParams {
+  int64_t m = 0, d = 0;
+  int64_t rows_pad = 0, kp = 0;        // packed code shape (q only)
+  const uint16_t* x_in = nullptr;      // token stream in, bf16 m x d
+  uint16_t* x_out = nullptr;           // token stream out (may alias x_in)
+  const void* part = nullptr;          // splits x m x d partial sums, or null
+  int splits = 1;
+  bool part_f32 = false;               // fp32 partials (bf16 layer) or int32 (INT8 layer)
+  const float* s_t = nullptr;          // int32 partials: per-token scale
+  const float* s_i = nullptr;          //                 per-column scale
+  uint16_t* a = nullptr;               // pre-norm output, bf16 m x d (optional)
+  const float* delta = nullptr;        // smoothing of the INT8 consumer (may be null)
+  int8_t* q = nullptr;                 // packed codes of the pre-norm output (optional)
+  float* s = nullptr;                  // their per-row scales
+};
+hipError_t launch_glue(const GlueParams& g, hipStream_t st);
+
 }  // namespace w8a8

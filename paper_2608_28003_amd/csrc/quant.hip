@@ -96,28 +96,6 @@ __device__ __forceinline__ float block_max(float v) {
   return m;
 }
 
-// q = rne(v / s) clamped to [-127, 127], with v / s the correctly rounded
-// binary32 quotient.  Fast path: v * inv with inv = 1/s differs from v / s by at
-// most 2.3e-5 for |v / s| <= 127.5 (two roundings of 2^-24 each plus the one of
-// the quotient), so whenever v * inv is more than 2^-10 away from a half-integer
-// both round to the same integer; otherwise (or when inv is not finite) the
-// exact quotient is formed.
-__device__ __forceinline__ int8_t code_of(float v, float s, float inv, bool fast) {
-  float c;
-  if (fast) {
-    float q = v * inv;
-    float fr = fabsf(q - truncf(q));
-    if (fabsf(fr - 0.5f) > 0.0009765625f)
-      c = rintf(q);
-    else
-      c = rintf(v / s);
-  } else {
-    c = rintf(v / s);
-  }
-  c = fminf(fmaxf(c, -127.0f), 127.0f);
-  return (int8_t)(int)c;
-}
-
 template <typename T, bool MUL>
 __device__ __forceinline__ void smooth16(const T* __restrict__ xr, const float* __restrict__ delta,
                                          int64_t c, float (&v)[16]) {

@@ -471,6 +471,43 @@ def test_stack_precision_map_matches_oracle():
         assert err <= 1e-2
 
 
+@pytest.mark.parametrize("m", [16, 128, 300])
+def test_stack_fused_glue_equals_composition(m):
+    """The stack fuses each layer boundary (split-K reduction, dequant,
+    post-norm residual, next pre-norm and its quantisation) into one launch;
+    the result must equal, bit for bit, the chain of standalone entry points
+    (rmsnorm -> ffn / bf16_ffn -> rmsnorm_residual -> ... -> rmsnorm ->
+    lm_head / bf16_linear)."""
+    say("stack fused glue vs composition", m)
+    n_layers, vocab = 4, 4096
+    cfg = synth.stack_config(m=m, n_layers=n_layers, vocab=vocab)
+    torch.manual_seed(7)
+    i8, bf = [], []
+    for L in cfg["layers"]:
+        wg, wu, wd = dev_bf16(L["w_gate"]), dev_bf16(L["w_up"]), dev_bf16(L["w_down"])
+        d_gu = (torch.rand(1152, device=DEV) + 0.5).contiguous()
+        d_dn = (torch.rand(6912, device=DEV) + 0.5).contiguous()
+        i8.append(w8a8.FfnW8A8.from_weights(wg, wu, wd, d_gu, d_dn))
+        bf.append(w8a8.FfnBF16.from_weights(wg, wu, wd))
+    w_lm = dev_bf16(cfg["w_lm"])
+    lm8 = w8a8.LinearW8A8.from_weight(w_lm, (torch.rand(1152, device=DEV) + 0.5).contiguous())
+    lm16 = w8a8.pack_bf16(w_lm)
+    stack = w8a8.Stack(i8, bf, lm8, lm16, vocab)
+    x = dev_bf16(cfg["x"])
+    for prec, lm_int8 in [([1, 0, 0, 1], True), ([0, 1, 1, 0], False), ([1, 1, 1, 1], True)]:
+        prec = np.array(prec, np.uint8)
+        y = host_bf16(stack.run(x, prec, lm_int8))
+        xc = x.clone()
+        for l in range(n_layers):
+            a = w8a8.rmsnorm(xc)
+            f = w8a8.ffn(i8[l], a) if prec[l] else w8a8.bf16_ffn(bf[l], a)
+            xc = w8a8.rmsnorm_residual(xc, f)
+        a = w8a8.rmsnorm(xc)
+        ref = w8a8.lm_head(lm8, a) if lm_int8 else w8a8.bf16_linear(a, lm16, vocab, 1152)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(y, host_bf16(ref), err_msg="map %s" % prec)
+
+
 # ------------------------------------------------------------------ graph replay
 
 def test_graph_replay_matches_eager():
