@@ -76,7 +76,8 @@ int64_t tiles_of(int tile, int64_t m, int64_t n) {
 // Streaming plan for M <= 128, or false if the A panel cannot fit in LDS.
 bool plan_stream(Plan& p, int64_t m, int64_t n, int64_t kb, bool glu) {
   const int64_t nbc = ceil_div(n, 16);
-  const int64_t lds_kb = 160;  // LDS per workgroup, KiB (one fragment = 1 KiB)
+  const int64_t lds_kb = 158;  // dynamic LDS per workgroup, KiB (one fragment = 1 KiB); the
+                               // kernel's static LDS (scales, reduction scratch) takes the rest
   p.mb = m <= 16 ? 1 : (m <= 32 ? 2 : (m <= 64 ? 4 : 8));
   auto lds = [&](int64_t kchunk, int wk) { return p.mb * kchunk + (wk - 1) * (glu ? 2 : 1) * p.mb; };
   if (glu) {  // gate/up pair: no K split across workgroups (the epilogue needs full sums)
@@ -95,11 +96,12 @@ bool plan_stream(Plan& p, int64_t m, int64_t n, int64_t kb, bool glu) {
   if (nbc >= 1024) {  // wide output (lm_head): every wave owns its column blocks
     if (p.mb * kb > 144) return false;
     p.wk = 1;
-    p.nw = p.mb == 1 ? 1 : 4;
+    p.nw = env_int("W8A8_WIDE_NW", 4);
     p.splits = 1;
     p.kchunk = (int)kb;
-    p.nbpb = p.nw == 1 ? (int)std::max<int64_t>(1, ceil_div(nbc, 2048))
-                       : (int)round_up(std::max<int64_t>(4, ceil_div(nbc, 512)), 4);
+    const int64_t wgs = env_int("W8A8_WIDE_WGS", 512);
+    p.nbpb = p.nw == 1 ? (int)std::max<int64_t>(1, ceil_div(nbc, wgs))
+                       : (int)round_up(std::max<int64_t>(4, ceil_div(nbc, wgs)), 4);
     return true;
   }
   // narrow output, long K (down projection): waves of a workgroup split one
@@ -181,11 +183,30 @@ size_t plan_ws_bytes(const Plan& p, int64_t m, int64_t n) {
 // Run one GEMM with a plan.  A: packed codes (int8) or row-major bf16;
 // B (and B2 for the gated epilogue): packed weights.  A K-split plan writes
 // partial sums to gemm_ws and a second launch reduces them into `out`.
+// Quantise-on-load source of a GEMM's A operand (bf16 rows), see GemmParams.
+struct QLoad {
+  const uint16_t* x = nullptr;
+  const float* delta = nullptr;
+  float* s_out = nullptr;  // where to leave the per-row scales (optional)
+};
+
+// Streaming int8 plans over at most 16 rows quantise their bf16 input
+// themselves; every other plan reads codes produced by quant_rows_kernel.
+bool plan_qloads(const Plan& pl, int64_t m, int64_t k) {
+  if (env_int("W8A8_NO_QLOAD", 0)) return false;
+  return pl.stream && pl.mb == 1 && m * (k / 16) <= qload_capacity(pl.nw);
+}
+
 w8a8_status run_gemm(const Plan& pl, bool bf16, int epi, const void* A, int64_t lda, int64_t m,
                      const void* B, const void* B2, int64_t n, int64_t k, const float* s_a,
                      const float* s_b, const float* s_b2, void* out, int64_t ldo, void* gemm_ws,
-                     hipStream_t st) {
+                     hipStream_t st, QLoad ql = QLoad()) {
   GemmParams p{};
+  p.a_x = ql.x;
+  p.a_delta = ql.delta;
+  p.a_ld = k;
+  p.a_k = (int)k;
+  p.a_s_out = ql.s_out;
   p.A = A;
   p.B = B;
   p.B2 = B2;
@@ -215,8 +236,14 @@ w8a8_status run_gemm(const Plan& pl, bool bf16, int epi, const void* A, int64_t 
 // part[split][m][n] (one split: a plain m x n matrix), for a consumer that
 // reduces them itself.
 w8a8_status run_gemm_raw(const Plan& pl, bool bf16, const void* A, int64_t lda, int64_t m,
-                         const void* B, int64_t n, int64_t k, void* part, hipStream_t st) {
+                         const void* B, int64_t n, int64_t k, void* part, hipStream_t st,
+                         QLoad ql = QLoad()) {
   GemmParams p{};
+  p.a_x = ql.x;
+  p.a_delta = ql.delta;
+  p.a_ld = k;
+  p.a_k = (int)k;
+  p.a_s_out = ql.s_out;
   p.A = A;
   p.B = B;
   p.lda = lda;
@@ -365,6 +392,9 @@ w8a8_status linear_impl(const w8a8_linear_desc* d, const void* x, bool x_bf16, i
   LinearWs w = linear_ws(m, d->n, d->k);
   char* base = (char*)ws;
   Plan pl = plan_gemm(m, d->n, d->k, false, false);
+  if (x_bf16 && plan_qloads(pl, m, d->k))  // one launch: the GEMM quantises x itself
+    return run_gemm(pl, false, epi, nullptr, 0, m, d->wq, nullptr, d->n, d->k, nullptr, d->s_w,
+                    nullptr, y, d->n, base + w.gemm, st, QLoad{(const uint16_t*)x, d->delta});
   CHECK(quant_act_impl(x, x_bf16, m, d->k, d->delta, base + w.qx, (float*)(base + w.sx), st));
   return run_gemm(pl, false, epi, base + w.qx, 0, m, d->wq, nullptr, d->n, d->k,
                   (const float*)(base + w.sx), d->s_w, nullptr, y, d->n, base + w.gemm, st);
@@ -374,11 +404,22 @@ w8a8_status ffn_impl(const w8a8_ffn_desc* d, const void* x, int64_t m, void* y, 
                      hipStream_t st) {
   FfnWs w = ffn_ws(m, d->d, d->f);
   char* base = (char*)ws;
-  CHECK(quant_act_impl(x, true, m, d->d, d->delta_gu, base + w.qx, (float*)(base + w.sx), st));
   Plan pg = plan_gemm(m, d->f, d->d, false, true);
-  CHECK(run_gemm(pg, false, EPI_GLU, base + w.qx, 0, m, d->wq_gate, d->wq_up, d->f, d->d,
-                 (const float*)(base + w.sx), d->s_gate, d->s_up, base + w.h, d->f, nullptr, st));
+  if (plan_qloads(pg, m, d->d)) {
+    CHECK(run_gemm(pg, false, EPI_GLU, nullptr, 0, m, d->wq_gate, d->wq_up, d->f, d->d, nullptr,
+                   d->s_gate, d->s_up, base + w.h, d->f, nullptr, st,
+                   QLoad{(const uint16_t*)x, d->delta_gu}));
+  } else {
+    CHECK(quant_act_impl(x, true, m, d->d, d->delta_gu, base + w.qx, (float*)(base + w.sx), st));
+    CHECK(run_gemm(pg, false, EPI_GLU, base + w.qx, 0, m, d->wq_gate, d->wq_up, d->f, d->d,
+                   (const float*)(base + w.sx), d->s_gate, d->s_up, base + w.h, d->f, nullptr,
+                   st));
+  }
   Plan pd = plan_gemm(m, d->d, d->f, false, false);
+  if (plan_qloads(pd, m, d->f))
+    return run_gemm(pd, false, EPI_BF16, nullptr, 0, m, d->wq_down, nullptr, d->d, d->f, nullptr,
+                    d->s_down, nullptr, y, d->d, base + w.gemm, st,
+                    QLoad{(const uint16_t*)(base + w.h), d->delta_down});
   CHECK(quant_act_impl(base + w.h, true, m, d->f, d->delta_down, base + w.qh,
                        (float*)(base + w.sh), st));
   return run_gemm(pd, false, EPI_BF16, base + w.qh, 0, m, d->wq_down, nullptr, d->d, d->f,
@@ -828,8 +869,13 @@ w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec, int
       const w8a8_ffn_desc* L = &desc->int8_ffn[l];
       CHECK(run_gemm(pg8, false, EPI_GLU, q, 0, m, L->wq_gate, L->wq_up, f, d, s, L->s_gate,
                      L->s_up, h, f, nullptr, st));
-      CHECK(quant_act_impl(h, true, m, f, L->delta_down, qh, sh, st));
-      CHECK(run_gemm_raw(p8, false, qh, 0, m, L->wq_down, d, f, part, st));
+      if (plan_qloads(p8, m, f)) {
+        CHECK(run_gemm_raw(p8, false, nullptr, 0, m, L->wq_down, d, f, part, st,
+                           QLoad{h, L->delta_down, sh}));
+      } else {
+        CHECK(quant_act_impl(h, true, m, f, L->delta_down, qh, sh, st));
+        CHECK(run_gemm_raw(p8, false, qh, 0, m, L->wq_down, d, f, part, st));
+      }
     } else {
       const w8a8_bf16_ffn_desc* L = &desc->bf16_ffn[l];
       CHECK(run_gemm(pg16, true, EPI_GLU, a, d, m, L->wp_gate, L->wp_up, f, d, nullptr, nullptr,

@@ -403,6 +403,93 @@ __global__ __launch_bounds__(64 * NW) void gemm_tile_kernel(GemmParams p) {
 // double buffered in registers, so the loads of batch i+1 are in flight while
 // the MFMAs (MB per fragment) and the epilogue of batch i run.  Cross-workgroup
 // K splits (a grid dimension) write partial sums for the reduction kernel.
+// Quantise-on-load of at most 16 bf16 rows for one streaming workgroup:
+// x_hat = x / delta, per-row scale s = max|x_hat| / 127 over the whole row,
+// codes as quant_rows_kernel computes them (same binary32 operations), for the
+// workgroup's fragment columns [kb0, kb0 + kc) into LDS (rows >= M and columns
+// >= a_k are zero codes).  Each thread loads whole 16-column groups once (at
+// most MAXG of them, which the host guarantees: M * a_k / 16 <= MAXG * 64 * NW)
+// and keeps the smoothed values in registers between the absmax and the
+// rounding.  One group per thread: with more, the redundant per-workgroup
+// divisions cost more than the separate quantisation launch they replace.  The caller's barrier publishes lds_a and s_row.
+template <int NW>
+constexpr int qload_max_groups() { return 1; }
+
+template <int NW>
+__device__ __forceinline__ void quantize_panel(const GemmParams& p, int kb0, int kc, v4i* lds_a,
+                                               float* s_row) {
+  constexpr int NT = NW * 64;
+  constexpr int MAXG = qload_max_groups<NW>();
+  __shared__ unsigned int amax_bits[16];
+  const int tid = threadIdx.x;
+  const int rows = min(p.M, 16);
+  const int G = p.a_k / 16;  // 16-column groups per row
+  float v[MAXG][16];
+  float mx[MAXG];
+#pragma unroll
+  for (int i = 0; i < MAXG; ++i) {
+    const int gi = tid + i * NT;
+    mx[i] = 0.0f;
+    if (gi < rows * G) {
+      const int r = gi / G, c0 = (gi % G) * 16;
+      const uint16_t* xr = p.a_x + (int64_t)r * p.a_ld + c0;
+      const uint4 r0 = *reinterpret_cast<const uint4*>(xr);
+      const uint4 r1 = *reinterpret_cast<const uint4*>(xr + 8);
+      const uint32_t w[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        v[i][e] = bf16_bits_to_float((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xffffu));
+      if (p.a_delta) {
+        const float4* dp = reinterpret_cast<const float4*>(p.a_delta + c0);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 d4 = dp[q];
+          v[i][4 * q + 0] = v[i][4 * q + 0] / d4.x;
+          v[i][4 * q + 1] = v[i][4 * q + 1] / d4.y;
+          v[i][4 * q + 2] = v[i][4 * q + 2] / d4.z;
+          v[i][4 * q + 3] = v[i][4 * q + 3] / d4.w;
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mx[i] = fmaxf(mx[i], fabsf(v[i][e]));
+    }
+  }
+  // zero codes everywhere first (padding rows and columns stay zero)
+  for (int idx = tid; idx < kc * 64; idx += NT) lds_a[idx] = v4i{0, 0, 0, 0};
+  if (tid < 16) amax_bits[tid] = 0u;
+  __syncthreads();
+  // non-negative binary32 values order like their bit patterns: the maximum
+  // does not depend on the order of the atomic updates
+#pragma unroll
+  for (int i = 0; i < MAXG; ++i) {
+    const int gi = tid + i * NT;
+    if (gi < rows * G) atomicMax(&amax_bits[gi / G], __float_as_uint(mx[i]));
+  }
+  __syncthreads();
+  if (tid < rows) {
+    const float s = __uint_as_float(amax_bits[tid]) / 127.0f;
+    s_row[tid] = s;
+    if (p.a_s_out && blockIdx.x == 0 && blockIdx.y == 0) p.a_s_out[tid] = s;
+  }
+#pragma unroll
+  for (int i = 0; i < MAXG; ++i) {
+    const int gi = tid + i * NT;
+    if (gi >= rows * G) continue;
+    const int r = gi / G, g = gi % G;
+    const int f = g / 4 - kb0;
+    if (f < 0 || f >= kc) continue;
+    const float sr = __uint_as_float(amax_bits[r]) / 127.0f;
+    if (sr == 0.0f) continue;
+    const float inv = 1.0f / sr;
+    const bool fast = isfinite(inv);
+    int32_t packed[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      packed[e >> 2] |= ((int32_t)code_of(v[i][e], sr, inv, fast) & 0xff) << (8 * (e & 3));
+    lds_a[f * 64 + r + 16 * (g & 3)] = v4i{packed[0], packed[1], packed[2], packed[3]};
+  }
+}
+
 template <bool BF16, int MB, int EPI, int NW, int WK>
 __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int nb_per_block) {
   static_assert(WK == 1 || WK == NW, "either every wave owns its column blocks or all share one");
@@ -447,15 +534,19 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
              frag_offset(min(mb, p.rb_a - 1), kb0 + kk, p.kb_count) + lane * 16;
     }
   };
-  if constexpr (WK > 1) {
-    for (int f = 0; f < MB * my_k; ++f) {
-      const int mb = f / my_k, kk = ks0 + f % my_k;
-      to_lds_async(a_src(mb, kk), &lds_a[(mb * p.kchunk + kk) * 64]);
-    }
-  } else {
-    for (int f = wave; f < MB * kc; f += NW) {
-      const int mb = f / kc, kk = f % kc;
-      to_lds_async(a_src(mb, kk), &lds_a[(mb * p.kchunk + kk) * 64]);
+  constexpr bool QLOAD_OK = !BF16 && MB == 1;
+  const bool qload = QLOAD_OK && p.a_x != nullptr;
+  if (!qload) {
+    if constexpr (WK > 1) {
+      for (int f = 0; f < MB * my_k; ++f) {
+        const int mb = f / my_k, kk = ks0 + f % my_k;
+        to_lds_async(a_src(mb, kk), &lds_a[(mb * p.kchunk + kk) * 64]);
+      }
+    } else {
+      for (int f = wave; f < MB * kc; f += NW) {
+        const int mb = f / kc, kk = f % kc;
+        to_lds_async(a_src(mb, kk), &lds_a[(mb * p.kchunk + kk) * 64]);
+      }
     }
   }
 
@@ -472,8 +563,27 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
     }
   };
   if (total > 0) load_batch(0, b0, u0);  // first weights go out with the A fragments
+  __shared__ float s_row[16];             // quantise-on-load: per-row scales
+  if constexpr (QLOAD_OK) {
+    if (qload) quantize_panel<NW>(p, kb0, kc, lds_a, s_row);  // overlaps the first weight loads
+  }
   wait_vmcnt<0>();
-  if (WK == 1 && NW > 1) lds_barrier();  // the shared panel is read by every wave
+  if ((WK == 1 && NW > 1) || qload) lds_barrier();  // the shared panel is read by every wave
+  // Scales live in registers: the token scales of this lane's rows from the
+  // start, the channel scales of a column block loaded with its first weights
+  // (their latency then hides behind that block's products).
+  const bool scaled = !BF16 && (GLU || ((EPI == EPI_F32 || EPI == EPI_BF16) && p.splits == 1));
+  float sa_r[MB][4];
+  float sb_c = 0.0f, sb2_c = 0.0f;
+  if (scaled) {
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = min(mb * 16 + (lane >> 4) * 4 + r, p.M - 1);
+        sa_r[mb][r] = qload ? s_row[row] : p.s_a[row];
+      }
+  }
 
   AccT acc[MB], accu[GLU ? MB : 1];
   auto epilogue = [&](int nb) {
@@ -484,12 +594,31 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
       for (int r = 0; r < 4; ++r) {
         const int row = mb * 16 + (lane >> 4) * 4 + r;
         if (row >= p.M || col >= p.N) continue;
+        const int64_t o = (int64_t)row * p.ldo + col;
         if constexpr (GLU) {
-          store_glu<BF16>(p, row, col, (float)acc[mb][r], (float)accu[mb][r]);
+          float gv, uv;
+          if constexpr (BF16) {
+            gv = (float)acc[mb][r];
+            uv = (float)accu[mb][r];
+          } else {
+            gv = ((float)acc[mb][r] * sa_r[mb][r]) * sb_c;
+            uv = ((float)accu[mb][r] * sa_r[mb][r]) * sb2_c;
+          }
+          reinterpret_cast<uint16_t*>(p.out)[o] = float_to_bf16_bits(gelu_tanh(gv) * uv);
         } else if (p.splits > 1) {
           write_partial<BF16>(p, z, row, col, BF16 ? 0 : (int32_t)acc[mb][r], (float)acc[mb][r]);
+        } else if constexpr (EPI == EPI_I32) {
+          reinterpret_cast<int32_t*>(p.out)[o] = (int32_t)acc[mb][r];
         } else {
-          store_elem<BF16, EPI>(p, row, col, BF16 ? 0 : (int32_t)acc[mb][r], (float)acc[mb][r]);
+          float y;
+          if constexpr (BF16)
+            y = (float)acc[mb][r];
+          else
+            y = ((float)acc[mb][r] * sa_r[mb][r]) * sb_c;
+          if constexpr (EPI == EPI_F32)
+            reinterpret_cast<float*>(p.out)[o] = y;
+          else
+            reinterpret_cast<uint16_t*>(p.out)[o] = float_to_bf16_bits(y);
         }
       }
   };
@@ -502,6 +631,11 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
       for (int mb = 0; mb < MB; ++mb) {
         acc[mb] = Acc<BF16>::zero();
         if constexpr (GLU) accu[mb] = Acc<BF16>::zero();
+      }
+      if (scaled) {
+        const int col = min(nb * 16 + (lane & 15), p.N - 1);
+        sb_c = p.s_b[col];
+        if constexpr (GLU) sb2_c = p.s_b2[col];
       }
     }
 #pragma unroll
@@ -663,15 +797,21 @@ static size_t stream_lds_bytes(int mb, int kchunk, int wk, bool glu) {
 template <bool BF16, int MB, int EPI, int NW, int WK>
 static hipError_t stream_launch(const GemmParams& p, int nbpb, hipStream_t st) {
   auto kern = gemm_stream_kernel<BF16, MB, EPI, NW, WK>;
-  static bool attr_set = false;  // benign race: every caller sets the same value
+  static size_t static_lds = 0;  // benign race: every caller computes the same values
+  static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    hipFuncAttributes fa;
+    hipError_t e = hipFuncGetAttributes(&fa, reinterpret_cast<const void*>(kern));
+    if (e != hipSuccess) return e;
+    static_lds = fa.sharedSizeBytes;
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                            hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)(160 * 1024 - static_lds));
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   const size_t lds = stream_lds_bytes(MB, p.kchunk, WK, EPI == EPI_GLU);
-  if (lds > 160 * 1024) return hipErrorInvalidValue;
+  if (lds + static_lds > 160 * 1024) return hipErrorInvalidValue;
   const int groups = NW / WK;
   dim3 grid((unsigned)((p.rb_b + nbpb - 1) / nbpb), (unsigned)p.splits);
   (void)groups;
@@ -690,7 +830,7 @@ static hipError_t stream_waves(int nw, int wk, const GemmParams& p, int nbpb, hi
   if constexpr (MB <= 4 || EPI != EPI_GLU) {
     if (nw == 4 && wk == 4) return stream_launch<BF16, MB, EPI, 4, 4>(p, nbpb, st);
   }
-  if constexpr (MB == 1) {
+  if constexpr (MB == 1 && EPI != EPI_GLU) {  // the gated 16-wave variant would spill
     if (nw == 16 && wk == 16) return stream_launch<BF16, MB, EPI, 16, 16>(p, nbpb, st);
   }
   return hipErrorInvalidValue;

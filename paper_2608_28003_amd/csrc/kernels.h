@@ -28,6 +28,15 @@ struct GemmParams {
   void* out;              // int32 / f32 / bf16 output
   int64_t ldo;            // row stride of out in elements
   void* part;             // K-split partial sums: splits x M x N (int32 or f32)
+  // Quantise-on-load (streaming kernel, int8 path, at most 16 rows): when
+  // a_x is set, A is not read; every workgroup smooths and quantises the bf16
+  // rows a_x itself (per-row absmax over all a_k columns, then its own K
+  // range into LDS) and uses the resulting per-row scales in its epilogue.
+  const uint16_t* a_x = nullptr;
+  const float* a_delta = nullptr;  // may be null (no smoothing)
+  int64_t a_ld = 0;                // row stride of a_x in elements
+  int a_k = 0;                     // logical columns of a_x
+  float* a_s_out = nullptr;        // optional: the per-row scales, written once
 };
 
 // tile shapes selectable at run time
@@ -56,6 +65,8 @@ hipError_t launch_pack_bf16(const void* w, int64_t n, int64_t k, void* wp, hipSt
 hipError_t launch_gemm_tile(bool bf16, int epi, int tile, const GemmParams& p, hipStream_t st);
 // streaming MFMA GEMM for M <= 128: weights streamed from HBM, A staged in
 // LDS; nw waves per workgroup, wk of them splitting one column block's K range
+// Largest M * K / 16 a streaming workgroup of nw waves can quantise on load.
+inline int64_t qload_capacity(int nw) { return (int64_t)64 * nw; }
 hipError_t launch_gemm_stream(bool bf16, int epi, int mb, int nw, int wk, const GemmParams& p,
                               int nb_per_block, hipStream_t st);
 size_t gemm_stream_lds_bytes(int mb, int kchunk, int wk, bool glu);

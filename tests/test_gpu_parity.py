@@ -471,7 +471,27 @@ def test_stack_precision_map_matches_oracle():
         assert err <= 1e-2
 
 
-@pytest.mark.parametrize("m", [16, 128, 300])
+@pytest.mark.parametrize("m", [1, 2, 5])
+def test_quantise_on_load_equals_separate_quantisation(m, monkeypatch):
+    """At decode sizes the streaming GEMM quantises its bf16 input itself; its
+    codes and scales, hence every output, must equal those of the separate
+    quantisation launch (the tuning switch W8A8_NO_QLOAD forces the latter)."""
+    say("quantise-on-load", m)
+    cfg, q, layer = _ffn_setup(m)
+    x = dev_bf16(cfg["x"])
+    lm_cfg = synth.lm_head_config(m=m, vocab=8192)
+    lm = w8a8.LinearW8A8.from_weight(dev_bf16(lm_cfg["w"]),
+                                     dev_f32(oracle.smooth_calibrate(lm_cfg["x_cal"], [lm_cfg["w"]])))
+    xl = dev_bf16(lm_cfg["x"])
+    outs = []
+    for flag in ("0", "1"):
+        monkeypatch.setenv("W8A8_NO_QLOAD", flag)
+        outs.append((host_bf16(w8a8.ffn(layer, x)), host_bf16(w8a8.lm_head(lm, xl))))
+    np.testing.assert_array_equal(outs[0][0], outs[1][0])
+    np.testing.assert_array_equal(outs[0][1], outs[1][1])
+
+
+@pytest.mark.parametrize("m", [1, 16, 128, 300])
 def test_stack_fused_glue_equals_composition(m):
     """The stack fuses each layer boundary (split-K reduction, dequant,
     post-norm residual, next pre-norm and its quantisation) into one launch;
