@@ -185,22 +185,25 @@ def main():
 
     # ------------------------------------------------------------ dominant kernel roofline
     # INT8 gate/up GEMM with the fused GeGLU epilogue, same shapes and launch
-    # configuration as inside the step, timed per launch with HIP events on the
-    # stream the library launches on (torch's current stream).
+    # configuration as inside the step: a captured graph of its 26 per-layer
+    # launches (back to back, as in the step) is replayed between two HIP
+    # events recorded on the stream the library launches on (torch's current
+    # stream); the average launch duration is the elapsed time / launches.
     qx, sx = w8a8.quantize_act(x, int8_layers[0].gate.delta)
     h = torch.empty((M, F), dtype=torch.bfloat16, device=dev)
-    reps = 4
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(NL * reps)]
-    for L in int8_layers:
-        w8a8.ffn_gate_up(L, qx, sx, M, out=h)
+    g_gu = make_graph(lambda: [w8a8.ffn_gate_up(L, qx, sx, M, out=h) for L in int8_layers])
+    reps = 20
+    for _ in range(3):
+        g_gu.replay()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    for i, (e0, e1) in enumerate(evs):
-        e0.record()
-        w8a8.ffn_gate_up(int8_layers[i % NL], qx, sx, M, out=h)
-        e1.record()
+    e0.record()
+    for _ in range(reps):
+        g_gu.replay()
+    e1.record()
     torch.cuda.synchronize()
-    gu_us = float(np.mean([e0.elapsed_time(e1) for e0, e1 in evs])) * 1e3
+    gu_us = e0.elapsed_time(e1) * 1e3 / (reps * NL)
+    del g_gu
     gu_bytes = 2 * F * D + 2 * F * 4 + M * D + M * 4 + M * F * 2
     gu_ops = 2.0 * M * D * 2 * F
     achieved = gu_bytes / (gu_us * 1e-6) / 1e9

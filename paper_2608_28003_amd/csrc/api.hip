@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <cstdint>
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <string>
@@ -63,6 +64,11 @@ void tile_shape(int tile, int* bm, int* bn) {
     case TILE_GLU_128x64: *bm = 128; *bn = 64; break;
     case TILE_256x256: *bm = 256; *bn = 256; break;
     case TILE_GLU_256x128: *bm = 256; *bn = 128; break;
+    case TILE_GLU_128x32_K2: *bm = 128; *bn = 32; break;
+    case TILE_64x64_K2: *bm = 64; *bn = 64; break;
+    case TILE_128x128_K2: *bm = 128; *bn = 128; break;
+    case TILE_GLU_64x64_K2: *bm = 64; *bn = 64; break;
+    case TILE_GLU_256x64: *bm = 256; *bn = 64; break;
     default: *bm = 128; *bn = 128;
   }
 }
@@ -149,10 +155,26 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, bool bf16, bool glu) {
     p.stream = true;
     return p;
   }
+  if (glu && m <= 128) {  // experiment hook: "nw,wk,nbpb" forces a streaming plan
+    const char* f = std::getenv("W8A8_GLU_STREAM");
+    int nw = 0, wk = 0, nbpb = 0;
+    if (f && std::sscanf(f, "%d,%d,%d", &nw, &wk, &nbpb) == 3) {
+      p.stream = true;
+      p.mb = m <= 16 ? 1 : (m <= 32 ? 2 : (m <= 64 ? 4 : 8));
+      p.nw = nw;
+      p.wk = wk;
+      p.nbpb = nbpb;
+      p.splits = 1;
+      p.kchunk = (int)kb;
+      return p;
+    }
+  }
   p = Plan();
   if (glu) {
     if (m <= 128)
-      p.tile = TILE_GLU_128x32;
+      p.tile = TILE_GLU_128x32_K2;
+    else if (tiles_of(TILE_GLU_256x64, m, n) >= 512)  // two resident per CU
+      p.tile = TILE_GLU_256x64;
     else
       p.tile = tiles_of(TILE_GLU_128x64, m, n) >= 256 ? TILE_GLU_128x64 : TILE_GLU_64x64;
   } else {

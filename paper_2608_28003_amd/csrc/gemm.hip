@@ -150,8 +150,8 @@ __device__ __forceinline__ void wait_outstanding(int n) {
 // Workgroups are dealt to the 8 XCDs round-robin by ID; the tile order gives
 // every XCD a contiguous range of tiles (M tile fastest), so the A and B
 // panels a range touches stay in that XCD's L2.
-template <bool BF16, int BM, int BN, int WAVES_M, int NW, int EPI, int S>
-__global__ __launch_bounds__(64 * NW) void gemm_tile_kernel(GemmParams p) {
+template <bool BF16, int BM, int BN, int WAVES_M, int NW, int EPI, int S, int KS>
+__global__ __launch_bounds__(64 * NW, 2) void gemm_tile_kernel(GemmParams p) {
   constexpr bool GLU = (EPI == EPI_GLU);
   constexpr int WAVES_N = NW / WAVES_M;
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
@@ -160,10 +160,10 @@ __global__ __launch_bounds__(64 * NW) void gemm_tile_kernel(GemmParams p) {
   constexpr int NB = (BN / 16) * (GLU ? 2 : 1);
   constexpr int NF = NA + NB;
   static_assert(NF % NW == 0, "fragments per stage must split over the waves");
-  constexpr int PF = NF / NW;  // fragments each wave fetches per stage
+  constexpr int PF = NF / NW;  // fragment rows each wave fetches per stage (KS fragments each)
   typedef typename Acc<BF16>::T AccT;
 
-  __shared__ v4i lds[S][NF * 64];
+  __shared__ v4i lds[S][NF * KS * 64];
 
   const int lane = lane_id();
   const int wave = threadIdx.x >> 6;
@@ -214,14 +214,23 @@ __global__ __launch_bounds__(64 * NW) void gemm_tile_kernel(GemmParams p) {
   // Each workgroup walks its K range from a different starting point, so the
   // operand panels shared by many workgroups (A by every N tile, B by every
   // M tile) are not all requested from the same L2 lines at the same time.
-  const int rot = nk > 0 ? (int)((blockIdx.x * 5u) % (unsigned)nk) : 0;
-  auto issue = [&](int j) {  // stage j (relative to kb0) into slot j % S
+  // A stage holds KS consecutive fragment columns; a ragged last stage loads
+  // its last valid column again (uniform load counts) and skips its products.
+  const int nsteps = (nk + KS - 1) / KS;
+  const int rot = nsteps > 0 ? (int)((blockIdx.x * 5u) % (unsigned)nsteps) : 0;
+  auto stage_of = [&](int j) {
     int jj = j + rot;
-    if (jj >= nk) jj -= nk;
-    const int kb = kb0 + jj;
+    if (jj >= nsteps) jj -= nsteps;
+    return jj;
+  };
+  auto issue = [&](int j) {  // stage j (relative to kb0) into slot j % S
+    const int kb = kb0 + stage_of(j) * KS;
 #pragma unroll
     for (int i = 0; i < PF; ++i)
-      to_lds_async(src[i] + (int64_t)kb * src_step[i], &lds[j % S][(wave + NW * i) * 64]);
+#pragma unroll
+      for (int k = 0; k < KS; ++k)
+        to_lds_async(src[i] + (int64_t)min(kb + k, kb1 - 1) * src_step[i],
+                     &lds[j % S][((wave + NW * i) * KS + k) * 64]);
   };
 
   AccT acc[TM][TN];
@@ -238,44 +247,54 @@ __global__ __launch_bounds__(64 * NW) void gemm_tile_kernel(GemmParams p) {
   // issued right after the barrier and complete while the MFMAs of stage j
   // (already in registers) run.
   struct Frags {
-    v4i a[TM];
-    v4i b[TN];
-    v4i bu[GLU ? TN : 1];
+    v4i a[KS][TM];
+    v4i b[KS][TN];
+    v4i bu[KS][GLU ? TN : 1];
   };
   auto read_frags = [&](int j, Frags& F) {
     const v4i* St = lds[j % S];
 #pragma unroll
-    for (int i = 0; i < TM; ++i) F.a[i] = St[(wm * TM + i) * 64 + lane];
+    for (int k = 0; k < KS; ++k) {
 #pragma unroll
-    for (int t = 0; t < TN; ++t) F.b[t] = St[(NA + wn * TN + t) * 64 + lane];
-    if constexpr (GLU) {
+      for (int i = 0; i < TM; ++i) F.a[k][i] = St[((wm * TM + i) * KS + k) * 64 + lane];
 #pragma unroll
-      for (int t = 0; t < TN; ++t) F.bu[t] = St[(NA + BN / 16 + wn * TN + t) * 64 + lane];
+      for (int t = 0; t < TN; ++t) F.b[k][t] = St[((NA + wn * TN + t) * KS + k) * 64 + lane];
+      if constexpr (GLU) {
+#pragma unroll
+        for (int t = 0; t < TN; ++t)
+          F.bu[k][t] = St[((NA + BN / 16 + wn * TN + t) * KS + k) * 64 + lane];
+      }
     }
   };
-  auto mma_frags = [&](const Frags& F) {
+  auto mma_frags = [&](const Frags& F, int j) {
+    const int nv = min(KS, nk - stage_of(j) * KS);  // valid fragment columns of stage j
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int t = 0; t < TN; ++t) acc[i][t] = Acc<BF16>::mma(F.a[i], F.b[t], acc[i][t]);
-    if constexpr (GLU) {
+    for (int k = 0; k < KS; ++k) {
+      if (k > 0 && k >= nv) break;
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int t = 0; t < TN; ++t) accu[i][t] = Acc<BF16>::mma(F.a[i], F.bu[t], accu[i][t]);
+        for (int t = 0; t < TN; ++t) acc[i][t] = Acc<BF16>::mma(F.a[k][i], F.b[k][t], acc[i][t]);
+      if constexpr (GLU) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int t = 0; t < TN; ++t)
+            accu[i][t] = Acc<BF16>::mma(F.a[k][i], F.bu[k][t], accu[i][t]);
+      }
     }
   };
 
   int issued = -1;  // last stage handed to the LDS-DMA
 #pragma unroll
   for (int j = 0; j < S - 1; ++j)
-    if (j < nk) {
+    if (j < nsteps) {
       issue(j);
       issued = j;
     }
   Frags F0, F1;
-  if (nk > 0) {
-    wait_outstanding<PF, S - 2>(issued);
+  if (nsteps > 0) {
+    wait_outstanding<PF * KS, S - 2>(issued);
     lds_barrier();
     read_frags(0, F0);
   }
@@ -283,18 +302,18 @@ __global__ __launch_bounds__(64 * NW) void gemm_tile_kernel(GemmParams p) {
   // other waves'); the slot of stage j-1 is free (its fragments were read one
   // step earlier), so stage j+S-1 goes into it.
   auto step = [&](int j, Frags& Fc, Frags& Fn) {
-    if (j + 1 < nk) wait_outstanding<PF, S - 2>(issued - (j + 1));
+    if (j + 1 < nsteps) wait_outstanding<PF * KS, S - 2>(issued - (j + 1));
     lds_barrier();
-    if (j + S - 1 < nk) {
+    if (j + S - 1 < nsteps) {
       issue(j + S - 1);
       issued = j + S - 1;
     }
-    if (j + 1 < nk) read_frags(j + 1, Fn);
-    mma_frags(Fc);
+    if (j + 1 < nsteps) read_frags(j + 1, Fn);
+    mma_frags(Fc, j);
   };
-  for (int j = 0; j < nk; j += 2) {
+  for (int j = 0; j < nsteps; j += 2) {
     step(j, F0, F1);
-    if (j + 1 < nk) step(j + 1, F1, F0);
+    if (j + 1 < nsteps) step(j + 1, F1, F0);
   }
 
   // ---------------- epilogue
@@ -330,7 +349,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_tile_kernel(GemmParams p) {
   char* dst = partial ? reinterpret_cast<char*>(p.part) + (int64_t)z * p.M * p.N * 4
                       : reinterpret_cast<char*>(p.out);
   const int64_t ld = partial ? p.N : p.ldo;
-  static_assert(NW * 16 * WN * 4 <= S * NF * 64 * 16, "epilogue staging must fit in the ring");
+  static_assert(NW * 16 * WN * 4 <= S * NF * KS * 64 * 16, "epilogue staging must fit in the ring");
   char* stage = reinterpret_cast<char*>(&lds[0][0]) + wave * (16 * WN * 4);
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
@@ -733,16 +752,25 @@ static hipError_t tile_dispatch(int tile, const GemmParams& p, hipStream_t st) {
   if constexpr (EPI == EPI_GLU) {
     switch (tile) {
       case TILE_GLU_128x32:
-        gemm_tile_kernel<BF16, 128, 32, 4, 4, EPI, 12><<<grid_for(128, 32), 256, 0, st>>>(p);
+        gemm_tile_kernel<BF16, 128, 32, 4, 4, EPI, 12, 1><<<grid_for(128, 32), 256, 0, st>>>(p);
         break;
       case TILE_GLU_64x64:
-        gemm_tile_kernel<BF16, 64, 64, 2, 4, EPI, 6><<<grid_for(64, 64), 256, 0, st>>>(p);
+        gemm_tile_kernel<BF16, 64, 64, 2, 4, EPI, 6, 1><<<grid_for(64, 64), 256, 0, st>>>(p);
         break;
       case TILE_GLU_128x64:
-        gemm_tile_kernel<BF16, 128, 64, 2, 4, EPI, 5><<<grid_for(128, 64), 256, 0, st>>>(p);
+        gemm_tile_kernel<BF16, 128, 64, 2, 4, EPI, 5, 1><<<grid_for(128, 64), 256, 0, st>>>(p);
         break;
       case TILE_GLU_256x128:
-        gemm_tile_kernel<BF16, 256, 128, 2, 8, EPI, 5><<<grid_for(256, 128), 512, 0, st>>>(p);
+        gemm_tile_kernel<BF16, 256, 128, 2, 8, EPI, 5, 1><<<grid_for(256, 128), 512, 0, st>>>(p);
+        break;
+      case TILE_GLU_128x32_K2:
+        gemm_tile_kernel<BF16, 128, 32, 4, 4, EPI, 6, 2><<<grid_for(128, 32), 256, 0, st>>>(p);
+        break;
+      case TILE_GLU_64x64_K2:
+        gemm_tile_kernel<BF16, 64, 64, 2, 4, EPI, 3, 2><<<grid_for(64, 64), 256, 0, st>>>(p);
+        break;
+      case TILE_GLU_256x64:
+        gemm_tile_kernel<BF16, 256, 64, 2, 4, EPI, 3, 1><<<grid_for(256, 64), 256, 0, st>>>(p);
         break;
       default:
         return hipErrorInvalidValue;
@@ -750,19 +778,25 @@ static hipError_t tile_dispatch(int tile, const GemmParams& p, hipStream_t st) {
   } else {
     switch (tile) {
       case TILE_128x128:
-        gemm_tile_kernel<BF16, 128, 128, 2, 4, EPI, 5><<<grid_for(128, 128), 256, 0, st>>>(p);
+        gemm_tile_kernel<BF16, 128, 128, 2, 4, EPI, 5, 1><<<grid_for(128, 128), 256, 0, st>>>(p);
         break;
       case TILE_128x64:
-        gemm_tile_kernel<BF16, 128, 64, 2, 4, EPI, 6><<<grid_for(128, 64), 256, 0, st>>>(p);
+        gemm_tile_kernel<BF16, 128, 64, 2, 4, EPI, 6, 1><<<grid_for(128, 64), 256, 0, st>>>(p);
         break;
       case TILE_64x64:
-        gemm_tile_kernel<BF16, 64, 64, 2, 4, EPI, 6><<<grid_for(64, 64), 256, 0, st>>>(p);
+        gemm_tile_kernel<BF16, 64, 64, 2, 4, EPI, 6, 1><<<grid_for(64, 64), 256, 0, st>>>(p);
         break;
       case TILE_256x128:
-        gemm_tile_kernel<BF16, 256, 128, 2, 8, EPI, 5><<<grid_for(256, 128), 512, 0, st>>>(p);
+        gemm_tile_kernel<BF16, 256, 128, 2, 8, EPI, 5, 1><<<grid_for(256, 128), 512, 0, st>>>(p);
         break;
       case TILE_256x256:
-        gemm_tile_kernel<BF16, 256, 256, 2, 8, EPI, 5><<<grid_for(256, 256), 512, 0, st>>>(p);
+        gemm_tile_kernel<BF16, 256, 256, 2, 8, EPI, 5, 1><<<grid_for(256, 256), 512, 0, st>>>(p);
+        break;
+      case TILE_64x64_K2:
+        gemm_tile_kernel<BF16, 64, 64, 2, 4, EPI, 3, 2><<<grid_for(64, 64), 256, 0, st>>>(p);
+        break;
+      case TILE_128x128_K2:
+        gemm_tile_kernel<BF16, 128, 128, 2, 4, EPI, 3, 2><<<grid_for(128, 128), 256, 0, st>>>(p);
         break;
       default:
         return hipErrorInvalidValue;

@@ -50,6 +50,11 @@ enum TileCfg {
   TILE_GLU_128x64 = 6,  // gated: 4 waves of 64 x (32 + 32)
   TILE_256x256 = 7,     // 8 waves of 128 x 64
   TILE_GLU_256x128 = 8, // gated: 8 waves of 128 x (32 + 32)
+  TILE_GLU_128x32_K2 = 9,  // as TILE_GLU_128x32 with two fragment columns per stage
+  TILE_64x64_K2 = 10,      // as TILE_64x64, two fragment columns per stage
+  TILE_128x128_K2 = 11,    // as TILE_128x128, two fragment columns per stage
+  TILE_GLU_64x64_K2 = 12,  // as TILE_GLU_64x64, two fragment columns per stage
+  TILE_GLU_256x64 = 13,    // gated: 4 waves of 128 x (32 + 32), 72 KiB LDS (2 per CU)
 };
 
 hipError_t launch_col_absmax(const void* x, bool bf16, int64_t rows, int64_t k, float* amax,

@@ -209,7 +209,7 @@ def test_gemm_split_k_is_bit_identical(m, n, k, splits, monkeypatch):
     A = torch.from_numpy(w8a8.rowmajor_to_frag(qa)).to(DEV)
     B = torch.from_numpy(w8a8.rowmajor_to_frag(qb)).to(DEV)
     monkeypatch.setenv("W8A8_GEMM_SPLITS", str(splits))
-    for tile in (0, 1, 2, 3, 7):
+    for tile in (0, 1, 2, 3, 7, 10, 11):
         monkeypatch.setenv("W8A8_GEMM_TILE", str(tile))
         acc = w8a8.gemm_i8_i32(A, m, B, n, k)
         torch.cuda.synchronize()
@@ -288,7 +288,7 @@ def test_gate_up_tiles_bit_identical(m, monkeypatch):
     qx = torch.from_numpy(w8a8.rowmajor_to_frag(qx_o)).to(DEV)
     sx = dev_f32(sx_o)
     ref = None
-    for tile in (4, 5, 6, 8):
+    for tile in (4, 5, 6, 8, 9, 12, 13):
         monkeypatch.setenv("W8A8_GLU_TILE", str(tile))
         h = host_bf16(w8a8.ffn_gate_up(layer, qx, sx, m))
         if ref is None:
