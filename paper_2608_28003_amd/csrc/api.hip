@@ -5,7 +5,6 @@
 
 #include <algorithm>
 #include <cstdint>
-#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <string>
@@ -155,20 +154,6 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, bool bf16, bool glu) {
     p.stream = true;
     return p;
   }
-  if (glu && m <= 128) {  // experiment hook: "nw,wk,nbpb" forces a streaming plan
-    const char* f = std::getenv("W8A8_GLU_STREAM");
-    int nw = 0, wk = 0, nbpb = 0;
-    if (f && std::sscanf(f, "%d,%d,%d", &nw, &wk, &nbpb) == 3) {
-      p.stream = true;
-      p.mb = m <= 16 ? 1 : (m <= 32 ? 2 : (m <= 64 ? 4 : 8));
-      p.nw = nw;
-      p.wk = wk;
-      p.nbpb = nbpb;
-      p.splits = 1;
-      p.kchunk = (int)kb;
-      return p;
-    }
-  }
   p = Plan();
   if (glu) {
     if (m <= 128)
@@ -246,6 +231,8 @@ w8a8_status run_gemm(const Plan& pl, bool bf16, int epi, const void* A, int64_t 
   p.out = out;
   p.ldo = ldo;
   p.part = pl.splits > 1 ? gemm_ws : nullptr;
+  p.group_m = env_int("W8A8_GROUP_M", 0);
+  p.rotate = env_int("W8A8_ROTATE", 1);
   hipError_t e = pl.stream ? launch_gemm_stream(bf16, epi, pl.mb, pl.nw, pl.wk, p, pl.nbpb, st)
                            : launch_gemm_tile(bf16, epi, pl.tile, p, st);
   w8a8_status s = hip_check(e, pl.stream ? "gemm_stream" : "gemm_tile");
@@ -279,6 +266,8 @@ w8a8_status run_gemm_raw(const Plan& pl, bool bf16, const void* A, int64_t lda, 
   p.out = part;
   p.ldo = n;
   p.part = pl.splits > 1 ? part : nullptr;
+  p.group_m = env_int("W8A8_GROUP_M", 0);
+  p.rotate = env_int("W8A8_ROTATE", 1);
   const int epi = bf16 ? EPI_F32 : EPI_I32;
   hipError_t e = pl.stream ? launch_gemm_stream(bf16, epi, pl.mb, pl.nw, pl.wk, p, pl.nbpb, st)
                            : launch_gemm_tile(bf16, epi, pl.tile, p, st);
@@ -379,12 +368,26 @@ size_t bf16_linear_ws(int64_t m, int64_t n, int64_t k) {
 // Stack workspace: token stream, next-consumer input (bf16 and codes), FFN
 // intermediates, the down projection's raw partial sums, the lm_head's GEMM
 // workspace.
+// INT8 down projection inside the stack: its split-K sums are reduced by the
+// glue launch, so the plan may split K more freely than a standalone call.
+// Experiment hooks: W8A8_DOWN_TILE, W8A8_DOWN_SPLITS.
+Plan stack_down_plan(int64_t m, int64_t d, int64_t f) {
+  Plan p = plan_gemm(m, d, f, false, false);
+  if (p.stream) return p;
+  p.tile = env_int("W8A8_DOWN_TILE", p.tile);
+  const int64_t kb = ceil_div(f, kFragK8);
+  const int splits = std::max(1, env_int("W8A8_DOWN_SPLITS", p.splits));
+  p.kchunk = (int)ceil_div(kb, splits);
+  p.splits = (int)ceil_div(kb, p.kchunk);
+  return p;
+}
+
 struct StackWs {
   size_t x, a, q, s, h, qh, sh, part, lm, total;
 };
 StackWs stack_ws(int64_t m, int64_t d, int64_t f, int64_t vocab) {
   StackWs w;
-  const Plan p8 = plan_gemm(m, d, f, false, false), p16 = plan_gemm(m, d, f, true, false);
+  const Plan p8 = stack_down_plan(m, d, f), p16 = plan_gemm(m, d, f, true, false);
   const size_t part = (size_t)std::max(p8.splits, p16.splits) * m * d * 4;
   const size_t lm = std::max(plan_ws_bytes(plan_gemm(m, vocab, d, false, false), m, vocab),
                              bf16_linear_ws(m, vocab, d));
@@ -849,7 +852,7 @@ w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec, int
   int8_t* qh = (int8_t*)(base + w.qh);
   float* sh = (float*)(base + w.sh);
   void* part = base + w.part;
-  const Plan p8 = plan_gemm(m, d, f, false, false), p16 = plan_gemm(m, d, f, true, false);
+  const Plan p8 = stack_down_plan(m, d, f), p16 = plan_gemm(m, d, f, true, false);
   const Plan pg8 = plan_gemm(m, f, d, false, true), pg16 = plan_gemm(m, f, d, true, true);
 
   // Glue launch l (0..n_layers): FFN output of layer l-1 into the token

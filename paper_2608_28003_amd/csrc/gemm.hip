@@ -175,8 +175,17 @@ __global__ __launch_bounds__(64 * NW, 2) void gemm_tile_kernel(GemmParams p) {
   const int per_xcd = (n_total + 7) / 8;
   const int t = (int)(blockIdx.x % 8) * per_xcd + (int)(blockIdx.x / 8);
   if (t >= n_total) return;  // whole workgroup, before any barrier
-  const int mt = t % m_tiles;
-  const int nt = t / m_tiles;
+  int mt, nt;
+  if (p.group_m > 0 && p.group_m < m_tiles) {  // bands of group_m M tiles, N within a band
+    const int band_tiles = p.group_m * n_tiles;
+    const int band = t / band_tiles, in_band = t % band_tiles;
+    const int gm = min(p.group_m, m_tiles - band * p.group_m);
+    mt = band * p.group_m + in_band % gm;
+    nt = in_band / gm;
+  } else {
+    mt = t % m_tiles;
+    nt = t / m_tiles;
+  }
   const int z = blockIdx.y;
   const int kb0 = z * p.kchunk;
   const int kb1 = min(p.kb_count, kb0 + p.kchunk);
@@ -217,7 +226,7 @@ __global__ __launch_bounds__(64 * NW, 2) void gemm_tile_kernel(GemmParams p) {
   // A stage holds KS consecutive fragment columns; a ragged last stage loads
   // its last valid column again (uniform load counts) and skips its products.
   const int nsteps = (nk + KS - 1) / KS;
-  const int rot = nsteps > 0 ? (int)((blockIdx.x * 5u) % (unsigned)nsteps) : 0;
+  const int rot = (nsteps > 0 && p.rotate) ? (int)((blockIdx.x * 5u) % (unsigned)nsteps) : 0;
   auto stage_of = [&](int j) {
     int jj = j + rot;
     if (jj >= nsteps) jj -= nsteps;

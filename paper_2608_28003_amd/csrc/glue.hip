@@ -119,10 +119,46 @@ __global__ __launch_bounds__(1024) void glue_kernel(GlueParams g) {
   }
   const bool own = t < chunks;
   const int64_t col0 = (int64_t)t * 8;
+  // every global operand of the row is requested up front, so the launch pays
+  // one memory round trip before its three workgroup reductions
   float xv[8];
+  uint4 xraw = make_uint4(0, 0, 0, 0);
+  float4 d0 = make_float4(1.f, 1.f, 1.f, 1.f), d1 = d0;
+  float4 si0 = make_float4(0.f, 0.f, 0.f, 0.f), si1 = si0;
+  float st = 0.0f;
+  constexpr int MAXZ = 8;  // partial sums held in registers; more splits stream
+  int4 pi[MAXZ][2];
+  float4 pf[MAXZ][2];
+  const int64_t plane = g.m * d;
   if (own) {
-    uint4 raw = *reinterpret_cast<const uint4*>(g.x_in + r * d + col0);
-    uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+    xraw = *reinterpret_cast<const uint4*>(g.x_in + r * d + col0);
+    if (g.q && g.delta) {
+      d0 = *reinterpret_cast<const float4*>(g.delta + col0);
+      d1 = *reinterpret_cast<const float4*>(g.delta + col0 + 4);
+    }
+    if (g.part) {
+      if (g.part_f32) {
+        const float* pp = reinterpret_cast<const float*>(g.part) + r * d + col0;
+#pragma unroll
+        for (int z = 0; z < MAXZ; ++z)
+          if (z < g.splits) {
+            pf[z][0] = *reinterpret_cast<const float4*>(pp + z * plane);
+            pf[z][1] = *reinterpret_cast<const float4*>(pp + z * plane + 4);
+          }
+      } else {
+        const int32_t* pp = reinterpret_cast<const int32_t*>(g.part) + r * d + col0;
+#pragma unroll
+        for (int z = 0; z < MAXZ; ++z)
+          if (z < g.splits) {
+            pi[z][0] = *reinterpret_cast<const int4*>(pp + z * plane);
+            pi[z][1] = *reinterpret_cast<const int4*>(pp + z * plane + 4);
+          }
+        st = g.s_t[r];
+        si0 = *reinterpret_cast<const float4*>(g.s_i + col0);
+        si1 = *reinterpret_cast<const float4*>(g.s_i + col0 + 4);
+      }
+    }
+    uint32_t w[4] = {xraw.x, xraw.y, xraw.z, xraw.w};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       xv[2 * j] = bf16_bits_to_float(w[j] & 0xffffu);
@@ -133,11 +169,16 @@ __global__ __launch_bounds__(1024) void glue_kernel(GlueParams g) {
     float y[8];
     float ss = 0.0f;
     if (own) {
-      const int64_t plane = g.m * d;
       if (g.part_f32) {
         const float* pp = reinterpret_cast<const float*>(g.part) + r * d + col0;
         float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-        for (int z = 0; z < g.splits; ++z) {
+#pragma unroll
+        for (int z = 0; z < MAXZ; ++z)
+          if (z < g.splits) {
+            acc[0] += pf[z][0].x; acc[1] += pf[z][0].y; acc[2] += pf[z][0].z; acc[3] += pf[z][0].w;
+            acc[4] += pf[z][1].x; acc[5] += pf[z][1].y; acc[6] += pf[z][1].z; acc[7] += pf[z][1].w;
+          }
+        for (int z = MAXZ; z < g.splits; ++z) {
           float4 a0 = *reinterpret_cast<const float4*>(pp + z * plane);
           float4 a1 = *reinterpret_cast<const float4*>(pp + z * plane + 4);
           acc[0] += a0.x; acc[1] += a0.y; acc[2] += a0.z; acc[3] += a0.w;
@@ -148,16 +189,22 @@ __global__ __launch_bounds__(1024) void glue_kernel(GlueParams g) {
       } else {
         const int32_t* pp = reinterpret_cast<const int32_t*>(g.part) + r * d + col0;
         int32_t acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        for (int z = 0; z < g.splits; ++z) {
+#pragma unroll
+        for (int z = 0; z < MAXZ; ++z)
+          if (z < g.splits) {
+            acc[0] += pi[z][0].x; acc[1] += pi[z][0].y; acc[2] += pi[z][0].z; acc[3] += pi[z][0].w;
+            acc[4] += pi[z][1].x; acc[5] += pi[z][1].y; acc[6] += pi[z][1].z; acc[7] += pi[z][1].w;
+          }
+        for (int z = MAXZ; z < g.splits; ++z) {
           int4 a0 = *reinterpret_cast<const int4*>(pp + z * plane);
           int4 a1 = *reinterpret_cast<const int4*>(pp + z * plane + 4);
           acc[0] += a0.x; acc[1] += a0.y; acc[2] += a0.z; acc[3] += a0.w;
           acc[4] += a1.x; acc[5] += a1.y; acc[6] += a1.z; acc[7] += a1.w;
         }
-        const float st = g.s_t[r];
+        const float si[8] = {si0.x, si0.y, si0.z, si0.w, si1.x, si1.y, si1.z, si1.w};
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          float v = ((float)acc[e] * st) * g.s_i[col0 + e];
+          float v = ((float)acc[e] * st) * si[e];
           y[e] = bf16_bits_to_float(float_to_bf16_bits(v));
         }
       }
@@ -206,9 +253,10 @@ __global__ __launch_bounds__(1024) void glue_kernel(GlueParams g) {
   if (!g.q) return;
   float amax = 0.0f;
   if (own) {
+    const float dl[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      if (g.delta) a[e] = a[e] / g.delta[col0 + e];
+      if (g.delta) a[e] = a[e] / dl[e];
       amax = fmaxf(amax, fabsf(a[e]));
     }
   }

@@ -37,6 +37,10 @@ struct GemmParams {
   int64_t a_ld = 0;                // row stride of a_x in elements
   int a_k = 0;                     // logical columns of a_x
   float* a_s_out = nullptr;        // optional: the per-row scales, written once
+  // Tiled kernel walk order: tiles in bands of group_m M tiles (0: one band
+  // of all M tiles); rotate: start each workgroup's K walk at a different step.
+  int group_m = 0;
+  int rotate = 1;
 };
 
 // tile shapes selectable at run time
