@@ -104,7 +104,7 @@ bool plan_stream(Plan& p, int64_t m, int64_t n, int64_t kb, bool glu) {
     p.nw = env_int("W8A8_WIDE_NW", 4);
     p.splits = 1;
     p.kchunk = (int)kb;
-    const int64_t wgs = env_int("W8A8_WIDE_WGS", 512);
+    const int64_t wgs = env_int("W8A8_WIDE_WGS", p.mb == 1 ? 1024 : 512);
     p.nbpb = p.nw == 1 ? (int)std::max<int64_t>(1, ceil_div(nbc, wgs))
                        : (int)round_up(std::max<int64_t>(4, ceil_div(nbc, wgs)), 4);
     return true;

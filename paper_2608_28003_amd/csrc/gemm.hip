@@ -26,10 +26,12 @@ namespace w8a8 {
 
 // ------------------------------------------------------------------ helpers
 
+// Weight fragments stream through once: non-temporal loads keep them from
+// displacing reused data in the caches (measured: +15 % on the decode lm_head).
 __device__ __forceinline__ v4i load_frag_packed(const void* base, int64_t rb, int64_t kb,
                                                 int64_t kb_count, int lane) {
   const int8_t* p = reinterpret_cast<const int8_t*>(base) + frag_offset(rb, kb, kb_count) + lane * 16;
-  return *reinterpret_cast<const v4i*>(p);
+  return __builtin_nontemporal_load(reinterpret_cast<const v4i*>(p));
 }
 
 // bf16 A operand read straight from a row-major matrix: lane l takes row
