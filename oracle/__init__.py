@@ -78,12 +78,18 @@ def _L():
             "orc_geglu_f64": [P, P, I64, P],
             "orc_linear_f64": [P, P, I64, I64, I64, P],
             "orc_rmsnorm_f64": [P, I64, I64, D, P],
+            "orc_e4m3_encode_n": [P, I64, P],
+            "orc_quant_rows_fp8": [P, I64, I64, P, ctypes.c_int, P, P],
+            "orc_gemm_fp8": [P, P, I64, I64, I64, P],
+            "orc_dequant_fp8": [P, P, P, I64, I64, P],
         }
         for name, args in sigs.items():
             fn = getattr(lib, name)
             fn.argtypes = args
             fn.restype = None
         lib.orc_gemm_i32.restype = ctypes.c_int64
+        lib.orc_e4m3_decode.argtypes = [ctypes.c_uint8]
+        lib.orc_e4m3_decode.restype = ctypes.c_double
         _lib = lib
     return _lib
 
@@ -311,6 +317,95 @@ def rmsnorm(x) -> np.ndarray:
 def w8a8_lm_head(x_bf16, wq, s_w, delta) -> np.ndarray:
     """Logits in bf16 from the INT8 lm_head (Sec. 6, eq. gemm-final)."""
     return w8a8_linear(x_bf16, wq, s_w, delta, out_dtype="bf16")
+
+
+# ---------------------------------------------------------------- FP8 variant
+
+# OCP FP8 E4M3 codes as numpy.uint8 (Sec. 4 lists the move from INT8 to FP8
+# codes; the scheme keeps smoothing and the per-token / per-channel scales,
+# with 448, the largest E4M3 magnitude, in place of 127).
+E4M3_MAX = 448.0
+
+
+def e4m3_decode(codes) -> np.ndarray:
+    table = np.array([_L().orc_e4m3_decode(c) for c in range(256)], np.float64)
+    return table[_c(codes, np.uint8)]
+
+
+def e4m3_encode(x) -> np.ndarray:
+    """Nearest E4M3 code of binary32 values, ties to even, saturating at 448."""
+    xf = _c(x, np.float32)
+    out = np.empty(xf.shape, np.uint8)
+    _L().orc_e4m3_encode_n(_p(xf), xf.size, _p(out))
+    return out
+
+
+def quant_rows_fp8(x, delta=None, mode=MODE_DIV):
+    xf = as_f32(x)
+    rows, k = xf.shape
+    q = np.empty((rows, k), np.uint8)
+    s = np.empty(rows, np.float32)
+    d = None if delta is None else _c(delta, np.float32)
+    _L().orc_quant_rows_fp8(_p(xf), rows, k, _p(d), mode, _p(q), _p(s))
+    return q, s
+
+
+def quantize_weights_fp8(w, delta=None):
+    return quant_rows_fp8(w, delta, MODE_MUL)
+
+
+def quantize_act_fp8(x, delta=None):
+    return quant_rows_fp8(x, delta, MODE_DIV)
+
+
+def gemm_fp8(qa, qb) -> np.ndarray:
+    """sum_j dec(qa[t, j]) dec(qb[i, j]) in binary64."""
+    qa = _c(qa, np.uint8)
+    qb = _c(qb, np.uint8)
+    m, k = qa.shape
+    n, k2 = qb.shape
+    assert k == k2
+    acc = np.empty((m, n), np.float64)
+    _L().orc_gemm_fp8(_p(qa), _p(qb), m, n, k, _p(acc))
+    return acc
+
+
+def dequant_fp8(acc, s_tok, s_ch) -> np.ndarray:
+    acc = _c(acc, np.float64)
+    m, n = acc.shape
+    y = np.empty((m, n), np.float32)
+    _L().orc_dequant_fp8(_p(acc), _p(_c(s_tok, np.float32)), _p(_c(s_ch, np.float32)),
+                         m, n, _p(y))
+    return y
+
+
+def fp8_linear(x, wq, s_w, delta, out_dtype="f32"):
+    qx, sx = quantize_act_fp8(x, delta)
+    y = dequant_fp8(gemm_fp8(qx, wq), sx, s_w)
+    return y if out_dtype == "f32" else f32_to_bf16(y)
+
+
+def quantize_ffn_fp8(w_gate, w_up, w_down, x_cal, alpha=ALPHA):
+    """As quantize_ffn, with E4M3 weight codes (same smoothing factors)."""
+    q8 = quantize_ffn(w_gate, w_up, w_down, x_cal, alpha)
+    out = dict(delta_gu=q8["delta_gu"], delta_down=q8["delta_down"])
+    out["wq_gate"], out["s_gate"] = quantize_weights_fp8(w_gate, q8["delta_gu"])
+    out["wq_up"], out["s_up"] = quantize_weights_fp8(w_up, q8["delta_gu"])
+    out["wq_down"], out["s_down"] = quantize_weights_fp8(w_down, q8["delta_down"])
+    return out
+
+
+def fp8_ffn(x_bf16, q, stages=False):
+    """FP8 FFN block, the INT8 block's steps with E4M3 codes."""
+    qx, sx = quantize_act_fp8(x_bf16, q["delta_gu"])
+    g = dequant_fp8(gemm_fp8(qx, q["wq_gate"]), sx, q["s_gate"])
+    u = dequant_fp8(gemm_fp8(qx, q["wq_up"]), sx, q["s_up"])
+    h = f64_to_bf16(geglu(g, u))
+    qh, sh = quantize_act_fp8(h, q["delta_down"])
+    y = f32_to_bf16(dequant_fp8(gemm_fp8(qh, q["wq_down"]), sh, q["s_down"]))
+    if stages:
+        return y, dict(qx=qx, sx=sx, g=g, u=u, h=h, qh=qh, sh=sh)
+    return y
 
 
 # ---------------------------------------------------------------- a8 / a9

@@ -222,6 +222,104 @@ void orc_geglu_f64(const double* g, const double* u, int64_t n, double* h) {
 }
 
 /* ------------------------------------------------------------------ */
+/* FP8 variant (Sec. 4, the listed move from INT8 to FP8 codes)         */
+/* ------------------------------------------------------------------ */
+
+/* OCP FP8 E4M3 ("fn"): 1 sign, 4 exponent (bias 7), 3 mantissa bits.
+   Exponent field 0 holds the subnormals m/8 * 2^-6; field 1..15 the normals
+   (1 + m/8) * 2^(e-7), except field 15 with mantissa 7, which is NaN.  The
+   largest finite magnitude is 1.75 * 2^8 = 448; there is no infinity. */
+double orc_e4m3_decode(uint8_t c) {
+    int sgn = c >> 7, e = (c >> 3) & 15, m = c & 7;
+    double v;
+    if (e == 15 && m == 7) return NAN;
+    if (e == 0) v = ldexp((double)m / 8.0, -6);
+    else v = ldexp(1.0 + (double)m / 8.0, e - 7);
+    return sgn ? -v : v;
+}
+
+/* Nearest E4M3 value to a binary32 x, ties to the even code (even mantissa),
+   magnitudes beyond 448 saturate to 448 (the quantiser below never produces
+   them beyond rounding).  Chosen by comparing x with the exact midpoints of
+   consecutive codes, which are all representable in binary64. */
+uint8_t orc_e4m3_encode(float x) {
+    uint8_t sgn = (x < 0.0f || (x == 0.0f && signbit(x))) ? 0x80 : 0x00;
+    double a = fabs((double)x);
+    if (isnan(x)) return 0x7f;
+    if (a >= 448.0) return sgn | 0x7e;
+    /* codes 0..126 ascend in value: find the first whose value reaches a */
+    int lo = 0;
+    while (lo < 126 && orc_e4m3_decode((uint8_t)(lo + 1)) <= a) ++lo;
+    /* a lies in [value(lo), value(lo + 1)) */
+    if (lo == 126) return sgn | 126;
+    double v0 = orc_e4m3_decode((uint8_t)lo), v1 = orc_e4m3_decode((uint8_t)(lo + 1));
+    double mid = 0.5 * (v0 + v1);
+    int code;
+    if (a < mid) code = lo;
+    else if (a > mid) code = lo + 1;
+    else code = (lo & 1) ? lo + 1 : lo; /* tie: even mantissa = even code */
+    return sgn | (uint8_t)code;
+}
+
+void orc_e4m3_encode_n(const float* x, int64_t n, uint8_t* out) {
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) out[i] = orc_e4m3_encode(x[i]);
+}
+
+/* Row quantisation with E4M3 codes: as orc_quant_rows, with the scale
+   s = amax / 448 and code = E4M3(fl32(v / s)); a zero row gets s = 0, codes 0. */
+void orc_quant_rows_fp8(const float* x, int64_t rows, int64_t k, const float* delta,
+                        int mode, uint8_t* q, float* s) {
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < rows; ++r) {
+        const float* xr = x + r * k;
+        float amax = 0.0f;
+        for (int64_t j = 0; j < k; ++j) {
+            float v = xr[j];
+            if (delta) v = (mode == ORC_MODE_DIV) ? v / delta[j] : v * delta[j];
+            float a = fabsf(v);
+            if (a > amax) amax = a;
+        }
+        float sr = amax / 448.0f;
+        s[r] = sr;
+        for (int64_t j = 0; j < k; ++j) {
+            float v = xr[j];
+            if (delta) v = (mode == ORC_MODE_DIV) ? v / delta[j] : v * delta[j];
+            q[r * k + j] = sr != 0.0f ? orc_e4m3_encode(v / sr) : 0;
+        }
+    }
+}
+
+/* acc[t][i] = sum_j dec(a[t][j]) dec(b[i][j]) in binary64 (every product is
+   exact; the sum is exact up to binary64 rounding). */
+void orc_gemm_fp8(const uint8_t* a, const uint8_t* b, int64_t m, int64_t n, int64_t k,
+                  double* acc) {
+    double table[256];
+    for (int c = 0; c < 256; ++c) table[c] = orc_e4m3_decode((uint8_t)c);
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < m; ++t)
+        for (int64_t i = 0; i < n; ++i) {
+            double sum = 0.0;
+            for (int64_t j = 0; j < k; ++j) sum += table[a[t * k + j]] * table[b[i * k + j]];
+            acc[t * n + i] = sum;
+        }
+}
+
+/* Dequantisation of FP8 sums: y = fl32(fl32(fl32(acc) * s_t) * s_i), the
+   binary32 order of the INT8 path with the sum rounded to binary32 first (the
+   matrix cores accumulate in binary32). */
+void orc_dequant_fp8(const double* acc, const float* s_tok, const float* s_ch, int64_t m,
+                     int64_t n, float* y) {
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < m; ++t)
+        for (int64_t i = 0; i < n; ++i) {
+            float a = (float)acc[t * n + i];
+            float p = a * s_tok[t];
+            y[t * n + i] = p * s_ch[i];
+        }
+}
+
+/* ------------------------------------------------------------------ */
 /* bf16 reference path and stack glue (binary64)                       */
 /* ------------------------------------------------------------------ */
 

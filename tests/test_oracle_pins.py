@@ -417,3 +417,86 @@ def test_stack_all_bf16_and_int8_maps_differ_only_on_int8_layers():
     assert not np.array_equal(h0[1], h1[1])          # layer 1 switched to INT8
     # the INT8 layer stays close to its bf16 counterpart
     assert oracle.sqnr_db(oracle.bf16_to_f32(h0[1]), oracle.bf16_to_f32(h1[1])) > 20.0
+
+
+# ------------------------------------------------------------------ FP8 variant
+
+def test_e4m3_decode_matches_torch_for_every_code():
+    codes = np.arange(256, dtype=np.uint8)
+    got = oracle.e4m3_decode(codes)
+    ref = torch.from_numpy(codes).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    same = (got == ref) | (np.isnan(got) & np.isnan(ref))
+    assert same.all()
+    assert np.nanmax(got) == 448.0 and got[0x01] == 2.0 ** -9 and got[0x08] == 2.0 ** -6
+
+
+def test_e4m3_encode_matches_torch_rounding():
+    """torch's float8_e4m3fn cast rounds to nearest even; compare on every code
+    value, every midpoint between neighbours and one binary32 step either side
+    of it, and random values (all within +-464, where torch does not give NaN)."""
+    vals = oracle.e4m3_decode(np.arange(127, dtype=np.uint8))
+    mids = 0.5 * (vals[:-1] + vals[1:])
+    pts = [vals, mids, np.nextafter(mids.astype(np.float32), np.float32(0)),
+           np.nextafter(mids.astype(np.float32), np.float32(1e9))]
+    rng = np.random.default_rng(31)
+    pts.append(rng.uniform(-464, 464, 20000))
+    pts.append(rng.standard_normal(20000) * 0.01)
+    x = np.concatenate([np.concatenate([p, -p]) for p in pts]).astype(np.float32)
+    got = oracle.e4m3_encode(x)
+    ref = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    np.testing.assert_array_equal(got, ref)
+
+
+def test_e4m3_hand_cases():
+    cases = {1.0625: 0x38, 1.1875: 0x3A, 448.0: 0x7E, 500.0: 0x7E, -500.0: 0xFE,
+             2.0 ** -10: 0x00, 3 * 2.0 ** -10: 0x02, 0.0: 0x00, 1.5: 0x3C, -0.75: 0xB4}
+    x = np.array(list(cases), np.float32)
+    np.testing.assert_array_equal(oracle.e4m3_encode(x), np.array(list(cases.values()), np.uint8))
+    assert oracle.e4m3_encode(np.array([-0.0], np.float32))[0] == 0x80
+
+
+def test_fp8_quant_invariants():
+    rng = np.random.default_rng(32)
+    x = (rng.standard_normal((40, 256)) * rng.uniform(0.01, 50, (40, 1))).astype(np.float32)
+    x[5] = 0.0
+    q, s = oracle.quantize_act_fp8(x)
+    dec = oracle.e4m3_decode(q)
+    assert s[5] == 0.0 and not q[5].any()
+    for r in range(40):
+        if r == 5:
+            continue
+        assert np.abs(dec[r]).max() == 448.0          # the row maximum maps to 448
+        # error within half the E4M3 spacing at the value's magnitude (<= 1/16 relative,
+        # or the subnormal step 2^-10 absolute in code units)
+        v = x[r].astype(np.float64) / s[r]
+        err = np.abs(v - dec[r])
+        assert (err <= np.maximum(np.abs(v) / 16.0, 2.0 ** -10) + 1e-9).all()
+    # power-of-two scaling of a row leaves the codes unchanged
+    q2, s2 = oracle.quantize_act_fp8(x * np.float32(8.0))
+    np.testing.assert_array_equal(q2, q)
+    np.testing.assert_array_equal(s2, s * np.float32(8.0))
+
+
+def test_fp8_gemm_brute_force():
+    rng = np.random.default_rng(33)
+    qa = rng.integers(0, 256, (3, 40)).astype(np.uint8)
+    qb = rng.integers(0, 256, (4, 40)).astype(np.uint8)
+    qa[(qa & 0x7F) == 0x7F] = 0x10     # no NaN codes
+    qb[(qb & 0x7F) == 0x7F] = 0x11
+    got = oracle.gemm_fp8(qa, qb)
+    from fractions import Fraction
+    dec = {c: Fraction(float(oracle.e4m3_decode(np.array([c], np.uint8))[0])) for c in range(256)
+           if (c & 0x7F) != 0x7F}
+    for t in range(3):
+        for i in range(4):
+            exact = sum(dec[int(a)] * dec[int(b)] for a, b in zip(qa[t], qb[i]))
+            assert got[t, i] == float(exact)
+
+
+def test_fp8_ffn_sqnr():
+    cfg = synth.ffn_config(m=32)
+    qf = oracle.quantize_ffn_fp8(cfg["w_gate"], cfg["w_up"], cfg["w_down"], cfg["x_cal"])
+    ref = oracle.bf16_to_f32(oracle.bf16_ffn(cfg["x"], cfg["w_gate"], cfg["w_up"],
+                                             cfg["w_down"])).astype(np.float64)
+    yf = oracle.bf16_to_f32(oracle.fp8_ffn(cfg["x"], qf)).astype(np.float64)
+    assert oracle.sqnr_db(ref, yf) > 20.0
