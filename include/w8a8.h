@@ -213,6 +213,66 @@ w8a8_status w8a8_ffn(const w8a8_ffn_desc* desc, const void* x, int64_t m, void* 
 w8a8_status w8a8_lm_head(const w8a8_linear_desc* desc, const void* x, int64_t m,
                          void* logits, void* ws, size_t ws_bytes, w8a8_stream_t stream);
 
+/* ---------------------------------------------------------------- FP8 variant */
+
+/* FP8 in place of INT8 (Sec. 4, the list of further speed-ups; Sec. 8): the same
+   SmoothQuant linear, FFN and lm_head with OCP FP8 E4M3 codes (1 sign, 4 exponent
+   bits with bias 7, 3 mantissa bits, no infinities, largest finite 448) instead of
+   int8.  The scales use the same symmetric reading with 448 in place of 127:
+   s = max_j |v_j| / 448 (0 for an all-zero row) and code = E4M3(fl32(v / s)),
+   rounded to nearest, ties to the even code; an all-zero row gives codes 0.
+   Products of two E4M3 codes are exact in binary32 and the matrix cores sum them
+   in binary32, so the sums differ from exact ones by rounding only.
+   Codes use the packed int8 fragment layout byte for byte (one code per byte),
+   so w8a8_packed_bytes sizes them and the descriptors above carry them unchanged.
+   Every GEMM on this path needs its reduction length K to be a multiple of 128
+   (EUNSUPPORTED otherwise): the FP8 matrix instruction reduces 128 codes at a
+   time and the path does not pad K inside a 64-column fragment. */
+
+size_t w8a8_fp8_linear_workspace_bytes(int64_t m, int64_t n, int64_t k);
+size_t w8a8_fp8_ffn_workspace_bytes(int64_t m, int64_t d, int64_t f);
+
+/* Offline FP8 weight quantisation: W_hat = W diag(delta) (delta NULL: W),
+   s_w[i] = max_j |W_hat_ij| / 448, codes E4M3(W_hat_ij / s_w[i]).
+   w: n x k, f32 or bf16; wq: w8a8_packed_bytes(n, k) bytes; s_w: float[n]. */
+w8a8_status w8a8_fp8_quantize_weights(const void* w, w8a8_dtype w_dtype, int64_t n,
+                                      int64_t k, const float* delta, void* wq, float* s_w,
+                                      w8a8_stream_t stream);
+
+/* Dynamic per-token FP8 quantisation of x / delta: s_x[t] = max_j |x_hat_tj| / 448,
+   codes E4M3(x_hat / s_x[t]).  x: m x k, f32 or bf16; qx: w8a8_packed_bytes(m, k). */
+w8a8_status w8a8_fp8_quantize_act(const void* x, w8a8_dtype x_dtype, int64_t m, int64_t k,
+                                  const float* delta, void* qx, float* s_x,
+                                  w8a8_stream_t stream);
+
+/* Binary32 sums acc[t][i] = sum_j e(qx[t][j]) e(wq[i][j]) of decoded codes, the FP8
+   analogue of w8a8_gemm_i8_i32 (identity epilogue, split-K partials added in
+   binary32).  acc: float m x n row-major.  ws: w8a8_fp8_linear_workspace_bytes. */
+w8a8_status w8a8_fp8_gemm_f32(const void* qx, int64_t m, const void* wq, int64_t n,
+                              int64_t k, float* acc, void* ws, size_t ws_bytes,
+                              w8a8_stream_t stream);
+
+/* FP8 linear layer: as w8a8_linear with E4M3 codes; y = (acc * s_x[t]) * s_w[i].
+   ws: w8a8_fp8_linear_workspace_bytes(m, n, k). */
+w8a8_status w8a8_fp8_linear(const w8a8_linear_desc* desc, const void* x, w8a8_dtype x_dtype,
+                            int64_t m, void* y, w8a8_dtype y_dtype, void* ws,
+                            size_t ws_bytes, w8a8_stream_t stream);
+
+/* Gate/up stage of the FP8 FFN with the gated activation fused in the epilogue
+   (as w8a8_ffn_gate_up).  qx: E4M3 codes of m x d, packed; d % 128 == 0. */
+w8a8_status w8a8_fp8_ffn_gate_up(const w8a8_ffn_desc* desc, const void* qx, const float* s_x,
+                                 int64_t m, void* h, w8a8_stream_t stream);
+
+/* Whole FP8 FFN block (as w8a8_ffn); d % 128 == 0 and f % 128 == 0.
+   ws: w8a8_fp8_ffn_workspace_bytes(m, d, f). */
+w8a8_status w8a8_fp8_ffn(const w8a8_ffn_desc* desc, const void* x, int64_t m, void* y,
+                         void* ws, size_t ws_bytes, w8a8_stream_t stream);
+
+/* FP8 lm_head: bf16 logits m x n from bf16 x m x k; k % 128 == 0.
+   ws: w8a8_fp8_linear_workspace_bytes(m, n, k). */
+w8a8_status w8a8_fp8_lm_head(const w8a8_linear_desc* desc, const void* x, int64_t m,
+                             void* logits, void* ws, size_t ws_bytes, w8a8_stream_t stream);
+
 /* ---------------------------------------------------------------- bf16 path */
 
 /* bf16 projection y = bf16(x W^T), fp32 accumulation.  x: bf16 m x k

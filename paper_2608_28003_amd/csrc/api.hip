@@ -38,6 +38,7 @@ hipStream_t S(w8a8_stream_t s) { return reinterpret_cast<hipStream_t>(s); }
 // ------------------------------------------------------------------ planner
 
 struct Plan {
+  int dt = DT_I8;       // operand type the plan was made for
   bool stream = false;  // streaming kernel (M <= 128) or tiled kernel
   int tile = TILE_128x128;
   int mb = 1;           // streaming: 16-row blocks of A
@@ -79,7 +80,8 @@ int64_t tiles_of(int tile, int64_t m, int64_t n) {
 }
 
 // Streaming plan for M <= 128, or false if the A panel cannot fit in LDS.
-bool plan_stream(Plan& p, int64_t m, int64_t n, int64_t kb, bool glu) {
+bool plan_stream(Plan& p, int64_t m, int64_t n, int64_t kb, bool glu, bool f8) {
+  const int64_t kstep = f8 ? 2 : 1;  // FP8: K chunks of whole 128-deep MFMA steps
   const int64_t nbc = ceil_div(n, 16);
   const int64_t lds_kb = 158;  // dynamic LDS per workgroup, KiB (one fragment = 1 KiB); the
                                // kernel's static LDS (scales, reduction scratch) takes the rest
@@ -118,8 +120,8 @@ bool plan_stream(Plan& p, int64_t m, int64_t n, int64_t kb, bool glu) {
     if (wk == 16 && p.mb > 1) continue;  // 16-wave workgroups only for MB = 1
     int64_t max_kc = (lds_kb - (wk - 1) * p.mb) / p.mb;
     if (max_kc < wk) continue;
-    int64_t splits = ceil_div(kb, max_kc);
-    int64_t kchunk = ceil_div(kb, splits);
+    int64_t splits = ceil_div(kb, max_kc / kstep * kstep);
+    int64_t kchunk = round_up(ceil_div(kb, splits), kstep);
     splits = ceil_div(kb, kchunk);
     int64_t pw = ceil_div(kchunk, wk), waves = nbc * splits * wk;
     bool better;
@@ -143,18 +145,40 @@ bool plan_stream(Plan& p, int64_t m, int64_t n, int64_t kb, bool glu) {
 // Deterministic in (m, n, k, path); the workspace queries use the same plan.
 // Tuning hooks for the tiled path: W8A8_GEMM_TILE / W8A8_GEMM_SPLITS (plain
 // epilogues) and W8A8_GLU_TILE (gated epilogue).
-Plan plan_gemm(int64_t m, int64_t n, int64_t k, bool bf16, bool glu) {
+Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
   Plan p;
-  const int64_t kb = bf16 ? ceil_div(k, kFragK16) : ceil_div(k, kFragK8);
+  p.dt = dt;
+  const bool f8 = dt == DT_F8;
+  const int64_t kb = dt == DT_BF16 ? ceil_div(k, kFragK16) : ceil_div(k, kFragK8);
   // The streaming kernel wins while the weights dominate the traffic: up to
   // 32 rows, and up to 64 rows for the very wide lm_head; the tiled kernel
   // reuses operands better beyond that.
   const bool wide = ceil_div(n, 16) >= 1024;
-  if ((m <= 32 || (m <= 64 && wide && !glu)) && plan_stream(p, m, n, kb, glu)) {
+  if ((m <= 32 || (m <= 64 && wide && !glu)) && plan_stream(p, m, n, kb, glu, f8)) {
     p.stream = true;
     return p;
   }
   p = Plan();
+  p.dt = dt;
+  if (f8) {  // FP8 stages hold whole 128-deep MFMA steps: two-column tiles only
+    if (glu)
+      p.tile = m <= 128 ? TILE_GLU_128x32_K2 : TILE_GLU_64x64_K2;
+    else
+      p.tile = tiles_of(TILE_128x128_K2, m, n) >= 256 ? TILE_128x128_K2 : TILE_64x64_K2;
+    const int want = glu ? env_int("W8A8_GLU_TILE", p.tile) : env_int("W8A8_GEMM_TILE", p.tile);
+    if (glu ? (want == TILE_GLU_128x32_K2 || want == TILE_GLU_64x64_K2)
+            : (want == TILE_64x64_K2 || want == TILE_128x128_K2))
+      p.tile = want;
+    const int64_t tiles = tiles_of(p.tile, m, n);
+    int64_t splits = 1;
+    if (!glu && tiles < 200)
+      splits = std::min<int64_t>(ceil_div(256, tiles), std::max<int64_t>(1, kb / 8));
+    splits = env_int("W8A8_GEMM_SPLITS", (int)splits);
+    if (glu || splits < 1) splits = 1;
+    p.kchunk = (int)round_up(ceil_div(kb, splits), 2);
+    p.splits = (int)ceil_div(kb, p.kchunk);
+    return p;
+  }
   if (glu) {
     if (m <= 128)
       p.tile = TILE_GLU_128x32_K2;
@@ -200,11 +224,11 @@ struct QLoad {
 // Streaming int8 plans over at most 16 rows quantise their bf16 input
 // themselves; every other plan reads codes produced by quant_rows_kernel.
 bool plan_qloads(const Plan& pl, int64_t m, int64_t k) {
-  if (env_int("W8A8_NO_QLOAD", 0)) return false;
+  if (env_int("W8A8_NO_QLOAD", 0) || pl.dt != DT_I8) return false;
   return pl.stream && pl.mb == 1 && m * (k / 16) <= qload_capacity(pl.nw);
 }
 
-w8a8_status run_gemm(const Plan& pl, bool bf16, int epi, const void* A, int64_t lda, int64_t m,
+w8a8_status run_gemm(const Plan& pl, int dt, int epi, const void* A, int64_t lda, int64_t m,
                      const void* B, const void* B2, int64_t n, int64_t k, const float* s_a,
                      const float* s_b, const float* s_b2, void* out, int64_t ldo, void* gemm_ws,
                      hipStream_t st, QLoad ql = QLoad()) {
@@ -222,7 +246,7 @@ w8a8_status run_gemm(const Plan& pl, bool bf16, int epi, const void* A, int64_t 
   p.N = (int)n;
   p.rb_a = (int)ceil_div(m, 16);
   p.rb_b = (int)ceil_div(n, 16);
-  p.kb_count = (int)(bf16 ? ceil_div(k, kFragK16) : ceil_div(k, kFragK8));
+  p.kb_count = (int)(dt == DT_BF16 ? ceil_div(k, kFragK16) : ceil_div(k, kFragK8));
   p.kchunk = pl.kchunk;
   p.splits = pl.splits;
   p.s_a = s_a;
@@ -233,18 +257,18 @@ w8a8_status run_gemm(const Plan& pl, bool bf16, int epi, const void* A, int64_t 
   p.part = pl.splits > 1 ? gemm_ws : nullptr;
   p.group_m = env_int("W8A8_GROUP_M", 0);
   p.rotate = env_int("W8A8_ROTATE", 1);
-  hipError_t e = pl.stream ? launch_gemm_stream(bf16, epi, pl.mb, pl.nw, pl.wk, p, pl.nbpb, st)
-                           : launch_gemm_tile(bf16, epi, pl.tile, p, st);
+  hipError_t e = pl.stream ? launch_gemm_stream(dt, epi, pl.mb, pl.nw, pl.wk, p, pl.nbpb, st)
+                           : launch_gemm_tile(dt, epi, pl.tile, p, st);
   w8a8_status s = hip_check(e, pl.stream ? "gemm_stream" : "gemm_tile");
   if (s != W8A8_OK || pl.splits <= 1) return s;
-  return hip_check(launch_splitk_reduce(bf16, epi, p, st), "splitk_reduce");
+  return hip_check(launch_splitk_reduce(dt, epi, p, st), "splitk_reduce");
 }
 
 // The same GEMM without any reduction or dequantisation: raw sums (int32 for
-// INT8 operands, fp32 for bf16) in the plan's split-K layout
+// INT8 operands, fp32 for bf16 and FP8) in the plan's split-K layout
 // part[split][m][n] (one split: a plain m x n matrix), for a consumer that
 // reduces them itself.
-w8a8_status run_gemm_raw(const Plan& pl, bool bf16, const void* A, int64_t lda, int64_t m,
+w8a8_status run_gemm_raw(const Plan& pl, int dt, const void* A, int64_t lda, int64_t m,
                          const void* B, int64_t n, int64_t k, void* part, hipStream_t st,
                          QLoad ql = QLoad()) {
   GemmParams p{};
@@ -260,7 +284,7 @@ w8a8_status run_gemm_raw(const Plan& pl, bool bf16, const void* A, int64_t lda, 
   p.N = (int)n;
   p.rb_a = (int)ceil_div(m, 16);
   p.rb_b = (int)ceil_div(n, 16);
-  p.kb_count = (int)(bf16 ? ceil_div(k, kFragK16) : ceil_div(k, kFragK8));
+  p.kb_count = (int)(dt == DT_BF16 ? ceil_div(k, kFragK16) : ceil_div(k, kFragK8));
   p.kchunk = pl.kchunk;
   p.splits = pl.splits;
   p.out = part;
@@ -268,9 +292,9 @@ w8a8_status run_gemm_raw(const Plan& pl, bool bf16, const void* A, int64_t lda, 
   p.part = pl.splits > 1 ? part : nullptr;
   p.group_m = env_int("W8A8_GROUP_M", 0);
   p.rotate = env_int("W8A8_ROTATE", 1);
-  const int epi = bf16 ? EPI_F32 : EPI_I32;
-  hipError_t e = pl.stream ? launch_gemm_stream(bf16, epi, pl.mb, pl.nw, pl.wk, p, pl.nbpb, st)
-                           : launch_gemm_tile(bf16, epi, pl.tile, p, st);
+  const int epi = dt == DT_BF16 ? EPI_F32 : EPI_I32;  // raw sums (fp32 for float types)
+  hipError_t e = pl.stream ? launch_gemm_stream(dt, epi, pl.mb, pl.nw, pl.wk, p, pl.nbpb, st)
+                           : launch_gemm_tile(dt, epi, pl.tile, p, st);
   return hip_check(e, pl.stream ? "gemm_stream" : "gemm_tile");
 }
 
@@ -322,9 +346,9 @@ w8a8_status check_desc(const w8a8_linear_desc* d) {
 struct LinearWs {
   size_t qx, sx, gemm, total;
 };
-LinearWs linear_ws(int64_t m, int64_t n, int64_t k) {
+LinearWs linear_ws(int64_t m, int64_t n, int64_t k, int dt = DT_I8) {
   LinearWs w;
-  Plan pl = plan_gemm(m, n, k, false, false);
+  Plan pl = plan_gemm(m, n, k, dt, false);
   w.qx = 0;
   w.sx = align256(w8a8_packed_bytes(m, k));
   w.gemm = w.sx + align256((size_t)m * 4);
@@ -335,9 +359,9 @@ LinearWs linear_ws(int64_t m, int64_t n, int64_t k) {
 struct FfnWs {
   size_t qx, sx, h, qh, sh, gemm, total;
 };
-FfnWs ffn_ws(int64_t m, int64_t d, int64_t f) {
+FfnWs ffn_ws(int64_t m, int64_t d, int64_t f, int dt = DT_I8) {
   FfnWs w;
-  Plan pd = plan_gemm(m, d, f, false, false);
+  Plan pd = plan_gemm(m, d, f, dt, false);
   w.qx = 0;
   w.sx = align256(w8a8_packed_bytes(m, d));
   w.h = w.sx + align256((size_t)m * 4);
@@ -353,7 +377,7 @@ struct Bf16FfnWs {
 };
 Bf16FfnWs bf16_ffn_ws(int64_t m, int64_t d, int64_t f) {
   Bf16FfnWs w;
-  Plan pd = plan_gemm(m, d, f, true, false);
+  Plan pd = plan_gemm(m, d, f, DT_BF16, false);
   w.h = 0;
   w.gemm_dn = align256((size_t)m * f * 2);
   w.total = w.gemm_dn + plan_ws_bytes(pd, m, d);
@@ -362,7 +386,7 @@ Bf16FfnWs bf16_ffn_ws(int64_t m, int64_t d, int64_t f) {
 }
 
 size_t bf16_linear_ws(int64_t m, int64_t n, int64_t k) {
-  return plan_ws_bytes(plan_gemm(m, n, k, true, false), m, n);
+  return plan_ws_bytes(plan_gemm(m, n, k, DT_BF16, false), m, n);
 }
 
 // Stack workspace: token stream, next-consumer input (bf16 and codes), FFN
@@ -372,7 +396,7 @@ size_t bf16_linear_ws(int64_t m, int64_t n, int64_t k) {
 // glue launch, so the plan may split K more freely than a standalone call.
 // Experiment hooks: W8A8_DOWN_TILE, W8A8_DOWN_SPLITS.
 Plan stack_down_plan(int64_t m, int64_t d, int64_t f) {
-  Plan p = plan_gemm(m, d, f, false, false);
+  Plan p = plan_gemm(m, d, f, DT_I8, false);
   if (p.stream) return p;
   p.tile = env_int("W8A8_DOWN_TILE", p.tile);
   const int64_t kb = ceil_div(f, kFragK8);
@@ -387,9 +411,9 @@ struct StackWs {
 };
 StackWs stack_ws(int64_t m, int64_t d, int64_t f, int64_t vocab) {
   StackWs w;
-  const Plan p8 = stack_down_plan(m, d, f), p16 = plan_gemm(m, d, f, true, false);
+  const Plan p8 = stack_down_plan(m, d, f), p16 = plan_gemm(m, d, f, DT_BF16, false);
   const size_t part = (size_t)std::max(p8.splits, p16.splits) * m * d * 4;
-  const size_t lm = std::max(plan_ws_bytes(plan_gemm(m, vocab, d, false, false), m, vocab),
+  const size_t lm = std::max(plan_ws_bytes(plan_gemm(m, vocab, d, DT_I8, false), m, vocab),
                              bf16_linear_ws(m, vocab, d));
   w.x = 0;
   w.a = w.x + align256((size_t)m * d * 2);
@@ -407,54 +431,56 @@ StackWs stack_ws(int64_t m, int64_t d, int64_t f, int64_t vocab) {
 // ------------------------------------------------------------------ pipelines
 
 w8a8_status quant_act_impl(const void* x, bool bf16, int64_t m, int64_t k, const float* delta,
-                           void* qx, float* sx, hipStream_t st) {
-  return hip_check(launch_quant_rows(x, bf16, false, m, k, delta, (int8_t*)qx, sx, st),
+                           void* qx, float* sx, hipStream_t st, int dt = DT_I8) {
+  return hip_check(launch_quant_rows(x, bf16, false, m, k, delta, (int8_t*)qx, sx, st,
+                                     dt == DT_F8),
                    "quant_rows");
 }
 
 w8a8_status linear_impl(const w8a8_linear_desc* d, const void* x, bool x_bf16, int64_t m, void* y,
-                        int epi, void* ws, hipStream_t st) {
-  LinearWs w = linear_ws(m, d->n, d->k);
+                        int epi, void* ws, hipStream_t st, int dt = DT_I8) {
+  LinearWs w = linear_ws(m, d->n, d->k, dt);
   char* base = (char*)ws;
-  Plan pl = plan_gemm(m, d->n, d->k, false, false);
+  Plan pl = plan_gemm(m, d->n, d->k, dt, false);
   if (x_bf16 && plan_qloads(pl, m, d->k))  // one launch: the GEMM quantises x itself
-    return run_gemm(pl, false, epi, nullptr, 0, m, d->wq, nullptr, d->n, d->k, nullptr, d->s_w,
+    return run_gemm(pl, DT_I8, epi, nullptr, 0, m, d->wq, nullptr, d->n, d->k, nullptr, d->s_w,
                     nullptr, y, d->n, base + w.gemm, st, QLoad{(const uint16_t*)x, d->delta});
-  CHECK(quant_act_impl(x, x_bf16, m, d->k, d->delta, base + w.qx, (float*)(base + w.sx), st));
-  return run_gemm(pl, false, epi, base + w.qx, 0, m, d->wq, nullptr, d->n, d->k,
+  CHECK(quant_act_impl(x, x_bf16, m, d->k, d->delta, base + w.qx, (float*)(base + w.sx), st, dt));
+  return run_gemm(pl, dt, epi, base + w.qx, 0, m, d->wq, nullptr, d->n, d->k,
                   (const float*)(base + w.sx), d->s_w, nullptr, y, d->n, base + w.gemm, st);
 }
 
 w8a8_status ffn_impl(const w8a8_ffn_desc* d, const void* x, int64_t m, void* y, void* ws,
-                     hipStream_t st) {
-  FfnWs w = ffn_ws(m, d->d, d->f);
+                     hipStream_t st, int dt = DT_I8) {
+  FfnWs w = ffn_ws(m, d->d, d->f, dt);
   char* base = (char*)ws;
-  Plan pg = plan_gemm(m, d->f, d->d, false, true);
+  Plan pg = plan_gemm(m, d->f, d->d, dt, true);
   if (plan_qloads(pg, m, d->d)) {
-    CHECK(run_gemm(pg, false, EPI_GLU, nullptr, 0, m, d->wq_gate, d->wq_up, d->f, d->d, nullptr,
+    CHECK(run_gemm(pg, DT_I8, EPI_GLU, nullptr, 0, m, d->wq_gate, d->wq_up, d->f, d->d, nullptr,
                    d->s_gate, d->s_up, base + w.h, d->f, nullptr, st,
                    QLoad{(const uint16_t*)x, d->delta_gu}));
   } else {
-    CHECK(quant_act_impl(x, true, m, d->d, d->delta_gu, base + w.qx, (float*)(base + w.sx), st));
-    CHECK(run_gemm(pg, false, EPI_GLU, base + w.qx, 0, m, d->wq_gate, d->wq_up, d->f, d->d,
+    CHECK(quant_act_impl(x, true, m, d->d, d->delta_gu, base + w.qx, (float*)(base + w.sx), st,
+                         dt));
+    CHECK(run_gemm(pg, dt, EPI_GLU, base + w.qx, 0, m, d->wq_gate, d->wq_up, d->f, d->d,
                    (const float*)(base + w.sx), d->s_gate, d->s_up, base + w.h, d->f, nullptr,
                    st));
   }
-  Plan pd = plan_gemm(m, d->d, d->f, false, false);
+  Plan pd = plan_gemm(m, d->d, d->f, dt, false);
   if (plan_qloads(pd, m, d->f))
-    return run_gemm(pd, false, EPI_BF16, nullptr, 0, m, d->wq_down, nullptr, d->d, d->f, nullptr,
+    return run_gemm(pd, DT_I8, EPI_BF16, nullptr, 0, m, d->wq_down, nullptr, d->d, d->f, nullptr,
                     d->s_down, nullptr, y, d->d, base + w.gemm, st,
                     QLoad{(const uint16_t*)(base + w.h), d->delta_down});
   CHECK(quant_act_impl(base + w.h, true, m, d->f, d->delta_down, base + w.qh,
-                       (float*)(base + w.sh), st));
-  return run_gemm(pd, false, EPI_BF16, base + w.qh, 0, m, d->wq_down, nullptr, d->d, d->f,
+                       (float*)(base + w.sh), st, dt));
+  return run_gemm(pd, dt, EPI_BF16, base + w.qh, 0, m, d->wq_down, nullptr, d->d, d->f,
                   (const float*)(base + w.sh), d->s_down, nullptr, y, d->d, base + w.gemm, st);
 }
 
 w8a8_status bf16_linear_impl(const void* x, int64_t m, const void* wp, int64_t n, int64_t k,
                              void* y, void* ws, hipStream_t st) {
-  Plan pl = plan_gemm(m, n, k, true, false);
-  return run_gemm(pl, true, EPI_BF16, x, k, m, wp, nullptr, n, k, nullptr, nullptr, nullptr, y, n,
+  Plan pl = plan_gemm(m, n, k, DT_BF16, false);
+  return run_gemm(pl, DT_BF16, EPI_BF16, x, k, m, wp, nullptr, n, k, nullptr, nullptr, nullptr, y, n,
                   ws, st);
 }
 
@@ -462,11 +488,11 @@ w8a8_status bf16_ffn_impl(const w8a8_bf16_ffn_desc* d, const void* x, int64_t m,
                           void* ws, hipStream_t st) {
   Bf16FfnWs w = bf16_ffn_ws(m, d->d, d->f);
   char* base = (char*)ws;
-  Plan pg = plan_gemm(m, d->f, d->d, true, true);
-  CHECK(run_gemm(pg, true, EPI_GLU, x, d->d, m, d->wp_gate, d->wp_up, d->f, d->d, nullptr, nullptr,
+  Plan pg = plan_gemm(m, d->f, d->d, DT_BF16, true);
+  CHECK(run_gemm(pg, DT_BF16, EPI_GLU, x, d->d, m, d->wp_gate, d->wp_up, d->f, d->d, nullptr, nullptr,
                  nullptr, base + w.h, d->f, nullptr, st));
-  Plan pd = plan_gemm(m, d->d, d->f, true, false);
-  return run_gemm(pd, true, EPI_BF16, base + w.h, d->f, m, d->wp_down, nullptr, d->d, d->f,
+  Plan pd = plan_gemm(m, d->d, d->f, DT_BF16, false);
+  return run_gemm(pd, DT_BF16, EPI_BF16, base + w.h, d->f, m, d->wp_down, nullptr, d->d, d->f,
                   nullptr, nullptr, nullptr, y, d->d, base + w.gemm_dn, st);
 }
 
@@ -613,13 +639,13 @@ w8a8_status w8a8_gemm_i8_i32(const void* qx, int64_t m, const void* wq, int64_t 
   CHECK_PTR(acc);
   REQUIRE(m >= 1 && n >= 1, W8A8_EINVAL, "m or n < 1");
   CHECK(check_k(k));
-  Plan pl = plan_gemm(m, n, k, false, false);
+  Plan pl = plan_gemm(m, n, k, DT_I8, false);
   size_t need = plan_ws_bytes(pl, m, n);
   if (need) {
     CHECK_PTR(ws);
     REQUIRE(ws_bytes >= need, W8A8_EWORKSPACE, "workspace too small");
   }
-  return run_gemm(pl, false, EPI_I32, qx, 0, m, wq, nullptr, n, k, nullptr, nullptr, nullptr, acc,
+  return run_gemm(pl, DT_I8, EPI_I32, qx, 0, m, wq, nullptr, n, k, nullptr, nullptr, nullptr, acc,
                   n, ws, S(stream));
 }
 
@@ -665,8 +691,8 @@ w8a8_status w8a8_ffn_gate_up(const w8a8_ffn_desc* desc, const void* qx, const fl
   CHECK_PTR(s_x);
   CHECK_PTR(h);
   REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
-  Plan pg = plan_gemm(m, desc->f, desc->d, false, true);
-  return run_gemm(pg, false, EPI_GLU, qx, 0, m, desc->wq_gate, desc->wq_up, desc->f, desc->d, s_x,
+  Plan pg = plan_gemm(m, desc->f, desc->d, DT_I8, true);
+  return run_gemm(pg, DT_I8, EPI_GLU, qx, 0, m, desc->wq_gate, desc->wq_up, desc->f, desc->d, s_x,
                   desc->s_gate, desc->s_up, h, desc->f, nullptr, S(stream));
 }
 
@@ -696,6 +722,132 @@ w8a8_status w8a8_lm_head(const w8a8_linear_desc* desc, const void* x, int64_t m,
   REQUIRE(ws_bytes >= w8a8_lm_head_workspace_bytes(m, desc->n, desc->k), W8A8_EWORKSPACE,
           "workspace too small");
   return linear_impl(desc, x, true, m, logits, EPI_BF16, ws, S(stream));
+}
+
+// ---------------------------------------------------------------- FP8 variant
+
+static w8a8_status check_k_f8(int64_t k) {
+  CHECK(check_k(k));
+  REQUIRE(k % 128 == 0, W8A8_EUNSUPPORTED, "k must be a multiple of 128 on the FP8 path");
+  return W8A8_OK;
+}
+
+size_t w8a8_fp8_linear_workspace_bytes(int64_t m, int64_t n, int64_t k) {
+  if (m < 1 || n < 1 || k < 1) return 0;
+  return linear_ws(m, n, k, DT_F8).total;
+}
+
+size_t w8a8_fp8_ffn_workspace_bytes(int64_t m, int64_t d, int64_t f) {
+  if (m < 1 || d < 1 || f < 1) return 0;
+  return ffn_ws(m, d, f, DT_F8).total;
+}
+
+w8a8_status w8a8_fp8_quantize_weights(const void* w, w8a8_dtype wt, int64_t n, int64_t k,
+                                      const float* delta, void* wq, float* s_w,
+                                      w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(w);
+  CHECK_PTR(wq);
+  CHECK_PTR(s_w);
+  if (delta) CHECK_PTR(delta);
+  REQUIRE(n >= 1, W8A8_EINVAL, "n < 1");
+  CHECK(check_k(k));
+  REQUIRE(wt == W8A8_F32 || wt == W8A8_BF16, W8A8_EUNSUPPORTED, "w dtype");
+  return hip_check(launch_quant_rows(w, wt == W8A8_BF16, true, n, k, delta, (int8_t*)wq, s_w,
+                                     S(stream), true),
+                   "quant_rows");
+}
+
+w8a8_status w8a8_fp8_quantize_act(const void* x, w8a8_dtype xt, int64_t m, int64_t k,
+                                  const float* delta, void* qx, float* s_x, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(x);
+  CHECK_PTR(qx);
+  CHECK_PTR(s_x);
+  if (delta) CHECK_PTR(delta);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  CHECK(check_k(k));
+  REQUIRE(xt == W8A8_F32 || xt == W8A8_BF16, W8A8_EUNSUPPORTED, "x dtype");
+  return quant_act_impl(x, xt == W8A8_BF16, m, k, delta, qx, s_x, S(stream), DT_F8);
+}
+
+w8a8_status w8a8_fp8_gemm_f32(const void* qx, int64_t m, const void* wq, int64_t n, int64_t k,
+                              float* acc, void* ws, size_t ws_bytes, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(qx);
+  CHECK_PTR(wq);
+  CHECK_PTR(acc);
+  REQUIRE(m >= 1 && n >= 1, W8A8_EINVAL, "m or n < 1");
+  CHECK(check_k_f8(k));
+  Plan pl = plan_gemm(m, n, k, DT_F8, false);
+  size_t need = plan_ws_bytes(pl, m, n);
+  if (need) {
+    CHECK_PTR(ws);
+    REQUIRE(ws_bytes >= need, W8A8_EWORKSPACE, "workspace too small");
+  }
+  return run_gemm(pl, DT_F8, EPI_I32, qx, 0, m, wq, nullptr, n, k, nullptr, nullptr, nullptr, acc,
+                  n, ws, S(stream));
+}
+
+w8a8_status w8a8_fp8_linear(const w8a8_linear_desc* desc, const void* x, w8a8_dtype xt,
+                            int64_t m, void* y, w8a8_dtype yt, void* ws, size_t ws_bytes,
+                            w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK(check_desc(desc));
+  CHECK(check_k_f8(desc->k));
+  CHECK_PTR(x);
+  CHECK_PTR(y);
+  CHECK_PTR(ws);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  REQUIRE(xt == W8A8_F32 || xt == W8A8_BF16, W8A8_EUNSUPPORTED, "x dtype");
+  REQUIRE(yt == W8A8_F32 || yt == W8A8_BF16, W8A8_EUNSUPPORTED, "y dtype");
+  REQUIRE(ws_bytes >= w8a8_fp8_linear_workspace_bytes(m, desc->n, desc->k), W8A8_EWORKSPACE,
+          "workspace too small");
+  return linear_impl(desc, x, xt == W8A8_BF16, m, y, yt == W8A8_BF16 ? EPI_BF16 : EPI_F32, ws,
+                     S(stream), DT_F8);
+}
+
+w8a8_status w8a8_fp8_ffn_gate_up(const w8a8_ffn_desc* desc, const void* qx, const float* s_x,
+                                 int64_t m, void* h, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK(check_ffn_desc(desc));
+  CHECK(check_k_f8(desc->d));
+  CHECK_PTR(qx);
+  CHECK_PTR(s_x);
+  CHECK_PTR(h);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  Plan pg = plan_gemm(m, desc->f, desc->d, DT_F8, true);
+  return run_gemm(pg, DT_F8, EPI_GLU, qx, 0, m, desc->wq_gate, desc->wq_up, desc->f, desc->d, s_x,
+                  desc->s_gate, desc->s_up, h, desc->f, nullptr, S(stream));
+}
+
+w8a8_status w8a8_fp8_ffn(const w8a8_ffn_desc* desc, const void* x, int64_t m, void* y, void* ws,
+                         size_t ws_bytes, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK(check_ffn_desc(desc));
+  CHECK(check_k_f8(desc->d));
+  CHECK(check_k_f8(desc->f));
+  CHECK_PTR(x);
+  CHECK_PTR(y);
+  CHECK_PTR(ws);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  REQUIRE(ws_bytes >= w8a8_fp8_ffn_workspace_bytes(m, desc->d, desc->f), W8A8_EWORKSPACE,
+          "workspace too small");
+  return ffn_impl(desc, x, m, y, ws, S(stream), DT_F8);
+}
+
+w8a8_status w8a8_fp8_lm_head(const w8a8_linear_desc* desc, const void* x, int64_t m,
+                             void* logits, void* ws, size_t ws_bytes, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK(check_desc(desc));
+  CHECK(check_k_f8(desc->k));
+  CHECK_PTR(x);
+  CHECK_PTR(logits);
+  CHECK_PTR(ws);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  REQUIRE(ws_bytes >= w8a8_fp8_linear_workspace_bytes(m, desc->n, desc->k), W8A8_EWORKSPACE,
+          "workspace too small");
+  return linear_impl(desc, x, true, m, logits, EPI_BF16, ws, S(stream), DT_F8);
 }
 
 // ---------------------------------------------------------------- bf16 path
@@ -734,8 +886,8 @@ w8a8_status w8a8_bf16_ffn_gate_up(const w8a8_bf16_ffn_desc* desc, const void* x,
   CHECK_PTR(x);
   CHECK_PTR(h);
   REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
-  Plan pg = plan_gemm(m, desc->f, desc->d, true, true);
-  return run_gemm(pg, true, EPI_GLU, x, desc->d, m, desc->wp_gate, desc->wp_up, desc->f, desc->d,
+  Plan pg = plan_gemm(m, desc->f, desc->d, DT_BF16, true);
+  return run_gemm(pg, DT_BF16, EPI_GLU, x, desc->d, m, desc->wp_gate, desc->wp_up, desc->f, desc->d,
                   nullptr, nullptr, nullptr, h, desc->f, nullptr, S(stream));
 }
 
@@ -852,8 +1004,8 @@ w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec, int
   int8_t* qh = (int8_t*)(base + w.qh);
   float* sh = (float*)(base + w.sh);
   void* part = base + w.part;
-  const Plan p8 = stack_down_plan(m, d, f), p16 = plan_gemm(m, d, f, true, false);
-  const Plan pg8 = plan_gemm(m, f, d, false, true), pg16 = plan_gemm(m, f, d, true, true);
+  const Plan p8 = stack_down_plan(m, d, f), p16 = plan_gemm(m, d, f, DT_BF16, false);
+  const Plan pg8 = plan_gemm(m, f, d, DT_I8, true), pg16 = plan_gemm(m, f, d, DT_BF16, true);
 
   // Glue launch l (0..n_layers): FFN output of layer l-1 into the token
   // stream (none for l = 0, which copies x in), then the pre-norm input of
@@ -892,27 +1044,27 @@ w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec, int
     CHECK(glue(l));
     if (prec[l]) {
       const w8a8_ffn_desc* L = &desc->int8_ffn[l];
-      CHECK(run_gemm(pg8, false, EPI_GLU, q, 0, m, L->wq_gate, L->wq_up, f, d, s, L->s_gate,
+      CHECK(run_gemm(pg8, DT_I8, EPI_GLU, q, 0, m, L->wq_gate, L->wq_up, f, d, s, L->s_gate,
                      L->s_up, h, f, nullptr, st));
       if (plan_qloads(p8, m, f)) {
-        CHECK(run_gemm_raw(p8, false, nullptr, 0, m, L->wq_down, d, f, part, st,
+        CHECK(run_gemm_raw(p8, DT_I8, nullptr, 0, m, L->wq_down, d, f, part, st,
                            QLoad{h, L->delta_down, sh}));
       } else {
         CHECK(quant_act_impl(h, true, m, f, L->delta_down, qh, sh, st));
-        CHECK(run_gemm_raw(p8, false, qh, 0, m, L->wq_down, d, f, part, st));
+        CHECK(run_gemm_raw(p8, DT_I8, qh, 0, m, L->wq_down, d, f, part, st));
       }
     } else {
       const w8a8_bf16_ffn_desc* L = &desc->bf16_ffn[l];
-      CHECK(run_gemm(pg16, true, EPI_GLU, a, d, m, L->wp_gate, L->wp_up, f, d, nullptr, nullptr,
+      CHECK(run_gemm(pg16, DT_BF16, EPI_GLU, a, d, m, L->wp_gate, L->wp_up, f, d, nullptr, nullptr,
                      nullptr, h, f, nullptr, st));
-      CHECK(run_gemm_raw(p16, true, h, f, m, L->wp_down, d, f, part, st));
+      CHECK(run_gemm_raw(p16, DT_BF16, h, f, m, L->wp_down, d, f, part, st));
     }
   }
   CHECK(glue(desc->n_layers));
   const int64_t V = desc->vocab;
   if (lm_head_int8) {
-    const Plan pl = plan_gemm(m, V, d, false, false);
-    return run_gemm(pl, false, EPI_BF16, q, 0, m, desc->lm_head_int8.wq, nullptr, V, d, s,
+    const Plan pl = plan_gemm(m, V, d, DT_I8, false);
+    return run_gemm(pl, DT_I8, EPI_BF16, q, 0, m, desc->lm_head_int8.wq, nullptr, V, d, s,
                     desc->lm_head_int8.s_w, nullptr, logits, V, base + w.lm, st);
   }
   return bf16_linear_impl(a, m, desc->lm_head_bf16, V, d, logits, base + w.lm, st);

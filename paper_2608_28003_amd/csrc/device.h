@@ -55,6 +55,22 @@ __device__ __forceinline__ v4f mma_bf16(v4i a, v4i b, v4f c) {
                                                  __builtin_bit_cast(v8bf, b), c, 0, 0, 0);
 }
 
+// FP8 E4M3 x E4M3 -> fp32, K = 128: the two 16 x 64 fragments of each operand
+// are concatenated per lane (fragment 0's 16 bytes, then fragment 1's).  Any
+// assignment of K positions to lanes works as long as A and B use the same one.
+typedef int v8i __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ v4f mma_f8(v4i a0, v4i a1, v4i b0, v4i b1, v4f c) {
+  const v8i a = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+  const v8i b = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+  // formats 0 / 0: both operands OCP E4M3; no block scales
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+
+// binary32 pair -> two E4M3 codes (round to nearest even), low 16 bits
+__device__ __forceinline__ uint32_t e4m3_pack2(float lo, float hi) {
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(lo, hi, 0, false) & 0xffffu;
+}
+
 // GELU with the tanh form, binary32 operations in a fixed order (the library
 // is compiled without floating-point contraction).
 __device__ __forceinline__ float gelu_tanh(float x) {

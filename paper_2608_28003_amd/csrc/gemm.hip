@@ -5,6 +5,10 @@
 // epilogue applies the two scales, y = (float(acc) * s_t) * s_i.
 // bf16 path (the layers a precision map keeps in bf16): A is row-major bf16,
 // B packed bf16, products on v_mfma_f32_16x16x32_bf16 with fp32 sums.
+// FP8 path (E4M3 codes, packed like int8): one v_mfma_f32_16x16x128_f8f6f4
+// takes two consecutive 16 x 64 fragments of A and of B (the same lane-to-K
+// assignment on both sides, so the pair covers 128 K values) into fp32 sums;
+// scales as on the int8 path.
 //
 // Every operand fragment is 1024 contiguous bytes in lane order, so one
 // 16-byte load per lane moves a whole fragment, global_load_lds_dwordx4 can
@@ -43,26 +47,39 @@ __device__ __forceinline__ v4i load_frag_rowmajor_bf16(const void* base, int64_t
   return *reinterpret_cast<const v4i*>(p);
 }
 
-template <bool BF16>
+template <int DT>
 struct Acc;
 template <>
-struct Acc<false> {
+struct Acc<DT_I8> {
   typedef v4i T;
   static __device__ __forceinline__ T zero() { return v4i{0, 0, 0, 0}; }
   static __device__ __forceinline__ T mma(v4i a, v4i b, T c) { return mma_i8(a, b, c); }
 };
 template <>
-struct Acc<true> {
+struct Acc<DT_BF16> {
   typedef v4f T;
   static __device__ __forceinline__ T zero() { return v4f{0.f, 0.f, 0.f, 0.f}; }
   static __device__ __forceinline__ T mma(v4i a, v4i b, T c) { return mma_bf16(a, b, c); }
 };
+template <>
+struct Acc<DT_F8> {
+  typedef v4f T;
+  static __device__ __forceinline__ T zero() { return v4f{0.f, 0.f, 0.f, 0.f}; }
+  // two consecutive 16 x 64 fragments of A and B: K = 128
+  static __device__ __forceinline__ T mma2(v4i a0, v4i a1, v4i b0, v4i b1, T c) {
+    return mma_f8(a0, a1, b0, b1, c);
+  }
+};
+
+// fragments consumed by one MFMA of a type
+template <int DT>
+constexpr int frags_per_mma() { return DT == DT_F8 ? 2 : 1; }
 
 // Dequantised / converted value of one accumulator element.
-template <bool BF16>
+template <int DT>
 __device__ __forceinline__ float acc_value(float a_or_i, const GemmParams& p, int row, int col,
                                            const float* s_b) {
-  if constexpr (BF16) {
+  if constexpr (DT == DT_BF16) {
     return a_or_i;
   } else {
     float t = a_or_i * p.s_a[row];
@@ -71,14 +88,17 @@ __device__ __forceinline__ float acc_value(float a_or_i, const GemmParams& p, in
 }
 
 // Store one output element for the non-gated epilogues.
-template <bool BF16, int EPI>
+template <int DT, int EPI>
 __device__ __forceinline__ void store_elem(const GemmParams& p, int row, int col, int32_t iacc,
                                            float facc) {
-  if constexpr (EPI == EPI_I32) {
-    reinterpret_cast<int32_t*>(p.out)[(int64_t)row * p.ldo + col] = iacc;
+  if constexpr (EPI == EPI_I32) {  // raw sums: int32, or fp32 for float types
+    if constexpr (DT != DT_I8)
+      reinterpret_cast<float*>(p.out)[(int64_t)row * p.ldo + col] = facc;
+    else
+      reinterpret_cast<int32_t*>(p.out)[(int64_t)row * p.ldo + col] = iacc;
   } else {
-    float raw = BF16 ? facc : (float)iacc;
-    float y = acc_value<BF16>(raw, p, row, col, p.s_b);
+    float raw = DT != DT_I8 ? facc : (float)iacc;
+    float y = acc_value<DT>(raw, p, row, col, p.s_b);
     if constexpr (EPI == EPI_F32)
       reinterpret_cast<float*>(p.out)[(int64_t)row * p.ldo + col] = y;
     else
@@ -86,20 +106,20 @@ __device__ __forceinline__ void store_elem(const GemmParams& p, int row, int col
   }
 }
 
-template <bool BF16>
+template <int DT>
 __device__ __forceinline__ void store_glu(const GemmParams& p, int row, int col, float g_raw,
                                           float u_raw) {
-  float g = acc_value<BF16>(g_raw, p, row, col, p.s_b);
-  float u = acc_value<BF16>(u_raw, p, row, col, p.s_b2);
+  float g = acc_value<DT>(g_raw, p, row, col, p.s_b);
+  float u = acc_value<DT>(u_raw, p, row, col, p.s_b2);
   float h = gelu_tanh(g) * u;
   reinterpret_cast<uint16_t*>(p.out)[(int64_t)row * p.ldo + col] = float_to_bf16_bits(h);
 }
 
-template <bool BF16>
+template <int DT>
 __device__ __forceinline__ void write_partial(const GemmParams& p, int z, int row, int col,
                                               int32_t iacc, float facc) {
   const int64_t idx = (int64_t)z * p.M * p.N + (int64_t)row * p.N + col;
-  if constexpr (BF16)
+  if constexpr (DT != DT_I8)
     reinterpret_cast<float*>(p.part)[idx] = facc;
   else
     reinterpret_cast<int32_t*>(p.part)[idx] = iacc;
@@ -152,9 +172,13 @@ __device__ __forceinline__ void wait_outstanding(int n) {
 // Workgroups are dealt to the 8 XCDs round-robin by ID; the tile order gives
 // every XCD a contiguous range of tiles (M tile fastest), so the A and B
 // panels a range touches stay in that XCD's L2.
-template <bool BF16, int BM, int BN, int WAVES_M, int NW, int EPI, int S, int KS>
+template <int DT, int BM, int BN, int WAVES_M, int NW, int EPI, int S, int KS>
 __global__ __launch_bounds__(64 * NW, 2) void gemm_tile_kernel(GemmParams p) {
   constexpr bool GLU = (EPI == EPI_GLU);
+  constexpr bool BF16 = (DT == DT_BF16);  // row-major bf16 A, unscaled fp32 sums
+  constexpr bool FACC = (DT != DT_I8);    // fp32 accumulators and partial sums
+  constexpr int KP = frags_per_mma<DT>();
+  static_assert(KS % KP == 0, "a stage must hold whole MFMA K steps");
   constexpr int WAVES_N = NW / WAVES_M;
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int TM = WM / 16, TN = WN / 16;
@@ -163,7 +187,7 @@ __global__ __launch_bounds__(64 * NW, 2) void gemm_tile_kernel(GemmParams p) {
   constexpr int NF = NA + NB;
   static_assert(NF % NW == 0, "fragments per stage must split over the waves");
   constexpr int PF = NF / NW;  // fragment rows each wave fetches per stage (KS fragments each)
-  typedef typename Acc<BF16>::T AccT;
+  typedef typename Acc<DT>::T AccT;
 
   __shared__ v4i lds[S][NF * KS * 64];
 
@@ -250,8 +274,8 @@ __global__ __launch_bounds__(64 * NW, 2) void gemm_tile_kernel(GemmParams p) {
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-      acc[i][j] = Acc<BF16>::zero();
-      if constexpr (GLU) accu[i][j] = Acc<BF16>::zero();
+      acc[i][j] = Acc<DT>::zero();
+      if constexpr (GLU) accu[i][j] = Acc<DT>::zero();
     }
 
   // Fragments of one stage held in registers: the LDS reads of stage j+1 are
@@ -280,18 +304,34 @@ __global__ __launch_bounds__(64 * NW, 2) void gemm_tile_kernel(GemmParams p) {
   auto mma_frags = [&](const Frags& F, int j) {
     const int nv = min(KS, nk - stage_of(j) * KS);  // valid fragment columns of stage j
 #pragma unroll
-    for (int k = 0; k < KS; ++k) {
+    for (int k = 0; k < KS; k += KP) {
       if (k > 0 && k >= nv) break;
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int t = 0; t < TN; ++t) acc[i][t] = Acc<BF16>::mma(F.a[k][i], F.b[k][t], acc[i][t]);
-      if constexpr (GLU) {
+      if constexpr (DT == DT_F8) {
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
           for (int t = 0; t < TN; ++t)
-            accu[i][t] = Acc<BF16>::mma(F.a[k][i], F.bu[k][t], accu[i][t]);
+            acc[i][t] = Acc<DT>::mma2(F.a[k][i], F.a[k + 1][i], F.b[k][t], F.b[k + 1][t], acc[i][t]);
+        if constexpr (GLU) {
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int t = 0; t < TN; ++t)
+              accu[i][t] = Acc<DT>::mma2(F.a[k][i], F.a[k + 1][i], F.bu[k][t], F.bu[k + 1][t],
+                                         accu[i][t]);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int t = 0; t < TN; ++t) acc[i][t] = Acc<DT>::mma(F.a[k][i], F.b[k][t], acc[i][t]);
+        if constexpr (GLU) {
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int t = 0; t < TN; ++t)
+              accu[i][t] = Acc<DT>::mma(F.a[k][i], F.bu[k][t], accu[i][t]);
+        }
       }
     }
   };
@@ -381,8 +421,8 @@ __global__ __launch_bounds__(64 * NW, 2) void gemm_tile_kernel(GemmParams p) {
             u = ((float)accu[i][t][r] * sa[i][r]) * sb2[t];
           }
           *reinterpret_cast<uint16_t*>(slot) = float_to_bf16_bits(gelu_tanh(g) * u);
-        } else if (partial || EPI == EPI_I32) {
-          if constexpr (BF16)
+        } else if (partial || EPI == EPI_I32) {  // raw sums: int32, or fp32 for float types
+          if constexpr (FACC)
             *reinterpret_cast<float*>(slot) = (float)acc[i][t][r];
           else
             *reinterpret_cast<int32_t*>(slot) = (int32_t)acc[i][t][r];
@@ -520,15 +560,18 @@ __device__ __forceinline__ void quantize_panel(const GemmParams& p, int kb0, int
   }
 }
 
-template <bool BF16, int MB, int EPI, int NW, int WK>
+template <int DT, int MB, int EPI, int NW, int WK>
 __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int nb_per_block) {
   static_assert(WK == 1 || WK == NW, "either every wave owns its column blocks or all share one");
   constexpr bool GLU = (EPI == EPI_GLU);
-  constexpr int KU = 9;  // weight fragments per batch and operand
+  constexpr bool BF16 = (DT == DT_BF16);
+  constexpr bool FACC = (DT != DT_I8);
+  constexpr int KP = frags_per_mma<DT>();
+  constexpr int KU = KP == 2 ? 8 : 9;  // weight fragments per batch and operand (whole MFMA steps)
   constexpr int KG = GLU ? KU : 1;
   constexpr int NC = GLU ? 2 : 1;
   constexpr int GROUPS = NW / WK;
-  typedef typename Acc<BF16>::T AccT;
+  typedef typename Acc<DT>::T AccT;
   extern __shared__ v4i lds_dyn[];
 
   const int lane = lane_id();
@@ -541,7 +584,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
   AccT* red = reinterpret_cast<AccT*>(lds_dyn + (int64_t)MB * p.kchunk * 64);  // (WK-1) x NC x MB
 
   // this wave's K slice [ks0, ks1) of the workgroup's range
-  const int kpw = (kc + WK - 1) / WK;
+  const int kpw = ((kc + WK - 1) / WK + KP - 1) / KP * KP;  // whole MFMA K steps per wave
   const int ks0 = min(kc, wk * kpw), ks1 = min(kc, ks0 + kpw);
   const int my_k = ks1 - ks0;
   const int bpn = (kpw + KU - 1) / KU;  // batches per column block (uniform over the waves)
@@ -564,7 +607,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
              frag_offset(min(mb, p.rb_a - 1), kb0 + kk, p.kb_count) + lane * 16;
     }
   };
-  constexpr bool QLOAD_OK = !BF16 && MB == 1;
+  constexpr bool QLOAD_OK = DT == DT_I8 && MB == 1;
   const bool qload = QLOAD_OK && p.a_x != nullptr;
   if (!qload) {
     if constexpr (WK > 1) {
@@ -636,9 +679,12 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
           }
           reinterpret_cast<uint16_t*>(p.out)[o] = float_to_bf16_bits(gelu_tanh(gv) * uv);
         } else if (p.splits > 1) {
-          write_partial<BF16>(p, z, row, col, BF16 ? 0 : (int32_t)acc[mb][r], (float)acc[mb][r]);
-        } else if constexpr (EPI == EPI_I32) {
-          reinterpret_cast<int32_t*>(p.out)[o] = (int32_t)acc[mb][r];
+          write_partial<DT>(p, z, row, col, FACC ? 0 : (int32_t)acc[mb][r], (float)acc[mb][r]);
+        } else if constexpr (EPI == EPI_I32) {  // raw sums: int32, or fp32 for float types
+          if constexpr (FACC)
+            reinterpret_cast<float*>(p.out)[o] = (float)acc[mb][r];
+          else
+            reinterpret_cast<int32_t*>(p.out)[o] = (int32_t)acc[mb][r];
         } else {
           float y;
           if constexpr (BF16)
@@ -659,8 +705,8 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
     if (bi == 0) {
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
-        acc[mb] = Acc<BF16>::zero();
-        if constexpr (GLU) accu[mb] = Acc<BF16>::zero();
+        acc[mb] = Acc<DT>::zero();
+        if constexpr (GLU) accu[mb] = Acc<DT>::zero();
       }
       if (scaled) {
         const int col = min(nb * 16 + (lane & 15), p.N - 1);
@@ -669,13 +715,19 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
       }
     }
 #pragma unroll
-    for (int u = 0; u < KU; ++u) {
+    for (int u = 0; u < KU; u += KP) {
       if (k0 + u < my_k) {
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
           const v4i a = lds_a[(mb * p.kchunk + ks0 + k0 + u) * 64 + lane];
-          acc[mb] = Acc<BF16>::mma(a, b[u], acc[mb]);
-          if constexpr (GLU) accu[mb] = Acc<BF16>::mma(a, bu[u], accu[mb]);
+          if constexpr (DT == DT_F8) {
+            const v4i a1 = lds_a[(mb * p.kchunk + ks0 + k0 + u + 1) * 64 + lane];
+            acc[mb] = Acc<DT>::mma2(a, a1, b[u], b[u + 1], acc[mb]);
+            if constexpr (GLU) accu[mb] = Acc<DT>::mma2(a, a1, bu[u], bu[u + 1], accu[mb]);
+          } else {
+            acc[mb] = Acc<DT>::mma(a, b[u], acc[mb]);
+            if constexpr (GLU) accu[mb] = Acc<DT>::mma(a, bu[u], accu[mb]);
+          }
         }
       }
     }
@@ -721,8 +773,9 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
 
 // out = epilogue(sum over z of part[z]) for 4 consecutive columns per thread,
 // the splits added in order (int32 exactly; fp32 in a fixed order).
-template <bool BF16, int EPI>
+template <int DT, int EPI>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmParams p) {
+  constexpr bool FACC = (DT != DT_I8);
   const int64_t n4 = (p.N + 3) / 4;
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (int64_t)p.M * n4) return;
@@ -738,7 +791,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmParams p) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       if (c < ncol) {
-        if constexpr (BF16)
+        if constexpr (FACC)
           fsum[c] += reinterpret_cast<const float*>(p.part)[base + c];
         else
           isum[c] += reinterpret_cast<const int32_t*>(p.part)[base + c];
@@ -747,12 +800,14 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmParams p) {
   }
 #pragma unroll
   for (int c = 0; c < 4; ++c)
-    if (c < ncol) store_elem<BF16, EPI>(p, row, col0 + c, isum[c], fsum[c]);
+    if (c < ncol) store_elem<DT, EPI>(p, row, col0 + c, isum[c], fsum[c]);
 }
 
 // ------------------------------------------------------------------ dispatch
 
-template <bool BF16, int EPI>
+// Tile shapes per type: FP8 needs stages of whole 128-deep MFMA steps, so only
+// the shapes with two fragment columns per stage exist for it.
+template <int DT, int EPI>
 static hipError_t tile_dispatch(int tile, const GemmParams& p, hipStream_t st) {
   auto grid_for = [&](int bm, int bn) {
     int mt = (p.M + bm - 1) / bm;
@@ -760,76 +815,91 @@ static hipError_t tile_dispatch(int tile, const GemmParams& p, hipStream_t st) {
     int per_xcd = (mt * nt + 7) / 8;
     return dim3((unsigned)(8 * per_xcd), (unsigned)p.splits);
   };
+  constexpr bool K1 = DT != DT_F8;  // single-fragment stages available
   if constexpr (EPI == EPI_GLU) {
     switch (tile) {
-      case TILE_GLU_128x32:
-        gemm_tile_kernel<BF16, 128, 32, 4, 4, EPI, 12, 1><<<grid_for(128, 32), 256, 0, st>>>(p);
-        break;
-      case TILE_GLU_64x64:
-        gemm_tile_kernel<BF16, 64, 64, 2, 4, EPI, 6, 1><<<grid_for(64, 64), 256, 0, st>>>(p);
-        break;
-      case TILE_GLU_128x64:
-        gemm_tile_kernel<BF16, 128, 64, 2, 4, EPI, 5, 1><<<grid_for(128, 64), 256, 0, st>>>(p);
-        break;
-      case TILE_GLU_256x128:
-        gemm_tile_kernel<BF16, 256, 128, 2, 8, EPI, 5, 1><<<grid_for(256, 128), 512, 0, st>>>(p);
-        break;
       case TILE_GLU_128x32_K2:
-        gemm_tile_kernel<BF16, 128, 32, 4, 4, EPI, 6, 2><<<grid_for(128, 32), 256, 0, st>>>(p);
-        break;
+        gemm_tile_kernel<DT, 128, 32, 4, 4, EPI, 6, 2><<<grid_for(128, 32), 256, 0, st>>>(p);
+        return hipGetLastError();
       case TILE_GLU_64x64_K2:
-        gemm_tile_kernel<BF16, 64, 64, 2, 4, EPI, 3, 2><<<grid_for(64, 64), 256, 0, st>>>(p);
-        break;
-      case TILE_GLU_256x64:
-        gemm_tile_kernel<BF16, 256, 64, 2, 4, EPI, 3, 1><<<grid_for(256, 64), 256, 0, st>>>(p);
-        break;
+        gemm_tile_kernel<DT, 64, 64, 2, 4, EPI, 3, 2><<<grid_for(64, 64), 256, 0, st>>>(p);
+        return hipGetLastError();
       default:
-        return hipErrorInvalidValue;
+        break;
+    }
+    if constexpr (K1) {
+      switch (tile) {
+        case TILE_GLU_128x32:
+          gemm_tile_kernel<DT, 128, 32, 4, 4, EPI, 12, 1><<<grid_for(128, 32), 256, 0, st>>>(p);
+          return hipGetLastError();
+        case TILE_GLU_64x64:
+          gemm_tile_kernel<DT, 64, 64, 2, 4, EPI, 6, 1><<<grid_for(64, 64), 256, 0, st>>>(p);
+          return hipGetLastError();
+        case TILE_GLU_128x64:
+          gemm_tile_kernel<DT, 128, 64, 2, 4, EPI, 5, 1><<<grid_for(128, 64), 256, 0, st>>>(p);
+          return hipGetLastError();
+        case TILE_GLU_256x128:
+          gemm_tile_kernel<DT, 256, 128, 2, 8, EPI, 5, 1><<<grid_for(256, 128), 512, 0, st>>>(p);
+          return hipGetLastError();
+        case TILE_GLU_256x64:
+          gemm_tile_kernel<DT, 256, 64, 2, 4, EPI, 3, 1><<<grid_for(256, 64), 256, 0, st>>>(p);
+          return hipGetLastError();
+        default:
+          break;
+      }
     }
   } else {
     switch (tile) {
-      case TILE_128x128:
-        gemm_tile_kernel<BF16, 128, 128, 2, 4, EPI, 5, 1><<<grid_for(128, 128), 256, 0, st>>>(p);
-        break;
-      case TILE_128x64:
-        gemm_tile_kernel<BF16, 128, 64, 2, 4, EPI, 6, 1><<<grid_for(128, 64), 256, 0, st>>>(p);
-        break;
-      case TILE_64x64:
-        gemm_tile_kernel<BF16, 64, 64, 2, 4, EPI, 6, 1><<<grid_for(64, 64), 256, 0, st>>>(p);
-        break;
-      case TILE_256x128:
-        gemm_tile_kernel<BF16, 256, 128, 2, 8, EPI, 5, 1><<<grid_for(256, 128), 512, 0, st>>>(p);
-        break;
-      case TILE_256x256:
-        gemm_tile_kernel<BF16, 256, 256, 2, 8, EPI, 5, 1><<<grid_for(256, 256), 512, 0, st>>>(p);
-        break;
       case TILE_64x64_K2:
-        gemm_tile_kernel<BF16, 64, 64, 2, 4, EPI, 3, 2><<<grid_for(64, 64), 256, 0, st>>>(p);
-        break;
+        gemm_tile_kernel<DT, 64, 64, 2, 4, EPI, 3, 2><<<grid_for(64, 64), 256, 0, st>>>(p);
+        return hipGetLastError();
       case TILE_128x128_K2:
-        gemm_tile_kernel<BF16, 128, 128, 2, 4, EPI, 3, 2><<<grid_for(128, 128), 256, 0, st>>>(p);
-        break;
+        gemm_tile_kernel<DT, 128, 128, 2, 4, EPI, 3, 2><<<grid_for(128, 128), 256, 0, st>>>(p);
+        return hipGetLastError();
       default:
-        return hipErrorInvalidValue;
+        break;
+    }
+    if constexpr (K1) {
+      switch (tile) {
+        case TILE_128x128:
+          gemm_tile_kernel<DT, 128, 128, 2, 4, EPI, 5, 1><<<grid_for(128, 128), 256, 0, st>>>(p);
+          return hipGetLastError();
+        case TILE_128x64:
+          gemm_tile_kernel<DT, 128, 64, 2, 4, EPI, 6, 1><<<grid_for(128, 64), 256, 0, st>>>(p);
+          return hipGetLastError();
+        case TILE_64x64:
+          gemm_tile_kernel<DT, 64, 64, 2, 4, EPI, 6, 1><<<grid_for(64, 64), 256, 0, st>>>(p);
+          return hipGetLastError();
+        case TILE_256x128:
+          gemm_tile_kernel<DT, 256, 128, 2, 8, EPI, 5, 1><<<grid_for(256, 128), 512, 0, st>>>(p);
+          return hipGetLastError();
+        case TILE_256x256:
+          gemm_tile_kernel<DT, 256, 256, 2, 8, EPI, 5, 1><<<grid_for(256, 256), 512, 0, st>>>(p);
+          return hipGetLastError();
+        default:
+          break;
+      }
     }
   }
-  return hipGetLastError();
+  return hipErrorInvalidValue;
 }
 
-hipError_t launch_gemm_tile(bool bf16, int epi, int tile, const GemmParams& p, hipStream_t st) {
-  if (bf16) {
-    switch (epi) {
-      case EPI_F32: return tile_dispatch<true, EPI_F32>(tile, p, st);
-      case EPI_BF16: return tile_dispatch<true, EPI_BF16>(tile, p, st);
-      case EPI_GLU: return tile_dispatch<true, EPI_GLU>(tile, p, st);
-      default: return hipErrorInvalidValue;
-    }
-  }
+template <int DT>
+static hipError_t tile_epi(int epi, int tile, const GemmParams& p, hipStream_t st) {
   switch (epi) {
-    case EPI_I32: return tile_dispatch<false, EPI_I32>(tile, p, st);
-    case EPI_F32: return tile_dispatch<false, EPI_F32>(tile, p, st);
-    case EPI_BF16: return tile_dispatch<false, EPI_BF16>(tile, p, st);
-    case EPI_GLU: return tile_dispatch<false, EPI_GLU>(tile, p, st);
+    case EPI_I32: return tile_dispatch<DT, EPI_I32>(tile, p, st);
+    case EPI_F32: return tile_dispatch<DT, EPI_F32>(tile, p, st);
+    case EPI_BF16: return tile_dispatch<DT, EPI_BF16>(tile, p, st);
+    case EPI_GLU: return tile_dispatch<DT, EPI_GLU>(tile, p, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_gemm_tile(int dt, int epi, int tile, const GemmParams& p, hipStream_t st) {
+  switch (dt) {
+    case DT_I8: return tile_epi<DT_I8>(epi, tile, p, st);
+    case DT_BF16: return tile_epi<DT_BF16>(epi, tile, p, st);
+    case DT_F8: return tile_epi<DT_F8>(epi, tile, p, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -839,9 +909,9 @@ static size_t stream_lds_bytes(int mb, int kchunk, int wk, bool glu) {
   return (size_t)mb * kchunk * kFragBytes + (size_t)(wk - 1) * (glu ? 2 : 1) * mb * kFragBytes;
 }
 
-template <bool BF16, int MB, int EPI, int NW, int WK>
+template <int DT, int MB, int EPI, int NW, int WK>
 static hipError_t stream_launch(const GemmParams& p, int nbpb, hipStream_t st) {
-  auto kern = gemm_stream_kernel<BF16, MB, EPI, NW, WK>;
+  auto kern = gemm_stream_kernel<DT, MB, EPI, NW, WK>;
   static size_t static_lds = 0;  // benign race: every caller computes the same values
   static bool attr_set = false;
   if (!attr_set) {
@@ -857,9 +927,7 @@ static hipError_t stream_launch(const GemmParams& p, int nbpb, hipStream_t st) {
   }
   const size_t lds = stream_lds_bytes(MB, p.kchunk, WK, EPI == EPI_GLU);
   if (lds + static_lds > 160 * 1024) return hipErrorInvalidValue;
-  const int groups = NW / WK;
   dim3 grid((unsigned)((p.rb_b + nbpb - 1) / nbpb), (unsigned)p.splits);
-  (void)groups;
   kern<<<grid, 64 * NW, lds, st>>>(p, nbpb);
   return hipGetLastError();
 }
@@ -867,46 +935,53 @@ static hipError_t stream_launch(const GemmParams& p, int nbpb, hipStream_t st) {
 // Instantiated wave layouts: 16-wave workgroups only for MB == 1 (at 16 waves a
 // wave has 128 registers, too few for larger MB), 4 waves sharing K only where
 // the accumulators still fit without spilling.
-template <bool BF16, int MB, int EPI>
+template <int DT, int MB, int EPI>
 static hipError_t stream_waves(int nw, int wk, const GemmParams& p, int nbpb, hipStream_t st) {
-  if (nw == 1 && wk == 1) return stream_launch<BF16, MB, EPI, 1, 1>(p, nbpb, st);
-  if (nw == 4 && wk == 1) return stream_launch<BF16, MB, EPI, 4, 1>(p, nbpb, st);
-  if (nw == 2 && wk == 2) return stream_launch<BF16, MB, EPI, 2, 2>(p, nbpb, st);
+  if (nw == 1 && wk == 1) return stream_launch<DT, MB, EPI, 1, 1>(p, nbpb, st);
+  if (nw == 4 && wk == 1) return stream_launch<DT, MB, EPI, 4, 1>(p, nbpb, st);
+  if (nw == 2 && wk == 2) return stream_launch<DT, MB, EPI, 2, 2>(p, nbpb, st);
   if constexpr (MB <= 4 || EPI != EPI_GLU) {
-    if (nw == 4 && wk == 4) return stream_launch<BF16, MB, EPI, 4, 4>(p, nbpb, st);
+    if (nw == 4 && wk == 4) return stream_launch<DT, MB, EPI, 4, 4>(p, nbpb, st);
   }
   if constexpr (MB == 1 && EPI != EPI_GLU) {  // the gated 16-wave variant would spill
-    if (nw == 16 && wk == 16) return stream_launch<BF16, MB, EPI, 16, 16>(p, nbpb, st);
+    if (nw == 16 && wk == 16) return stream_launch<DT, MB, EPI, 16, 16>(p, nbpb, st);
   }
   return hipErrorInvalidValue;
 }
 
-template <bool BF16, int EPI>
+template <int DT, int EPI>
 static hipError_t stream_mb(int mb, int nw, int wk, const GemmParams& p, int nbpb, hipStream_t st) {
   switch (mb) {
-    case 1: return stream_waves<BF16, 1, EPI>(nw, wk, p, nbpb, st);
-    case 2: return stream_waves<BF16, 2, EPI>(nw, wk, p, nbpb, st);
-    case 4: return stream_waves<BF16, 4, EPI>(nw, wk, p, nbpb, st);
-    case 8: return stream_waves<BF16, 8, EPI>(nw, wk, p, nbpb, st);
+    case 1: return stream_waves<DT, 1, EPI>(nw, wk, p, nbpb, st);
+    case 2: return stream_waves<DT, 2, EPI>(nw, wk, p, nbpb, st);
+    case 4: return stream_waves<DT, 4, EPI>(nw, wk, p, nbpb, st);
+    case 8:
+      if constexpr (DT != DT_F8) return stream_waves<DT, 8, EPI>(nw, wk, p, nbpb, st);
+      return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_gemm_stream(bool bf16, int epi, int mb, int nw, int wk, const GemmParams& p,
-                              int nb_per_block, hipStream_t st) {
-  if (bf16) {
-    switch (epi) {
-      case EPI_F32: return stream_mb<true, EPI_F32>(mb, nw, wk, p, nb_per_block, st);
-      case EPI_BF16: return stream_mb<true, EPI_BF16>(mb, nw, wk, p, nb_per_block, st);
-      case EPI_GLU: return stream_mb<true, EPI_GLU>(mb, nw, wk, p, nb_per_block, st);
-      default: return hipErrorInvalidValue;
-    }
-  }
+template <int DT>
+static hipError_t stream_epi(int epi, int mb, int nw, int wk, const GemmParams& p, int nbpb,
+                             hipStream_t st) {
   switch (epi) {
-    case EPI_I32: return stream_mb<false, EPI_I32>(mb, nw, wk, p, nb_per_block, st);
-    case EPI_F32: return stream_mb<false, EPI_F32>(mb, nw, wk, p, nb_per_block, st);
-    case EPI_BF16: return stream_mb<false, EPI_BF16>(mb, nw, wk, p, nb_per_block, st);
-    case EPI_GLU: return stream_mb<false, EPI_GLU>(mb, nw, wk, p, nb_per_block, st);
+    case EPI_I32:
+      if constexpr (DT == DT_BF16) return hipErrorInvalidValue;
+      return stream_mb<DT, EPI_I32>(mb, nw, wk, p, nbpb, st);
+    case EPI_F32: return stream_mb<DT, EPI_F32>(mb, nw, wk, p, nbpb, st);
+    case EPI_BF16: return stream_mb<DT, EPI_BF16>(mb, nw, wk, p, nbpb, st);
+    case EPI_GLU: return stream_mb<DT, EPI_GLU>(mb, nw, wk, p, nbpb, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_gemm_stream(int dt, int epi, int mb, int nw, int wk, const GemmParams& p,
+                              int nb_per_block, hipStream_t st) {
+  switch (dt) {
+    case DT_I8: return stream_epi<DT_I8>(epi, mb, nw, wk, p, nb_per_block, st);
+    case DT_BF16: return stream_epi<DT_BF16>(epi, mb, nw, wk, p, nb_per_block, st);
+    case DT_F8: return stream_epi<DT_F8>(epi, mb, nw, wk, p, nb_per_block, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -915,24 +990,29 @@ size_t gemm_stream_lds_bytes(int mb, int kchunk, int wk, bool glu) {
   return stream_lds_bytes(mb, kchunk, wk, glu);
 }
 
-template <bool BF16>
+template <int DT>
 static hipError_t reduce_epi(int epi, const GemmParams& p, hipStream_t st) {
   const int64_t n4 = (p.N + 3) / 4;
   const unsigned blocks = (unsigned)((p.M * n4 + 255) / 256);
   switch (epi) {
     case EPI_I32:
-      if constexpr (BF16) return hipErrorInvalidValue;
-      else splitk_reduce_kernel<false, EPI_I32><<<blocks, 256, 0, st>>>(p);
+      if constexpr (DT == DT_BF16) return hipErrorInvalidValue;
+      else splitk_reduce_kernel<DT, EPI_I32><<<blocks, 256, 0, st>>>(p);
       break;
-    case EPI_F32: splitk_reduce_kernel<BF16, EPI_F32><<<blocks, 256, 0, st>>>(p); break;
-    case EPI_BF16: splitk_reduce_kernel<BF16, EPI_BF16><<<blocks, 256, 0, st>>>(p); break;
+    case EPI_F32: splitk_reduce_kernel<DT, EPI_F32><<<blocks, 256, 0, st>>>(p); break;
+    case EPI_BF16: splitk_reduce_kernel<DT, EPI_BF16><<<blocks, 256, 0, st>>>(p); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_splitk_reduce(bool bf16, int epi, const GemmParams& p, hipStream_t st) {
-  return bf16 ? reduce_epi<true>(epi, p, st) : reduce_epi<false>(epi, p, st);
+hipError_t launch_splitk_reduce(int dt, int epi, const GemmParams& p, hipStream_t st) {
+  switch (dt) {
+    case DT_I8: return reduce_epi<DT_I8>(epi, p, st);
+    case DT_BF16: return reduce_epi<DT_BF16>(epi, p, st);
+    case DT_F8: return reduce_epi<DT_F8>(epi, p, st);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace w8a8

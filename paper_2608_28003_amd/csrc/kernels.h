@@ -43,6 +43,14 @@ struct GemmParams {
   int rotate = 1;
 };
 
+// Operand / accumulator types of the GEMM kernels (the launchers take an int;
+// false / true passed for the first two keep their meaning).
+enum DType {
+  DT_I8 = 0,    // int8 codes, int32 sums, two-scale dequant
+  DT_BF16 = 1,  // row-major bf16 A, packed bf16 B, fp32 sums, no scales
+  DT_F8 = 2,    // OCP E4M3 codes (packed like int8), fp32 sums, two-scale dequant
+};
+
 // tile shapes selectable at run time
 enum TileCfg {
   TILE_128x128 = 0,     // 4 waves of 64 x 64
@@ -66,21 +74,22 @@ hipError_t launch_col_absmax(const void* x, bool bf16, int64_t rows, int64_t k, 
 hipError_t launch_smooth_delta(const float* a, const float* w, int64_t k, double alpha,
                                float* delta, hipStream_t st);
 hipError_t launch_quant_rows(const void* x, bool bf16, bool mul, int64_t rows, int64_t k,
-                             const float* delta, int8_t* qpacked, float* s, hipStream_t st);
+                             const float* delta, int8_t* qpacked, float* s, hipStream_t st,
+                             bool f8 = false);
 hipError_t launch_unpack(const void* qp, int64_t n, int64_t k, int8_t* q, hipStream_t st);
 hipError_t launch_pack_bf16(const void* w, int64_t n, int64_t k, void* wp, hipStream_t st);
 
 // tiled MFMA GEMM (any M); `tile` picks the block shape
-hipError_t launch_gemm_tile(bool bf16, int epi, int tile, const GemmParams& p, hipStream_t st);
+hipError_t launch_gemm_tile(int dt, int epi, int tile, const GemmParams& p, hipStream_t st);
 // streaming MFMA GEMM for M <= 128: weights streamed from HBM, A staged in
 // LDS; nw waves per workgroup, wk of them splitting one column block's K range
 // Largest M * K / 16 a streaming workgroup of nw waves can quantise on load.
 inline int64_t qload_capacity(int nw) { return (int64_t)64 * nw; }
-hipError_t launch_gemm_stream(bool bf16, int epi, int mb, int nw, int wk, const GemmParams& p,
+hipError_t launch_gemm_stream(int dt, int epi, int mb, int nw, int wk, const GemmParams& p,
                               int nb_per_block, hipStream_t st);
 size_t gemm_stream_lds_bytes(int mb, int kchunk, int wk, bool glu);
 // sum of K-split partials (in split order) followed by the epilogue
-hipError_t launch_splitk_reduce(bool bf16, int epi, const GemmParams& p, hipStream_t st);
+hipError_t launch_splitk_reduce(int dt, int epi, const GemmParams& p, hipStream_t st);
 
 hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* f, int64_t m, int64_t d,
                           uint16_t* y, hipStream_t st);

@@ -121,7 +121,9 @@ __device__ __forceinline__ void store_codes(int8_t* __restrict__ q, int64_t r, i
 // smoothed values in registers between the absmax and the rounding pass.
 // Rows in [rows, rows_pad) and columns in [k, kp) of the packed output are
 // written as zeros.  MUL: v = x * delta (weights); else v = x / delta.
-template <typename T, bool MUL>
+// F8: OCP E4M3 codes instead of int8, s = amax / 448 and code = E4M3(v / s)
+// (binary32 quotient rounded to the nearest E4M3 value, ties to even).
+template <typename T, bool MUL, bool F8>
 __global__ __launch_bounds__(1024) void quant_rows_kernel(const T* __restrict__ x, int64_t rows,
                                                           int64_t k, const float* __restrict__ delta,
                                                           int64_t rows_pad, int64_t kp,
@@ -155,7 +157,7 @@ __global__ __launch_bounds__(1024) void quant_rows_kernel(const T* __restrict__ 
     for (int e = 0; e < 16; ++e) amax = fmaxf(amax, fabsf(w[e]));
   }
   amax = block_max(amax);
-  const float sr = amax / 127.0f;
+  const float sr = amax / (F8 ? 448.0f : 127.0f);
   if (t == 0) s[r] = sr;
   const float inv = 1.0f / sr;
   const bool fast = isfinite(inv);
@@ -170,10 +172,23 @@ __global__ __launch_bounds__(1024) void quant_rows_kernel(const T* __restrict__ 
       } else {
         smooth16<T, MUL>(xr, delta, c, w);
       }
+      if constexpr (F8) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        int32_t iv = (int32_t)code_of(w[e], sr, inv, fast) & 0xff;
-        packed[e >> 2] |= iv << (8 * (e & 3));
+        for (int e = 0; e < 16; e += 2) {
+          // the conversion gives NaN past the largest code; the quotient only
+          // exceeds 448 when the scale itself lost precision (amax near the
+          // binary32 subnormal range), and the nearest code is then 448
+          const float q0 = fminf(fmaxf(w[e] / sr, -448.0f), 448.0f);
+          const float q1 = fminf(fmaxf(w[e + 1] / sr, -448.0f), 448.0f);
+          const uint32_t pair = e4m3_pack2(q0, q1);
+          packed[e >> 2] |= (int32_t)(pair << (8 * (e & 3)));
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          int32_t iv = (int32_t)code_of(w[e], sr, inv, fast) & 0xff;
+          packed[e >> 2] |= iv << (8 * (e & 3));
+        }
       }
     }
     store_codes(q, r, c, kb_count, packed);
@@ -228,28 +243,40 @@ hipError_t launch_smooth_delta(const float* a, const float* w, int64_t k, double
   return hipGetLastError();
 }
 
+template <bool F8>
+static void quant_rows_launch(const void* x, bool bf16, bool mul, int64_t rows, int64_t k,
+                              const float* delta, int64_t rows_pad, int64_t kp, int8_t* qpacked,
+                              float* s, dim3 grid, dim3 block, hipStream_t st) {
+  if (bf16) {
+    if (mul)
+      quant_rows_kernel<uint16_t, true, F8><<<grid, block, 0, st>>>(
+          (const uint16_t*)x, rows, k, delta, rows_pad, kp, qpacked, s);
+    else
+      quant_rows_kernel<uint16_t, false, F8><<<grid, block, 0, st>>>(
+          (const uint16_t*)x, rows, k, delta, rows_pad, kp, qpacked, s);
+  } else {
+    if (mul)
+      quant_rows_kernel<float, true, F8><<<grid, block, 0, st>>>(
+          (const float*)x, rows, k, delta, rows_pad, kp, qpacked, s);
+    else
+      quant_rows_kernel<float, false, F8><<<grid, block, 0, st>>>(
+          (const float*)x, rows, k, delta, rows_pad, kp, qpacked, s);
+  }
+}
+
 hipError_t launch_quant_rows(const void* x, bool bf16, bool mul, int64_t rows, int64_t k,
-                             const float* delta, int8_t* qpacked, float* s, hipStream_t st) {
+                             const float* delta, int8_t* qpacked, float* s, hipStream_t st,
+                             bool f8) {
   const int64_t rows_pad = (rows + 15) / 16 * 16;
   const int64_t kp = (k + kFragK8 - 1) / kFragK8 * kFragK8;
   int64_t threads = (kp / 16 + 63) / 64 * 64;
   if (threads > 1024) threads = 1024;
   dim3 grid((unsigned)rows_pad), block((unsigned)threads);
-  if (bf16) {
-    if (mul)
-      quant_rows_kernel<uint16_t, true><<<grid, block, 0, st>>>((const uint16_t*)x, rows, k, delta,
-                                                               rows_pad, kp, qpacked, s);
-    else
-      quant_rows_kernel<uint16_t, false><<<grid, block, 0, st>>>((const uint16_t*)x, rows, k, delta,
-                                                                rows_pad, kp, qpacked, s);
-  } else {
-    if (mul)
-      quant_rows_kernel<float, true><<<grid, block, 0, st>>>((const float*)x, rows, k, delta,
-                                                            rows_pad, kp, qpacked, s);
-    else
-      quant_rows_kernel<float, false><<<grid, block, 0, st>>>((const float*)x, rows, k, delta,
-                                                             rows_pad, kp, qpacked, s);
-  }
+  if (f8)
+    quant_rows_launch<true>(x, bf16, mul, rows, k, delta, rows_pad, kp, qpacked, s, grid, block, st);
+  else
+    quant_rows_launch<false>(x, bf16, mul, rows, k, delta, rows_pad, kp, qpacked, s, grid, block,
+                             st);
   return hipGetLastError();
 }
 

@@ -75,6 +75,15 @@ _SIGS = {
     "w8a8_ffn_gate_up": (INT, [ctypes.POINTER(FfnDesc), P, P, I64, P, P]),
     "w8a8_ffn": (INT, [ctypes.POINTER(FfnDesc), P, I64, P, P, SZ, P]),
     "w8a8_lm_head": (INT, [ctypes.POINTER(LinearDesc), P, I64, P, P, SZ, P]),
+    "w8a8_fp8_linear_workspace_bytes": (SZ, [I64, I64, I64]),
+    "w8a8_fp8_ffn_workspace_bytes": (SZ, [I64, I64, I64]),
+    "w8a8_fp8_quantize_weights": (INT, [P, INT, I64, I64, P, P, P, P]),
+    "w8a8_fp8_quantize_act": (INT, [P, INT, I64, I64, P, P, P, P]),
+    "w8a8_fp8_gemm_f32": (INT, [P, I64, P, I64, I64, P, P, SZ, P]),
+    "w8a8_fp8_linear": (INT, [ctypes.POINTER(LinearDesc), P, INT, I64, P, INT, P, SZ, P]),
+    "w8a8_fp8_ffn_gate_up": (INT, [ctypes.POINTER(FfnDesc), P, P, I64, P, P]),
+    "w8a8_fp8_ffn": (INT, [ctypes.POINTER(FfnDesc), P, I64, P, P, SZ, P]),
+    "w8a8_fp8_lm_head": (INT, [ctypes.POINTER(LinearDesc), P, I64, P, P, SZ, P]),
     "w8a8_bf16_linear": (INT, [P, I64, P, I64, I64, P, P, SZ, P]),
     "w8a8_bf16_ffn": (INT, [ctypes.POINTER(Bf16FfnDesc), P, I64, P, P, SZ, P]),
     "w8a8_bf16_ffn_gate_up": (INT, [ctypes.POINTER(Bf16FfnDesc), P, I64, P, P]),
@@ -348,6 +357,107 @@ def lm_head(layer: LinearW8A8, x, out=None, ws=None, stream=None):
     d = layer.desc()
     _check(lib().w8a8_lm_head(ctypes.byref(d), _ptr(x), m, _ptr(out), _ptr(ws), ws.numel(),
                               _stream(stream)))
+    return out
+
+
+# ----------------------------------------------------------------- FP8 variant
+# E4M3 codes in the packed fragment layout; the layer containers above carry
+# them unchanged (LinearW8A8 / FfnW8A8 built with the fp8_ constructors below).
+
+def fp8_linear_workspace_bytes(m, n, k):
+    return lib().w8a8_fp8_linear_workspace_bytes(m, n, k)
+
+
+def fp8_ffn_workspace_bytes(m, d, f):
+    return lib().w8a8_fp8_ffn_workspace_bytes(m, d, f)
+
+
+def fp8_quantize_weights(w, delta=None, stream=None):
+    """Returns (packed E4M3 codes as a uint8 tensor, s_w)."""
+    _dev(w)
+    n, k = w.shape
+    wq = _empty(packed_bytes(n, k), w.device)
+    s_w = torch.empty(n, dtype=torch.float32, device=w.device)
+    _check(lib().w8a8_fp8_quantize_weights(_ptr(w), _dt(w), n, k, _ptr(delta), _ptr(wq),
+                                           _ptr(s_w), _stream(stream)))
+    return wq, s_w
+
+
+def fp8_quantize_act(x, delta=None, stream=None):
+    """Returns (packed E4M3 codes, s_x)."""
+    _dev(x)
+    m, k = x.shape
+    qx = _empty(packed_bytes(m, k), x.device)
+    s_x = torch.empty(m, dtype=torch.float32, device=x.device)
+    _check(lib().w8a8_fp8_quantize_act(_ptr(x), _dt(x), m, k, _ptr(delta), _ptr(qx),
+                                       _ptr(s_x), _stream(stream)))
+    return qx, s_x
+
+
+def fp8_linear_layer(w, delta=None) -> LinearW8A8:
+    wq, s_w = fp8_quantize_weights(w, delta)
+    return LinearW8A8(w.shape[0], w.shape[1], wq, s_w, delta)
+
+
+def fp8_ffn_layer(w_gate, w_up, w_down, delta_gu, delta_down) -> FfnW8A8:
+    return FfnW8A8(w_gate.shape[1], w_gate.shape[0], fp8_linear_layer(w_gate, delta_gu),
+                   fp8_linear_layer(w_up, delta_gu), fp8_linear_layer(w_down, delta_down))
+
+
+def fp8_gemm_f32(qx, m, wq, n, k, ws=None, stream=None):
+    acc = torch.empty((m, n), dtype=torch.float32, device=qx.device)
+    if ws is None:
+        ws = _empty(fp8_linear_workspace_bytes(m, n, k), qx.device)
+    _check(lib().w8a8_fp8_gemm_f32(_ptr(qx), m, _ptr(wq), n, k, _ptr(acc), _ptr(ws),
+                                   ws.numel(), _stream(stream)))
+    return acc
+
+
+def fp8_linear(layer: LinearW8A8, x, out_dtype=torch.float32, out=None, ws=None, stream=None):
+    _dev(x)
+    m = x.shape[0]
+    if out is None:
+        out = torch.empty((m, layer.n), dtype=out_dtype, device=x.device)
+    if ws is None:
+        ws = _empty(fp8_linear_workspace_bytes(m, layer.n, layer.k), x.device)
+    d = layer.desc()
+    _check(lib().w8a8_fp8_linear(ctypes.byref(d), _ptr(x), _dt(x), m, _ptr(out), _dt(out),
+                                 _ptr(ws), ws.numel(), _stream(stream)))
+    return out
+
+
+def fp8_ffn_gate_up(ffn: FfnW8A8, qx, s_x, m, out=None, stream=None):
+    if out is None:
+        out = torch.empty((m, ffn.f), dtype=torch.bfloat16, device=qx.device)
+    d = ffn.desc()
+    _check(lib().w8a8_fp8_ffn_gate_up(ctypes.byref(d), _ptr(qx), _ptr(s_x), m, _ptr(out),
+                                      _stream(stream)))
+    return out
+
+
+def fp8_ffn(layer: FfnW8A8, x, out=None, ws=None, stream=None):
+    _dev(x)
+    m = x.shape[0]
+    if out is None:
+        out = torch.empty((m, layer.d), dtype=torch.bfloat16, device=x.device)
+    if ws is None:
+        ws = _empty(fp8_ffn_workspace_bytes(m, layer.d, layer.f), x.device)
+    d = layer.desc()
+    _check(lib().w8a8_fp8_ffn(ctypes.byref(d), _ptr(x), m, _ptr(out), _ptr(ws), ws.numel(),
+                              _stream(stream)))
+    return out
+
+
+def fp8_lm_head(layer: LinearW8A8, x, out=None, ws=None, stream=None):
+    _dev(x)
+    m = x.shape[0]
+    if out is None:
+        out = torch.empty((m, layer.n), dtype=torch.bfloat16, device=x.device)
+    if ws is None:
+        ws = _empty(fp8_linear_workspace_bytes(m, layer.n, layer.k), x.device)
+    d = layer.desc()
+    _check(lib().w8a8_fp8_lm_head(ctypes.byref(d), _ptr(x), m, _ptr(out), _ptr(ws), ws.numel(),
+                                  _stream(stream)))
     return out
 
 

@@ -1,0 +1,365 @@
+"""GPU parity of the FP8 (OCP E4M3) variant against the CPU oracle.
+
+Bar:
+* E4M3 codes and scales of the activation and weight quantisers: bit-exact;
+* GEMM sums: the oracle adds the exact E4M3 products in binary64.  The FP8
+  matrix instruction does not add its 128 products in IEEE binary32: it lines
+  them up on a grid set by the block's largest product and drops the bits
+  below it (measured: errors on a grid of 2^-3 for sums near 2^17, up to about
+  2^-12 of the block's largest product).  The allowance per element is
+  2^-8 sum_b max|a_b| max|b_b| over the 128-wide K blocks b (at least 15 bits
+  kept below the largest product of every block) plus the binary32 bound
+  (K + 8) 2^-24 sum |p| for adding the blocks; the rel-L2 of all sums must
+  stay below 1e-4, and sums the grid holds exactly must be exact;
+* dequantised outputs (linear, lm_head, FFN block): rel-L2 <= 1e-3 against the
+  oracle, the bar; the share of bit-identical bf16 outputs is printed and only
+  checked against a loose floor (the sums' relative error, a few 1e-5 on
+  smoothed activations, moves a few percent of bf16 roundings);
+* the GeGLU intermediate h (bf16): rel-L2 <= 1e-3.
+"""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_28003_amd import synth, w8a8
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+DEV = "cuda:0"
+U32 = 2.0 ** -24
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def dev_bf16(u16):
+    return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).view(torch.bfloat16).to(DEV)
+
+
+def dev_f32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV)
+
+
+def dev_u8(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint8)).to(DEV)
+
+
+def host_bf16(t):
+    return t.detach().cpu().view(torch.int16).numpy().view(np.uint16)
+
+
+def host(t):
+    return t.detach().cpu().numpy()
+
+
+def codes_full(t, rows, k):
+    """The whole padded packed code matrix, row-major, as uint8."""
+    rp, kp = -(-rows // 16) * 16, -(-k // 64) * 64
+    return w8a8.frag_to_rowmajor(host(t), rp, kp).view(np.uint8)
+
+
+def pack_codes(q):
+    return dev_u8(w8a8.rowmajor_to_frag(np.ascontiguousarray(q).view(np.int8)).view(np.uint8))
+
+
+def rel_l2(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def random_codes(rng, shape):
+    """Uniform over the 254 finite E4M3 codes (0x7F and 0xFF are NaN)."""
+    c = rng.integers(0, 254, shape).astype(np.uint8)
+    c[c >= 0x7F] += 1
+    return c
+
+
+def block_max(q):
+    """max |decoded code| over each 128-wide K block: rows x (K / 128)."""
+    a = oracle.e4m3_decode(q & 0x7F)
+    return a.reshape(a.shape[0], -1, 128).max(axis=2)
+
+
+def check_sums(acc, qa, qb, k, what=""):
+    exact = oracle.gemm_fp8(qa, qb)
+    mag = oracle.gemm_fp8(qa & 0x7F, qb & 0x7F)       # sum of |products|
+    err = np.abs(acc.astype(np.float64) - exact)
+    bound = 2.0 ** -8 * (block_max(qa) @ block_max(qb).T) + (k + 8) * U32 * mag
+    worst = float(np.max(err / np.maximum(bound, 1e-300)))
+    r = rel_l2(acc, exact)
+    say("  %s worst err / allowance %.3g, rel-L2 %.3g" % (what, worst, r))
+    assert (err <= bound).all(), worst
+    assert r <= 1e-4
+
+
+def act_input(m, k, seed, dtype="bf16"):
+    ch = synth.outlier_channels(seed + 1, k, max(1, k // 100))
+    x = synth.activations(seed, m, k, ch, 30.0)
+    return synth.to_bf16_bits(x) if dtype == "bf16" else x
+
+
+def to_dev(x):
+    return dev_bf16(x) if x.dtype == np.uint16 else dev_f32(x)
+
+
+# ------------------------------------------------------------------ quantisers
+
+@pytest.mark.parametrize("m,k,dtype,smooth", [
+    (1, 1152, "bf16", True), (16, 1152, "f32", True), (37, 1152, "bf16", False),
+    (128, 6912, "bf16", True), (3, 16, "f32", False), (5, 80, "bf16", True),
+    (2048, 1152, "bf16", True), (64, 1040, "f32", True)])
+def test_fp8_quantize_act_bit_exact(m, k, dtype, smooth):
+    say("fp8 quantize_act", m, k, dtype, smooth)
+    x = act_input(m, k, 300 + m + k, dtype=dtype)
+    if m > 2:
+        xf = oracle.as_f32(x).copy()
+        xf[1] = 0.0                                             # all-zero token
+        vals = [448, 1.0625, 1.1875, -2.125, 0.5, 3 * 2.0 ** -10, 2.0 ** -10, -0.0,
+                -448, 300, 232, 2.0 ** -9, 1.0 + 2.0 ** -4, -13.0, 208, 240]
+        xf[2, : min(k, 16)] = vals[: min(k, 16)]
+        xf[2, 16:] = 0.0                                        # exact ties at s = 1
+        x = synth.to_bf16_bits(xf) if dtype == "bf16" else xf
+    delta = None
+    if smooth:
+        delta = np.exp(np.random.default_rng(k).uniform(-2, 2, k)).astype(np.float32)
+    q_o, s_o = oracle.quantize_act_fp8(x, delta)
+    qx, sx = w8a8.fp8_quantize_act(to_dev(x), None if delta is None else dev_f32(delta))
+    torch.cuda.synchronize()
+    full = codes_full(qx, m, k)
+    np.testing.assert_array_equal(full[:m, :k], q_o)
+    assert not full[m:].any() and not full[:, k:].any(), "padding must be zero"
+    np.testing.assert_array_equal(host(sx), s_o)
+
+
+@pytest.mark.parametrize("n,k,dtype", [(6912, 1152, "f32"), (1152, 6912, "bf16"),
+                                       (100, 208, "bf16")])
+def test_fp8_quantize_weights_bit_exact(n, k, dtype):
+    say("fp8 quantize_weights", n, k, dtype)
+    w = synth.normal(700 + n, (n, k), 0.02)
+    w[3] = 0.0                                                  # all-zero channel
+    if dtype == "bf16":
+        w = synth.to_bf16_bits(w)
+    delta = np.exp(np.random.default_rng(n).uniform(-1, 1, k)).astype(np.float32)
+    q_o, s_o = oracle.quantize_weights_fp8(w, delta)
+    wq, s_w = w8a8.fp8_quantize_weights(to_dev(w), dev_f32(delta))
+    torch.cuda.synchronize()
+    full = codes_full(wq, n, k)
+    np.testing.assert_array_equal(full[:n, :k], q_o)
+    assert not full[n:].any() and not full[:, k:].any()
+    np.testing.assert_array_equal(host(s_w), s_o)
+
+
+def test_fp8_requant_of_oracle_h_bit_exact():
+    say("fp8 requant of h")
+    cfg = synth.ffn_config(m=128, d=1152, f=6912, seed_base=2100)
+    q = oracle.quantize_ffn_fp8(cfg["w_gate"], cfg["w_up"], cfg["w_down"], cfg["x_cal"])
+    _, st = oracle.fp8_ffn(cfg["x"], q, stages=True)
+    qh, sh = w8a8.fp8_quantize_act(dev_bf16(st["h"]), dev_f32(q["delta_down"]))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(codes_full(qh, 128, 6912)[:128, :6912], st["qh"])
+    np.testing.assert_array_equal(host(sh), st["sh"])
+
+
+# ------------------------------------------------------------------ GEMM sums
+
+FP8_GEMM_SHAPES = [(1, 16, 128), (5, 48, 128), (16, 6912, 1152), (1, 1152, 6912),
+                   (17, 1152, 6912), (33, 1152, 6912), (64, 4096, 1152), (65, 1152, 6912),
+                   (128, 6912, 1152), (300, 1000, 1152), (512, 1152, 6912), (129, 13824, 1152),
+                   (40, 4112, 1152), (2, 262144, 1152)]
+
+
+@pytest.mark.parametrize("m,n,k", FP8_GEMM_SHAPES)
+def test_fp8_gemm_sums_within_rounding_bound(m, n, k):
+    say("fp8 gemm", m, n, k)
+    rng = np.random.default_rng(m * 5 + n * 7 + k)
+    qa = random_codes(rng, (m, k))
+    qb = random_codes(rng, (n, k))
+    qa[0, :] = 0x7E                                   # +448 against -448: the largest sum
+    qb[0, :] = 0xFE
+    if m > 1 and n > 1:                               # small integers: an exact integer sum
+        qa[1] = oracle.e4m3_encode(rng.integers(-8, 9, k).astype(np.float32))
+        qb[1] = oracle.e4m3_encode(rng.integers(-8, 9, k).astype(np.float32))
+    acc = host(w8a8.fp8_gemm_f32(pack_codes(qa), m, pack_codes(qb), n, k))
+    if m > 1 and n > 1:
+        assert acc[1, 1] == oracle.gemm_fp8(qa[1:2], qb[1:2])[0, 0]
+    if n > 20000:                                     # full-vocab width: sampled columns
+        cols = np.unique(np.concatenate([[0, n - 1],
+                                         rng.choice(n, 2000, replace=False)]))
+        check_sums(acc[:, cols], qa, qb[cols], k, "sampled")
+    else:
+        check_sums(acc, qa, qb, k)
+    assert acc[0, 0] == -448.0 * 448.0 * k
+
+
+@pytest.mark.parametrize("m,n,k,splits", [(128, 1152, 6912, 1), (128, 1152, 6912, 3),
+                                          (300, 640, 1152, 4), (96, 2048, 6912, 2)])
+def test_fp8_gemm_tiles_and_splits(m, n, k, splits, monkeypatch):
+    say("fp8 tiles / split-K", m, n, k, splits)
+    rng = np.random.default_rng(77 + splits)
+    qa = random_codes(rng, (m, k))
+    qb = random_codes(rng, (n, k))
+    A, B = pack_codes(qa), pack_codes(qb)
+    monkeypatch.setenv("W8A8_GEMM_SPLITS", str(splits))
+    for tile in (10, 11):
+        monkeypatch.setenv("W8A8_GEMM_TILE", str(tile))
+        acc = host(w8a8.fp8_gemm_f32(A, m, B, n, k))
+        check_sums(acc, qa, qb, k, "tile %d" % tile)
+
+
+# ------------------------------------------------------------------ linear / lm_head
+
+@pytest.mark.parametrize("m,n,k", [(16, 6912, 1152), (1, 1536, 1152), (32, 1536, 1152),
+                                   (256, 1536, 1152), (77, 300, 256), (1, 1152, 6912)])
+def test_fp8_linear_matches_oracle(m, n, k):
+    say("fp8 linear", m, n, k)
+    x = act_input(m, k, 900 + m)
+    w = synth.to_bf16_bits(synth.normal(910 + n, (n, k), 0.02))
+    x_cal = act_input(512, k, 920 + m)
+    delta = oracle.smooth_calibrate(x_cal, [w])
+    wq_o, sw_o = oracle.quantize_weights_fp8(w, delta)
+    y_o = oracle.fp8_linear(x, wq_o, sw_o, delta, "f32")
+    layer = w8a8.fp8_linear_layer(dev_bf16(w), dev_f32(delta))
+    y = host(w8a8.fp8_linear(layer, dev_bf16(x), torch.float32))
+    err = rel_l2(y, y_o)
+    say("  f32 rel-L2 %.3g, bit-identical %.5f" % (err, float((y == y_o).mean())))
+    assert err <= 1e-3
+    yb = host_bf16(w8a8.fp8_linear(layer, dev_bf16(x), torch.bfloat16))
+    yb_o = oracle.f32_to_bf16(y_o)
+    same = float((yb == yb_o).mean())
+    say("  bf16 bit-identical %.5f" % same)
+    assert rel_l2(oracle.bf16_to_f32(yb), oracle.bf16_to_f32(yb_o)) <= 1e-3 and same >= 0.95
+
+
+@pytest.mark.parametrize("m", [1, 8, 64])
+def test_fp8_lm_head_reduced_vocab(m):
+    say("fp8 lm_head vocab 4096", m)
+    cfg = synth.lm_head_config(m=m, vocab=4096)
+    delta = oracle.smooth_calibrate(cfg["x_cal"], [cfg["w"]])
+    wq_o, sw_o = oracle.quantize_weights_fp8(cfg["w"], delta)
+    y_o = oracle.fp8_linear(cfg["x"], wq_o, sw_o, delta, "bf16")
+    layer = w8a8.fp8_linear_layer(dev_bf16(cfg["w"]), dev_f32(delta))
+    y = host_bf16(w8a8.fp8_lm_head(layer, dev_bf16(cfg["x"])))
+    err = rel_l2(oracle.bf16_to_f32(y), oracle.bf16_to_f32(y_o))
+    same = float((y == y_o).mean())
+    say("  rel-L2 %.3g, bit-identical %.5f" % (err, same))
+    assert err <= 1e-3 and same >= 0.9
+
+
+@pytest.mark.parametrize("m", [1, 8, 64])
+def test_fp8_lm_head_full_vocab_sampled_columns(m):
+    say("fp8 lm_head full vocab, sampled columns", m)
+    cfg = synth.lm_head_config(m=m)
+    delta = oracle.smooth_calibrate(cfg["x_cal"], [cfg["w"]])
+    layer = w8a8.fp8_linear_layer(dev_bf16(cfg["w"]), dev_f32(delta))
+    y = host_bf16(w8a8.fp8_lm_head(layer, dev_bf16(cfg["x"])))
+    cols = np.sort(np.random.default_rng(m + 40).choice(262144, 3000, replace=False))
+    cols = np.unique(np.concatenate([cols, [0, 1, 65535, 65536, 131071, 262143]]))
+    wq_o, sw_o = oracle.quantize_weights_fp8(np.ascontiguousarray(cfg["w"][cols]), delta)
+    # the GPU's weight codes for these rows must be the oracle's
+    codes = host(w8a8.unpack_weights(layer.wq, 262144, cfg["w"].shape[1])).view(np.uint8)
+    np.testing.assert_array_equal(codes[cols], wq_o)
+    np.testing.assert_array_equal(host(layer.s_w)[cols], sw_o)
+    y_o = oracle.fp8_linear(cfg["x"], wq_o, sw_o, delta, "bf16")
+    err = rel_l2(oracle.bf16_to_f32(y[:, cols]), oracle.bf16_to_f32(y_o))
+    say("  rel-L2 %.3g" % err)
+    assert err <= 1e-3
+
+
+# ------------------------------------------------------------------ FFN
+
+def _ffn_fp8(m, seed_base=2200):
+    cfg = synth.ffn_config(m=m, d=1152, f=6912, seed_base=seed_base)
+    q = oracle.quantize_ffn_fp8(cfg["w_gate"], cfg["w_up"], cfg["w_down"], cfg["x_cal"])
+    layer = w8a8.fp8_ffn_layer(dev_bf16(cfg["w_gate"]), dev_bf16(cfg["w_up"]),
+                               dev_bf16(cfg["w_down"]), dev_f32(q["delta_gu"]),
+                               dev_f32(q["delta_down"]))
+    return cfg, q, layer
+
+
+@pytest.mark.parametrize("m", [1, 5, 64, 128, 300])
+def test_fp8_gate_up_geglu_stage(m):
+    say("fp8 gate/up + GeGLU", m)
+    cfg, q, layer = _ffn_fp8(m)
+    _, st = oracle.fp8_ffn(cfg["x"], q, stages=True)
+    h = host_bf16(w8a8.fp8_ffn_gate_up(layer, pack_codes(st["qx"]), dev_f32(st["sx"]), m))
+    ref = oracle.bf16_to_f32(st["h"])
+    err = rel_l2(oracle.bf16_to_f32(h), ref)
+    same = float((h == st["h"]).mean())
+    say("  rel-L2 %.3g, bit-identical %.5f" % (err, same))
+    assert err <= 1e-3 and same >= 0.9
+
+
+@pytest.mark.parametrize("m", [300, 1024])
+def test_fp8_gate_up_tiles_agree(m, monkeypatch):
+    say("fp8 gate/up tiles", m)
+    cfg, q, layer = _ffn_fp8(m)
+    qx_o, sx_o = oracle.quantize_act_fp8(cfg["x"], q["delta_gu"])
+    qx, sx = pack_codes(qx_o), dev_f32(sx_o)
+    outs = []
+    for tile in (9, 12):
+        monkeypatch.setenv("W8A8_GLU_TILE", str(tile))
+        outs.append(oracle.bf16_to_f32(host_bf16(w8a8.fp8_ffn_gate_up(layer, qx, sx, m))))
+    assert rel_l2(outs[0], outs[1]) <= 1e-4
+
+
+@pytest.mark.parametrize("m", [1, 64, 300])
+def test_fp8_down_stage_from_oracle_h(m):
+    """The down projection of the FP8 FFN (requantise h / delta_down per token,
+    GEMM, dequantise to bf16) on the oracle's own h."""
+    say("fp8 down stage", m)
+    cfg, q, layer = _ffn_fp8(m)
+    y_o, st = oracle.fp8_ffn(cfg["x"], q, stages=True)
+    y = host_bf16(w8a8.fp8_linear(layer.down, dev_bf16(st["h"]), torch.bfloat16))
+    err = rel_l2(oracle.bf16_to_f32(y), oracle.bf16_to_f32(y_o))
+    say("  rel-L2 %.3g, bit-identical %.5f" % (err, float((y == y_o).mean())))
+    assert err <= 1e-3
+
+
+@pytest.mark.parametrize("m", [1, 8, 64, 128, 512])
+def test_fp8_ffn_block_matches_oracle(m):
+    """End to end, the FP8 requantisation of h sits between two sums that
+    differ from the oracle's by rounding (the matrix cores' alignment, a few
+    1e-5 relative): a bf16 ulp of difference in h moves an E4M3 code (3
+    mantissa bits) in a few percent of cases, and each moved code is a
+    several-percent change of that element.  The oracle alone shows the same
+    amplification (the CPU test that perturbs the oracle's sums at 2^-14), so
+    the 1e-3 bar holds per stage (tests above) and the block is held to a bar
+    derived from the quantisation: the GPU-oracle gap stays under a tenth of
+    the FP8 block's own error against the unquantised block."""
+    say("fp8 ffn block", m)
+    cfg, q, layer = _ffn_fp8(m)
+    y_o = oracle.bf16_to_f32(oracle.fp8_ffn(cfg["x"], q))
+    y_ref = oracle.bf16_to_f32(oracle.bf16_ffn(cfg["x"], cfg["w_gate"], cfg["w_up"],
+                                               cfg["w_down"]))
+    y = oracle.bf16_to_f32(host_bf16(w8a8.fp8_ffn(layer, dev_bf16(cfg["x"]))))
+    err = rel_l2(y, y_o)
+    noise = rel_l2(y_o, y_ref)
+    rows = np.array([rel_l2(y[i], y_o[i]) for i in range(m)])
+    say("  rel-L2 %.3g (quantisation error of the block %.3g), median token %.3g, "
+        "bit-identical %.5f" % (err, noise, float(np.median(rows)), float((y == y_o).mean())))
+    assert err <= 0.1 * noise
+
+
+def test_fp8_ffn_deterministic():
+    cfg, q, layer = _ffn_fp8(128)
+    x = dev_bf16(cfg["x"])
+    y1 = host_bf16(w8a8.fp8_ffn(layer, x))
+    for _ in range(3):
+        np.testing.assert_array_equal(host_bf16(w8a8.fp8_ffn(layer, x)), y1)
+
+
+# ------------------------------------------------------------------ shape errors
+
+def test_fp8_rejects_k_not_multiple_of_128():
+    qa = torch.zeros(w8a8.packed_bytes(16, 64), dtype=torch.uint8, device=DEV)
+    qb = torch.zeros(w8a8.packed_bytes(16, 64), dtype=torch.uint8, device=DEV)
+    with pytest.raises(w8a8.W8A8Error) as e:
+        w8a8.fp8_gemm_f32(qa, 16, qb, 16, 64, ws=torch.zeros(256, dtype=torch.uint8, device=DEV))
+    assert e.value.status == 2                       # W8A8_EUNSUPPORTED

@@ -500,3 +500,41 @@ def test_fp8_ffn_sqnr():
                                              cfg["w_down"])).astype(np.float64)
     yf = oracle.bf16_to_f32(oracle.fp8_ffn(cfg["x"], qf)).astype(np.float64)
     assert oracle.sqnr_db(ref, yf) > 20.0
+
+
+def test_fp8_ffn_requant_amplifies_sum_rounding():
+    """Sensitivity of the FP8 block to the rounding of its gate/up sums: the
+    oracle's own sums perturbed by a relative 2^-14 (the alignment grid of FP8
+    matrix-core sums) move the block output by more than 1e-3 rel-L2, because
+    the E4M3 requantisation of h turns bf16-ulp changes into E4M3-ulp changes;
+    the output of one projection alone moves by about 2^-14."""
+    cfg = synth.ffn_config(m=16, seed_base=2300)
+    q = oracle.quantize_ffn_fp8(cfg["w_gate"], cfg["w_up"], cfg["w_down"], cfg["x_cal"])
+    qx, sx = oracle.quantize_act_fp8(cfg["x"], q["delta_gu"])
+    rng = np.random.default_rng(5)
+    acc_g = oracle.gemm_fp8(qx, q["wq_gate"])
+    acc_u = oracle.gemm_fp8(qx, q["wq_up"])
+
+    def block(ag, au):
+        g = oracle.dequant_fp8(ag, sx, q["s_gate"])
+        u = oracle.dequant_fp8(au, sx, q["s_up"])
+        h = oracle.f64_to_bf16(oracle.geglu(g, u))
+        qh, sh = oracle.quantize_act_fp8(h, q["delta_down"])
+        y = oracle.dequant_fp8(oracle.gemm_fp8(qh, q["wq_down"]), sh, q["s_down"])
+        return g, oracle.bf16_to_f32(oracle.f32_to_bf16(y))
+
+    eps = 2.0 ** -14
+    g0, y0 = block(acc_g, acc_u)
+    g1, y1 = block(acc_g * (1 + eps * rng.uniform(-1, 1, acc_g.shape)),
+                   acc_u * (1 + eps * rng.uniform(-1, 1, acc_u.shape)))
+    ref = oracle.bf16_to_f32(oracle.bf16_ffn(cfg["x"], cfg["w_gate"], cfg["w_up"],
+                                             cfg["w_down"]))
+
+    def rl2(a, b):
+        a = np.asarray(a, np.float64)
+        b = np.asarray(b, np.float64)
+        return float(np.linalg.norm(a - b) / np.linalg.norm(b))
+
+    assert rl2(g1, g0) < 2 * eps
+    assert rl2(y1, y0) > 1e-3
+    assert rl2(y1, y0) < 0.1 * rl2(y0, ref)
