@@ -95,7 +95,7 @@ def main():
     # ------------------------------------------------------------ offline: a1 + a2 on the GPU
     t0 = time.time()
     bf16_layers = [w8a8.FfnBF16.from_weights(L["w_gate"], L["w_up"], L["w_down"]) for L in w_layers]
-    int8_layers = []
+    int8_layers, fp8_layers = [], []
     a = torch.empty_like(x_cal)
     xc = x_cal.clone()
     ws_cal = torch.empty(w8a8.bf16_ffn_workspace_bytes(x_cal.shape[0], D, F), dtype=torch.uint8, device=dev)
@@ -108,11 +108,14 @@ def main():
         h = w8a8.bf16_ffn_gate_up(bf16_layers[l], a)
         d_dn = w8a8.smooth_calibrate(w8a8.col_absmax(h), w8a8.col_absmax(L["w_down"]))
         int8_layers.append(w8a8.FfnW8A8.from_weights(L["w_gate"], L["w_up"], L["w_down"], d_gu, d_dn))
+        if not args.no_extras:   # the FP8 (E4M3) variant, same smoothing factors
+            fp8_layers.append(w8a8.fp8_ffn_layer(L["w_gate"], L["w_up"], L["w_down"], d_gu, d_dn))
         w8a8.bf16_ffn(bf16_layers[l], a, out=fo, ws=ws_cal)
         w8a8.rmsnorm_residual(xc, fo, out=xc)
     w8a8.rmsnorm(xc, out=a)
     d_lm = w8a8.smooth_calibrate(w8a8.col_absmax(a), w8a8.col_absmax(w_lm))
     lm_int8 = w8a8.LinearW8A8.from_weight(w_lm, d_lm)
+    lm_fp8 = None if args.no_extras else w8a8.fp8_linear_layer(w_lm, d_lm)
     lm_bf16 = w8a8.pack_bf16(w_lm)
     torch.cuda.synchronize()
     del w_layers, ws_cal
@@ -233,7 +236,7 @@ def main():
     if not args.no_extras:
         result["groups"] = extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16,
                                   x_all, w_lm, M, D, F, V, NL, make_graph, time_graph, ops_int8,
-                                  ops_all, sec)
+                                  ops_all, sec, fp8_layers, lm_fp8)
 
     # ------------------------------------------------------------ oracle on the host
     if not args.no_cpu_baseline:
@@ -264,7 +267,7 @@ def measured_traffic(m):
 
 
 def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all, w_lm, M, D, F,
-           V, NL, make_graph, time_graph, ops_int8, ops_all, step_sec):
+           V, NL, make_graph, time_graph, ops_int8, ops_all, step_sec, fp8_layers, lm_fp8):
     dev = x_all.device
     groups = {}
 
@@ -275,10 +278,13 @@ def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all
         y = torch.empty((m, D), dtype=torch.bfloat16, device=dev)
         ws8 = torch.empty(w8a8.ffn_workspace_bytes(m, D, F), dtype=torch.uint8, device=dev)
         wsb = torch.empty(w8a8.bf16_ffn_workspace_bytes(m, D, F), dtype=torch.uint8, device=dev)
+        wsf = torch.empty(w8a8.fp8_ffn_workspace_bytes(m, D, F), dtype=torch.uint8, device=dev)
         g8 = make_graph(lambda: [w8a8.ffn(L, xm, out=y, ws=ws8) for L in int8_layers])
         gb = make_graph(lambda: [w8a8.bf16_ffn(L, xm, out=y, ws=wsb) for L in bf16_layers])
+        gf = make_graph(lambda: [w8a8.fp8_ffn(L, xm, out=y, ws=wsf) for L in fp8_layers])
         t8 = time_graph(g8, 10) / NL
         tb = time_graph(gb, 10) / NL
+        tf = time_graph(gf, 10) / NL
         bytes8 = 3 * F * D + 2 * F * 4 + D * 4 + F * 4 + D * 4 + m * D * 2 * 2
         bytesb = 3 * F * D * 2 + m * D * 2 * 2
         ops = 6.0 * m * D * F
@@ -288,9 +294,11 @@ def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all
             "int8_GBs": round(bytes8 / t8 / 1e9, 1), "int8_hbm_frac": round(bytes8 / t8 / 1e9 / HBM_PEAK_GBS, 3),
             "bf16_GBs": round(bytesb / tb / 1e9, 1),
             "int8_tops": round(ops / t8 / 1e12, 1), "int8_mfma_frac": round(ops / t8 / 1e12 / INT8_PEAK_TOPS, 4),
+            "fp8_us": round(tf * 1e6, 2), "fp8_speedup_vs_bf16": round(tb / tf, 3),
+            "fp8_vs_int8": round(t8 / tf, 3),
             "note": "per FFN block incl. activation quant, GeGLU and requant; graph of 26 distinct layers"}
-        del g8, gb
-        log("ffn m=%d: int8 %.2f us, bf16 %.2f us" % (m, t8 * 1e6, tb * 1e6))
+        del g8, gb, gf
+        log("ffn m=%d: int8 %.2f us, bf16 %.2f us, fp8 %.2f us" % (m, t8 * 1e6, tb * 1e6, tf * 1e6))
 
     # --- FFN GEMMs alone at M = 2048 (prefill), INT8 TOPS against the MFMA peak
     m = 2048
@@ -305,13 +313,25 @@ def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all
     g_dn = make_graph(lambda: [w8a8.gemm_i8_i32(qh, m, L.down.wq, D, F, ws=wsl) for L in int8_layers])
     t_gu = time_graph(g_gu, 10) / NL
     t_dn = time_graph(g_dn, 10) / NL
+    del g_gu, g_dn
+    fqx, fsx = w8a8.fp8_quantize_act(xm, fp8_layers[0].gate.delta)
+    fqh, _ = w8a8.fp8_quantize_act(h, fp8_layers[0].down.delta)
+    wsf = torch.empty(w8a8.fp8_linear_workspace_bytes(m, D, F), dtype=torch.uint8, device=dev)
+    f_gu = make_graph(lambda: [w8a8.fp8_ffn_gate_up(L, fqx, fsx, m, out=h) for L in fp8_layers])
+    f_dn = make_graph(lambda: [w8a8.fp8_gemm_f32(fqh, m, L.down.wq, D, F, ws=wsf) for L in fp8_layers])
+    tf_gu = time_graph(f_gu, 10) / NL
+    tf_dn = time_graph(f_dn, 10) / NL
+    del f_gu, f_dn
     groups["prefill_gemm_m2048"] = {
         "gate_up_us": round(t_gu * 1e6, 2), "gate_up_tops": round(4.0 * m * D * F / t_gu / 1e12, 1),
         "gate_up_mfma_frac": round(4.0 * m * D * F / t_gu / 1e12 / INT8_PEAK_TOPS, 4),
         "down_us": round(t_dn * 1e6, 2), "down_tops": round(2.0 * m * D * F / t_dn / 1e12, 1),
-        "down_mfma_frac": round(2.0 * m * D * F / t_dn / 1e12 / INT8_PEAK_TOPS, 4)}
-    del g_gu, g_dn
-    log("prefill gemms m=2048: gate/up %.2f us, down %.2f us" % (t_gu * 1e6, t_dn * 1e6))
+        "down_mfma_frac": round(2.0 * m * D * F / t_dn / 1e12 / INT8_PEAK_TOPS, 4),
+        "fp8_gate_up_us": round(tf_gu * 1e6, 2), "fp8_down_us": round(tf_dn * 1e6, 2),
+        "fp8_gate_up_tflops": round(4.0 * m * D * F / tf_gu / 1e12, 1),
+        "fp8_down_tflops": round(2.0 * m * D * F / tf_dn / 1e12, 1)}
+    log("prefill gemms m=2048: gate/up %.2f us, down %.2f us; fp8 %.2f / %.2f us"
+        % (t_gu * 1e6, t_dn * 1e6, tf_gu * 1e6, tf_dn * 1e6))
 
     # --- lm_head decode: INT8 vs our bf16 kernel vs torch.mm (hipBLASLt) bf16
     w_lm_t = w_lm.t().contiguous()           # d x V, a plain (non-transposed) right operand
@@ -324,18 +344,23 @@ def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all
         g8 = make_graph(lambda: w8a8.lm_head(lm_int8, xm, out=lg, ws=ws8))
         gb = make_graph(lambda: w8a8.bf16_linear(xm, lm_bf16, V, D, out=lg, ws=wsb if wsb_n else None))
         gt = make_graph(lambda: torch.mm(xm, w_lm_t, out=lg))
+        wsf = torch.empty(w8a8.fp8_linear_workspace_bytes(m, V, D), dtype=torch.uint8, device=dev)
+        gf = make_graph(lambda: w8a8.fp8_lm_head(lm_fp8, xm, out=lg, ws=wsf))
         t8 = time_graph(g8, 20)
         tb = time_graph(gb, 20)
         tt = time_graph(gt, 20)
+        tf = time_graph(gf, 20)
         b8 = V * D + V * 4 + D * 4 + m * D * 2 + m * V * 2
         bb = V * D * 2 + m * D * 2 + m * V * 2
         groups["lm_head_m%d" % m] = {
             "int8_us": round(t8 * 1e6, 2), "bf16_ours_us": round(tb * 1e6, 2),
             "bf16_torch_us": round(tt * 1e6, 2), "speedup": round(min(tb, tt) / t8, 3),
             "int8_GBs": round(b8 / t8 / 1e9, 1), "int8_hbm_frac": round(b8 / t8 / 1e9 / HBM_PEAK_GBS, 3),
-            "bf16_best_GBs": round(bb / min(tb, tt) / 1e9, 1)}
-        del g8, gb, gt
-        log("lm_head m=%d: int8 %.2f us, bf16 ours %.2f us, torch %.2f us" % (m, t8 * 1e6, tb * 1e6, tt * 1e6))
+            "bf16_best_GBs": round(bb / min(tb, tt) / 1e9, 1),
+            "fp8_us": round(tf * 1e6, 2), "fp8_GBs": round(b8 / tf / 1e9, 1)}
+        del g8, gb, gt, gf
+        log("lm_head m=%d: int8 %.2f us, bf16 ours %.2f us, torch %.2f us, fp8 %.2f us"
+            % (m, t8 * 1e6, tb * 1e6, tt * 1e6, tf * 1e6))
     del w_lm_t
 
     # --- the paper's precision maps on the whole step (same M as the step)
