@@ -116,11 +116,14 @@ bool plan_stream(Plan& p, int64_t m, int64_t n, int64_t kb, bool glu, bool f8) {
   // those that keep >= 768 waves busy
   bool found = false;
   int64_t best_pw = -1, best_waves = -1;
+  const int force_wk = env_int("W8A8_STREAM_WK", 0);
+  const int64_t min_splits = env_int("W8A8_STREAM_SPLITS", 1);
   for (int wk : {16, 4, 2}) {
     if (wk == 16 && p.mb > 1) continue;  // 16-wave workgroups only for MB = 1
+    if (force_wk && wk != force_wk) continue;
     int64_t max_kc = (lds_kb - (wk - 1) * p.mb) / p.mb;
     if (max_kc < wk) continue;
-    int64_t splits = ceil_div(kb, max_kc / kstep * kstep);
+    int64_t splits = std::max(min_splits, ceil_div(kb, max_kc / kstep * kstep));
     int64_t kchunk = round_up(ceil_div(kb, splits), kstep);
     splits = ceil_div(kb, kchunk);
     int64_t pw = ceil_div(kchunk, wk), waves = nbc * splits * wk;
@@ -250,6 +253,13 @@ w8a8_status run_gemm(const Plan& pl, int dt, int epi, const void* A, int64_t lda
   p.kchunk = pl.kchunk;
   p.splits = pl.splits;
   p.s_a = s_a;
+  if (ql.x) {
+    // quantise-on-load: the token scales exist only inside the GEMM, which
+    // leaves them at s_out; a split-K reduction dequantises from there
+    if (pl.splits > 1 && !ql.s_out)
+      return fail(W8A8_EINVAL, "internal: quantise-on-load with split-K needs a scale buffer");
+    p.s_a = ql.s_out;
+  }
   p.s_b = s_b;
   p.s_b2 = s_b2;
   p.out = out;
@@ -444,7 +454,8 @@ w8a8_status linear_impl(const w8a8_linear_desc* d, const void* x, bool x_bf16, i
   Plan pl = plan_gemm(m, d->n, d->k, dt, false);
   if (x_bf16 && plan_qloads(pl, m, d->k))  // one launch: the GEMM quantises x itself
     return run_gemm(pl, DT_I8, epi, nullptr, 0, m, d->wq, nullptr, d->n, d->k, nullptr, d->s_w,
-                    nullptr, y, d->n, base + w.gemm, st, QLoad{(const uint16_t*)x, d->delta});
+                    nullptr, y, d->n, base + w.gemm, st,
+                    QLoad{(const uint16_t*)x, d->delta, (float*)(base + w.sx)});
   CHECK(quant_act_impl(x, x_bf16, m, d->k, d->delta, base + w.qx, (float*)(base + w.sx), st, dt));
   return run_gemm(pl, dt, epi, base + w.qx, 0, m, d->wq, nullptr, d->n, d->k,
                   (const float*)(base + w.sx), d->s_w, nullptr, y, d->n, base + w.gemm, st);
@@ -458,7 +469,7 @@ w8a8_status ffn_impl(const w8a8_ffn_desc* d, const void* x, int64_t m, void* y, 
   if (plan_qloads(pg, m, d->d)) {
     CHECK(run_gemm(pg, DT_I8, EPI_GLU, nullptr, 0, m, d->wq_gate, d->wq_up, d->f, d->d, nullptr,
                    d->s_gate, d->s_up, base + w.h, d->f, nullptr, st,
-                   QLoad{(const uint16_t*)x, d->delta_gu}));
+                   QLoad{(const uint16_t*)x, d->delta_gu, (float*)(base + w.sx)}));
   } else {
     CHECK(quant_act_impl(x, true, m, d->d, d->delta_gu, base + w.qx, (float*)(base + w.sx), st,
                          dt));
@@ -470,7 +481,7 @@ w8a8_status ffn_impl(const w8a8_ffn_desc* d, const void* x, int64_t m, void* y, 
   if (plan_qloads(pd, m, d->f))
     return run_gemm(pd, DT_I8, EPI_BF16, nullptr, 0, m, d->wq_down, nullptr, d->d, d->f, nullptr,
                     d->s_down, nullptr, y, d->d, base + w.gemm, st,
-                    QLoad{(const uint16_t*)(base + w.h), d->delta_down});
+                    QLoad{(const uint16_t*)(base + w.h), d->delta_down, (float*)(base + w.sh)});
   CHECK(quant_act_impl(base + w.h, true, m, d->f, d->delta_down, base + w.qh,
                        (float*)(base + w.sh), st, dt));
   return run_gemm(pd, dt, EPI_BF16, base + w.qh, 0, m, d->wq_down, nullptr, d->d, d->f,

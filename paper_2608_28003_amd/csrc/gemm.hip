@@ -485,9 +485,41 @@ __global__ __launch_bounds__(64 * NW, 2) void gemm_tile_kernel(GemmParams p) {
 template <int NW>
 constexpr int qload_max_groups() { return 1; }
 
+// The bf16 activations and smoothing factors of this thread's groups, loaded
+// before the workgroup's first weight batch: loads return in issue order, so
+// the quantisation below then runs while the weights are still in flight.
+template <int NW>
+struct QloadRegs {
+  uint4 x[qload_max_groups<NW>()][2];
+  float4 d[qload_max_groups<NW>()][4];
+};
+
+template <int NW>
+__device__ __forceinline__ void quantize_fetch(const GemmParams& p, QloadRegs<NW>& R) {
+  constexpr int NT = NW * 64;
+  const int tid = threadIdx.x;
+  const int rows = min(p.M, 16);
+  const int G = p.a_k / 16;
+#pragma unroll
+  for (int i = 0; i < qload_max_groups<NW>(); ++i) {
+    const int gi = tid + i * NT;
+    if (gi < rows * G) {
+      const int r = gi / G, c0 = (gi % G) * 16;
+      const uint16_t* xr = p.a_x + (int64_t)r * p.a_ld + c0;
+      R.x[i][0] = *reinterpret_cast<const uint4*>(xr);
+      R.x[i][1] = *reinterpret_cast<const uint4*>(xr + 8);
+      if (p.a_delta) {
+        const float4* dp = reinterpret_cast<const float4*>(p.a_delta + c0);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) R.d[i][q] = dp[q];
+      }
+    }
+  }
+}
+
 template <int NW>
 __device__ __forceinline__ void quantize_panel(const GemmParams& p, int kb0, int kc, v4i* lds_a,
-                                               float* s_row) {
+                                               float* s_row, const QloadRegs<NW>& R) {
   constexpr int NT = NW * 64;
   constexpr int MAXG = qload_max_groups<NW>();
   __shared__ unsigned int amax_bits[16];
@@ -501,19 +533,15 @@ __device__ __forceinline__ void quantize_panel(const GemmParams& p, int kb0, int
     const int gi = tid + i * NT;
     mx[i] = 0.0f;
     if (gi < rows * G) {
-      const int r = gi / G, c0 = (gi % G) * 16;
-      const uint16_t* xr = p.a_x + (int64_t)r * p.a_ld + c0;
-      const uint4 r0 = *reinterpret_cast<const uint4*>(xr);
-      const uint4 r1 = *reinterpret_cast<const uint4*>(xr + 8);
-      const uint32_t w[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
+      const uint32_t w[8] = {R.x[i][0].x, R.x[i][0].y, R.x[i][0].z, R.x[i][0].w,
+                             R.x[i][1].x, R.x[i][1].y, R.x[i][1].z, R.x[i][1].w};
 #pragma unroll
       for (int e = 0; e < 16; ++e)
         v[i][e] = bf16_bits_to_float((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xffffu));
       if (p.a_delta) {
-        const float4* dp = reinterpret_cast<const float4*>(p.a_delta + c0);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const float4 d4 = dp[q];
+          const float4 d4 = R.d[i][q];
           v[i][4 * q + 0] = v[i][4 * q + 0] / d4.x;
           v[i][4 * q + 1] = v[i][4 * q + 1] / d4.y;
           v[i][4 * q + 2] = v[i][4 * q + 2] / d4.z;
@@ -635,10 +663,15 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
       }
     }
   };
+  QloadRegs<NW> qr;
+  if constexpr (QLOAD_OK) {
+    if (qload) quantize_fetch<NW>(p, qr);  // ahead of the weights: quantised while they arrive
+  }
+  __builtin_amdgcn_sched_barrier(0);
   if (total > 0) load_batch(0, b0, u0);  // first weights go out with the A fragments
   __shared__ float s_row[16];             // quantise-on-load: per-row scales
   if constexpr (QLOAD_OK) {
-    if (qload) quantize_panel<NW>(p, kb0, kc, lds_a, s_row);  // overlaps the first weight loads
+    if (qload) quantize_panel<NW>(p, kb0, kc, lds_a, s_row, qr);  // overlaps the weight loads
   }
   wait_vmcnt<0>();
   if ((WK == 1 && NW > 1) || qload) lds_barrier();  // the shared panel is read by every wave
@@ -895,7 +928,37 @@ static hipError_t tile_epi(int epi, int tile, const GemmParams& p, hipStream_t s
   }
 }
 
+// Host-side check, before any launch, that every buffer the kernel will read
+// or write is present and that the K split is consistent: a missing scale or
+// partial-sum buffer becomes an error return instead of a device access.
+//   kind 0: tiled kernel, 1: streaming kernel with nw waves, 2: split-K reduction
+static bool gemm_params_ok(int dt, int epi, const GemmParams& p, int kind, int nw = 1) {
+  const bool glu = epi == EPI_GLU;
+  if (p.M < 1 || p.N < 1 || p.kb_count < 1 || p.kchunk < 1 || p.splits < 1) return false;
+  if ((int64_t)p.kchunk * (p.splits - 1) >= p.kb_count) return false;  // no empty split
+  if ((int64_t)p.kchunk * p.splits < p.kb_count) return false;         // K fully covered
+  if (glu && p.splits != 1) return false;  // the gated epilogue needs whole sums
+  const bool qload = kind == 1 && dt == DT_I8 && p.a_x != nullptr;
+  if (kind == 0 && p.a_x) return false;  // the tiled kernel reads codes only
+  if (qload && (p.M > 16 || p.a_k < 16 || (int64_t)p.M * (p.a_k / 16) > (int64_t)64 * nw))
+    return false;
+  if (kind == 2) {
+    if (!p.part || !p.out) return false;
+  } else {
+    if (!p.B || (glu && !p.B2) || (!p.A && !qload)) return false;
+    if (p.splits > 1 ? !p.part : !p.out) return false;
+  }
+  // dequantising epilogues (int8 / E4M3 operands) read both scale vectors
+  const bool dequant = dt != DT_BF16 && epi != EPI_I32 && (kind == 2 || p.splits == 1);
+  if (dequant) {
+    if (!p.s_b || (glu && !p.s_b2)) return false;
+    if (!p.s_a && !qload) return false;  // quantise-on-load keeps its scales in LDS
+  }
+  return true;
+}
+
 hipError_t launch_gemm_tile(int dt, int epi, int tile, const GemmParams& p, hipStream_t st) {
+  if (!gemm_params_ok(dt, epi, p, 0)) return hipErrorInvalidValue;
   switch (dt) {
     case DT_I8: return tile_epi<DT_I8>(epi, tile, p, st);
     case DT_BF16: return tile_epi<DT_BF16>(epi, tile, p, st);
@@ -978,6 +1041,8 @@ static hipError_t stream_epi(int epi, int mb, int nw, int wk, const GemmParams& 
 
 hipError_t launch_gemm_stream(int dt, int epi, int mb, int nw, int wk, const GemmParams& p,
                               int nb_per_block, hipStream_t st) {
+  if (!gemm_params_ok(dt, epi, p, 1, nw)) return hipErrorInvalidValue;
+  if (p.M > 16 * mb || nb_per_block < 1) return hipErrorInvalidValue;
   switch (dt) {
     case DT_I8: return stream_epi<DT_I8>(epi, mb, nw, wk, p, nb_per_block, st);
     case DT_BF16: return stream_epi<DT_BF16>(epi, mb, nw, wk, p, nb_per_block, st);
@@ -1007,6 +1072,7 @@ static hipError_t reduce_epi(int epi, const GemmParams& p, hipStream_t st) {
 }
 
 hipError_t launch_splitk_reduce(int dt, int epi, const GemmParams& p, hipStream_t st) {
+  if (!gemm_params_ok(dt, epi, p, 2)) return hipErrorInvalidValue;
   switch (dt) {
     case DT_I8: return reduce_epi<DT_I8>(epi, p, st);
     case DT_BF16: return reduce_epi<DT_BF16>(epi, p, st);

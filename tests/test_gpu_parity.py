@@ -491,6 +491,38 @@ def test_quantise_on_load_equals_separate_quantisation(m, monkeypatch):
     np.testing.assert_array_equal(outs[0][1], outs[1][1])
 
 
+@pytest.mark.parametrize("m", [1, 2])
+def test_long_k_decode_linear_bit_exact(m):
+    """K = 16384 at decode: the streaming plan splits K over two workgroups
+    and quantises x on load, so the split-K reduction dequantises with the
+    scales the GEMM left in the workspace."""
+    say("long-K decode linear", m)
+    k, n = 16384, 1152
+    x = act_input(m, k, 5100 + m)
+    w = synth.to_bf16_bits(synth.normal(5200, (n, k), 0.02))
+    delta = oracle.smooth_calibrate(act_input(256, k, 5300), [w])
+    wq_o, sw_o = oracle.quantize_weights(w, delta)
+    y_o = oracle.w8a8_linear(x, wq_o, sw_o, delta, "bf16")
+    layer = w8a8.LinearW8A8.from_weight(dev_bf16(w), dev_f32(delta))
+    y = w8a8.linear(layer, dev_bf16(x), torch.bfloat16)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host_bf16(y), y_o)
+
+
+@pytest.mark.parametrize("wk,splits", [(16, 2), (16, 4), (4, 2), (4, 8), (2, 4)])
+def test_decode_down_stream_plans_bit_identical(wk, splits, monkeypatch):
+    """Every streaming plan of the M = 1 FFN down projection (wave split of
+    K, K split over workgroups, with or without quantise-on-load) gives the
+    same output: int32 sums are exact in any order."""
+    say("decode down plans", wk, splits)
+    cfg, q, layer = _ffn_setup(1)
+    x = dev_bf16(cfg["x"])
+    ref = host_bf16(w8a8.ffn(layer, x))
+    monkeypatch.setenv("W8A8_STREAM_WK", str(wk))
+    monkeypatch.setenv("W8A8_STREAM_SPLITS", str(splits))
+    np.testing.assert_array_equal(host_bf16(w8a8.ffn(layer, x)), ref)
+
+
 @pytest.mark.parametrize("m", [1, 16, 128, 300])
 def test_stack_fused_glue_equals_composition(m):
     """The stack fuses each layer boundary (split-K reduction, dequant,
