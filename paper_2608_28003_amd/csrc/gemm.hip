@@ -488,6 +488,10 @@ constexpr int qload_max_groups() { return 1; }
 // The bf16 activations and smoothing factors of this thread's groups, loaded
 // before the workgroup's first weight batch: loads return in issue order, so
 // the quantisation below then runs while the weights are still in flight.
+// The loads are issued by every thread without branching (threads past the
+// last group repeat a valid group; without quantise-on-load they read the
+// first bytes of B and are ignored), which lets the compiler wait for exactly
+// these loads rather than for every load outstanding.
 template <int NW>
 struct QloadRegs {
   uint4 x[qload_max_groups<NW>()][2];
@@ -495,25 +499,25 @@ struct QloadRegs {
 };
 
 template <int NW>
-__device__ __forceinline__ void quantize_fetch(const GemmParams& p, QloadRegs<NW>& R) {
+__device__ __forceinline__ void quantize_fetch(const GemmParams& p, bool qload, QloadRegs<NW>& R) {
   constexpr int NT = NW * 64;
   const int tid = threadIdx.x;
-  const int rows = min(p.M, 16);
-  const int G = p.a_k / 16;
+  const int rows = qload ? min(p.M, 16) : 1;
+  const int G = qload ? p.a_k / 16 : 1;
+  const uint16_t* xbase = qload ? p.a_x : reinterpret_cast<const uint16_t*>(p.B);
+  const float* dbase = (qload && p.a_delta) ? p.a_delta : reinterpret_cast<const float*>(p.B);
+  const int64_t ld = qload ? p.a_ld : 0;
+  const int cmul = qload ? 16 : 0;
 #pragma unroll
   for (int i = 0; i < qload_max_groups<NW>(); ++i) {
-    const int gi = tid + i * NT;
-    if (gi < rows * G) {
-      const int r = gi / G, c0 = (gi % G) * 16;
-      const uint16_t* xr = p.a_x + (int64_t)r * p.a_ld + c0;
-      R.x[i][0] = *reinterpret_cast<const uint4*>(xr);
-      R.x[i][1] = *reinterpret_cast<const uint4*>(xr + 8);
-      if (p.a_delta) {
-        const float4* dp = reinterpret_cast<const float4*>(p.a_delta + c0);
+    const int gi = min(tid + i * NT, rows * G - 1);
+    const int r = gi / G, c0 = (gi % G) * cmul;
+    const uint16_t* xr = xbase + (int64_t)r * ld + c0;
+    R.x[i][0] = *reinterpret_cast<const uint4*>(xr);
+    R.x[i][1] = *reinterpret_cast<const uint4*>(xr + 8);
+    const float4* dp = reinterpret_cast<const float4*>(dbase + ((qload && p.a_delta) ? c0 : 0));
 #pragma unroll
-        for (int q = 0; q < 4; ++q) R.d[i][q] = dp[q];
-      }
-    }
+    for (int q = 0; q < 4; ++q) R.d[i][q] = dp[q];
   }
 }
 
@@ -588,9 +592,10 @@ __device__ __forceinline__ void quantize_panel(const GemmParams& p, int kb0, int
   }
 }
 
-template <int DT, int MB, int EPI, int NW, int WK>
+template <int DT, int MB, int EPI, int NW, int WK, bool QL>
 __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int nb_per_block) {
   static_assert(WK == 1 || WK == NW, "either every wave owns its column blocks or all share one");
+  static_assert(!QL || (DT == DT_I8 && MB == 1), "quantise-on-load: int8, one row block");
   constexpr bool GLU = (EPI == EPI_GLU);
   constexpr bool BF16 = (DT == DT_BF16);
   constexpr bool FACC = (DT != DT_I8);
@@ -635,9 +640,12 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
              frag_offset(min(mb, p.rb_a - 1), kb0 + kk, p.kb_count) + lane * 16;
     }
   };
-  constexpr bool QLOAD_OK = DT == DT_I8 && MB == 1;
-  const bool qload = QLOAD_OK && p.a_x != nullptr;
-  if (!qload) {
+  // QL: the workgroup quantises its bf16 rows itself (p.a_x); a separate
+  // instantiation, so that the quantising kernel has no staging loop whose
+  // outstanding loads the compiler would have to wait for before quantising
+  constexpr bool QLOAD_OK = QL;
+  constexpr bool qload = QL;
+  if constexpr (!QL) {
     if constexpr (WK > 1) {
       for (int f = 0; f < MB * my_k; ++f) {
         const int mb = f / my_k, kk = ks0 + f % my_k;
@@ -651,8 +659,31 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
     }
   }
 
+  // Scales live in registers: the token scales of this lane's rows loaded
+  // before the weights, the channel scales of a column block together with
+  // its first weight batch, so neither adds a memory round trip after the
+  // weights have arrived.
+  const bool scaled = !BF16 && (GLU || ((EPI == EPI_F32 || EPI == EPI_BF16) && p.splits == 1));
+  float sa_r[MB][4];
+  float sb_c = 0.0f, sb2_c = 0.0f;
+  float sbn[2] = {0.0f, 0.0f}, sbn2[2] = {0.0f, 0.0f};  // per weight buffer
+  if constexpr (!QL) {  // branch-free (reads B's first bytes where the values are unused)
+    const bool from_sa = scaled;
+    const float* sa_src = from_sa ? p.s_a : reinterpret_cast<const float*>(p.B);
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        sa_r[mb][r] = sa_src[from_sa ? min(mb * 16 + (lane >> 4) * 4 + r, p.M - 1) : 0];
+  }
+  auto load_scales = [&](int nb, float& sbx, float& sbx2) {
+    const int col = min(nb * 16 + (lane & 15), p.N - 1);
+    sbx = p.s_b[col];
+    if constexpr (GLU) sbx2 = p.s_b2[col];
+  };
+
   v4i b0[KU], b1[KU], u0[KG], u1[KG];
-  auto load_batch = [&](int idx, v4i (&b)[KU], v4i (&bu)[KG]) {
+  auto load_batch = [&](int idx, v4i (&b)[KU], v4i (&bu)[KG], float& sbx, float& sbx2) {
     const int nb = my_first + GROUPS * (idx / bpn);
     const int k0 = (idx % bpn) * KU;
 #pragma unroll
@@ -662,33 +693,38 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
         if constexpr (GLU) bu[u] = load_frag_packed(p.B2, nb, kb0 + ks0 + k0 + u, p.kb_count, lane);
       }
     }
+    if (scaled && k0 == 0) load_scales(nb, sbx, sbx2);
+  };
+  // The first batch issues all KU loads per operand, indexes clamped into
+  // this wave's slice (or, for a wave without work, into the workgroup's
+  // range): a fixed number of loads follows the activation loads of
+  // quantise-on-load, so the wait before quantising covers those alone.
+  auto load_first = [&](v4i (&b)[KU], v4i (&bu)[KG], float& sbx, float& sbx2) {
+    const int nb = min(my_first, p.rb_b - 1);
+#pragma unroll
+    for (int u = 0; u < KU; ++u) {
+      const int kf = kb0 + min(ks0 + min(u, max(my_k - 1, 0)), kc - 1);
+      b[u] = load_frag_packed(p.B, nb, kf, p.kb_count, lane);
+      if constexpr (GLU) bu[u] = load_frag_packed(p.B2, nb, kf, p.kb_count, lane);
+    }
+    if (scaled) load_scales(nb, sbx, sbx2);
   };
   QloadRegs<NW> qr;
-  if constexpr (QLOAD_OK) {
-    if (qload) quantize_fetch<NW>(p, qr);  // ahead of the weights: quantised while they arrive
-  }
+  if constexpr (QLOAD_OK) quantize_fetch<NW>(p, true, qr);  // ahead of the weights
+
   __builtin_amdgcn_sched_barrier(0);
-  if (total > 0) load_batch(0, b0, u0);  // first weights go out with the A fragments
-  __shared__ float s_row[16];             // quantise-on-load: per-row scales
+  load_first(b0, u0, sbn[0], sbn2[0]);  // first weights go out with the A fragments
+  __shared__ float s_row[16];           // quantise-on-load: per-row scales
   if constexpr (QLOAD_OK) {
     if (qload) quantize_panel<NW>(p, kb0, kc, lds_a, s_row, qr);  // overlaps the weight loads
   }
   wait_vmcnt<0>();
   if ((WK == 1 && NW > 1) || qload) lds_barrier();  // the shared panel is read by every wave
-  // Scales live in registers: the token scales of this lane's rows from the
-  // start, the channel scales of a column block loaded with its first weights
-  // (their latency then hides behind that block's products).
-  const bool scaled = !BF16 && (GLU || ((EPI == EPI_F32 || EPI == EPI_BF16) && p.splits == 1));
-  float sa_r[MB][4];
-  float sb_c = 0.0f, sb2_c = 0.0f;
-  if (scaled) {
+  if (scaled && qload) {
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = min(mb * 16 + (lane >> 4) * 4 + r, p.M - 1);
-        sa_r[mb][r] = qload ? s_row[row] : p.s_a[row];
-      }
+      for (int r = 0; r < 4; ++r) sa_r[mb][r] = s_row[min(mb * 16 + (lane >> 4) * 4 + r, p.M - 1)];
   }
 
   AccT acc[MB], accu[GLU ? MB : 1];
@@ -731,7 +767,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
         }
       }
   };
-  auto compute = [&](int idx, const v4i (&b)[KU], const v4i (&bu)[KG]) {
+  auto compute = [&](int idx, const v4i (&b)[KU], const v4i (&bu)[KG], float sbx, float sbx2) {
     const int nb = my_first + GROUPS * (idx / bpn);
     const int bi = idx % bpn;
     const int k0 = bi * KU;
@@ -741,11 +777,8 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
         acc[mb] = Acc<DT>::zero();
         if constexpr (GLU) accu[mb] = Acc<DT>::zero();
       }
-      if (scaled) {
-        const int col = min(nb * 16 + (lane & 15), p.N - 1);
-        sb_c = p.s_b[col];
-        if constexpr (GLU) sb2_c = p.s_b2[col];
-      }
+      sb_c = sbx;
+      sb2_c = sbx2;
     }
 #pragma unroll
     for (int u = 0; u < KU; u += KP) {
@@ -793,11 +826,11 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
   };
 
   for (int idx = 0; idx < total; idx += 2) {
-    if (idx + 1 < total) load_batch(idx + 1, b1, u1);
-    compute(idx, b0, u0);
+    if (idx + 1 < total) load_batch(idx + 1, b1, u1, sbn[1], sbn2[1]);
+    compute(idx, b0, u0, sbn[0], sbn2[0]);
     if (idx + 1 < total) {
-      if (idx + 2 < total) load_batch(idx + 2, b0, u0);
-      compute(idx + 1, b1, u1);
+      if (idx + 2 < total) load_batch(idx + 2, b0, u0, sbn[0], sbn2[0]);
+      compute(idx + 1, b1, u1, sbn[1], sbn2[1]);
     }
   }
 }
@@ -972,9 +1005,9 @@ static size_t stream_lds_bytes(int mb, int kchunk, int wk, bool glu) {
   return (size_t)mb * kchunk * kFragBytes + (size_t)(wk - 1) * (glu ? 2 : 1) * mb * kFragBytes;
 }
 
-template <int DT, int MB, int EPI, int NW, int WK>
-static hipError_t stream_launch(const GemmParams& p, int nbpb, hipStream_t st) {
-  auto kern = gemm_stream_kernel<DT, MB, EPI, NW, WK>;
+template <int DT, int MB, int EPI, int NW, int WK, bool QL>
+static hipError_t stream_launch_ql(const GemmParams& p, int nbpb, hipStream_t st) {
+  auto kern = gemm_stream_kernel<DT, MB, EPI, NW, WK, QL>;
   static size_t static_lds = 0;  // benign race: every caller computes the same values
   static bool attr_set = false;
   if (!attr_set) {
@@ -993,6 +1026,14 @@ static hipError_t stream_launch(const GemmParams& p, int nbpb, hipStream_t st) {
   dim3 grid((unsigned)((p.rb_b + nbpb - 1) / nbpb), (unsigned)p.splits);
   kern<<<grid, 64 * NW, lds, st>>>(p, nbpb);
   return hipGetLastError();
+}
+
+template <int DT, int MB, int EPI, int NW, int WK>
+static hipError_t stream_launch(const GemmParams& p, int nbpb, hipStream_t st) {
+  if constexpr (DT == DT_I8 && MB == 1) {
+    if (p.a_x) return stream_launch_ql<DT, MB, EPI, NW, WK, true>(p, nbpb, st);
+  }
+  return stream_launch_ql<DT, MB, EPI, NW, WK, false>(p, nbpb, st);
 }
 
 // Instantiated wave layouts: 16-wave workgroups only for MB == 1 (at 16 waves a
