@@ -182,13 +182,21 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
     p.splits = (int)ceil_div(kb, p.kchunk);
     return p;
   }
+  // int8 choices from a sweep of the FFN shapes (d = 1152, f = 6912) at
+  // M = 128 ... 2048; the bf16 path keeps the older rule
+  const bool i8 = dt == DT_I8;
+  const bool long_k = i8 && !glu && k >= 4096 && n <= 4096;  // down-projection-like
   if (glu) {
     if (m <= 128)
       p.tile = TILE_GLU_128x32_K2;
-    else if (tiles_of(TILE_GLU_256x64, m, n) >= 512)  // two resident per CU
+    else if (tiles_of(TILE_GLU_256x64, m, n) >= (i8 ? 384 : 512))  // two resident per CU
       p.tile = TILE_GLU_256x64;
+    else if (i8)
+      p.tile = tiles_of(TILE_GLU_128x64, m, n) >= 400 ? TILE_GLU_128x64 : TILE_GLU_64x64_K2;
     else
       p.tile = tiles_of(TILE_GLU_128x64, m, n) >= 256 ? TILE_GLU_128x64 : TILE_GLU_64x64;
+  } else if (long_k) {
+    p.tile = TILE_64x64_K2;  // with K split until ~512 workgroups are in flight
   } else {
     if (tiles_of(TILE_128x128, m, n) >= 256)
       p.tile = TILE_128x128;
@@ -200,7 +208,10 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
   p.tile = glu ? env_int("W8A8_GLU_TILE", p.tile) : env_int("W8A8_GEMM_TILE", p.tile);
   const int64_t tiles = tiles_of(p.tile, m, n);
   int splits = 1;
-  if (!glu && tiles < 200)
+  if (long_k)
+    splits = (int)std::min<int64_t>(std::min<int64_t>(ceil_div(512, tiles), 6),
+                                    std::max<int64_t>(1, kb / 8));
+  else if (!glu && tiles < 200)
     splits = (int)std::min<int64_t>(ceil_div(256, tiles), std::max<int64_t>(1, kb / 4));
   splits = env_int("W8A8_GEMM_SPLITS", splits);
   if (glu || splits < 1) splits = 1;
@@ -407,7 +418,25 @@ size_t bf16_linear_ws(int64_t m, int64_t n, int64_t k) {
 // Experiment hooks: W8A8_DOWN_TILE, W8A8_DOWN_SPLITS.
 Plan stack_down_plan(int64_t m, int64_t d, int64_t f) {
   Plan p = plan_gemm(m, d, f, DT_I8, false);
-  if (p.stream) return p;
+  if (p.stream) {
+    // The glue adds split-K partial sums at no extra launch, so at decode
+    // sizes the long-K down projection is spread over twice as many
+    // workgroups as its d / 16 column blocks: one CU streams only ~25 GB/s,
+    // and 72 busy CUs would cap the projection near 1.8 TB/s (measured best:
+    // 2 splits of 16 waves; 4 splits leave too little work per wave).
+    const int64_t kb = ceil_div(f, kFragK8), nbc = ceil_div(d, 16);
+    const int splits = env_int("W8A8_DOWN_SPLITS", (int)std::min<int64_t>(
+                                                       std::max<int64_t>(1, kb / 16), ceil_div(144, nbc)));
+    const int wk = env_int("W8A8_DOWN_WK", p.wk);
+    if (splits > p.splits && (wk == 16 || wk == 4 || wk == 2) && !(wk == 16 && p.mb > 1)) {
+      Plan q = p;
+      q.nw = q.wk = wk;
+      q.kchunk = (int)ceil_div(kb, splits);
+      q.splits = (int)ceil_div(kb, q.kchunk);
+      if (q.mb * q.kchunk + (wk - 1) * q.mb <= 158) return q;  // dynamic LDS, KiB
+    }
+    return p;
+  }
   p.tile = env_int("W8A8_DOWN_TILE", p.tile);
   const int64_t kb = ceil_div(f, kFragK8);
   const int splits = std::max(1, env_int("W8A8_DOWN_SPLITS", p.splits));
