@@ -381,6 +381,40 @@ def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all
             base = ts
         maps[name] = {"ms": round(ts * 1e3, 4), "speedup_vs_bf16": round(base / ts, 3)}
     groups["stack_maps_m%d" % M] = maps
+    # the same maps at decode (one token per step: the paper's batch-1 setting)
+    x1 = x_all[:1].contiguous()
+    out1 = torch.empty((1, V), dtype=torch.bfloat16, device=dev)
+    ws1 = torch.empty(w8a8.stack_workspace_bytes(1, D, F, V), dtype=torch.uint8, device=dev)
+    maps1, base1 = {}, None
+    for name, mp, lm8 in [("bf16", "bf16", False), ("lm_head only", "bf16", True),
+                          ("FFN 5+5 + lm_head", "5+5", True), ("FFN 10+10 + lm_head", "10+10", True),
+                          ("FFN all26 + lm_head", "all26", True)]:
+        prec = w8a8.precision_map(mp)
+        gs = make_graph(lambda: stack.run(x1, prec, lm8, out=out1, ws=ws1))
+        ts = time_graph(gs, 10)
+        del gs
+        if base1 is None:
+            base1 = ts
+        maps1[name] = {"us": round(ts * 1e6, 1), "speedup_vs_bf16": round(base1 / ts, 3)}
+    groups["stack_maps_m1"] = maps1
+    # layer sensitivity (SQNR, dB) on 64 tokens and automatically chosen maps
+    xs = x_all[:64].contiguous()
+    iso, prop = stack.sensitivity(xs, w8a8.precision_map("all26"))
+    auto = {}
+    for budget in (30.0, 40.0):
+        prec, db = stack.select_map(xs, budget)
+        gs = make_graph(lambda: stack.run(xm, prec, True, out=out, ws=ws))
+        ts = time_graph(gs, 10)
+        del gs
+        auto["budget_%g_db" % budget] = {
+            "int8_layers": [int(i) for i in np.flatnonzero(prec)], "sqnr_db": round(db, 2),
+            "ms_m%d" % M: round(ts * 1e3, 4), "speedup_vs_bf16": round(base / ts, 3)}
+    groups["sensitivity_m64"] = {"isolated_db": [round(float(v), 2) for v in iso],
+                                 "propagated_all26_db": [round(float(v), 2) for v in prop],
+                                 "auto_maps": auto}
+    log("auto maps: " + ", ".join("%s: %d INT8 layers, %.1f dB" % (k, len(v["int8_layers"]), v["sqnr_db"])
+                                  for k, v in auto.items()))
+    log("stack at M=1: " + ", ".join("%s %.1f us" % (k, v["us"]) for k, v in maps1.items()))
     groups["paper_context"] = {"note": "RTX 5090 + TensorRT-LLM, end-to-end decode tok/s at batch 1; not a target",
                                "FFN 5+5 + lm_head": 1.110, "FFN all26 + lm_head": 1.191}
     return groups

@@ -321,6 +321,65 @@ w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec,
                            int lm_head_int8, const void* x, int64_t m, void* logits,
                            void* ws, size_t ws_bytes, w8a8_stream_t stream);
 
+/* ---------------------------------------------------------------- sensitivity and map selection */
+
+/* Signal-to-quantisation-noise ratio (Sec. 3 eq. sqnr-ffn; Sec. 5 eq. sqnr-block,
+   the same ratio over a block's output): out[0] = sum ref^2, out[1] =
+   sum (ref - test)^2, out[2] = 10 log10(out[0] / out[1]) in dB, all binary64
+   (+inf when the two agree exactly, -inf for an all-zero ref, NaN for both).
+   ref, test: n elements, f32 or bf16 (dtype); out: DEVICE double[3].
+   Deterministic: fixed grid and fixed-order reductions.
+   ws: w8a8_sqnr_workspace_bytes(n) bytes. */
+size_t w8a8_sqnr_workspace_bytes(int64_t n);
+w8a8_status w8a8_sqnr(const void* ref, const void* test, w8a8_dtype dtype, int64_t n,
+                      double* out, void* ws, size_t ws_bytes, w8a8_stream_t stream);
+
+/* w8a8_ffn_stack that also records the token stream after every layer:
+   hidden = n_layers consecutive bf16 m x d matrices (hidden[l] after layer l).
+   logits may be NULL (no lm_head; lm_head_int8 is then ignored).
+   ws: w8a8_stack_workspace_bytes(m, d, f, vocab). */
+w8a8_status w8a8_ffn_stack_trace(const w8a8_stack_desc* desc, const uint8_t* prec,
+                                 int lm_head_int8, const void* x, int64_t m, void* logits,
+                                 void* hidden, void* ws, size_t ws_bytes,
+                                 w8a8_stream_t stream);
+
+/* Layer sensitivity of the FFN stack (Sec. 3: SA-PTQ sensitivity by SQNR;
+   Sec. 5 / Sec. 7: block-output SQNR).  Needs both forms of every layer in
+   desc (int8_ffn and bf16_ffn).  With x (bf16 m x d, DEVICE) as input:
+     isolated_db[l]   = SQNR of layer l's INT8 FFN block output against its bf16
+                        FFN block output, both on layer l's input in the all-bf16
+                        stack (RMSNorm of it);
+     propagated_db[l] = SQNR of the token stream after layer l of the stack under
+                        prec (HOST uint8[n_layers]) against the all-bf16 stack.
+   Either output (HOST float[n_layers]) may be NULL (prec may then be NULL too).
+   Synchronous: returns after the stream has finished.
+   ws: w8a8_stack_sensitivity_workspace_bytes(m, d, f, vocab, n_layers). */
+size_t w8a8_stack_sensitivity_workspace_bytes(int64_t m, int64_t d, int64_t f, int64_t vocab,
+                                              int64_t n_layers);
+w8a8_status w8a8_stack_sensitivity(const w8a8_stack_desc* desc, const uint8_t* prec,
+                                   const void* x, int64_t m, float* isolated_db,
+                                   float* propagated_db, void* ws, size_t ws_bytes,
+                                   w8a8_stream_t stream);
+
+/* Order of layers by isolated SQNR, most robust first (descending dB; NaN
+   last; ties by layer index).  order: HOST int[n_layers].  Host-only; returns
+   0, or -1 for NULL arguments or n_layers < 1. */
+int w8a8_rank_layers(const float* isolated_db, int n_layers, int* order);
+
+/* Automatic precision map (Sec. 2: the fastest configuration within a quality
+   budget; Sec. 3: the most robust layers are quantised first).  Layers are
+   visited in w8a8_rank_layers order of their isolated SQNR; each is set to INT8
+   and kept there if the token stream after the last layer still has at least
+   budget_db SQNR against the all-bf16 stack on x, else set back to bf16.
+   prec: HOST uint8[n_layers] out; final_db (HOST float[1], may be NULL): the
+   SQNR of the chosen map (+inf if no layer is INT8).  Every INT8 layer of this
+   shape is faster than its bf16 form at prefill sizes, so more INT8 layers
+   within the budget is faster.  Synchronous.
+   ws: w8a8_stack_sensitivity_workspace_bytes(m, d, f, vocab, n_layers). */
+w8a8_status w8a8_select_precision_map(const w8a8_stack_desc* desc, const void* x, int64_t m,
+                                      float budget_db, uint8_t* prec, float* final_db,
+                                      void* ws, size_t ws_bytes, w8a8_stream_t stream);
+
 /* ---------------------------------------------------------------- errors */
 
 const char* w8a8_status_str(w8a8_status s);

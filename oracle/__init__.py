@@ -435,11 +435,10 @@ def residual_add(x, y) -> np.ndarray:
     return f64_to_bf16(as_f32(x).astype(np.float64) + as_f32(y).astype(np.float64))
 
 
-def stack(x_bf16, layers, prec, lm_head, lm_head_int8, return_hidden=False):
-    """FFN stack under a precision map (config glue, Sec. 3):
-    x <- bf16(x + RMSNorm(FFN_l(RMSNorm(x)))) for every layer, where FFN_l is
-    the INT8 block for layers in Q_FFN and the bf16 block otherwise; then the
-    final RMSNorm and the lm_head (INT8 or bf16)."""
+def stack_hidden(x_bf16, layers, prec):
+    """The token stream after every layer of the FFN stack under a precision
+    map (config glue, Sec. 3): x <- bf16(x + RMSNorm(FFN_l(RMSNorm(x)))), FFN_l
+    the INT8 block for layers in Q_FFN and the bf16 block otherwise."""
     x = _c(x_bf16, np.uint16)
     hidden = []
     for l, L in enumerate(layers):
@@ -451,6 +450,14 @@ def stack(x_bf16, layers, prec, lm_head, lm_head_int8, return_hidden=False):
         b = rmsnorm(f)
         x = residual_add(x, b)
         hidden.append(x)
+    return hidden
+
+
+def stack(x_bf16, layers, prec, lm_head, lm_head_int8, return_hidden=False):
+    """FFN stack under a precision map (stack_hidden), then the final RMSNorm
+    and the lm_head (INT8 or bf16)."""
+    hidden = stack_hidden(x_bf16, layers, prec)
+    x = hidden[-1] if hidden else _c(x_bf16, np.uint16)
     xf = rmsnorm(x)
     if lm_head_int8:
         logits = w8a8_lm_head(xf, lm_head["wq"], lm_head["s_w"], lm_head["delta"])
@@ -462,9 +469,67 @@ def stack(x_bf16, layers, prec, lm_head, lm_head_int8, return_hidden=False):
 # ---------------------------------------------------------------- metrics
 
 def sqnr_db(clean, dirty) -> float:
-    """10 log10(||y_clean||^2 / ||y_clean - y_dirty||^2)  (eq. sqnr-ffn)."""
+    """10 log10(||y_clean||^2 / ||y_clean - y_dirty||^2)  (eq. sqnr-ffn; eq.
+    sqnr-block is the same ratio of mean squares over a block's output)."""
     c = np.asarray(clean, np.float64)
     d = np.asarray(dirty, np.float64)
     num = float(np.sum(c * c))
     den = float(np.sum((c - d) ** 2))
     return float("inf") if den == 0.0 else 10.0 * np.log10(num / den)
+
+
+def stack_sensitivity(x_bf16, layers, prec=None):
+    """Per-layer sensitivity (Sec. 3, SA-PTQ by SQNR; Sec. 5 block SQNR).
+    isolated[l]: SQNR of layer l's INT8 FFN block output against its bf16 FFN
+    block output, both on RMSNorm of layer l's input in the all-bf16 stack.
+    propagated[l] (with a map): SQNR of the token stream after layer l under
+    the map against the all-bf16 stack.  Parity unpinned against the paper's
+    own heatmap (needs Gemma weights)."""
+    n = len(layers)
+    ref = stack_hidden(x_bf16, layers, np.zeros(n, np.uint8))
+    iso = np.zeros(n)
+    for l, L in enumerate(layers):
+        a = rmsnorm(x_bf16 if l == 0 else ref[l - 1])
+        yb = bf16_ffn(a, L["w_gate"], L["w_up"], L["w_down"])
+        y8 = w8a8_ffn(a, L["int8"])
+        iso[l] = sqnr_db(bf16_to_f32(yb), bf16_to_f32(y8))
+    prop = None
+    if prec is not None:
+        q = stack_hidden(x_bf16, layers, prec)
+        prop = np.array([sqnr_db(bf16_to_f32(ref[l]), bf16_to_f32(q[l])) for l in range(n)])
+    return iso, prop
+
+
+def rank_layers(isolated_db) -> np.ndarray:
+    """Layers by isolated SQNR, most robust first; NaN last; ties by index."""
+    iso = np.asarray(isolated_db, np.float64)
+    key = np.where(np.isnan(iso), -np.inf, iso)
+    return np.array(sorted(range(iso.size), key=lambda i: (-key[i], i)), np.int64)
+
+
+def select_map(x_bf16, layers, budget_db, return_trace=False):
+    """Automatic precision map under an SQNR budget (Sec. 2: the fastest
+    configuration within a quality budget; Sec. 3: the most robust layers are
+    quantised first): visit layers by rank_layers of their isolated SQNR, set
+    each to INT8, keep it there while the token stream after the last layer has
+    at least budget_db SQNR against the all-bf16 stack.  Returns (map, its
+    SQNR), and with return_trace the isolated SQNRs and every decision as
+    (layer, SQNR with it INT8, kept)."""
+    n = len(layers)
+    iso, _ = stack_sensitivity(x_bf16, layers)
+    ref_last = bf16_to_f32(stack_hidden(x_bf16, layers, np.zeros(n, np.uint8))[-1])
+    prec = np.zeros(n, np.uint8)
+    best = float("inf")
+    trace = []
+    for l in rank_layers(iso):
+        prec[l] = 1
+        db = sqnr_db(ref_last, bf16_to_f32(stack_hidden(x_bf16, layers, prec)[-1]))
+        keep = db >= budget_db
+        trace.append((int(l), db, keep))
+        if keep:
+            best = db
+        else:
+            prec[l] = 0
+    if return_trace:
+        return prec, best, iso, trace
+    return prec, best

@@ -8,6 +8,8 @@
 #include <cstdlib>
 #include <cstring>
 #include <string>
+#include <vector>
+#include <cmath>
 
 #include "../../include/w8a8.h"
 #include "kernels.h"
@@ -997,20 +999,17 @@ int w8a8_precision_map(const char* name, uint8_t* prec, int n_layers) {
   return count;
 }
 
-w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec, int lm_head_int8,
-                           const void* x, int64_t m, void* logits, void* ws, size_t ws_bytes,
-                           w8a8_stream_t stream) {
-  g_last_error.clear();
+}  // extern "C"
+
+namespace {
+
+// Validation shared by the stack entry points (host memory prec[n_layers]).
+w8a8_status check_stack(const w8a8_stack_desc* desc, const uint8_t* prec, int lm_head_int8,
+                        bool need_lm_head) {
   REQUIRE(desc, W8A8_EINVAL, "desc is NULL");
   REQUIRE(prec, W8A8_EINVAL, "prec is NULL");
-  CHECK_PTR(x);
-  CHECK_PTR(logits);
-  CHECK_PTR(ws);
-  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
   REQUIRE(desc->n_layers >= 1 && desc->d >= 1 && desc->f >= 1 && desc->vocab >= 1, W8A8_EINVAL,
           "stack sizes < 1");
-  REQUIRE(ws_bytes >= w8a8_stack_workspace_bytes(m, desc->d, desc->f, desc->vocab),
-          W8A8_EWORKSPACE, "workspace too small");
   const int64_t d = desc->d, f = desc->f;
   CHECK(check_norm_d(d));
   for (int64_t l = 0; l < desc->n_layers; ++l) {
@@ -1024,6 +1023,7 @@ w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec, int
       REQUIRE(desc->bf16_ffn[l].d == d && desc->bf16_ffn[l].f == f, W8A8_EINVAL, "layer shape");
     }
   }
+  if (!need_lm_head) return W8A8_OK;
   if (lm_head_int8) {
     CHECK(check_desc(&desc->lm_head_int8));
     REQUIRE(desc->lm_head_int8.n == desc->vocab && desc->lm_head_int8.k == d, W8A8_EINVAL,
@@ -1032,8 +1032,16 @@ w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec, int
     CHECK_PTR(desc->lm_head_bf16);
     REQUIRE(d % 32 == 0, W8A8_EUNSUPPORTED, "d must be a multiple of 32 on the bf16 path");
   }
+  return W8A8_OK;
+}
 
-  hipStream_t st = S(stream);
+// The stack over validated arguments.  logits NULL: no lm_head (the final
+// glue still runs).  hidden non-NULL: the token stream after every layer,
+// hidden[l] = bf16 m x d, n_layers of them back to back.
+w8a8_status stack_run(const w8a8_stack_desc* desc, const uint8_t* prec, int lm_head_int8,
+                      const void* x, int64_t m, void* logits, uint16_t* hidden, void* ws,
+                      hipStream_t st) {
+  const int64_t d = desc->d, f = desc->f;
   char* base = (char*)ws;
   const StackWs w = stack_ws(m, d, f, desc->vocab);
   uint16_t* xcur = (uint16_t*)(base + w.x);
@@ -1059,6 +1067,7 @@ w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec, int
     g.kp = round_up(d, 64);
     g.x_in = l == 0 ? (const uint16_t*)x : xcur;
     g.x_out = xcur;
+    if (hidden && l > 0) g.x_copy = hidden + (l - 1) * m * d;
     if (l > 0) {
       const bool i8 = prec[l - 1] != 0;
       g.part = part;
@@ -1101,6 +1110,7 @@ w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec, int
     }
   }
   CHECK(glue(desc->n_layers));
+  if (!logits) return W8A8_OK;
   const int64_t V = desc->vocab;
   if (lm_head_int8) {
     const Plan pl = plan_gemm(m, V, d, DT_I8, false);
@@ -1108,6 +1118,218 @@ w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec, int
                     desc->lm_head_int8.s_w, nullptr, logits, V, base + w.lm, st);
   }
   return bf16_linear_impl(a, m, desc->lm_head_bf16, V, d, logits, base + w.lm, st);
+}
+
+// Workspace of the sensitivity / selection calls: the stack's, two traces of
+// the token stream, the FFN stage buffers, SQNR scratch and results.
+struct SensWs {
+  size_t stack, ref, quant, a, yb, y8, ffn, part, res, total;
+};
+SensWs sens_ws(int64_t m, int64_t d, int64_t f, int64_t vocab, int64_t n_layers) {
+  SensWs w;
+  const size_t trace = align256((size_t)n_layers * m * d * 2), act = align256((size_t)m * d * 2);
+  w.stack = 0;
+  w.ref = align256(w8a8_stack_workspace_bytes(m, d, f, vocab));
+  w.quant = w.ref + trace;
+  w.a = w.quant + trace;
+  w.yb = w.a + act;
+  w.y8 = w.yb + act;
+  w.ffn = w.y8 + act;
+  w.part = w.ffn + align256(std::max(w8a8_ffn_workspace_bytes(m, d, f),
+                                     w8a8_bf16_ffn_workspace_bytes(m, d, f)));
+  w.res = w.part + align256((size_t)2 * kSqnrMaxGroups * sizeof(double));
+  w.total = w.res + align256((size_t)(2 * n_layers + 1) * 3 * sizeof(double));
+  return w;
+}
+
+// SQNR results (3 doubles each) into res[slot]
+w8a8_status sqnr_into(const void* ref, const void* test, int64_t n, char* base, const SensWs& w,
+                      int64_t slot, hipStream_t st) {
+  return hip_check(launch_sqnr(ref, test, true, n, (double*)(base + w.part),
+                               (double*)(base + w.res) + 3 * slot, st),
+                   "sqnr");
+}
+
+w8a8_status read_results(char* base, const SensWs& w, int64_t count, double* host,
+                         hipStream_t st) {
+  CHECK(hip_check(hipMemcpyAsync(host, base + w.res, (size_t)count * 3 * sizeof(double),
+                                 hipMemcpyDeviceToHost, st),
+                  "copy results"));
+  return hip_check(hipStreamSynchronize(st), "synchronize");
+}
+
+// Reference trace (all layers bf16) and the isolated SQNR of every layer's
+// FFN block on its reference input (results slots 0 .. n-1).
+w8a8_status isolated_sensitivity(const w8a8_stack_desc* desc, const void* x, int64_t m, char* base,
+                                 const SensWs& w, hipStream_t st) {
+  const int64_t n = desc->n_layers, d = desc->d, f = desc->f;
+  std::vector<uint8_t> bf(n, 0);
+  uint16_t* ref = (uint16_t*)(base + w.ref);
+  CHECK(stack_run(desc, bf.data(), 0, x, m, nullptr, ref, base + w.stack, st));
+  const size_t ffn_bytes = std::max(w8a8_ffn_workspace_bytes(m, d, f),
+                                    w8a8_bf16_ffn_workspace_bytes(m, d, f));
+  for (int64_t l = 0; l < n; ++l) {
+    const void* in = l == 0 ? x : (const void*)(ref + (l - 1) * m * d);
+    CHECK(hip_check(launch_rmsnorm(nullptr, (const uint16_t*)in, m, d, (uint16_t*)(base + w.a), st),
+                    "rmsnorm"));
+    CHECK(w8a8_bf16_ffn(&desc->bf16_ffn[l], base + w.a, m, base + w.yb, base + w.ffn, ffn_bytes,
+                        st));
+    CHECK(w8a8_ffn(&desc->int8_ffn[l], base + w.a, m, base + w.y8, base + w.ffn, ffn_bytes, st));
+    CHECK(sqnr_into(base + w.yb, base + w.y8, m * d, base, w, l, st));
+  }
+  return W8A8_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec, int lm_head_int8,
+                           const void* x, int64_t m, void* logits, void* ws, size_t ws_bytes,
+                           w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK(check_stack(desc, prec, lm_head_int8, true));
+  CHECK_PTR(x);
+  CHECK_PTR(logits);
+  CHECK_PTR(ws);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  REQUIRE(ws_bytes >= w8a8_stack_workspace_bytes(m, desc->d, desc->f, desc->vocab),
+          W8A8_EWORKSPACE, "workspace too small");
+  return stack_run(desc, prec, lm_head_int8, x, m, logits, nullptr, ws, S(stream));
+}
+
+w8a8_status w8a8_ffn_stack_trace(const w8a8_stack_desc* desc, const uint8_t* prec,
+                                 int lm_head_int8, const void* x, int64_t m, void* logits,
+                                 void* hidden, void* ws, size_t ws_bytes, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK(check_stack(desc, prec, lm_head_int8, logits != nullptr));
+  CHECK_PTR(x);
+  if (logits) CHECK_PTR(logits);
+  CHECK_PTR(hidden);
+  CHECK_PTR(ws);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  REQUIRE(ws_bytes >= w8a8_stack_workspace_bytes(m, desc->d, desc->f, desc->vocab),
+          W8A8_EWORKSPACE, "workspace too small");
+  return stack_run(desc, prec, lm_head_int8, x, m, logits, (uint16_t*)hidden, ws, S(stream));
+}
+
+size_t w8a8_sqnr_workspace_bytes(int64_t n) {
+  if (n < 1) return 0;
+  return (size_t)2 * sqnr_groups(n) * sizeof(double);
+}
+
+w8a8_status w8a8_sqnr(const void* ref, const void* test, w8a8_dtype dtype, int64_t n, double* out,
+                      void* ws, size_t ws_bytes, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(ref);
+  CHECK_PTR(test);
+  CHECK_PTR(out);
+  CHECK_PTR(ws);
+  REQUIRE(n >= 1, W8A8_EINVAL, "n < 1");
+  REQUIRE(dtype == W8A8_F32 || dtype == W8A8_BF16, W8A8_EUNSUPPORTED, "dtype");
+  REQUIRE(ws_bytes >= w8a8_sqnr_workspace_bytes(n), W8A8_EWORKSPACE, "workspace too small");
+  return hip_check(launch_sqnr(ref, test, dtype == W8A8_BF16, n, (double*)ws, out, S(stream)),
+                   "sqnr");
+}
+
+size_t w8a8_stack_sensitivity_workspace_bytes(int64_t m, int64_t d, int64_t f, int64_t vocab,
+                                              int64_t n_layers) {
+  if (m < 1 || d < 1 || f < 1 || vocab < 1 || n_layers < 1) return 0;
+  return sens_ws(m, d, f, vocab, n_layers).total;
+}
+
+static w8a8_status check_sens(const w8a8_stack_desc* desc, const void* x, int64_t m, void* ws,
+                              size_t ws_bytes) {
+  REQUIRE(desc, W8A8_EINVAL, "desc is NULL");
+  std::vector<uint8_t> all(desc->n_layers > 0 ? desc->n_layers : 1, 1), none(all.size(), 0);
+  CHECK(check_stack(desc, all.data(), 0, false));   // every layer needs both forms
+  CHECK(check_stack(desc, none.data(), 0, false));
+  CHECK_PTR(x);
+  CHECK_PTR(ws);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  REQUIRE(ws_bytes >= w8a8_stack_sensitivity_workspace_bytes(m, desc->d, desc->f, desc->vocab,
+                                                             desc->n_layers),
+          W8A8_EWORKSPACE, "workspace too small");
+  return W8A8_OK;
+}
+
+w8a8_status w8a8_stack_sensitivity(const w8a8_stack_desc* desc, const uint8_t* prec,
+                                   const void* x, int64_t m, float* isolated_db,
+                                   float* propagated_db, void* ws, size_t ws_bytes,
+                                   w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK(check_sens(desc, x, m, ws, ws_bytes));
+  REQUIRE(prec || !propagated_db, W8A8_EINVAL, "prec is NULL");
+  const int64_t n = desc->n_layers, d = desc->d;
+  hipStream_t st = S(stream);
+  char* base = (char*)ws;
+  const SensWs w = sens_ws(m, d, desc->f, desc->vocab, n);
+  CHECK(isolated_sensitivity(desc, x, m, base, w, st));  // also leaves the reference trace
+  if (propagated_db) {
+    uint16_t* ref = (uint16_t*)(base + w.ref);
+    uint16_t* quant = (uint16_t*)(base + w.quant);
+    CHECK(stack_run(desc, prec, 0, x, m, nullptr, quant, base + w.stack, st));
+    for (int64_t l = 0; l < n; ++l)
+      CHECK(sqnr_into(ref + l * m * d, quant + l * m * d, m * d, base, w, n + l, st));
+  }
+  std::vector<double> res((size_t)(2 * n) * 3);
+  CHECK(read_results(base, w, propagated_db ? 2 * n : n, res.data(), st));
+  for (int64_t l = 0; l < n; ++l) {
+    if (isolated_db) isolated_db[l] = (float)res[3 * l + 2];
+    if (propagated_db) propagated_db[l] = (float)res[3 * (n + l) + 2];
+  }
+  return W8A8_OK;
+}
+
+w8a8_status w8a8_select_precision_map(const w8a8_stack_desc* desc, const void* x, int64_t m,
+                                      float budget_db, uint8_t* prec, float* final_db, void* ws,
+                                      size_t ws_bytes, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK(check_sens(desc, x, m, ws, ws_bytes));
+  REQUIRE(prec, W8A8_EINVAL, "prec is NULL");
+  const int64_t n = desc->n_layers, d = desc->d;
+  hipStream_t st = S(stream);
+  char* base = (char*)ws;
+  const SensWs w = sens_ws(m, d, desc->f, desc->vocab, n);
+  CHECK(isolated_sensitivity(desc, x, m, base, w, st));
+  std::vector<double> res((size_t)(2 * n + 1) * 3);
+  CHECK(read_results(base, w, n, res.data(), st));
+  std::vector<float> iso(n);
+  for (int64_t l = 0; l < n; ++l) iso[l] = (float)res[3 * l + 2];
+  std::vector<int> order(n);
+  w8a8_rank_layers(iso.data(), (int)n, order.data());
+  // most robust layers first; a layer stays INT8 while the last layer's
+  // output keeps at least budget_db against the all-bf16 stack
+  uint16_t* ref_last = (uint16_t*)(base + w.ref) + (n - 1) * m * d;
+  uint16_t* quant = (uint16_t*)(base + w.quant);
+  for (int64_t l = 0; l < n; ++l) prec[l] = 0;
+  double best = INFINITY;
+  for (int64_t i = 0; i < n; ++i) {
+    const int l = order[i];
+    prec[l] = 1;
+    CHECK(stack_run(desc, prec, 0, x, m, nullptr, quant, base + w.stack, st));
+    CHECK(sqnr_into(ref_last, quant + (n - 1) * m * d, m * d, base, w, 2 * n, st));
+    std::vector<double> r(3);
+    CHECK(hip_check(hipMemcpyAsync(r.data(), (double*)(base + w.res) + 3 * (2 * n), 3 * sizeof(double),
+                                   hipMemcpyDeviceToHost, st),
+                    "copy result"));
+    CHECK(hip_check(hipStreamSynchronize(st), "synchronize"));
+    if (r[2] >= (double)budget_db)
+      best = r[2];
+    else
+      prec[l] = 0;
+  }
+  if (final_db) final_db[0] = (float)best;
+  return W8A8_OK;
+}
+
+int w8a8_rank_layers(const float* isolated_db, int n_layers, int* order) {
+  if (!isolated_db || !order || n_layers < 1) return -1;
+  for (int i = 0; i < n_layers; ++i) order[i] = i;
+  // descending SQNR (most robust first), NaN last, ties by layer index
+  auto key = [&](int i) { return std::isnan(isolated_db[i]) ? -INFINITY : isolated_db[i]; };
+  std::stable_sort(order, order + n_layers, [&](int a, int b) { return key(a) > key(b); });
+  return 0;
 }
 
 }  // extern "C"

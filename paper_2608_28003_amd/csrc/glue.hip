@@ -221,13 +221,15 @@ __global__ __launch_bounds__(1024) void glue_kernel(GlueParams g) {
       }
     }
   }
-  if (own && g.x_out && (g.part || g.x_out != g.x_in)) {
+  const bool write_out = g.x_out && (g.part || g.x_out != g.x_in);
+  if (own && (write_out || g.x_copy)) {
     uint4 o;
     o.x = (uint32_t)float_to_bf16_bits(xv[0]) | ((uint32_t)float_to_bf16_bits(xv[1]) << 16);
     o.y = (uint32_t)float_to_bf16_bits(xv[2]) | ((uint32_t)float_to_bf16_bits(xv[3]) << 16);
     o.z = (uint32_t)float_to_bf16_bits(xv[4]) | ((uint32_t)float_to_bf16_bits(xv[5]) << 16);
     o.w = (uint32_t)float_to_bf16_bits(xv[6]) | ((uint32_t)float_to_bf16_bits(xv[7]) << 16);
-    *reinterpret_cast<uint4*>(g.x_out + r * d + col0) = o;
+    if (write_out) *reinterpret_cast<uint4*>(g.x_out + r * d + col0) = o;
+    if (g.x_copy) *reinterpret_cast<uint4*>(g.x_copy + r * d + col0) = o;
   }
   if (!g.a && !g.q) return;  // uniform over the workgroup
   float ss = 0.0f;

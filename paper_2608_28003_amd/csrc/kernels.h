@@ -111,7 +111,16 @@ struct GlueParams {
   const float* delta = nullptr;        // smoothing of the INT8 consumer (may be null)
   int8_t* q = nullptr;                 // packed codes of the pre-norm output (optional)
   float* s = nullptr;                  // their per-row scales
+  uint16_t* x_copy = nullptr;          // second copy of the token stream out (optional)
 };
 hipError_t launch_glue(const GlueParams& g, hipStream_t st);
+
+// SQNR of test against ref over n elements (bf16 or f32): part holds
+// 2 * sqnr_groups(n) doubles of scratch, out receives {sum ref^2,
+// sum (ref - test)^2, 10 log10 of their ratio}.
+constexpr int kSqnrMaxGroups = 1024;
+int sqnr_groups(int64_t n);
+hipError_t launch_sqnr(const void* ref, const void* test, bool bf16, int64_t n, double* part,
+                       double* out, hipStream_t st);
 
 }  // namespace w8a8

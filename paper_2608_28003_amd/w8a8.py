@@ -91,6 +91,14 @@ _SIGS = {
     "w8a8_rmsnorm_residual": (INT, [P, P, I64, I64, P, P]),
     "w8a8_precision_map": (INT, [ctypes.c_char_p, P, INT]),
     "w8a8_ffn_stack": (INT, [ctypes.POINTER(StackDesc), P, INT, P, I64, P, P, SZ, P]),
+    "w8a8_ffn_stack_trace": (INT, [ctypes.POINTER(StackDesc), P, INT, P, I64, P, P, P, SZ, P]),
+    "w8a8_sqnr_workspace_bytes": (SZ, [I64]),
+    "w8a8_sqnr": (INT, [P, P, INT, I64, P, P, SZ, P]),
+    "w8a8_stack_sensitivity_workspace_bytes": (SZ, [I64, I64, I64, I64, I64]),
+    "w8a8_stack_sensitivity": (INT, [ctypes.POINTER(StackDesc), P, P, I64, P, P, P, SZ, P]),
+    "w8a8_rank_layers": (INT, [P, INT, P]),
+    "w8a8_select_precision_map": (INT, [ctypes.POINTER(StackDesc), P, I64, ctypes.c_float, P, P,
+                                        P, SZ, P]),
     "w8a8_status_str": (ctypes.c_char_p, [INT]),
     "w8a8_last_error": (ctypes.c_char_p, []),
 }
@@ -550,6 +558,73 @@ class Stack:
                                     int(lm_head_int8), _ptr(_dev(x)), m, _ptr(out), _ptr(ws),
                                     ws.numel(), _stream(stream)))
         return out
+
+    def trace(self, x, prec: np.ndarray, lm_head_int8: bool = False, logits: bool = False,
+              ws=None, stream=None):
+        """Token stream after every layer, (n_layers, m, d) bf16; with logits=True
+        also the logits: returns (hidden, logits)."""
+        m = x.shape[0]
+        hidden = torch.empty((self.n_layers, m, self.d), dtype=torch.bfloat16, device=x.device)
+        out = (torch.empty((m, self.vocab), dtype=torch.bfloat16, device=x.device)
+               if logits else None)
+        if ws is None:
+            ws = _empty(stack_workspace_bytes(m, self.d, self.f, self.vocab), x.device)
+        prec = np.ascontiguousarray(prec, dtype=np.uint8)
+        _check(lib().w8a8_ffn_stack_trace(ctypes.byref(self._desc), prec.ctypes.data_as(P),
+                                          int(lm_head_int8), _ptr(_dev(x)), m, _ptr(out),
+                                          _ptr(hidden), _ptr(ws), ws.numel(), _stream(stream)))
+        return (hidden, out) if logits else hidden
+
+    def _sens_ws(self, m, device):
+        return _empty(lib().w8a8_stack_sensitivity_workspace_bytes(m, self.d, self.f, self.vocab,
+                                                                   self.n_layers), device)
+
+    def sensitivity(self, x, prec=None, stream=None):
+        """(isolated_db, propagated_db) per layer as float32 arrays; propagated
+        is None without a precision map."""
+        m = x.shape[0]
+        iso = np.zeros(self.n_layers, np.float32)
+        prop = None if prec is None else np.zeros(self.n_layers, np.float32)
+        pr = None if prec is None else np.ascontiguousarray(prec, dtype=np.uint8)
+        ws = self._sens_ws(m, x.device)
+        _check(lib().w8a8_stack_sensitivity(
+            ctypes.byref(self._desc), None if pr is None else pr.ctypes.data_as(P), _ptr(_dev(x)),
+            m, iso.ctypes.data_as(P), None if prop is None else prop.ctypes.data_as(P), _ptr(ws),
+            ws.numel(), _stream(stream)))
+        return iso, prop
+
+    def select_map(self, x, budget_db, stream=None):
+        """Automatic precision map: (prec uint8[n_layers], SQNR of the chosen map)."""
+        m = x.shape[0]
+        prec = np.zeros(self.n_layers, np.uint8)
+        fin = np.zeros(1, np.float32)
+        ws = self._sens_ws(m, x.device)
+        _check(lib().w8a8_select_precision_map(ctypes.byref(self._desc), _ptr(_dev(x)), m,
+                                               float(budget_db), prec.ctypes.data_as(P),
+                                               fin.ctypes.data_as(P), _ptr(ws), ws.numel(),
+                                               _stream(stream)))
+        return prec, float(fin[0])
+
+
+def sqnr(ref, test, stream=None):
+    """(sum ref^2, sum (ref - test)^2, SQNR dB), computed on the GPU in binary64."""
+    _dev(ref)
+    _dev(test)
+    assert ref.dtype == test.dtype and ref.numel() == test.numel()
+    n = ref.numel()
+    out = torch.empty(3, dtype=torch.float64, device=ref.device)
+    ws = _empty(lib().w8a8_sqnr_workspace_bytes(n), ref.device)
+    _check(lib().w8a8_sqnr(_ptr(ref), _ptr(test), _dt(ref), n, _ptr(out), _ptr(ws), ws.numel(),
+                           _stream(stream)))
+    return tuple(float(v) for v in out.cpu())
+
+
+def rank_layers(isolated_db) -> np.ndarray:
+    iso = np.ascontiguousarray(isolated_db, dtype=np.float32)
+    order = np.zeros(iso.size, np.int32)
+    if lib().w8a8_rank_layers(iso.ctypes.data_as(P), iso.size, order.ctypes.data_as(P)) != 0:
+        raise ValueError("rank_layers: bad arguments")
+    return order
 
 
 # ----------------------------------------------------------------- layout helpers

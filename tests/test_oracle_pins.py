@@ -538,3 +538,80 @@ def test_fp8_ffn_requant_amplifies_sum_rounding():
     assert rl2(g1, g0) < 2 * eps
     assert rl2(y1, y0) > 1e-3
     assert rl2(y1, y0) < 0.1 * rl2(y0, ref)
+
+
+# ---------------------------------------------------------------- sensitivity and map selection
+
+def test_sqnr_closed_forms():
+    # 10 log10(25 / 1): y = (3, 4), error (0, 1)
+    assert oracle.sqnr_db([3.0, 4.0], [3.0, 5.0]) == pytest.approx(10 * math.log10(25.0), abs=1e-12)
+    # a relative error eps on every element gives -20 log10 eps exactly
+    y = np.random.default_rng(1).standard_normal(1000)
+    assert oracle.sqnr_db(y, y * (1 + 2.0 ** -10)) == pytest.approx(20 * 10 * math.log10(2.0),
+                                                                    abs=1e-9)
+    assert oracle.sqnr_db(y, y) == float("inf")
+
+
+def test_rank_layers_hand_case():
+    iso = [20.0, 30.0, float("nan"), 30.0, 10.0]
+    # descending dB, the tie 30/30 by index, NaN last
+    np.testing.assert_array_equal(oracle.rank_layers(iso), [1, 3, 0, 4, 2])
+
+
+def test_rank_layers_library_matches_hand_case():
+    """The library's host-side ranking (no GPU involved) on the same case."""
+    from paper_2608_28003_amd import w8a8
+    iso = [20.0, 30.0, float("nan"), 30.0, 10.0]
+    np.testing.assert_array_equal(w8a8.rank_layers(iso), [1, 3, 0, 4, 2])
+    np.testing.assert_array_equal(w8a8.rank_layers([5.0]), [0])
+
+
+@pytest.fixture(scope="module")
+def small_stack():
+    cfg = synth.stack_config(m=16, n_layers=4, d=256, f=512, vocab=512)
+    layers = [dict(L, int8=oracle.quantize_ffn(L["w_gate"], L["w_up"], L["w_down"], cfg["x_cal"]))
+              for L in cfg["layers"]]
+    return cfg, layers
+
+
+def test_sensitivity_extreme_maps(small_stack):
+    cfg, layers = small_stack
+    n = len(layers)
+    iso, prop0 = oracle.stack_sensitivity(cfg["x"], layers, np.zeros(n, np.uint8))
+    assert np.all(np.isinf(prop0))                # the all-bf16 map is the reference
+    assert np.all(np.isfinite(iso)) and np.all(iso > 20)
+    # one INT8 layer: identical (inf) before it, finite from it on
+    prec = np.zeros(n, np.uint8)
+    prec[2] = 1
+    _, prop = oracle.stack_sensitivity(cfg["x"], layers, prec)
+    assert np.all(np.isinf(prop[:2])) and np.all(np.isfinite(prop[2:]))
+
+
+def test_select_map_budget_extremes(small_stack):
+    cfg, layers = small_stack
+    n = len(layers)
+    prec, db = oracle.select_map(cfg["x"], layers, -1e9)
+    np.testing.assert_array_equal(prec, np.ones(n))
+    prec, db = oracle.select_map(cfg["x"], layers, 1e9)
+    np.testing.assert_array_equal(prec, np.zeros(n))
+    assert db == float("inf")
+
+
+def test_select_map_respects_budget_and_is_greedy(small_stack):
+    cfg, layers = small_stack
+    n = len(layers)
+    _, _, iso, _ = oracle.select_map(cfg["x"], layers, 0.0, return_trace=True)
+    _, prop_all = oracle.stack_sensitivity(cfg["x"], layers, np.ones(n, np.uint8))
+    budget = float(prop_all[-1]) + 1.0            # all-INT8 misses it by 1 dB
+    prec, db, iso2, trace = oracle.select_map(cfg["x"], layers, budget, return_trace=True)
+    assert db >= budget and 0 < prec.sum() < n
+    np.testing.assert_array_equal(iso, iso2)
+    # decisions in rank order; each kept layer's SQNR meets the budget, each
+    # rejected one misses it; the final map is exactly the kept ones
+    assert [t[0] for t in trace] == list(oracle.rank_layers(iso))
+    assert all((t[1] >= budget) == t[2] for t in trace)
+    np.testing.assert_array_equal(np.flatnonzero(prec), sorted(t[0] for t in trace if t[2]))
+    # the reported SQNR is that of the chosen map
+    ref = oracle.bf16_to_f32(oracle.stack_hidden(cfg["x"], layers, np.zeros(n, np.uint8))[-1])
+    q = oracle.bf16_to_f32(oracle.stack_hidden(cfg["x"], layers, prec)[-1])
+    assert oracle.sqnr_db(ref, q) == pytest.approx(db, abs=1e-9)
