@@ -237,10 +237,10 @@ struct QLoad {
   float* s_out = nullptr;  // where to leave the per-row scales (optional)
 };
 
-// Streaming int8 plans over at most 16 rows quantise their bf16 input
+// Streaming int8 / E4M3 plans over at most 16 rows quantise their bf16 input
 // themselves; every other plan reads codes produced by quant_rows_kernel.
 bool plan_qloads(const Plan& pl, int64_t m, int64_t k) {
-  if (env_int("W8A8_NO_QLOAD", 0) || pl.dt != DT_I8) return false;
+  if (env_int("W8A8_NO_QLOAD", 0) || (pl.dt != DT_I8 && pl.dt != DT_F8)) return false;
   return pl.stream && pl.mb == 1 && m * (k / 16) <= qload_capacity(pl.nw);
 }
 
@@ -484,7 +484,7 @@ w8a8_status linear_impl(const w8a8_linear_desc* d, const void* x, bool x_bf16, i
   char* base = (char*)ws;
   Plan pl = plan_gemm(m, d->n, d->k, dt, false);
   if (x_bf16 && plan_qloads(pl, m, d->k))  // one launch: the GEMM quantises x itself
-    return run_gemm(pl, DT_I8, epi, nullptr, 0, m, d->wq, nullptr, d->n, d->k, nullptr, d->s_w,
+    return run_gemm(pl, dt, epi, nullptr, 0, m, d->wq, nullptr, d->n, d->k, nullptr, d->s_w,
                     nullptr, y, d->n, base + w.gemm, st,
                     QLoad{(const uint16_t*)x, d->delta, (float*)(base + w.sx)});
   CHECK(quant_act_impl(x, x_bf16, m, d->k, d->delta, base + w.qx, (float*)(base + w.sx), st, dt));
@@ -498,7 +498,7 @@ w8a8_status ffn_impl(const w8a8_ffn_desc* d, const void* x, int64_t m, void* y, 
   char* base = (char*)ws;
   Plan pg = plan_gemm(m, d->f, d->d, dt, true);
   if (plan_qloads(pg, m, d->d)) {
-    CHECK(run_gemm(pg, DT_I8, EPI_GLU, nullptr, 0, m, d->wq_gate, d->wq_up, d->f, d->d, nullptr,
+    CHECK(run_gemm(pg, dt, EPI_GLU, nullptr, 0, m, d->wq_gate, d->wq_up, d->f, d->d, nullptr,
                    d->s_gate, d->s_up, base + w.h, d->f, nullptr, st,
                    QLoad{(const uint16_t*)x, d->delta_gu, (float*)(base + w.sx)}));
   } else {
@@ -510,7 +510,7 @@ w8a8_status ffn_impl(const w8a8_ffn_desc* d, const void* x, int64_t m, void* y, 
   }
   Plan pd = plan_gemm(m, d->d, d->f, dt, false);
   if (plan_qloads(pd, m, d->f))
-    return run_gemm(pd, DT_I8, EPI_BF16, nullptr, 0, m, d->wq_down, nullptr, d->d, d->f, nullptr,
+    return run_gemm(pd, dt, EPI_BF16, nullptr, 0, m, d->wq_down, nullptr, d->d, d->f, nullptr,
                     d->s_down, nullptr, y, d->d, base + w.gemm, st,
                     QLoad{(const uint16_t*)(base + w.h), d->delta_down, (float*)(base + w.sh)});
   CHECK(quant_act_impl(base + w.h, true, m, d->f, d->delta_down, base + w.qh,

@@ -521,9 +521,11 @@ __device__ __forceinline__ void quantize_fetch(const GemmParams& p, bool qload, 
   }
 }
 
-template <int NW>
+// F8: E4M3 codes (scale amax / 448, the quantiser's conversion) instead of int8
+template <int NW, bool F8>
 __device__ __forceinline__ void quantize_panel(const GemmParams& p, int kb0, int kc, v4i* lds_a,
                                                float* s_row, const QloadRegs<NW>& R) {
+  constexpr float QMAX = F8 ? 448.0f : 127.0f;
   constexpr int NT = NW * 64;
   constexpr int MAXG = qload_max_groups<NW>();
   __shared__ unsigned int amax_bits[16];
@@ -569,7 +571,7 @@ __device__ __forceinline__ void quantize_panel(const GemmParams& p, int kb0, int
   }
   __syncthreads();
   if (tid < rows) {
-    const float s = __uint_as_float(amax_bits[tid]) / 127.0f;
+    const float s = __uint_as_float(amax_bits[tid]) / QMAX;
     s_row[tid] = s;
     if (p.a_s_out && blockIdx.x == 0 && blockIdx.y == 0) p.a_s_out[tid] = s;
   }
@@ -580,14 +582,23 @@ __device__ __forceinline__ void quantize_panel(const GemmParams& p, int kb0, int
     const int r = gi / G, g = gi % G;
     const int f = g / 4 - kb0;
     if (f < 0 || f >= kc) continue;
-    const float sr = __uint_as_float(amax_bits[r]) / 127.0f;
+    const float sr = __uint_as_float(amax_bits[r]) / QMAX;
     if (sr == 0.0f) continue;
-    const float inv = 1.0f / sr;
-    const bool fast = isfinite(inv);
     int32_t packed[4] = {0, 0, 0, 0};
+    if constexpr (F8) {  // the same binary32 steps as quant_rows_kernel's E4M3 mode
 #pragma unroll
-    for (int e = 0; e < 16; ++e)
-      packed[e >> 2] |= ((int32_t)code_of(v[i][e], sr, inv, fast) & 0xff) << (8 * (e & 3));
+      for (int e = 0; e < 16; e += 2) {
+        const float q0 = fminf(fmaxf(v[i][e] / sr, -448.0f), 448.0f);
+        const float q1 = fminf(fmaxf(v[i][e + 1] / sr, -448.0f), 448.0f);
+        packed[e >> 2] |= (int32_t)(e4m3_pack2(q0, q1) << (8 * (e & 3)));
+      }
+    } else {
+      const float inv = 1.0f / sr;
+      const bool fast = isfinite(inv);
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        packed[e >> 2] |= ((int32_t)code_of(v[i][e], sr, inv, fast) & 0xff) << (8 * (e & 3));
+    }
     lds_a[f * 64 + r + 16 * (g & 3)] = v4i{packed[0], packed[1], packed[2], packed[3]};
   }
 }
@@ -595,7 +606,8 @@ __device__ __forceinline__ void quantize_panel(const GemmParams& p, int kb0, int
 template <int DT, int MB, int EPI, int NW, int WK, bool QL>
 __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int nb_per_block) {
   static_assert(WK == 1 || WK == NW, "either every wave owns its column blocks or all share one");
-  static_assert(!QL || (DT == DT_I8 && MB == 1), "quantise-on-load: int8, one row block");
+  static_assert(!QL || ((DT == DT_I8 || DT == DT_F8) && MB == 1),
+                "quantise-on-load: int8 or E4M3 codes, one row block");
   constexpr bool GLU = (EPI == EPI_GLU);
   constexpr bool BF16 = (DT == DT_BF16);
   constexpr bool FACC = (DT != DT_I8);
@@ -716,7 +728,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
   load_first(b0, u0, sbn[0], sbn2[0]);  // first weights go out with the A fragments
   __shared__ float s_row[16];           // quantise-on-load: per-row scales
   if constexpr (QLOAD_OK) {
-    if (qload) quantize_panel<NW>(p, kb0, kc, lds_a, s_row, qr);  // overlaps the weight loads
+    if (qload) quantize_panel<NW, DT == DT_F8>(p, kb0, kc, lds_a, s_row, qr);  // overlaps the weights
   }
   wait_vmcnt<0>();
   if ((WK == 1 && NW > 1) || qload) lds_barrier();  // the shared panel is read by every wave
@@ -971,7 +983,7 @@ static bool gemm_params_ok(int dt, int epi, const GemmParams& p, int kind, int n
   if ((int64_t)p.kchunk * (p.splits - 1) >= p.kb_count) return false;  // no empty split
   if ((int64_t)p.kchunk * p.splits < p.kb_count) return false;         // K fully covered
   if (glu && p.splits != 1) return false;  // the gated epilogue needs whole sums
-  const bool qload = kind == 1 && dt == DT_I8 && p.a_x != nullptr;
+  const bool qload = kind == 1 && (dt == DT_I8 || dt == DT_F8) && p.a_x != nullptr;
   if (kind == 0 && p.a_x) return false;  // the tiled kernel reads codes only
   if (qload && (p.M > 16 || p.a_k < 16 || (int64_t)p.M * (p.a_k / 16) > (int64_t)64 * nw))
     return false;
@@ -1030,7 +1042,7 @@ static hipError_t stream_launch_ql(const GemmParams& p, int nbpb, hipStream_t st
 
 template <int DT, int MB, int EPI, int NW, int WK>
 static hipError_t stream_launch(const GemmParams& p, int nbpb, hipStream_t st) {
-  if constexpr (DT == DT_I8 && MB == 1) {
+  if constexpr ((DT == DT_I8 || DT == DT_F8) && MB == 1) {
     if (p.a_x) return stream_launch_ql<DT, MB, EPI, NW, WK, true>(p, nbpb, st);
   }
   return stream_launch_ql<DT, MB, EPI, NW, WK, false>(p, nbpb, st);

@@ -355,6 +355,26 @@ def test_fp8_ffn_deterministic():
         np.testing.assert_array_equal(host_bf16(w8a8.fp8_ffn(layer, x)), y1)
 
 
+@pytest.mark.parametrize("m", [1, 2, 5])
+def test_fp8_quantise_on_load_equals_separate_quantisation(m, monkeypatch):
+    """At decode sizes the FP8 streaming GEMM quantises its bf16 input to E4M3
+    itself: same codes and scales as the separate quantiser, so the same sums
+    in the same order and bit-identical outputs."""
+    say("fp8 quantise-on-load", m)
+    cfg, q, layer = _ffn_fp8(m)
+    x = dev_bf16(cfg["x"])
+    lm_cfg = synth.lm_head_config(m=m, vocab=8192)
+    delta = oracle.smooth_calibrate(lm_cfg["x_cal"], [lm_cfg["w"]])
+    lm = w8a8.fp8_linear_layer(dev_bf16(lm_cfg["w"]), dev_f32(delta))
+    xl = dev_bf16(lm_cfg["x"])
+    outs = []
+    for flag in ("0", "1"):
+        monkeypatch.setenv("W8A8_NO_QLOAD", flag)
+        outs.append((host_bf16(w8a8.fp8_ffn(layer, x)), host_bf16(w8a8.fp8_lm_head(lm, xl))))
+    np.testing.assert_array_equal(outs[0][0], outs[1][0])
+    np.testing.assert_array_equal(outs[0][1], outs[1][1])
+
+
 # ------------------------------------------------------------------ shape errors
 
 def test_fp8_rejects_k_not_multiple_of_128():
