@@ -235,6 +235,15 @@ struct QLoad {
   const uint16_t* x = nullptr;
   const float* delta = nullptr;
   float* s_out = nullptr;  // where to leave the per-row scales (optional)
+  // fused layer glue instead of x (one token row): see GemmParams::g_*
+  const uint16_t* g_x_in = nullptr;
+  uint16_t* g_x_out = nullptr;
+  uint16_t* g_x_copy = nullptr;
+  const void* g_part = nullptr;
+  int g_splits = 0;
+  bool g_part_f32 = false;
+  const float* g_st = nullptr;
+  const float* g_si = nullptr;
 };
 
 // Streaming int8 / E4M3 plans over at most 16 rows quantise their bf16 input
@@ -254,6 +263,14 @@ w8a8_status run_gemm(const Plan& pl, int dt, int epi, const void* A, int64_t lda
   p.a_ld = k;
   p.a_k = (int)k;
   p.a_s_out = ql.s_out;
+  p.g_x_in = ql.g_x_in;
+  p.g_x_out = ql.g_x_out;
+  p.g_x_copy = ql.g_x_copy;
+  p.g_part = ql.g_part;
+  p.g_splits = ql.g_splits;
+  p.g_part_f32 = ql.g_part_f32 ? 1 : 0;
+  p.g_st = ql.g_st;
+  p.g_si = ql.g_si;
   p.A = A;
   p.B = B;
   p.B2 = B2;
@@ -266,7 +283,7 @@ w8a8_status run_gemm(const Plan& pl, int dt, int epi, const void* A, int64_t lda
   p.kchunk = pl.kchunk;
   p.splits = pl.splits;
   p.s_a = s_a;
-  if (ql.x) {
+  if (ql.x || ql.g_x_in) {
     // quantise-on-load: the token scales exist only inside the GEMM, which
     // leaves them at s_out; a split-K reduction dequantises from there
     if (pl.splits > 1 && !ql.s_out)
@@ -300,6 +317,14 @@ w8a8_status run_gemm_raw(const Plan& pl, int dt, const void* A, int64_t lda, int
   p.a_ld = k;
   p.a_k = (int)k;
   p.a_s_out = ql.s_out;
+  p.g_x_in = ql.g_x_in;
+  p.g_x_out = ql.g_x_out;
+  p.g_x_copy = ql.g_x_copy;
+  p.g_part = ql.g_part;
+  p.g_splits = ql.g_splits;
+  p.g_part_f32 = ql.g_part_f32 ? 1 : 0;
+  p.g_st = ql.g_st;
+  p.g_si = ql.g_si;
   p.A = A;
   p.B = B;
   p.lda = lda;
@@ -448,7 +473,7 @@ Plan stack_down_plan(int64_t m, int64_t d, int64_t f) {
 }
 
 struct StackWs {
-  size_t x, a, q, s, h, qh, sh, part, lm, total;
+  size_t x, x2, a, q, s, h, qh, sh, part, lm, total;
 };
 StackWs stack_ws(int64_t m, int64_t d, int64_t f, int64_t vocab) {
   StackWs w;
@@ -457,7 +482,8 @@ StackWs stack_ws(int64_t m, int64_t d, int64_t f, int64_t vocab) {
   const size_t lm = std::max(plan_ws_bytes(plan_gemm(m, vocab, d, DT_I8, false), m, vocab),
                              bf16_linear_ws(m, vocab, d));
   w.x = 0;
-  w.a = w.x + align256((size_t)m * d * 2);
+  w.x2 = w.x + align256((size_t)m * d * 2);  // the token stream alternates between x and x2
+  w.a = w.x2 + align256((size_t)m * d * 2);
   w.q = w.a + align256((size_t)m * d * 2);
   w.s = w.q + align256(w8a8_packed_bytes(m, d));
   w.h = w.s + align256((size_t)m * 4);
@@ -1044,7 +1070,9 @@ w8a8_status stack_run(const w8a8_stack_desc* desc, const uint8_t* prec, int lm_h
   const int64_t d = desc->d, f = desc->f;
   char* base = (char*)ws;
   const StackWs w = stack_ws(m, d, f, desc->vocab);
-  uint16_t* xcur = (uint16_t*)(base + w.x);
+  uint16_t* xbuf[2] = {(uint16_t*)(base + w.x), (uint16_t*)(base + w.x2)};
+  const uint16_t* xin = (const uint16_t*)x;  // the latest token stream
+  int nxt = 0;                               // the buffer the next update writes
   uint16_t* a = (uint16_t*)(base + w.a);
   int8_t* q = (int8_t*)(base + w.q);
   float* s = (float*)(base + w.s);
@@ -1065,8 +1093,8 @@ w8a8_status stack_run(const w8a8_stack_desc* desc, const uint8_t* prec, int lm_h
     g.d = d;
     g.rows_pad = round_up(m, 16);
     g.kp = round_up(d, 64);
-    g.x_in = l == 0 ? (const uint16_t*)x : xcur;
-    g.x_out = xcur;
+    g.x_in = xin;
+    g.x_out = xbuf[nxt];
     if (hidden && l > 0) g.x_copy = hidden + (l - 1) * m * d;
     if (l > 0) {
       const bool i8 = prec[l - 1] != 0;
@@ -1086,15 +1114,53 @@ w8a8_status stack_run(const w8a8_stack_desc* desc, const uint8_t* prec, int lm_h
     } else {
       g.a = a;
     }
-    return hip_check(launch_glue(g, st), "glue");
+    CHECK(hip_check(launch_glue(g, st), "glue"));
+    xin = xbuf[nxt];
+    nxt ^= 1;
+    return W8A8_OK;
+  };
+
+  // At one token the glue in front of an INT8 layer runs inside that layer's
+  // gate/up GEMM (every workgroup computes it for the row while its weights
+  // arrive; workgroup 0 writes the token stream), one launch and one memory
+  // round trip less per layer.
+  const bool fuse_ok = m == 1 && !env_int("W8A8_NO_FUSED_GLUE", 0) && pg8.stream &&
+                       pg8.mb == 1 && d % 8 == 0 && d / 8 <= 64 * pg8.nw;
+  auto fused = [&](int64_t l) {
+    if (!fuse_ok || !prec[l]) return false;
+    return l == 0 || (prec[l - 1] ? p8.splits : p16.splits) <= kGlueMaxSplits;
   };
 
   for (int64_t l = 0; l < desc->n_layers; ++l) {
-    CHECK(glue(l));
+    if (fused(l)) {
+      const w8a8_ffn_desc* L = &desc->int8_ffn[l];
+      QLoad ql;
+      ql.delta = L->delta_gu;
+      ql.g_x_in = xin;
+      ql.g_x_out = xbuf[nxt];
+      if (l > 0) {
+        const bool i8 = prec[l - 1] != 0;
+        ql.g_x_copy = hidden ? hidden + (l - 1) * m * d : nullptr;
+        ql.g_part = part;
+        ql.g_splits = i8 ? p8.splits : p16.splits;
+        ql.g_part_f32 = !i8;
+        if (i8) {
+          ql.g_st = sh;
+          ql.g_si = desc->int8_ffn[l - 1].s_down;
+        }
+      }
+      CHECK(run_gemm(pg8, DT_I8, EPI_GLU, nullptr, 0, m, L->wq_gate, L->wq_up, f, d, nullptr,
+                     L->s_gate, L->s_up, h, f, nullptr, st, ql));
+      xin = xbuf[nxt];
+      nxt ^= 1;
+    } else {
+      CHECK(glue(l));
+    }
     if (prec[l]) {
       const w8a8_ffn_desc* L = &desc->int8_ffn[l];
-      CHECK(run_gemm(pg8, DT_I8, EPI_GLU, q, 0, m, L->wq_gate, L->wq_up, f, d, s, L->s_gate,
-                     L->s_up, h, f, nullptr, st));
+      if (!fused(l))
+        CHECK(run_gemm(pg8, DT_I8, EPI_GLU, q, 0, m, L->wq_gate, L->wq_up, f, d, s, L->s_gate,
+                       L->s_up, h, f, nullptr, st));
       if (plan_qloads(p8, m, f)) {
         CHECK(run_gemm_raw(p8, DT_I8, nullptr, 0, m, L->wq_down, d, f, part, st,
                            QLoad{h, L->delta_down, sh}));

@@ -87,6 +87,28 @@ __device__ __forceinline__ float gelu_tanh(float x) {
   return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(a));
 }
 
+// Workgroup reductions over the per-thread values of one row; each call site
+// passes its own LDS array, so consecutive reductions need no extra barrier.
+// The sum adds the per-wave sums in wave order, so waves whose threads all
+// contribute 0 (a larger workgroup over the same row) leave it unchanged.
+__device__ __forceinline__ float block_sum_in(float v, float* red) {
+  v = wave_sum(v);
+  if (lane_id() == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  float s = 0.0f;
+  for (int i = 0; i < (int)(blockDim.x >> 6); ++i) s += red[i];
+  return s;
+}
+
+__device__ __forceinline__ float block_max_in(float v, float* red) {
+  v = wave_max(v);
+  if (lane_id() == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  float m = red[0];
+  for (int i = 1; i < (int)(blockDim.x >> 6); ++i) m = fmaxf(m, red[i]);
+  return m;
+}
+
 // q = rne(v / s) clamped to [-127, 127], with v / s the correctly rounded
 // binary32 quotient.  Fast path: v * inv with inv = 1/s differs from v / s by at
 // most 2.3e-5 for |v / s| <= 127.5 (two roundings of 2^-24 each plus the one of

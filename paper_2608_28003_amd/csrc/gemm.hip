@@ -603,11 +603,157 @@ __device__ __forceinline__ void quantize_panel(const GemmParams& p, int kb0, int
   }
 }
 
-template <int DT, int MB, int EPI, int NW, int WK, bool QL>
+// Fused layer glue for one token row (see GemmParams): thread t owns the row's
+// columns [8t, 8t + 8), as in the glue kernel, so every sum and reduction runs
+// in the glue kernel's order and the codes and scale come out identical.  All
+// operands are loaded without branches before the first weight batch (threads
+// past the row, absent partial sums or scales read valid bytes of B instead).
+struct GlueRegs {
+  uint4 x;
+  int4 part[kGlueMaxSplits][2];  // int32 sums, or the bits of fp32 sums
+  float4 si0, si1, d0, d1;
+  float st;
+};
+
+__device__ __forceinline__ void glue_fetch(const GemmParams& p, GlueRegs& R) {
+  const int d = p.a_k;
+  const int c0 = min((int)threadIdx.x, d / 8 - 1) * 8;
+  const bool has_part = p.g_part != nullptr;
+  const bool scaled = has_part && !p.g_part_f32;
+  const int4* dummy = reinterpret_cast<const int4*>(p.B);  // >= 4 KiB of packed weights
+  R.x = *reinterpret_cast<const uint4*>(p.g_x_in + c0);
+  const int32_t* pp = has_part ? reinterpret_cast<const int32_t*>(p.g_part) + c0
+                               : reinterpret_cast<const int32_t*>(dummy);
+  const int64_t plane = has_part ? (int64_t)p.M * d : 0;
+#pragma unroll
+  for (int z = 0; z < kGlueMaxSplits; ++z) {
+    const int zz = min(z, max(p.g_splits - 1, 0));
+    R.part[z][0] = *reinterpret_cast<const int4*>(pp + zz * plane);
+    R.part[z][1] = *reinterpret_cast<const int4*>(pp + zz * plane + 4);
+  }
+  const float* si = scaled ? p.g_si + c0 : reinterpret_cast<const float*>(dummy);
+  R.si0 = *reinterpret_cast<const float4*>(si);
+  R.si1 = *reinterpret_cast<const float4*>(si + 4);
+  R.st = *(scaled ? p.g_st : reinterpret_cast<const float*>(dummy));
+  const float* dl = p.a_delta ? p.a_delta + c0 : reinterpret_cast<const float*>(dummy);
+  R.d0 = *reinterpret_cast<const float4*>(dl);
+  R.d1 = *reinterpret_cast<const float4*>(dl + 4);
+}
+
+template <int NW>
+__device__ __forceinline__ void glue_panel(const GemmParams& p, int kb0, int kc, v4i* lds_a,
+                                           float* s_row, const GlueRegs& R) {
+  constexpr int NT = NW * 64;
+  __shared__ float red_y[NW], red_x[NW], red_q[NW];
+  const int t = threadIdx.x;
+  const int d = p.a_k;
+  const bool own = t < d / 8;
+  const int c0 = t * 8;
+  for (int idx = t; idx < kc * 64; idx += NT) lds_a[idx] = v4i{0, 0, 0, 0};  // padding stays 0
+  float xv[8];
+  {
+    const uint32_t w[4] = {R.x.x, R.x.y, R.x.z, R.x.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      xv[2 * j] = bf16_bits_to_float(w[j] & 0xffffu);
+      xv[2 * j + 1] = bf16_bits_to_float(w[j] >> 16);
+    }
+  }
+  if (p.g_part) {  // uniform: post-norm of the previous layer's output, residual add
+    float y[8];
+    if (p.g_part_f32) {
+      float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int z = 0; z < kGlueMaxSplits; ++z)
+        if (z < p.g_splits) {
+          const int4 a0 = R.part[z][0], a1 = R.part[z][1];
+          acc[0] += __int_as_float(a0.x); acc[1] += __int_as_float(a0.y);
+          acc[2] += __int_as_float(a0.z); acc[3] += __int_as_float(a0.w);
+          acc[4] += __int_as_float(a1.x); acc[5] += __int_as_float(a1.y);
+          acc[6] += __int_as_float(a1.z); acc[7] += __int_as_float(a1.w);
+        }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) y[e] = bf16_bits_to_float(float_to_bf16_bits(acc[e]));
+    } else {
+      int32_t acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+      for (int z = 0; z < kGlueMaxSplits; ++z)
+        if (z < p.g_splits) {
+          const int4 a0 = R.part[z][0], a1 = R.part[z][1];
+          acc[0] += a0.x; acc[1] += a0.y; acc[2] += a0.z; acc[3] += a0.w;
+          acc[4] += a1.x; acc[5] += a1.y; acc[6] += a1.z; acc[7] += a1.w;
+        }
+      const float si[8] = {R.si0.x, R.si0.y, R.si0.z, R.si0.w, R.si1.x, R.si1.y, R.si1.z, R.si1.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        y[e] = bf16_bits_to_float(float_to_bf16_bits(((float)acc[e] * R.st) * si[e]));
+    }
+    float ss = 0.0f;
+    if (own) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss += y[e] * y[e];
+    }
+    ss = block_sum_in(ss, red_y);
+    const float inv = 1.0f / sqrtf(ss / (float)d + 1e-6f);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float b = bf16_bits_to_float(float_to_bf16_bits(y[e] * inv));
+      xv[e] = bf16_bits_to_float(float_to_bf16_bits(xv[e] + b));
+    }
+  }
+  if (own && blockIdx.x == 0 && blockIdx.y == 0) {  // the token stream, written once
+    uint4 o;
+    o.x = (uint32_t)float_to_bf16_bits(xv[0]) | ((uint32_t)float_to_bf16_bits(xv[1]) << 16);
+    o.y = (uint32_t)float_to_bf16_bits(xv[2]) | ((uint32_t)float_to_bf16_bits(xv[3]) << 16);
+    o.z = (uint32_t)float_to_bf16_bits(xv[4]) | ((uint32_t)float_to_bf16_bits(xv[5]) << 16);
+    o.w = (uint32_t)float_to_bf16_bits(xv[6]) | ((uint32_t)float_to_bf16_bits(xv[7]) << 16);
+    if (p.g_x_out) *reinterpret_cast<uint4*>(p.g_x_out + c0) = o;
+    if (p.g_x_copy) *reinterpret_cast<uint4*>(p.g_x_copy + c0) = o;
+  }
+  float ss = 0.0f;
+  if (own) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss += xv[e] * xv[e];
+  }
+  ss = block_sum_in(ss, red_x);
+  const float inv = 1.0f / sqrtf(ss / (float)d + 1e-6f);
+  float a[8];
+  float amax = 0.0f;
+  const float dl[8] = {R.d0.x, R.d0.y, R.d0.z, R.d0.w, R.d1.x, R.d1.y, R.d1.z, R.d1.w};
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    a[e] = bf16_bits_to_float(float_to_bf16_bits(xv[e] * inv));
+    if (p.a_delta) a[e] = a[e] / dl[e];
+    if (own) amax = fmaxf(amax, fabsf(a[e]));
+  }
+  amax = block_max_in(amax, red_q);
+  const float sr = amax / 127.0f;
+  if (t == 0) {
+    s_row[0] = sr;
+    if (p.a_s_out && blockIdx.x == 0 && blockIdx.y == 0) p.a_s_out[0] = sr;
+  }
+  const int f = c0 / kFragK8 - kb0;  // this thread's fragment column in the panel
+  if (own && sr != 0.0f && f >= 0 && f < kc) {
+    const float sinv = 1.0f / sr;
+    const bool fast = isfinite(sinv);
+    uint32_t lo = 0, hi = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      lo |= ((uint32_t)code_of(a[e], sr, sinv, fast) & 0xffu) << (8 * e);
+      hi |= ((uint32_t)code_of(a[e + 4], sr, sinv, fast) & 0xffu) << (8 * e);
+    }
+    // row 0 of the fragment: lane 16 * ((c0 % 64) / 16), bytes c0 % 16 .. + 7
+    uint2* dst = reinterpret_cast<uint2*>(&lds_a[f * 64 + 16 * ((c0 % kFragK8) / 16)]) + (c0 % 16) / 8;
+    *dst = make_uint2(lo, hi);
+  }
+}
+
+template <int DT, int MB, int EPI, int NW, int WK, int QL>
 __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int nb_per_block) {
   static_assert(WK == 1 || WK == NW, "either every wave owns its column blocks or all share one");
   static_assert(!QL || ((DT == DT_I8 || DT == DT_F8) && MB == 1),
                 "quantise-on-load: int8 or E4M3 codes, one row block");
+  static_assert(QL != 2 || DT == DT_I8, "fused layer glue: int8 codes");
   constexpr bool GLU = (EPI == EPI_GLU);
   constexpr bool BF16 = (DT == DT_BF16);
   constexpr bool FACC = (DT != DT_I8);
@@ -652,11 +798,12 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
              frag_offset(min(mb, p.rb_a - 1), kb0 + kk, p.kb_count) + lane * 16;
     }
   };
-  // QL: the workgroup quantises its bf16 rows itself (p.a_x); a separate
-  // instantiation, so that the quantising kernel has no staging loop whose
-  // outstanding loads the compiler would have to wait for before quantising
-  constexpr bool QLOAD_OK = QL;
-  constexpr bool qload = QL;
+  // QL 1: the workgroup quantises its bf16 rows itself (p.a_x); QL 2: it runs
+  // the layer glue for its one token row first (p.g_*).  Separate
+  // instantiations, so that a quantising kernel has no staging loop whose
+  // outstanding loads the compiler would have to wait for before quantising.
+  constexpr bool QLOAD_OK = QL != 0;
+  constexpr bool qload = QL != 0;
   if constexpr (!QL) {
     if constexpr (WK > 1) {
       for (int f = 0; f < MB * my_k; ++f) {
@@ -722,14 +869,15 @@ __global__ __launch_bounds__(64 * NW) void gemm_stream_kernel(GemmParams p, int 
     if (scaled) load_scales(nb, sbx, sbx2);
   };
   QloadRegs<NW> qr;
-  if constexpr (QLOAD_OK) quantize_fetch<NW>(p, true, qr);  // ahead of the weights
+  GlueRegs gr;
+  if constexpr (QL == 1) quantize_fetch<NW>(p, true, qr);  // ahead of the weights
+  if constexpr (QL == 2) glue_fetch(p, gr);
 
   __builtin_amdgcn_sched_barrier(0);
   load_first(b0, u0, sbn[0], sbn2[0]);  // first weights go out with the A fragments
   __shared__ float s_row[16];           // quantise-on-load: per-row scales
-  if constexpr (QLOAD_OK) {
-    if (qload) quantize_panel<NW, DT == DT_F8>(p, kb0, kc, lds_a, s_row, qr);  // overlaps the weights
-  }
+  if constexpr (QL == 1) quantize_panel<NW, DT == DT_F8>(p, kb0, kc, lds_a, s_row, qr);
+  if constexpr (QL == 2) glue_panel<NW>(p, kb0, kc, lds_a, s_row, gr);  // both overlap the weights
   wait_vmcnt<0>();
   if ((WK == 1 && NW > 1) || qload) lds_barrier();  // the shared panel is read by every wave
   if (scaled && qload) {
@@ -983,8 +1131,15 @@ static bool gemm_params_ok(int dt, int epi, const GemmParams& p, int kind, int n
   if ((int64_t)p.kchunk * (p.splits - 1) >= p.kb_count) return false;  // no empty split
   if ((int64_t)p.kchunk * p.splits < p.kb_count) return false;         // K fully covered
   if (glu && p.splits != 1) return false;  // the gated epilogue needs whole sums
-  const bool qload = kind == 1 && (dt == DT_I8 || dt == DT_F8) && p.a_x != nullptr;
+  const bool glue = kind == 1 && dt == DT_I8 && p.g_x_in != nullptr;
+  const bool qload = (kind == 1 && (dt == DT_I8 || dt == DT_F8) && p.a_x != nullptr) || glue;
+  if ((kind != 1 || dt != DT_I8) && p.g_x_in) return false;  // fused glue: int8 streaming only
   if (kind == 0 && p.a_x) return false;  // the tiled kernel reads codes only
+  if (glue) {
+    if (p.a_x || p.M != 1 || p.a_k < 8 || p.a_k % 8 || p.a_k / 8 > 64 * nw) return false;
+    if (p.g_part && (p.g_splits < 1 || p.g_splits > kGlueMaxSplits)) return false;
+    if (p.g_part && !p.g_part_f32 && (!p.g_st || !p.g_si)) return false;
+  }
   if (qload && (p.M > 16 || p.a_k < 16 || (int64_t)p.M * (p.a_k / 16) > (int64_t)64 * nw))
     return false;
   if (kind == 2) {
@@ -1017,7 +1172,7 @@ static size_t stream_lds_bytes(int mb, int kchunk, int wk, bool glu) {
   return (size_t)mb * kchunk * kFragBytes + (size_t)(wk - 1) * (glu ? 2 : 1) * mb * kFragBytes;
 }
 
-template <int DT, int MB, int EPI, int NW, int WK, bool QL>
+template <int DT, int MB, int EPI, int NW, int WK, int QL>
 static hipError_t stream_launch_ql(const GemmParams& p, int nbpb, hipStream_t st) {
   auto kern = gemm_stream_kernel<DT, MB, EPI, NW, WK, QL>;
   static size_t static_lds = 0;  // benign race: every caller computes the same values
@@ -1042,10 +1197,13 @@ static hipError_t stream_launch_ql(const GemmParams& p, int nbpb, hipStream_t st
 
 template <int DT, int MB, int EPI, int NW, int WK>
 static hipError_t stream_launch(const GemmParams& p, int nbpb, hipStream_t st) {
-  if constexpr ((DT == DT_I8 || DT == DT_F8) && MB == 1) {
-    if (p.a_x) return stream_launch_ql<DT, MB, EPI, NW, WK, true>(p, nbpb, st);
+  if constexpr (DT == DT_I8 && MB == 1) {
+    if (p.g_x_in) return stream_launch_ql<DT, MB, EPI, NW, WK, 2>(p, nbpb, st);
   }
-  return stream_launch_ql<DT, MB, EPI, NW, WK, false>(p, nbpb, st);
+  if constexpr ((DT == DT_I8 || DT == DT_F8) && MB == 1) {
+    if (p.a_x) return stream_launch_ql<DT, MB, EPI, NW, WK, 1>(p, nbpb, st);
+  }
+  return stream_launch_ql<DT, MB, EPI, NW, WK, 0>(p, nbpb, st);
 }
 
 // Instantiated wave layouts: 16-wave workgroups only for MB == 1 (at 16 waves a

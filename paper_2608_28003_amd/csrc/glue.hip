@@ -69,26 +69,6 @@ __global__ __launch_bounds__(1024) void rmsnorm_kernel(const uint16_t* x,
 
 // ------------------------------------------------------------------ fused row glue
 
-// Workgroup reductions over the per-thread values of one row; each call site
-// passes its own LDS array, so consecutive reductions need no extra barrier.
-__device__ __forceinline__ float block_sum_in(float v, float* red) {
-  v = wave_sum(v);
-  if (lane_id() == 0) red[threadIdx.x >> 6] = v;
-  __syncthreads();
-  float s = 0.0f;
-  for (int i = 0; i < (int)(blockDim.x >> 6); ++i) s += red[i];
-  return s;
-}
-
-__device__ __forceinline__ float block_max_in(float v, float* red) {
-  v = wave_max(v);
-  if (lane_id() == 0) red[threadIdx.x >> 6] = v;
-  __syncthreads();
-  float m = red[0];
-  for (int i = 1; i < (int)(blockDim.x >> 6); ++i) m = fmaxf(m, red[i]);
-  return m;
-}
-
 // One row r per workgroup, thread t owns columns [8t, 8t + 8).  Steps, each
 // optional and in this order (the arithmetic of every step is the one of the
 // standalone kernels: split-K reduction + dequant epilogue, rmsnorm_kernel,

@@ -37,6 +37,21 @@ struct GemmParams {
   int64_t a_ld = 0;                // row stride of a_x in elements
   int a_k = 0;                     // logical columns of a_x
   float* a_s_out = nullptr;        // optional: the per-row scales, written once
+  // Fused layer glue (streaming kernel, int8, one token row, a_x null): the
+  // row is the previous layer's output,  y = bf16(dequant(sum of g_splits
+  // int32 partial sums)) or bf16(sum of fp32 partials),  x = bf16(g_x_in +
+  // bf16(RMSNorm(y)))  (x = g_x_in without partials), written by workgroup 0
+  // to g_x_out (and g_x_copy), then  a = bf16(RMSNorm(x))  is smoothed by
+  // a_delta and quantised as with a_x (a_k = the row length).  The arithmetic
+  // and reduction order are those of the glue kernel.
+  const uint16_t* g_x_in = nullptr;
+  uint16_t* g_x_out = nullptr;
+  uint16_t* g_x_copy = nullptr;
+  const void* g_part = nullptr;
+  int g_splits = 0;
+  int g_part_f32 = 0;
+  const float* g_st = nullptr;     // int32 partials: token scale [1]
+  const float* g_si = nullptr;     //                 column scales [a_k]
   // Tiled kernel walk order: tiles in bands of group_m M tiles (0: one band
   // of all M tiles); rotate: start each workgroup's K walk at a different step.
   int group_m = 0;
@@ -85,6 +100,8 @@ hipError_t launch_gemm_tile(int dt, int epi, int tile, const GemmParams& p, hipS
 // LDS; nw waves per workgroup, wk of them splitting one column block's K range
 // Largest M * K / 16 a streaming workgroup of nw waves can quantise on load.
 inline int64_t qload_capacity(int nw) { return (int64_t)64 * nw; }
+// Fused layer glue: K splits of the previous layer it can add (loaded up front).
+constexpr int kGlueMaxSplits = 4;
 hipError_t launch_gemm_stream(int dt, int epi, int mb, int nw, int wk, const GemmParams& p,
                               int nb_per_block, hipStream_t st);
 size_t gemm_stream_lds_bytes(int mb, int kchunk, int wk, bool glu);

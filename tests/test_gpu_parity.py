@@ -523,6 +523,58 @@ def test_decode_down_stream_plans_bit_identical(wk, splits, monkeypatch):
     np.testing.assert_array_equal(host_bf16(w8a8.ffn(layer, x)), ref)
 
 
+def _stack_from_cfg(cfg, vocab):
+    layers_o, i8, bf = [], [], []
+    for L in cfg["layers"]:
+        qL = oracle.quantize_ffn(L["w_gate"], L["w_up"], L["w_down"], cfg["x_cal"])
+        layers_o.append(dict(L, int8=qL))
+        i8.append(w8a8.FfnW8A8.from_weights(dev_bf16(L["w_gate"]), dev_bf16(L["w_up"]),
+                                            dev_bf16(L["w_down"]), dev_f32(qL["delta_gu"]),
+                                            dev_f32(qL["delta_down"])))
+        bf.append(w8a8.FfnBF16.from_weights(dev_bf16(L["w_gate"]), dev_bf16(L["w_up"]),
+                                            dev_bf16(L["w_down"])))
+    d_lm = oracle.smooth_calibrate(cfg["x_cal"], [cfg["w_lm"]])
+    return layers_o, w8a8.Stack(i8, bf,
+                                w8a8.LinearW8A8.from_weight(dev_bf16(cfg["w_lm"]), dev_f32(d_lm)),
+                                w8a8.pack_bf16(dev_bf16(cfg["w_lm"])), vocab)
+
+
+@pytest.mark.parametrize("prec", [[1, 1, 1, 1, 1, 1], [0, 1, 1, 0, 1, 1], [1, 0, 0, 1, 1, 0],
+                                  [0, 0, 0, 0, 0, 0]])
+def test_decode_fused_layer_glue_bit_identical(prec, monkeypatch):
+    """At one token an INT8 layer's gate/up GEMM runs the layer glue itself;
+    the token stream after every layer and the logits must equal those of the
+    separate glue launch bit for bit (same arithmetic, same reduction order)."""
+    say("fused glue", prec)
+    cfg = synth.stack_config(m=1, n_layers=6, d=256, f=512, vocab=512)
+    _, stack = _stack_from_cfg(cfg, 512)
+    x = dev_bf16(cfg["x"])
+    prec = np.array(prec, np.uint8)
+    outs = []
+    for flag in ("0", "1"):
+        monkeypatch.setenv("W8A8_NO_FUSED_GLUE", flag)
+        hid, logits = stack.trace(x, prec, lm_head_int8=True, logits=True)
+        outs.append((host_bf16(hid), host_bf16(logits), host_bf16(stack.run(x, prec, False))))
+    for a, b in zip(outs[0], outs[1]):
+        np.testing.assert_array_equal(a, b)
+
+
+@pytest.mark.parametrize("name", ["5+5", "all26"])
+def test_decode_fused_layer_glue_full_size(name, monkeypatch):
+    say("fused glue full size", name)
+    cfg = synth.stack_config(m=1, vocab=4096)
+    _, stack = _stack_from_cfg(cfg, 4096)
+    x = dev_bf16(cfg["x"])
+    prec = w8a8.precision_map(name)
+    outs = []
+    for flag in ("0", "1"):
+        monkeypatch.setenv("W8A8_NO_FUSED_GLUE", flag)
+        hid, logits = stack.trace(x, prec, lm_head_int8=True, logits=True)
+        outs.append((host_bf16(hid), host_bf16(logits)))
+    np.testing.assert_array_equal(outs[0][0], outs[1][0])
+    np.testing.assert_array_equal(outs[0][1], outs[1][1])
+
+
 @pytest.mark.parametrize("m", [1, 16, 128, 300])
 def test_stack_fused_glue_equals_composition(m):
     """The stack fuses each layer boundary (split-K reduction, dequant,
