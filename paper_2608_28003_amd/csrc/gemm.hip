@@ -625,11 +625,13 @@ __device__ __forceinline__ void glue_fetch(const GemmParams& p, GlueRegs& R) {
   const int32_t* pp = has_part ? reinterpret_cast<const int32_t*>(p.g_part) + c0
                                : reinterpret_cast<const int32_t*>(dummy);
   const int64_t plane = has_part ? (int64_t)p.M * d : 0;
+  // planes past g_splits read one fixed 32-byte block (the same address in
+  // every lane, one request per wave) rather than a second copy of the row
 #pragma unroll
   for (int z = 0; z < kGlueMaxSplits; ++z) {
-    const int zz = min(z, max(p.g_splits - 1, 0));
-    R.part[z][0] = *reinterpret_cast<const int4*>(pp + zz * plane);
-    R.part[z][1] = *reinterpret_cast<const int4*>(pp + zz * plane + 4);
+    const int32_t* src = z < p.g_splits ? pp + z * plane : reinterpret_cast<const int32_t*>(dummy);
+    R.part[z][0] = *reinterpret_cast<const int4*>(src);
+    R.part[z][1] = *reinterpret_cast<const int4*>(src + 4);
   }
   const float* si = scaled ? p.g_si + c0 : reinterpret_cast<const float*>(dummy);
   R.si0 = *reinterpret_cast<const float4*>(si);
