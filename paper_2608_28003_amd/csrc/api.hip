@@ -71,6 +71,7 @@ void tile_shape(int tile, int* bm, int* bn) {
     case TILE_128x128_K2: *bm = 128; *bn = 128; break;
     case TILE_GLU_64x64_K2: *bm = 64; *bn = 64; break;
     case TILE_GLU_256x64: *bm = 256; *bn = 64; break;
+    case TILE_GLU_256x64_K2_W8: *bm = 256; *bn = 64; break;
     default: *bm = 128; *bn = 128;
   }
 }
@@ -166,12 +167,15 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
   p = Plan();
   p.dt = dt;
   if (f8) {  // FP8 stages hold whole 128-deep MFMA steps: two-column tiles only
-    if (glu)
-      p.tile = m <= 128 ? TILE_GLU_128x32_K2 : TILE_GLU_64x64_K2;
+    if (glu)  // measured: the 8-wave 256 x 64 tile from M = 512 (216 tiles) on
+      p.tile = m <= 128 ? TILE_GLU_128x32_K2
+                        : (tiles_of(TILE_GLU_256x64_K2_W8, m, n) >= 128 ? TILE_GLU_256x64_K2_W8
+                                                                       : TILE_GLU_64x64_K2);
     else
       p.tile = tiles_of(TILE_128x128_K2, m, n) >= 256 ? TILE_128x128_K2 : TILE_64x64_K2;
     const int want = glu ? env_int("W8A8_GLU_TILE", p.tile) : env_int("W8A8_GEMM_TILE", p.tile);
-    if (glu ? (want == TILE_GLU_128x32_K2 || want == TILE_GLU_64x64_K2)
+    if (glu ? (want == TILE_GLU_128x32_K2 || want == TILE_GLU_64x64_K2 ||
+               want == TILE_GLU_256x64_K2_W8)
             : (want == TILE_64x64_K2 || want == TILE_128x128_K2))
       p.tile = want;
     const int64_t tiles = tiles_of(p.tile, m, n);

@@ -172,8 +172,10 @@ __device__ __forceinline__ void wait_outstanding(int n) {
 // Workgroups are dealt to the 8 XCDs round-robin by ID; the tile order gives
 // every XCD a contiguous range of tiles (M tile fastest), so the A and B
 // panels a range touches stay in that XCD's L2.
-template <int DT, int BM, int BN, int WAVES_M, int NW, int EPI, int S, int KS>
-__global__ __launch_bounds__(64 * NW, 2) void gemm_tile_kernel(GemmParams p) {
+// MINB: workgroups per CU the register budget is sized for (2: two co-resident
+// workgroups; 1: one, with twice the registers per wave)
+template <int DT, int BM, int BN, int WAVES_M, int NW, int EPI, int S, int KS, int MINB = 2>
+__global__ __launch_bounds__(64 * NW, MINB) void gemm_tile_kernel(GemmParams p) {
   constexpr bool GLU = (EPI == EPI_GLU);
   constexpr bool BF16 = (DT == DT_BF16);  // row-major bf16 A, unscaled fp32 sums
   constexpr bool FACC = (DT != DT_I8);    // fp32 accumulators and partial sums
@@ -1051,6 +1053,9 @@ static hipError_t tile_dispatch(int tile, const GemmParams& p, hipStream_t st) {
         return hipGetLastError();
       case TILE_GLU_64x64_K2:
         gemm_tile_kernel<DT, 64, 64, 2, 4, EPI, 3, 2><<<grid_for(64, 64), 256, 0, st>>>(p);
+        return hipGetLastError();
+      case TILE_GLU_256x64_K2_W8:  // 144 KiB of LDS: one workgroup per CU
+        gemm_tile_kernel<DT, 256, 64, 4, 8, EPI, 3, 2, 1><<<grid_for(256, 64), 512, 0, st>>>(p);
         return hipGetLastError();
       default:
         break;

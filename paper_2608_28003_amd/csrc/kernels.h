@@ -82,6 +82,8 @@ enum TileCfg {
   TILE_128x128_K2 = 11,    // as TILE_128x128, two fragment columns per stage
   TILE_GLU_64x64_K2 = 12,  // as TILE_GLU_64x64, two fragment columns per stage
   TILE_GLU_256x64 = 13,    // gated: 4 waves of 128 x (32 + 32), 72 KiB LDS (2 per CU)
+  TILE_GLU_256x64_K2_W8 = 14,  // gated: 8 waves of 64 x (32 + 32), two fragment columns
+                               // per stage, 144 KiB LDS (1 per CU); FP8-capable
 };
 
 hipError_t launch_col_absmax(const void* x, bool bf16, int64_t rows, int64_t k, float* amax,

@@ -303,10 +303,11 @@ def test_fp8_gate_up_tiles_agree(m, monkeypatch):
     qx_o, sx_o = oracle.quantize_act_fp8(cfg["x"], q["delta_gu"])
     qx, sx = pack_codes(qx_o), dev_f32(sx_o)
     outs = []
-    for tile in (9, 12):
+    for tile in (9, 12, 14):
         monkeypatch.setenv("W8A8_GLU_TILE", str(tile))
         outs.append(oracle.bf16_to_f32(host_bf16(w8a8.fp8_ffn_gate_up(layer, qx, sx, m))))
-    assert rel_l2(outs[0], outs[1]) <= 1e-4
+    for o in outs[1:]:
+        assert rel_l2(o, outs[0]) <= 1e-4
 
 
 @pytest.mark.parametrize("m", [1, 64, 300])
