@@ -477,12 +477,14 @@ Plan stack_down_plan(int64_t m, int64_t d, int64_t f) {
 }
 
 struct StackWs {
-  size_t x, x2, a, q, s, h, qh, sh, part, lm, total;
+  size_t x, x2, a, q, s, h, qh, sh, part, lm, ctl, dec, total;
 };
 StackWs stack_ws(int64_t m, int64_t d, int64_t f, int64_t vocab) {
   StackWs w;
   const Plan p8 = stack_down_plan(m, d, f), p16 = plan_gemm(m, d, f, DT_BF16, false);
-  const size_t part = (size_t)std::max(p8.splits, p16.splits) * m * d * 4;
+  // at one token the persistent decode kernel may write up to kGlueMaxSplits planes
+  const int planes = std::max({p8.splits, p16.splits, m == 1 ? kGlueMaxSplits : 1});
+  const size_t part = (size_t)planes * m * d * 4;
   const size_t lm = std::max(plan_ws_bytes(plan_gemm(m, vocab, d, DT_I8, false), m, vocab),
                              bf16_linear_ws(m, vocab, d));
   w.x = 0;
@@ -495,7 +497,11 @@ StackWs stack_ws(int64_t m, int64_t d, int64_t f, int64_t vocab) {
   w.sh = w.qh + align256(w8a8_packed_bytes(m, f));
   w.part = w.sh + align256((size_t)m * 4);
   w.lm = w.part + align256(part);
-  w.total = w.lm + align256(lm);
+  // the persistent decode kernel's barrier counters and per-layer buffers
+  w.ctl = w.lm + align256(lm);
+  w.dec = w.ctl + align256(sizeof(DecCtl));
+  const size_t dec = m == 1 ? (size_t)kDecMaxLayers * decode_layout(d, f, kGlueMaxSplits).layer_bytes : 0;
+  w.total = w.dec + align256(dec);
   return w;
 }
 
@@ -1087,6 +1093,20 @@ w8a8_status stack_run(const w8a8_stack_desc* desc, const uint8_t* prec, int lm_h
   const Plan p8 = stack_down_plan(m, d, f), p16 = plan_gemm(m, d, f, DT_BF16, false);
   const Plan pg8 = plan_gemm(m, f, d, DT_I8, true), pg16 = plan_gemm(m, f, d, DT_BF16, true);
 
+  // At one token, runs of consecutive INT8 layers go to the persistent decode
+  // kernel (one launch per run of up to kDecMaxLayers layers) when the device
+  // holds one of its workgroups per CU and the shape fits it.
+  int dec_grid = 0, dec_splits = 0;
+  if (m == 1 && !env_int("W8A8_NO_PERSISTENT", 0)) {
+    int dev = 0;
+    CHECK(hip_check(hipGetDevice(&dev), "hipGetDevice"));
+    dec_grid = decode_grid(dev);
+    dec_splits = decode_splits(d, f, dec_grid);
+  }
+  // K-split planes of each layer's down projection output
+  std::vector<int> out_splits(desc->n_layers, 0);
+  auto splits_of = [&](int64_t l) { return out_splits[l]; };
+
   // Glue launch l (0..n_layers): FFN output of layer l-1 into the token
   // stream (none for l = 0, which copies x in), then the pre-norm input of
   // layer l (or of the lm_head for l = n_layers), as codes for an INT8
@@ -1103,7 +1123,7 @@ w8a8_status stack_run(const w8a8_stack_desc* desc, const uint8_t* prec, int lm_h
     if (l > 0) {
       const bool i8 = prec[l - 1] != 0;
       g.part = part;
-      g.splits = i8 ? p8.splits : p16.splits;
+      g.splits = splits_of(l - 1);
       g.part_f32 = !i8;
       if (i8) {
         g.s_t = sh;
@@ -1132,10 +1152,51 @@ w8a8_status stack_run(const w8a8_stack_desc* desc, const uint8_t* prec, int lm_h
                        pg8.mb == 1 && d % 8 == 0 && d / 8 <= 64 * pg8.nw;
   auto fused = [&](int64_t l) {
     if (!fuse_ok || !prec[l]) return false;
-    return l == 0 || (prec[l - 1] ? p8.splits : p16.splits) <= kGlueMaxSplits;
+    return l == 0 || splits_of(l - 1) <= kGlueMaxSplits;
   };
 
   for (int64_t l = 0; l < desc->n_layers; ++l) {
+    if (dec_splits && prec[l]) {
+      int64_t l1 = l;
+      while (l1 < desc->n_layers && prec[l1] && l1 - l < kDecMaxLayers) ++l1;
+      DecParams P;
+      P.n_layers = (int)(l1 - l);
+      P.l0 = (int)l;
+      P.d = (int)d;
+      P.f = (int)f;
+      for (int64_t j = l; j < l1; ++j) {
+        const w8a8_ffn_desc* L = &desc->int8_ffn[j];
+        P.L[j - l] = DecLayer{L->wq_gate, L->wq_up, L->s_gate, L->s_up,
+                              L->delta_gu, L->wq_down, L->s_down, L->delta_down};
+      }
+      P.x_in = xin;
+      if (l > 0) {
+        const bool i8 = prec[l - 1] != 0;
+        P.part_in = part;
+        P.splits_in = splits_of(l - 1);
+        P.part_f32_in = !i8;
+        if (i8) {
+          P.st_in = sh;
+          P.si_in = desc->int8_ffn[l - 1].s_down;
+        }
+      }
+      P.x_out = xbuf[nxt];
+      P.part = (int32_t*)part;
+      P.sh = sh;
+      P.hidden = hidden;
+      P.scratch = base + w.dec;
+      P.layout = decode_layout(d, f, dec_splits);
+      P.splits = dec_splits;
+      P.ctl = (DecCtl*)(base + w.ctl);
+      P.spin_limit = env_int("W8A8_DEC_SPIN_LIMIT", P.spin_limit);  // failure-path tests
+      CHECK(hip_check(launch_decode_ffn(P, dec_grid, st), "decode_ffn"));
+      xin = xbuf[nxt];  // the token stream after layer l1 - 2
+      nxt ^= 1;
+      for (int64_t j = l; j < l1; ++j) out_splits[j] = dec_splits;
+      l = l1 - 1;
+      continue;
+    }
+    out_splits[l] = prec[l] ? p8.splits : p16.splits;
     if (fused(l)) {
       const w8a8_ffn_desc* L = &desc->int8_ffn[l];
       QLoad ql;
@@ -1146,7 +1207,7 @@ w8a8_status stack_run(const w8a8_stack_desc* desc, const uint8_t* prec, int lm_h
         const bool i8 = prec[l - 1] != 0;
         ql.g_x_copy = hidden ? hidden + (l - 1) * m * d : nullptr;
         ql.g_part = part;
-        ql.g_splits = i8 ? p8.splits : p16.splits;
+        ql.g_splits = splits_of(l - 1);
         ql.g_part_f32 = !i8;
         if (i8) {
           ql.g_st = sh;

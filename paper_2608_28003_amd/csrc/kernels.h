@@ -134,6 +134,72 @@ struct GlueParams {
 };
 hipError_t launch_glue(const GlueParams& g, hipStream_t st);
 
+// Persistent decode kernel (one token, a run of consecutive INT8 FFN blocks of
+// the stack in one launch; one workgroup per CU, grid-wide barriers between
+// the gate/up and down phases of every layer).
+constexpr int kDecMaxLayers = 32;  // layers per launch
+constexpr int kDecMaxFrags = 12;   // weight fragments a wave holds per phase
+constexpr int kDecMaxPanel = 64;   // activation fragments staged in LDS
+constexpr int kDecGroups = 8;      // barrier arrival groups (one counter each)
+struct DecCtl {                    // cleared before every launch; 256-byte lines
+  unsigned top[64];                // group completions (word 0)
+  unsigned grp[kDecGroups][64];    // arrivals per group (word 0)
+  unsigned err[64];                // word 0 nonzero: a wait gave up; the outputs are NaN
+};
+struct DecLayer {
+  const void* wg;      // packed gate weights (f x d)
+  const void* wu;      // packed up weights
+  const float* sg;     // their per-channel scales [f]
+  const float* su;
+  const float* dgu;    // smoothing of the gate/up input [d] (may be null)
+  const void* wd;      // packed down weights (d x f)
+  const float* sd;     // their per-channel scales [d]
+  const float* dd;     // smoothing of the down input [f] (may be null)
+};
+// Per-layer exchange buffers of the persistent kernel (all inside `scratch`,
+// layer j at j * layer_bytes): the token stream x (bf16 [d]), the down
+// projection's partial sums (int32, plane z, column block c at
+// (z * ncd + c) * 32), the token scale of the down input (float) and the FFN
+// intermediate h (bf16, 16-column item i at i * 64).  Every 128-byte line is
+// written by one workgroup and read only after the barrier that follows.
+struct DecLayout {
+  size_t part, sh, h, layer_bytes;
+};
+DecLayout decode_layout(int64_t d, int64_t f, int splits);
+struct DecParams {
+  DecLayer L[kDecMaxLayers];
+  int n_layers = 0;
+  int l0 = 0;                      // stack index of L[0]
+  int d = 0, f = 0;
+  // the first layer's glue input: the token stream, and the previous layer's
+  // K-split partial sums in planes of d (none: part_in null, splits_in 0)
+  const uint16_t* x_in = nullptr;
+  const void* part_in = nullptr;
+  int splits_in = 0;
+  int part_f32_in = 0;
+  const float* st_in = nullptr;    // int32 partials: token scale [1]
+  const float* si_in = nullptr;    //                 column scales [d]
+  // the run's results for the launches that follow: the token stream after
+  // the next-to-last layer, the last layer's partial sums (planes of d) and
+  // the token scale of its down input
+  uint16_t* x_out = nullptr;
+  int32_t* part = nullptr;
+  float* sh = nullptr;
+  uint16_t* hidden = nullptr;      // optional: token stream after stack layer i at hidden + i d
+  char* scratch = nullptr;         // n_layers x layout.layer_bytes
+  DecLayout layout{};
+  int splits = 0;                  // = decode_splits(d, f, grid)
+  DecCtl* ctl = nullptr;
+  int spin_limit = 1 << 20;        // polls per barrier before giving up
+};
+// Workgroups of the persistent kernel on `device` (one per CU), or 0 when a
+// workgroup per CU cannot be resident.
+int decode_grid(int device);
+// K splits of the down projection for this shape and grid, or 0 when the
+// shape does not fit the kernel.
+int decode_splits(int64_t d, int64_t f, int grid);
+hipError_t launch_decode_ffn(const DecParams& P, int grid, hipStream_t st);
+
 // SQNR of test against ref over n elements (bf16 or f32): part holds
 // 2 * sqnr_groups(n) doubles of scratch, out receives {sum ref^2,
 // sum (ref - test)^2, 10 log10 of their ratio}.

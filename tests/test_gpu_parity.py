@@ -551,6 +551,7 @@ def test_decode_fused_layer_glue_bit_identical(prec, monkeypatch):
     x = dev_bf16(cfg["x"])
     prec = np.array(prec, np.uint8)
     outs = []
+    monkeypatch.setenv("W8A8_NO_PERSISTENT", "1")  # the per-launch decode path
     for flag in ("0", "1"):
         monkeypatch.setenv("W8A8_NO_FUSED_GLUE", flag)
         hid, logits = stack.trace(x, prec, lm_head_int8=True, logits=True)
@@ -567,6 +568,7 @@ def test_decode_fused_layer_glue_full_size(name, monkeypatch):
     x = dev_bf16(cfg["x"])
     prec = w8a8.precision_map(name)
     outs = []
+    monkeypatch.setenv("W8A8_NO_PERSISTENT", "1")
     for flag in ("0", "1"):
         monkeypatch.setenv("W8A8_NO_FUSED_GLUE", flag)
         hid, logits = stack.trace(x, prec, lm_head_int8=True, logits=True)
