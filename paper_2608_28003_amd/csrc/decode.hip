@@ -110,10 +110,120 @@ __device__ __forceinline__ void poison(const DecParams& P) {
   if (threadIdx.x == 0) P.sh[0] = __builtin_nanf("");
 }
 
+// Columns of a row one thread handles in the spread quantisation below
+// (column c = t + 512 i): rows of up to 2560 values.
+constexpr int kDecCols = 5;
+
+// Byte of the LDS panel that holds the code of column c of row 0.
+__device__ __forceinline__ int panel_byte(int c) {
+  return ((c / kFragK8) * 64 + 16 * ((c % kFragK8) / 16)) * 16 + (c % 16);
+}
+
+// The layer glue of one token row.  The token-stream update and both
+// RMSNorm sums run on the threads that own 8 consecutive columns, in the order
+// of glue_panel (and of the glue kernel); the smoothing division, the absmax
+// and the codes then run over all threads of the workgroup, one column each
+// per step, with the same binary32 operations, so the codes and the scale are
+// identical while each thread does a third of the divisions.
+__device__ __forceinline__ void dec_glue(const GemmParams& p, const GlueRegs& R,
+                                         const float (&dk)[kDecCols], v4i* lds_a, float* xs,
+                                         float* s_row) {
+  __shared__ float red_x[kDecNW], red_q[kDecNW];
+  const int t = threadIdx.x, d = p.a_k;
+  const bool own = t < d / 8;
+  float xv[8];
+  glue_stream<kDecNW, true>(p, R, xv);
+  float ss = 0.0f;
+  if (own) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      ss += xv[e] * xv[e];
+      xs[t * 8 + e] = xv[e];
+    }
+  }
+  ss = block_sum_in(ss, red_x);  // its barrier also publishes xs
+  const float inv = 1.0f / sqrtf(ss / (float)d + 1e-6f);
+  float a[kDecCols];
+  float amax = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kDecCols; ++i) {
+    const int c = t + kDecThreads * i;
+    a[i] = 0.0f;
+    if (c < d) {
+      a[i] = bf16_bits_to_float(float_to_bf16_bits(xs[c] * inv));
+      if (p.a_delta) a[i] = a[i] / dk[i];
+      amax = fmaxf(amax, fabsf(a[i]));
+    }
+  }
+  amax = block_max_in(amax, red_q);
+  const float sr = amax / 127.0f;
+  if (t == 0) s_row[0] = sr;
+  const float sinv = 1.0f / sr;
+  const bool fast = isfinite(sinv);
+  int8_t* bytes = reinterpret_cast<int8_t*>(lds_a);
+#pragma unroll
+  for (int i = 0; i < kDecCols; ++i) {
+    const int c = t + kDecThreads * i;
+    if (c < d) bytes[panel_byte(c)] = sr != 0.0f ? code_of(a[i], sr, sinv, fast) : (int8_t)0;
+  }
+}
+
+// Per-token quantisation of the FFN intermediate h for the down phase: the
+// scale comes from the whole row, max |h / delta| / 127, the codes only for
+// the fragment columns [kb0, kb0 + kc).  Thread t < f / 16 holds item t (16
+// columns of h, R.x) and its smoothing factors (R.d); it forms the 16
+// quotients (independent divisions), their absmax, and stages the quotients of
+// the K range in LDS, from where the codes are formed one column per thread.
+// The binary32 operations are those of quantize_panel, so the codes and the
+// scale are identical.
+__device__ __forceinline__ void dec_quant(const QloadRegs<kDecNW>& R, bool has_delta, int f,
+                                          int kb0, int kc, v4i* lds_a, float* qs, float* s_row,
+                                          float* s_out) {
+  __shared__ float red_m[kDecNW];
+  const int t = threadIdx.x;
+  const bool item = t < f / 16;
+  const uint32_t w[8] = {R.x[0][0].x, R.x[0][0].y, R.x[0][0].z, R.x[0][0].w,
+                         R.x[0][1].x, R.x[0][1].y, R.x[0][1].z, R.x[0][1].w};
+  const float dl[16] = {R.d[0][0].x, R.d[0][0].y, R.d[0][0].z, R.d[0][0].w,
+                        R.d[0][1].x, R.d[0][1].y, R.d[0][1].z, R.d[0][1].w,
+                        R.d[0][2].x, R.d[0][2].y, R.d[0][2].z, R.d[0][2].w,
+                        R.d[0][3].x, R.d[0][3].y, R.d[0][3].z, R.d[0][3].w};
+  float v[16];
+  float mx = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    v[e] = bf16_bits_to_float((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xffffu));
+    if (has_delta) v[e] = v[e] / dl[e];
+    mx = fmaxf(mx, fabsf(v[e]));
+  }
+  if (!item) mx = 0.0f;
+  const int i0 = kb0 * (kFragK8 / 16), i1 = (kb0 + kc) * (kFragK8 / 16);
+  if (item && t >= i0 && t < i1) {
+    float4* dst = reinterpret_cast<float4*>(qs + (t - i0) * 16);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) dst[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+  }
+  const float amax = block_max_in(mx, red_m);  // its barrier also publishes qs
+  const float sr = amax / 127.0f;
+  if (t == 0) {
+    s_row[0] = sr;
+    if (s_out && blockIdx.x == 0) st_f32<true>(s_out, sr);
+  }
+  const float sinv = 1.0f / sr;
+  const bool fast = isfinite(sinv);
+  int8_t* bytes = reinterpret_cast<int8_t*>(lds_a);
+#pragma unroll
+  for (int i = 0; i < kDecCols; ++i) {
+    const int c = t + kDecThreads * i;
+    if (c < kc * kFragK8) bytes[panel_byte(c)] = sr != 0.0f ? code_of(qs[c], sr, sinv, fast) : (int8_t)0;
+  }
+}
+
 __global__ __launch_bounds__(kDecThreads) void decode_ffn_kernel(DecParams P) {
   __shared__ v4i lds_a[kDecMaxPanel * 64];
   __shared__ v4i red[kDecNW * 64];
   __shared__ float s_row[16];
+  __shared__ float xs[kDecMaxPanel * kFragK8];  // glue: the token stream; down: the quotients
   const int lane = lane_id(), wave = threadIdx.x >> 6;
   const int G = gridDim.x, b = blockIdx.x;
   const int d = P.d, f = P.f;
@@ -146,6 +256,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_ffn_kernel(DecParams P) {
   float sg = 0.0f, su = 0.0f;
   QloadRegs<kDecNW> qr;
   GlueRegs gr;
+  float dk[kDecCols];  // glue: smoothing factors of the columns t + 512 i
 
   auto load_g = [&](const DecLayer& L) {
     const void* src = (q & 1) ? L.wu : L.wg;
@@ -154,6 +265,9 @@ __global__ __launch_bounds__(kDecThreads) void decode_ffn_kernel(DecParams P) {
       if (j < g_cnt) w[j] = load_frag_packed(src, g_item, g_k0 + j * g_ks, kbd, lane);
     sg = L.sg[g_col];
     su = L.su[g_col];
+    const float* dsrc = L.dgu ? L.dgu : reinterpret_cast<const float*>(L.wg);  // >= 4 d bytes
+#pragma unroll
+    for (int i = 0; i < kDecCols; ++i) dk[i] = dsrc[min((int)threadIdx.x + kDecThreads * i, d - 1)];
   };
   // the down weights and the smoothing factors of this thread's 16-column
   // group of h (read-only: loaded ahead of the barrier)
@@ -212,7 +326,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_ffn_kernel(DecParams P) {
         p.g_si = P.L[j - 1].sd;
         glue_fetch<false, 32>(p, gr, ncd);
       }
-      glue_panel<kDecNW, true>(p, 0, kbd, lds_a, s_row, gr);
+      dec_glue(p, gr, dk, lds_a, xs, s_row);
       __syncthreads();
       v4i acc = {0, 0, 0, 0};
 #pragma unroll
@@ -244,17 +358,12 @@ __global__ __launch_bounds__(kDecThreads) void decode_ffn_kernel(DecParams P) {
     // ---------------- phase D
     if (!grid_wait(P.ctl, k, P.spin_limit)) return poison(P);
     if (d_item) {
-      GemmParams p{};
-      p.M = 1;
-      p.a_k = f;
-      p.a_delta = L.dd;
-      p.a_s_out = j == last ? P.sh : sbuf(j);  // written by workgroup 0
       {
         const uint16_t* xr = hbuf(j) + qg * 64;
         qr.x[0][0] = *reinterpret_cast<const uint4*>(xr);
         qr.x[0][1] = *reinterpret_cast<const uint4*>(xr + 8);
       }
-      quantize_panel<kDecNW, false, true>(p, d_k0, kcd, lds_a, s_row, qr);
+      dec_quant(qr, L.dd != nullptr, f, d_k0, kcd, lds_a, xs, s_row, j == last ? P.sh : sbuf(j));
       __syncthreads();
       v4i acc = {0, 0, 0, 0};
 #pragma unroll
@@ -301,7 +410,7 @@ int decode_grid(int device) {
 int decode_splits(int64_t d, int64_t f, int grid) {
   if (grid < 1 || d % kFragK8 || f % kFragK8) return 0;
   const int64_t kbd = d / kFragK8, kbf = f / kFragK8, ng = f / 16, ncd = d / 16;
-  if (d / 8 > kDecThreads || ng > kDecThreads || kbd > kDecMaxPanel) return 0;
+  if (d > (int64_t)kDecCols * kDecThreads || ng > kDecThreads || kbd > kDecMaxPanel) return 0;
   // gate/up: at most 4 items per workgroup, fragments per wave within the
   // register budget
   const int64_t n_gi = (ng + grid - 1) / grid;
@@ -313,7 +422,9 @@ int decode_splits(int64_t d, int64_t f, int grid) {
   for (int s = kGlueMaxSplits; s >= 1; --s) {
     if (ncd * s > grid || kbf % s) continue;
     const int64_t kcd = kbf / s;
-    if (kcd > kDecMaxPanel || (kcd + kDecNW - 1) / kDecNW > kDecMaxFrags) continue;
+    if (kcd > kDecMaxPanel || kcd * kFragK8 > kDecCols * kDecThreads ||
+        (kcd + kDecNW - 1) / kDecNW > kDecMaxFrags)
+      continue;
     return s;
   }
   return 0;

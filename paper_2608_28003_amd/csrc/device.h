@@ -23,16 +23,50 @@ __device__ __forceinline__ uint16_t float_to_bf16_bits(float f) {
   return __builtin_bit_cast(uint16_t, (__bf16)f);
 }
 
+// v[l ^ m] for the butterfly masks m = 32, 16, 8, 4, 2, 1: lane permutations
+// without an LDS round trip where the hardware has one (DPP within a row of
+// 16 lanes, a swizzle across 32, a permute across 64).  A permutation moves
+// values exactly, so the reductions below add the same pairs in the same
+// order as a butterfly of __shfl_xor and give the same bits.
+template <int M>
+__device__ __forceinline__ float lane_xor(float v) {
+  const int b = __float_as_int(v);
+  int r;
+  if constexpr (M == 1) {
+    r = __builtin_amdgcn_update_dpp(0, b, 0xB1, 0xF, 0xF, true);  // quad_perm [1, 0, 3, 2]
+  } else if constexpr (M == 2) {
+    r = __builtin_amdgcn_update_dpp(0, b, 0x4E, 0xF, 0xF, true);  // quad_perm [2, 3, 0, 1]
+  } else if constexpr (M == 4) {
+    // mirror within 8 lanes (l ^ 7), then reverse each quad (^ 3)
+    const int h = __builtin_amdgcn_update_dpp(0, b, 0x141, 0xF, 0xF, true);
+    r = __builtin_amdgcn_update_dpp(0, h, 0x1B, 0xF, 0xF, true);
+  } else if constexpr (M == 8) {
+    r = __builtin_amdgcn_update_dpp(0, b, 0x128, 0xF, 0xF, true);  // rotate a row of 16 by 8
+  } else if constexpr (M == 16) {
+    r = __builtin_amdgcn_ds_swizzle(b, 0x401F);  // bitmask swizzle: lane ^ 16 within 32
+  } else {
+    static_assert(M == 32, "butterfly masks 1 ... 32");
+    r = __builtin_amdgcn_ds_bpermute((int)((threadIdx.x & (kWave - 1)) ^ 32) << 2, b);
+  }
+  return __int_as_float(r);
+}
+
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, kWave));
-  return v;
+  v = fmaxf(v, lane_xor<32>(v));
+  v = fmaxf(v, lane_xor<16>(v));
+  v = fmaxf(v, lane_xor<8>(v));
+  v = fmaxf(v, lane_xor<4>(v));
+  v = fmaxf(v, lane_xor<2>(v));
+  return fmaxf(v, lane_xor<1>(v));
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
-  return v;
+  v += lane_xor<32>(v);
+  v += lane_xor<16>(v);
+  v += lane_xor<8>(v);
+  v += lane_xor<4>(v);
+  v += lane_xor<2>(v);
+  return v + lane_xor<1>(v);
 }
 
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (kWave - 1)); }

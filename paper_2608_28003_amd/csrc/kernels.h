@@ -138,7 +138,7 @@ hipError_t launch_glue(const GlueParams& g, hipStream_t st);
 // the stack in one launch; one workgroup per CU, grid-wide barriers between
 // the gate/up and down phases of every layer).
 constexpr int kDecMaxLayers = 32;  // layers per launch
-constexpr int kDecMaxFrags = 12;   // weight fragments a wave holds per phase
+constexpr int kDecMaxFrags = 10;   // weight fragments a wave holds per phase
 constexpr int kDecMaxPanel = 64;   // activation fragments staged in LDS
 constexpr int kDecGroups = 8;      // barrier arrival groups (one counter each)
 struct DecCtl {                    // cleared before every launch; 256-byte lines

@@ -229,17 +229,17 @@ __device__ __forceinline__ void glue_fetch(const GemmParams& p, GlueRegs& R, int
   R.d1 = *reinterpret_cast<const float4*>(dl + 4);
 }
 
+// The first half of the layer glue: xv = this thread's 8 columns [8t, 8t + 8)
+// of the updated token stream (post-norm of the previous layer's output added
+// to g_x_in), written by workgroup 0 to g_x_out and g_x_copy.  Threads past the
+// row hold unused values and add 0 to the row sum.
 template <int NW, bool COH = false>
-__device__ __forceinline__ void glue_panel(const GemmParams& p, int kb0, int kc, v4i* lds_a,
-                                           float* s_row, const GlueRegs& R) {
-  constexpr int NT = NW * 64;
-  __shared__ float red_y[NW], red_x[NW], red_q[NW];
+__device__ __forceinline__ void glue_stream(const GemmParams& p, const GlueRegs& R, float (&xv)[8]) {
+  __shared__ float red_y[NW];
   const int t = threadIdx.x;
   const int d = p.a_k;
   const bool own = t < d / 8;
   const int c0 = t * 8;
-  for (int idx = t; idx < kc * 64; idx += NT) lds_a[idx] = v4i{0, 0, 0, 0};  // padding stays 0
-  float xv[8];
   {
     const uint32_t w[4] = {R.x.x, R.x.y, R.x.z, R.x.w};
 #pragma unroll
@@ -299,6 +299,20 @@ __device__ __forceinline__ void glue_panel(const GemmParams& p, int kb0, int kc,
     if (p.g_x_out) st16<COH>(p.g_x_out + c0, o);
     if (p.g_x_copy) *reinterpret_cast<uint4*>(p.g_x_copy + c0) = o;
   }
+}
+
+template <int NW, bool COH = false>
+__device__ __forceinline__ void glue_panel(const GemmParams& p, int kb0, int kc, v4i* lds_a,
+                                           float* s_row, const GlueRegs& R) {
+  constexpr int NT = NW * 64;
+  __shared__ float red_x[NW], red_q[NW];
+  const int t = threadIdx.x;
+  const int d = p.a_k;
+  const bool own = t < d / 8;
+  const int c0 = t * 8;
+  for (int idx = t; idx < kc * 64; idx += NT) lds_a[idx] = v4i{0, 0, 0, 0};  // padding stays 0
+  float xv[8];
+  glue_stream<NW, COH>(p, R, xv);
   float ss = 0.0f;
   if (own) {
 #pragma unroll
