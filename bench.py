@@ -238,6 +238,11 @@ def main():
                                   x_all, w_lm, M, D, F, V, NL, make_graph, time_graph, ops_int8,
                                   ops_all, sec, fp8_layers, lm_fp8)
 
+    if "groups" in result:  # decode: one token through the all26 map and the INT8 lm_head
+        d1 = dict(result["groups"]["stack_maps_m1"]["FFN all26 + lm_head"])
+        d1["hbm_frac"] = round(d1["weight_GBs"] / HBM_PEAK_GBS, 4)
+        result["decode_m1"] = d1
+
     # ------------------------------------------------------------ oracle on the host
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(M)
@@ -385,6 +390,12 @@ def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all
     x1 = x_all[:1].contiguous()
     out1 = torch.empty((1, V), dtype=torch.bfloat16, device=dev)
     ws1 = torch.empty(w8a8.stack_workspace_bytes(1, D, F, V), dtype=torch.uint8, device=dev)
+    def weight_bytes(prec, lm8):
+        # bytes of weights, scales and smoothing factors one decode step streams
+        n8 = int(np.sum(prec))
+        b = n8 * (3 * F * D + (2 * F + D) * 4 + (D + F) * 4) + (NL - n8) * 3 * F * D * 2
+        return b + (V * D + 4 * V + 4 * D if lm8 else 2 * V * D)
+
     maps1, base1 = {}, None
     for name, mp, lm8 in [("bf16", "bf16", False), ("lm_head only", "bf16", True),
                           ("FFN 5+5 + lm_head", "5+5", True), ("FFN 10+10 + lm_head", "10+10", True),
@@ -395,7 +406,20 @@ def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all
         del gs
         if base1 is None:
             base1 = ts
-        maps1[name] = {"us": round(ts * 1e6, 1), "speedup_vs_bf16": round(base1 / ts, 3)}
+        wb = weight_bytes(prec, lm8)
+        maps1[name] = {"us": round(ts * 1e6, 1), "speedup_vs_bf16": round(base1 / ts, 3),
+                       "weight_GBs": round(wb / ts / 1e9, 1)}
+    # the INT8 runs of layers take the persistent decode kernel; the same step
+    # with one launch per GEMM, for reference
+    prec = w8a8.precision_map("all26")
+    os.environ["W8A8_NO_PERSISTENT"] = "1"
+    gs = make_graph(lambda: stack.run(x1, prec, True, out=out1, ws=ws1))
+    os.environ.pop("W8A8_NO_PERSISTENT")
+    ts = time_graph(gs, 10)
+    del gs
+    maps1["FFN all26 + lm_head, one launch per GEMM"] = {
+        "us": round(ts * 1e6, 1), "speedup_vs_bf16": round(base1 / ts, 3),
+        "weight_GBs": round(weight_bytes(prec, True) / ts / 1e9, 1)}
     groups["stack_maps_m1"] = maps1
     # layer sensitivity (SQNR, dB) on 64 tokens and automatically chosen maps
     xs = x_all[:64].contiguous()
