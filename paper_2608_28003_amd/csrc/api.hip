@@ -204,7 +204,11 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
   } else if (long_k) {
     p.tile = TILE_64x64_K2;  // with K split until ~512 workgroups are in flight
   } else {
-    if (tiles_of(TILE_128x128, m, n) >= 256)
+    // measured on the lm_head (N = 262144): 256 x 256 from M = 256 (133.7 vs
+    // 162.4 us at M = 256, 888 vs 924 us at M = 2048), 128 x 128 below
+    if (i8 && m >= 256 && tiles_of(TILE_256x256, m, n) >= 512)
+      p.tile = TILE_256x256;
+    else if (tiles_of(TILE_128x128, m, n) >= 256)
       p.tile = TILE_128x128;
     else if (tiles_of(TILE_128x64, m, n) >= 256)
       p.tile = TILE_128x64;

@@ -368,11 +368,17 @@ def lm_full():
     return cfg, delta, layer
 
 
-@pytest.mark.parametrize("m", [1, 8, 64])
+@pytest.mark.parametrize("m", [1, 8, 64, 256])
 def test_lm_head_full_vocab_sampled_columns(m, lm_full):
+    """M = 256 takes the 256 x 256 tile (rows beyond the fixture's 64 are
+    scaled and negated copies, so every row block holds distinct rows)."""
     say("lm_head full vocab, sampled columns", m)
     cfg, delta, layer = lm_full
-    x = np.ascontiguousarray(cfg["x"][:m])
+    x = cfg["x"]
+    if m > x.shape[0]:
+        xf = oracle.bf16_to_f32(x)
+        x = np.concatenate([x] + [synth.to_bf16_bits(xf * c) for c in (1.5, 0.75, -1.0)])
+    x = np.ascontiguousarray(x[:m])
     y = w8a8.lm_head(layer, dev_bf16(x))
     torch.cuda.synchronize()
     yg = host_bf16(y)
