@@ -338,6 +338,70 @@ def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all
     log("prefill gemms m=2048: gate/up %.2f us, down %.2f us; fp8 %.2f / %.2f us"
         % (t_gu * 1e6, t_dn * 1e6, tf_gu * 1e6, tf_dn * 1e6))
 
+    # --- attention projections (the same W8A8 linear on the attention shapes):
+    # fused QKV 1152 -> 1536 (4 query heads + 1 key + 1 value head of 256, one
+    # shared quantisation of x) and O 1024 -> 1152, 26 distinct layers per
+    # timed pass, INT8 (quantisation included) vs our bf16 kernel vs torch.mm
+    from paper_2608_28003_amd import synth
+    NQ, NKV = 1024, 256
+    NQKV = NQ + 2 * NKV
+    att = []
+    for l in range(NL):
+        wqkv = torch.from_numpy(synth.to_bf16_bits(np.concatenate(
+            [synth.normal(5100 + 4 * l + i, (n, D), synth.W_SIGMA) for i, n in enumerate((NQ, NKV, NKV))]))
+            .view(np.int16)).view(torch.bfloat16).to(dev)
+        wo = torch.from_numpy(synth.to_bf16_bits(synth.normal(5103 + 4 * l, (D, NQ), synth.W_SIGMA))
+                              .view(np.int16)).view(torch.bfloat16).to(dev)
+        att.append((wqkv, wo))
+    xa_all = torch.from_numpy(synth.to_bf16_bits(synth.activations(
+        5001, 256, D, synth.outlier_channels(5002, D, synth.n_outliers_1pct(D)), 30.0))
+        .view(np.int16)).view(torch.bfloat16).to(dev)
+    xo_all = torch.from_numpy(synth.to_bf16_bits(synth.activations(
+        5007, 256, NQ, synth.outlier_channels(5009, NQ, synth.n_outliers_1pct(NQ)), 30.0))
+        .view(np.int16)).view(torch.bfloat16).to(dev)
+    qkv8 = [w8a8.LinearW8A8.from_weight(wq_, w8a8.smooth_calibrate(w8a8.col_absmax(xa_all),
+                                                                   w8a8.col_absmax(wq_)))
+            for wq_, _ in att]
+    o8 = [w8a8.LinearW8A8.from_weight(wo_, w8a8.smooth_calibrate(w8a8.col_absmax(xo_all),
+                                                                 w8a8.col_absmax(wo_)))
+          for _, wo_ in att]
+    qkv16 = [w8a8.pack_bf16(wq_) for wq_, _ in att]
+    o16 = [w8a8.pack_bf16(wo_) for _, wo_ in att]
+    qkv_t = [wq_.t().contiguous() for wq_, _ in att]
+    o_t = [wo_.t().contiguous() for _, wo_ in att]
+    for m in (1, 32, 256):
+        entry = {}
+        for name, xs_, L8, L16, Lt, n, k in (("qkv", xa_all, qkv8, qkv16, qkv_t, NQKV, D),
+                                             ("o", xo_all, o8, o16, o_t, D, NQ)):
+            xm = xs_[:m].contiguous()
+            y = torch.empty((m, n), dtype=torch.bfloat16, device=dev)
+            ws8 = torch.empty(max(1, w8a8.linear_workspace_bytes(m, n, k)), dtype=torch.uint8, device=dev)
+            wsb_n = w8a8.bf16_linear_workspace_bytes(m, n, k)
+            wsb = torch.empty(max(wsb_n, 1), dtype=torch.uint8, device=dev)
+            g8 = make_graph(lambda: [w8a8.linear(L, xm, out=y, ws=ws8) for L in L8])
+            gb = make_graph(lambda: [w8a8.bf16_linear(xm, wp, n, k, out=y, ws=wsb if wsb_n else None)
+                                     for wp in L16])
+            gt = make_graph(lambda: [torch.mm(xm, wt, out=y) for wt in Lt])
+            t8, tb, tt = time_graph(g8, 20) / NL, time_graph(gb, 20) / NL, time_graph(gt, 20) / NL
+            del g8, gb, gt
+            b8 = n * k + n * 4 + k * 4 + m * k * 2 + m * n * 2
+            entry[name] = {"int8_us": round(t8 * 1e6, 2), "bf16_us": round(tb * 1e6, 2),
+                           "torch_bf16_us": round(tt * 1e6, 2),
+                           "speedup_vs_best_bf16": round(min(tb, tt) / t8, 3),
+                           "int8_GBs": round(b8 / t8 / 1e9, 1),
+                           "int8_tops": round(2.0 * m * n * k / t8 / 1e12, 2)}
+        entry["note"] = ("per call incl. activation quantisation; 26 distinct layers per pass "
+                         "(the INT8 weights, 46 MB, stay in the 256 MB memory-side cache)")
+        groups["attn_proj_m%d" % m] = entry
+    log("attention projections: " + ", ".join(
+        "m=%d qkv %.2f/%.2f us o %.2f/%.2f us (int8/best bf16)" % (
+            m, groups["attn_proj_m%d" % m]["qkv"]["int8_us"],
+            min(groups["attn_proj_m%d" % m]["qkv"]["bf16_us"], groups["attn_proj_m%d" % m]["qkv"]["torch_bf16_us"]),
+            groups["attn_proj_m%d" % m]["o"]["int8_us"],
+            min(groups["attn_proj_m%d" % m]["o"]["bf16_us"], groups["attn_proj_m%d" % m]["o"]["torch_bf16_us"]))
+        for m in (1, 32, 256)))
+    del att, qkv8, o8, qkv16, o16, qkv_t, o_t
+
     # --- lm_head decode: INT8 vs our bf16 kernel vs torch.mm (hipBLASLt) bf16
     w_lm_t = w_lm.t().contiguous()           # d x V, a plain (non-transposed) right operand
     for m in (1, 8, 64):

@@ -130,8 +130,13 @@ bool plan_stream(Plan& p, int64_t m, int64_t n, int64_t kb, bool glu, bool f8) {
     int64_t kchunk = round_up(ceil_div(kb, splits), kstep);
     splits = ceil_div(kb, kchunk);
     int64_t pw = ceil_div(kchunk, wk), waves = nbc * splits * wk;
+    // splits that leave a wave fewer than 4 fragments lose to the cross-wave
+    // reduction they add (measured: QKV 1152 -> 1536 at M = 1, 16 waves
+    // 6.85 us, 4 waves 5.33 us)
+    const bool fed = pw >= 4, best_fed = best_pw >= 4;
     bool better;
     if (!found) better = true;
+    else if (fed != best_fed) better = fed;
     else if ((waves >= 768) != (best_waves >= 768)) better = waves >= 768;
     else if (waves >= 768) better = pw > best_pw;
     else better = waves > best_waves;
@@ -212,8 +217,9 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
       p.tile = TILE_128x128;
     else if (tiles_of(TILE_128x64, m, n) >= 256)
       p.tile = TILE_128x64;
-    else
-      p.tile = TILE_64x64;
+    else  // measured on the attention projections at M = 64 ... 256: the
+          // two-column stage is faster when K allows it
+      p.tile = (i8 && kb % 2 == 0) ? TILE_64x64_K2 : TILE_64x64;
   }
   p.tile = glu ? env_int("W8A8_GLU_TILE", p.tile) : env_int("W8A8_GEMM_TILE", p.tile);
   const int64_t tiles = tiles_of(p.tile, m, n);
@@ -221,8 +227,9 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
   if (long_k)
     splits = (int)std::min<int64_t>(std::min<int64_t>(ceil_div(512, tiles), 6),
                                     std::max<int64_t>(1, kb / 8));
-  else if (!glu && tiles < 200)
-    splits = (int)std::min<int64_t>(ceil_div(256, tiles), std::max<int64_t>(1, kb / 4));
+  else if (!glu && tiles < 200)  // int8: at least 16 fragments per split (a split of a
+                                 // 1152-deep K costs more than the parallelism it adds)
+    splits = (int)std::min<int64_t>(ceil_div(256, tiles), std::max<int64_t>(1, kb / (i8 ? 16 : 4)));
   splits = env_int("W8A8_GEMM_SPLITS", splits);
   if (glu || splits < 1) splits = 1;
   p.kchunk = (int)ceil_div(kb, splits);
