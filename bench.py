@@ -432,24 +432,31 @@ def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all
             % (m, t8 * 1e6, tb * 1e6, tt * 1e6, tf * 1e6))
     del w_lm_t
 
-    # --- the paper's precision maps on the whole step (same M as the step)
-    xm = x_all[:M].contiguous()
-    out = torch.empty((M, V), dtype=torch.bfloat16, device=dev)
-    ws = torch.empty(w8a8.stack_workspace_bytes(M, D, F, V), dtype=torch.uint8, device=dev)
-    maps = {}
-    base = None
-    for name, mp, lm8 in [("bf16", "bf16", False), ("lm_head only", "bf16", True),
-                          ("FFN 5+5", "5+5", False), ("FFN 5+5 + lm_head", "5+5", True),
-                          ("FFN 10+10 + lm_head", "10+10", True), ("FFN all26", "all26", False),
-                          ("FFN all26 + lm_head", "all26", True)]:
-        prec = w8a8.precision_map(mp)
-        gs = make_graph(lambda: stack.run(xm, prec, lm8, out=out, ws=ws))
-        ts = time_graph(gs, 10)
-        del gs
-        if base is None:
-            base = ts
-        maps[name] = {"ms": round(ts * 1e3, 4), "speedup_vs_bf16": round(base / ts, 3)}
-    groups["stack_maps_m%d" % M] = maps
+    # --- the paper's precision maps on the whole step: at the step's M and at
+    # the 26-layer stack's prefill sizes M = 512 and 2048 (token rows repeat
+    # the synthetic ones beyond the rows drawn; rows are independent)
+    for mm in sorted({M, 512, 2048}):
+        xm = (x_all[:mm] if mm <= x_all.shape[0] else
+              x_all.repeat((mm + x_all.shape[0] - 1) // x_all.shape[0], 1)[:mm]).contiguous()
+        out = torch.empty((mm, V), dtype=torch.bfloat16, device=dev)
+        ws = torch.empty(w8a8.stack_workspace_bytes(mm, D, F, V), dtype=torch.uint8, device=dev)
+        maps = {}
+        base = None
+        for name, mp, lm8 in [("bf16", "bf16", False), ("lm_head only", "bf16", True),
+                              ("FFN 5+5", "5+5", False), ("FFN 5+5 + lm_head", "5+5", True),
+                              ("FFN 10+10 + lm_head", "10+10", True), ("FFN all26", "all26", False),
+                              ("FFN all26 + lm_head", "all26", True)]:
+            prec = w8a8.precision_map(mp)
+            gs = make_graph(lambda: stack.run(xm, prec, lm8, out=out, ws=ws))
+            ts = time_graph(gs, 10 if mm <= 512 else 5)
+            del gs
+            if base is None:
+                base = ts
+            maps[name] = {"ms": round(ts * 1e3, 4), "speedup_vs_bf16": round(base / ts, 3),
+                          "effective_tops": round(ops_all(mm) / ts / 1e12, 1)}
+        groups["stack_maps_m%d" % mm] = maps
+        del out, ws
+        log("stack at M=%d: " % mm + ", ".join("%s %.3f ms" % (k, v["ms"]) for k, v in maps.items()))
     # the same maps at decode (one token per step: the paper's batch-1 setting)
     x1 = x_all[:1].contiguous()
     out1 = torch.empty((1, V), dtype=torch.bfloat16, device=dev)
@@ -485,7 +492,12 @@ def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all
         "us": round(ts * 1e6, 1), "speedup_vs_bf16": round(base1 / ts, 3),
         "weight_GBs": round(weight_bytes(prec, True) / ts / 1e9, 1)}
     groups["stack_maps_m1"] = maps1
-    # layer sensitivity (SQNR, dB) on 64 tokens and automatically chosen maps
+    # layer sensitivity (SQNR, dB) on 64 tokens and automatically chosen maps,
+    # timed at the step's M against its all-bf16 step
+    xm = x_all[:M].contiguous()
+    out = torch.empty((M, V), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(w8a8.stack_workspace_bytes(M, D, F, V), dtype=torch.uint8, device=dev)
+    base = groups["stack_maps_m%d" % M]["bf16"]["ms"] * 1e-3
     xs = x_all[:64].contiguous()
     iso, prop = stack.sensitivity(xs, w8a8.precision_map("all26"))
     auto = {}
