@@ -583,7 +583,7 @@ def test_decode_fused_layer_glue_full_size(name, monkeypatch):
     np.testing.assert_array_equal(outs[0][1], outs[1][1])
 
 
-@pytest.mark.parametrize("m", [1, 16, 128, 300])
+@pytest.mark.parametrize("m", [1, 16, 128, 300, 1024, 2048])
 def test_stack_fused_glue_equals_composition(m):
     """The stack fuses each layer boundary (split-K reduction, dequant,
     post-norm residual, next pre-norm and its quantisation) into one launch;
