@@ -80,7 +80,11 @@ __global__ __launch_bounds__(1024) void rmsnorm_kernel(const uint16_t* x,
 //   3. smoothed by delta and quantised per row into the fragment layout
 //      (codes q, scale s); rows in [m, rows_pad) and columns in [d, kp) of
 //      the packed output are zero.
-__global__ __launch_bounds__(1024) void glue_kernel(GlueParams g) {
+// NT: the workgroup size it is compiled for (the row's threads rounded up to
+// whole waves); at 1152 columns 192 threads, whose registers then hold every
+// partial sum without spilling.
+template <int NT>
+__global__ __launch_bounds__(NT) void glue_kernel(GlueParams g) {
   __shared__ float red_y[16], red_x[16], red_q[16];
   const int64_t r = blockIdx.x;
   const int t = threadIdx.x;
@@ -107,8 +111,7 @@ __global__ __launch_bounds__(1024) void glue_kernel(GlueParams g) {
   float4 si0 = make_float4(0.f, 0.f, 0.f, 0.f), si1 = si0;
   float st = 0.0f;
   constexpr int MAXZ = 8;  // partial sums held in registers; more splits stream
-  int4 pi[MAXZ][2];
-  float4 pf[MAXZ][2];
+  int4 pr[MAXZ][2];  // int32 partial sums, or the bits of fp32 ones
   const int64_t plane = g.m * d;
   if (own) {
     xraw = *reinterpret_cast<const uint4*>(g.x_in + r * d + col0);
@@ -117,22 +120,14 @@ __global__ __launch_bounds__(1024) void glue_kernel(GlueParams g) {
       d1 = *reinterpret_cast<const float4*>(g.delta + col0 + 4);
     }
     if (g.part) {
-      if (g.part_f32) {
-        const float* pp = reinterpret_cast<const float*>(g.part) + r * d + col0;
+      const int32_t* pp = reinterpret_cast<const int32_t*>(g.part) + r * d + col0;
 #pragma unroll
-        for (int z = 0; z < MAXZ; ++z)
-          if (z < g.splits) {
-            pf[z][0] = *reinterpret_cast<const float4*>(pp + z * plane);
-            pf[z][1] = *reinterpret_cast<const float4*>(pp + z * plane + 4);
-          }
-      } else {
-        const int32_t* pp = reinterpret_cast<const int32_t*>(g.part) + r * d + col0;
-#pragma unroll
-        for (int z = 0; z < MAXZ; ++z)
-          if (z < g.splits) {
-            pi[z][0] = *reinterpret_cast<const int4*>(pp + z * plane);
-            pi[z][1] = *reinterpret_cast<const int4*>(pp + z * plane + 4);
-          }
+      for (int z = 0; z < MAXZ; ++z)
+        if (z < g.splits) {
+          pr[z][0] = *reinterpret_cast<const int4*>(pp + z * plane);
+          pr[z][1] = *reinterpret_cast<const int4*>(pp + z * plane + 4);
+        }
+      if (!g.part_f32) {
         st = g.s_t[r];
         si0 = *reinterpret_cast<const float4*>(g.s_i + col0);
         si1 = *reinterpret_cast<const float4*>(g.s_i + col0 + 4);
@@ -155,8 +150,11 @@ __global__ __launch_bounds__(1024) void glue_kernel(GlueParams g) {
 #pragma unroll
         for (int z = 0; z < MAXZ; ++z)
           if (z < g.splits) {
-            acc[0] += pf[z][0].x; acc[1] += pf[z][0].y; acc[2] += pf[z][0].z; acc[3] += pf[z][0].w;
-            acc[4] += pf[z][1].x; acc[5] += pf[z][1].y; acc[6] += pf[z][1].z; acc[7] += pf[z][1].w;
+            const int4 a0 = pr[z][0], a1 = pr[z][1];
+            acc[0] += __int_as_float(a0.x); acc[1] += __int_as_float(a0.y);
+            acc[2] += __int_as_float(a0.z); acc[3] += __int_as_float(a0.w);
+            acc[4] += __int_as_float(a1.x); acc[5] += __int_as_float(a1.y);
+            acc[6] += __int_as_float(a1.z); acc[7] += __int_as_float(a1.w);
           }
         for (int z = MAXZ; z < g.splits; ++z) {
           float4 a0 = *reinterpret_cast<const float4*>(pp + z * plane);
@@ -172,8 +170,8 @@ __global__ __launch_bounds__(1024) void glue_kernel(GlueParams g) {
 #pragma unroll
         for (int z = 0; z < MAXZ; ++z)
           if (z < g.splits) {
-            acc[0] += pi[z][0].x; acc[1] += pi[z][0].y; acc[2] += pi[z][0].z; acc[3] += pi[z][0].w;
-            acc[4] += pi[z][1].x; acc[5] += pi[z][1].y; acc[6] += pi[z][1].z; acc[7] += pi[z][1].w;
+            acc[0] += pr[z][0].x; acc[1] += pr[z][0].y; acc[2] += pr[z][0].z; acc[3] += pr[z][0].w;
+            acc[4] += pr[z][1].x; acc[5] += pr[z][1].y; acc[6] += pr[z][1].z; acc[7] += pr[z][1].w;
           }
         for (int z = MAXZ; z < g.splits; ++z) {
           int4 a0 = *reinterpret_cast<const int4*>(pp + z * plane);
@@ -264,7 +262,10 @@ hipError_t launch_glue(const GlueParams& g, hipStream_t st) {
   const int64_t rows = g.q ? g.rows_pad : g.m;
   const int64_t per_row = std::max(g.d / 8, g.q ? g.kp / 8 : 0);
   const int64_t threads = std::min<int64_t>((per_row + 63) / 64 * 64, 1024);
-  glue_kernel<<<(unsigned)rows, (unsigned)threads, 0, st>>>(g);
+  if (threads <= 256)
+    glue_kernel<256><<<(unsigned)rows, (unsigned)threads, 0, st>>>(g);
+  else
+    glue_kernel<1024><<<(unsigned)rows, (unsigned)threads, 0, st>>>(g);
   return hipGetLastError();
 }
 
