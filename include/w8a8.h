@@ -316,7 +316,16 @@ int w8a8_precision_map(const char* name, uint8_t* prec, int n_layers);
    for each layer x <- bf16(x + RMSNorm(FFN_l(RMSNorm(x)))), FFN_l INT8 or bf16 by
    prec[l]; then the final RMSNorm and the lm_head, INT8 if lm_head_int8 != 0.
    x: bf16 m x d (not modified), logits: bf16 m x vocab.
-   ws: w8a8_stack_workspace_bytes(m, d, f, vocab). */
+   ws: w8a8_stack_workspace_bytes(m, d, f, vocab); calls that share a workspace
+   must not overlap in time (the workspace holds the intermediates).
+   At m == 1 every run of consecutive INT8 layers (up to 32 per launch) runs in
+   one persistent launch with one workgroup per compute unit and device-wide
+   barriers in device memory (Sec. 5, decode at batch 1); the results are
+   identical to the per-layer launches.  It relies on all its workgroups being
+   resident at once: the library checks that one fits per compute unit, and
+   a barrier that is not reached within about a second (for instance because
+   other work keeps compute units busy that long) ends the launch and leaves
+   NaN in the token stream, so the failure is visible in the logits. */
 w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec,
                            int lm_head_int8, const void* x, int64_t m, void* logits,
                            void* ws, size_t ws_bytes, w8a8_stream_t stream);
