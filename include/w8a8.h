@@ -325,7 +325,8 @@ int w8a8_precision_map(const char* name, uint8_t* prec, int n_layers);
    resident at once: the library checks that one fits per compute unit, and
    a barrier that is not reached within about a second (for instance because
    other work keeps compute units busy that long) ends the launch and leaves
-   NaN in the token stream, so the failure is visible in the logits. */
+   NaN in the token stream: the bf16 lm_head's logits are then NaN, the INT8
+   lm_head's all zero (its absmax skips NaN and the row quantises to zeros). */
 w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec,
                            int lm_head_int8, const void* x, int64_t m, void* logits,
                            void* ws, size_t ws_bytes, w8a8_stream_t stream);
