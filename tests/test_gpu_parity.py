@@ -98,7 +98,8 @@ def to_dev(x):
 @pytest.mark.parametrize("m,k,dtype,smooth", [
     (1, 1152, "bf16", True), (16, 1152, "f32", True), (37, 1152, "bf16", False),
     (128, 6912, "bf16", True), (3, 16, "f32", False), (5, 80, "bf16", True),
-    (2048, 1152, "bf16", True), (64, 1040, "f32", True)])
+    (2048, 1152, "bf16", True), (64, 1040, "f32", True), (2048, 6912, "bf16", True),
+    (1030, 1152, "f32", True), (1030, 80, "bf16", False)])
 def test_quantize_act_bit_exact(m, k, dtype, smooth):
     say("quantize_act", m, k, dtype, smooth)
     x = act_input(m, k, 100 + m + k, dtype=dtype)
