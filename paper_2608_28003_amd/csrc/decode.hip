@@ -324,7 +324,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_ffn_kernel(DecParams P) {
         p.g_part_f32 = 0;
         p.g_st = sbuf(j - 1);
         p.g_si = P.L[j - 1].sd;
-        glue_fetch<false, 32>(p, gr, ncd);
+        glue_fetch<32>(p, gr, ncd);
       }
       dec_glue(p, gr, dk, lds_a, xs, s_row);
       __syncthreads();

@@ -10,22 +10,11 @@
 
 namespace w8a8 {
 
-// Loads and stores of data that other workgroups of the same launch write or
-// read (COH = true, the persistent decode kernel): relaxed device-scope
-// atomics, which bypass the per-XCD L2 and its non-coherent copies, so no L2
-// write-back or invalidation is needed around the grid barriers.  COH = false:
-// plain accesses (producer and consumer are separate launches).
-template <bool COH>
-__device__ __forceinline__ uint4 ld16(const void* p) {
-  if constexpr (COH) {
-    const uint64_t* q = reinterpret_cast<const uint64_t*>(p);
-    const uint64_t lo = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const uint64_t hi = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return make_uint4((uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32));
-  } else {
-    return *reinterpret_cast<const uint4*>(p);
-  }
-}
+// Stores of data that other workgroups of the same launch read after a grid
+// barrier (COH = true, the persistent decode kernel): relaxed device-scope
+// atomic stores, which write through the per-XCD L2, so no L2 write-back is
+// needed before the barrier.  COH = false: plain stores (the consumer is a
+// later launch).
 template <bool COH>
 __device__ __forceinline__ void st16(void* p, uint4 v) {
   if constexpr (COH) {
@@ -37,14 +26,6 @@ __device__ __forceinline__ void st16(void* p, uint4 v) {
   } else {
     *reinterpret_cast<uint4*>(p) = v;
   }
-}
-template <bool COH>
-__device__ __forceinline__ float ld_f32(const float* p) {
-  if constexpr (COH)
-    return __uint_as_float(__hip_atomic_load(reinterpret_cast<const uint32_t*>(p), __ATOMIC_RELAXED,
-                                             __HIP_MEMORY_SCOPE_AGENT));
-  else
-    return *p;
 }
 template <bool COH>
 __device__ __forceinline__ void st_f32(float* p, float v) {
@@ -104,7 +85,7 @@ __device__ __forceinline__ void quantize_fetch(const GemmParams& p, bool qload, 
 }
 
 // F8: E4M3 codes (scale amax / 448, the quantiser's conversion) instead of int8
-template <int NW, bool F8, bool COH = false>
+template <int NW, bool F8>
 __device__ __forceinline__ void quantize_panel(const GemmParams& p, int kb0, int kc, v4i* lds_a,
                                                float* s_row, const QloadRegs<NW>& R) {
   constexpr float QMAX = F8 ? 448.0f : 127.0f;
@@ -155,7 +136,7 @@ __device__ __forceinline__ void quantize_panel(const GemmParams& p, int kb0, int
   if (tid < rows) {
     const float s = __uint_as_float(amax_bits[tid]) / QMAX;
     s_row[tid] = s;
-    if (p.a_s_out && blockIdx.x == 0 && blockIdx.y == 0) st_f32<COH>(p.a_s_out + tid, s);
+    if (p.a_s_out && blockIdx.x == 0 && blockIdx.y == 0) p.a_s_out[tid] = s;
   }
 #pragma unroll
   for (int i = 0; i < MAXG; ++i) {
@@ -199,14 +180,14 @@ struct GlueRegs {
 
 // PAD = 0: partial sums in planes of M x a_k; PAD > 0: plane z holds column
 // block c (16 columns) at (z * ncd + c) * PAD elements.
-template <bool COH = false, int PAD = 0>
+template <int PAD = 0>
 __device__ __forceinline__ void glue_fetch(const GemmParams& p, GlueRegs& R, int ncd = 0) {
   const int d = p.a_k;
   const int c0 = min((int)threadIdx.x, d / 8 - 1) * 8;
   const bool has_part = p.g_part != nullptr;
   const bool scaled = has_part && !p.g_part_f32;
   const int4* dummy = reinterpret_cast<const int4*>(p.B);  // >= 4 KiB of packed weights
-  R.x = ld16<COH>(p.g_x_in + c0);
+  R.x = *reinterpret_cast<const uint4*>(p.g_x_in + c0);
   const int32_t* pp = has_part ? reinterpret_cast<const int32_t*>(p.g_part) +
                                    (PAD ? (c0 / 16) * PAD + c0 % 16 : c0)
                              : reinterpret_cast<const int32_t*>(dummy);
@@ -216,14 +197,13 @@ __device__ __forceinline__ void glue_fetch(const GemmParams& p, GlueRegs& R, int
 #pragma unroll
   for (int z = 0; z < kGlueMaxSplits; ++z) {
     const int32_t* src = z < p.g_splits ? pp + z * plane : reinterpret_cast<const int32_t*>(dummy);
-    const uint4 v0 = ld16<COH>(src), v1 = ld16<COH>(src + 4);
-    R.part[z][0] = make_int4((int)v0.x, (int)v0.y, (int)v0.z, (int)v0.w);
-    R.part[z][1] = make_int4((int)v1.x, (int)v1.y, (int)v1.z, (int)v1.w);
+    R.part[z][0] = *reinterpret_cast<const int4*>(src);
+    R.part[z][1] = *reinterpret_cast<const int4*>(src + 4);
   }
   const float* si = scaled ? p.g_si + c0 : reinterpret_cast<const float*>(dummy);
   R.si0 = *reinterpret_cast<const float4*>(si);
   R.si1 = *reinterpret_cast<const float4*>(si + 4);
-  R.st = ld_f32<COH>(scaled ? p.g_st : reinterpret_cast<const float*>(dummy));
+  R.st = *(scaled ? p.g_st : reinterpret_cast<const float*>(dummy));
   const float* dl = p.a_delta ? p.a_delta + c0 : reinterpret_cast<const float*>(dummy);
   R.d0 = *reinterpret_cast<const float4*>(dl);
   R.d1 = *reinterpret_cast<const float4*>(dl + 4);
@@ -301,7 +281,7 @@ __device__ __forceinline__ void glue_stream(const GemmParams& p, const GlueRegs&
   }
 }
 
-template <int NW, bool COH = false>
+template <int NW>
 __device__ __forceinline__ void glue_panel(const GemmParams& p, int kb0, int kc, v4i* lds_a,
                                            float* s_row, const GlueRegs& R) {
   constexpr int NT = NW * 64;
@@ -312,7 +292,7 @@ __device__ __forceinline__ void glue_panel(const GemmParams& p, int kb0, int kc,
   const int c0 = t * 8;
   for (int idx = t; idx < kc * 64; idx += NT) lds_a[idx] = v4i{0, 0, 0, 0};  // padding stays 0
   float xv[8];
-  glue_stream<NW, COH>(p, R, xv);
+  glue_stream<NW, false>(p, R, xv);
   float ss = 0.0f;
   if (own) {
 #pragma unroll
@@ -333,7 +313,7 @@ __device__ __forceinline__ void glue_panel(const GemmParams& p, int kb0, int kc,
   const float sr = amax / 127.0f;
   if (t == 0) {
     s_row[0] = sr;
-    if (p.a_s_out && blockIdx.x == 0 && blockIdx.y == 0) st_f32<COH>(p.a_s_out, sr);
+    if (p.a_s_out && blockIdx.x == 0 && blockIdx.y == 0) p.a_s_out[0] = sr;
   }
   const int f = c0 / kFragK8 - kb0;  // this thread's fragment column in the panel
   if (own && sr != 0.0f && f >= 0 && f < kc) {
