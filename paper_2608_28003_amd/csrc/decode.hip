@@ -170,40 +170,28 @@ __device__ __forceinline__ void dec_glue(const GemmParams& p, const GlueRegs& R,
 
 // Per-token quantisation of the FFN intermediate h for the down phase: the
 // scale comes from the whole row, max |h / delta| / 127, the codes only for
-// the fragment columns [kb0, kb0 + kc).  Thread t < f / 16 holds item t (16
-// columns of h, R.x) and its smoothing factors (R.d); it forms the 16
-// quotients (independent divisions), their absmax, and stages the quotients of
-// the K range in LDS, from where the codes are formed one column per thread.
-// The binary32 operations are those of quantize_panel, so the codes and the
-// scale are identical.
-__device__ __forceinline__ void dec_quant(const QloadRegs<kDecNW>& R, bool has_delta, int f,
-                                          int kb0, int kc, v4i* lds_a, float* qs, float* s_row,
+// the fragment columns [kb0, kb0 + kc).  The gate/up epilogue has left, with
+// every 16-column item of h, the absmax of its smoothed values (the same
+// binary32 quotients); thread t < f / 16 brings item t's values and absmax
+// (hv, pmax), the workgroup maximum of the item maxima is the row's, and the
+// codes of the K range are formed one column per thread from the staged h
+// and the smoothing factors dk (column kb0 * 64 + t + 512 i), with
+// quantize_panel's binary32 operations, so the codes and the scale are
+// identical to it.
+__device__ __forceinline__ void dec_quant(uint4 h0, uint4 h1, float pmax,
+                                          const float (&dk)[kDecCols], bool has_delta, int f,
+                                          int kb0, int kc, v4i* lds_a, uint16_t* hs, float* s_row,
                                           float* s_out) {
   __shared__ float red_m[kDecNW];
   const int t = threadIdx.x;
   const bool item = t < f / 16;
-  const uint32_t w[8] = {R.x[0][0].x, R.x[0][0].y, R.x[0][0].z, R.x[0][0].w,
-                         R.x[0][1].x, R.x[0][1].y, R.x[0][1].z, R.x[0][1].w};
-  const float dl[16] = {R.d[0][0].x, R.d[0][0].y, R.d[0][0].z, R.d[0][0].w,
-                        R.d[0][1].x, R.d[0][1].y, R.d[0][1].z, R.d[0][1].w,
-                        R.d[0][2].x, R.d[0][2].y, R.d[0][2].z, R.d[0][2].w,
-                        R.d[0][3].x, R.d[0][3].y, R.d[0][3].z, R.d[0][3].w};
-  float v[16];
-  float mx = 0.0f;
-#pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    v[e] = bf16_bits_to_float((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xffffu));
-    if (has_delta) v[e] = v[e] / dl[e];
-    mx = fmaxf(mx, fabsf(v[e]));
-  }
-  if (!item) mx = 0.0f;
   const int i0 = kb0 * (kFragK8 / 16), i1 = (kb0 + kc) * (kFragK8 / 16);
   if (item && t >= i0 && t < i1) {
-    float4* dst = reinterpret_cast<float4*>(qs + (t - i0) * 16);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) dst[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+    uint4* dst = reinterpret_cast<uint4*>(hs + (t - i0) * 16);
+    dst[0] = h0;
+    dst[1] = h1;
   }
-  const float amax = block_max_in(mx, red_m);  // its barrier also publishes qs
+  const float amax = block_max_in(item ? pmax : 0.0f, red_m);  // its barrier also publishes hs
   const float sr = amax / 127.0f;
   if (t == 0) {
     s_row[0] = sr;
@@ -215,7 +203,11 @@ __device__ __forceinline__ void dec_quant(const QloadRegs<kDecNW>& R, bool has_d
 #pragma unroll
   for (int i = 0; i < kDecCols; ++i) {
     const int c = t + kDecThreads * i;
-    if (c < kc * kFragK8) bytes[panel_byte(c)] = sr != 0.0f ? code_of(qs[c], sr, sinv, fast) : (int8_t)0;
+    if (c < kc * kFragK8) {
+      float v = bf16_bits_to_float(hs[c]);
+      if (has_delta) v = v / dk[i];
+      bytes[panel_byte(c)] = sr != 0.0f ? code_of(v, sr, sinv, fast) : (int8_t)0;
+    }
   }
 }
 
@@ -223,7 +215,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_ffn_kernel(DecParams P) {
   __shared__ v4i lds_a[kDecMaxPanel * 64];
   __shared__ v4i red[kDecNW * 64];
   __shared__ float s_row[16];
-  __shared__ float xs[kDecMaxPanel * kFragK8];  // glue: the token stream; down: the quotients
+  __shared__ float xs[kDecMaxPanel * kFragK8];  // glue: the token stream; down: h of the K range
   const int lane = lane_id(), wave = threadIdx.x >> 6;
   const int G = gridDim.x, b = blockIdx.x;
   const int d = P.d, f = P.f;
@@ -253,10 +245,11 @@ __global__ __launch_bounds__(kDecThreads) void decode_ffn_kernel(DecParams P) {
   const int d_cnt = d_item && wave < kcd ? (kcd - wave + kDecNW - 1) / kDecNW : 0;
 
   v4i w[kDecMaxFrags];
-  float sg = 0.0f, su = 0.0f;
-  QloadRegs<kDecNW> qr;
+  float sg = 0.0f, su = 0.0f, sdd = 1.0f;
   GlueRegs gr;
-  float dk[kDecCols];  // glue: smoothing factors of the columns t + 512 i
+  // smoothing factors of the columns t + 512 i of the phase's row: the glue's
+  // (delta_gu) in phase G, the K range's (delta_down) in phase D
+  float dk[kDecCols];
 
   auto load_g = [&](const DecLayer& L) {
     const void* src = (q & 1) ? L.wu : L.wg;
@@ -265,20 +258,22 @@ __global__ __launch_bounds__(kDecThreads) void decode_ffn_kernel(DecParams P) {
       if (j < g_cnt) w[j] = load_frag_packed(src, g_item, g_k0 + j * g_ks, kbd, lane);
     sg = L.sg[g_col];
     su = L.su[g_col];
+    if (L.dd) sdd = L.dd[g_col];  // smoothing of the epilogue's h column (down input)
     const float* dsrc = L.dgu ? L.dgu : reinterpret_cast<const float*>(L.wg);  // >= 4 d bytes
 #pragma unroll
     for (int i = 0; i < kDecCols; ++i) dk[i] = dsrc[min((int)threadIdx.x + kDecThreads * i, d - 1)];
   };
-  // the down weights and the smoothing factors of this thread's 16-column
-  // group of h (read-only: loaded ahead of the barrier)
-  const int qg = min((int)threadIdx.x, f / 16 - 1);
+  // the down weights and the smoothing factors of the K range (read-only:
+  // loaded ahead of the barrier)
+  const int qg = min((int)threadIdx.x, f / 16 - 1);  // this thread's item of h
   auto load_d = [&](const DecLayer& L) {
 #pragma unroll
     for (int j = 0; j < kDecMaxFrags; ++j)
       if (j < d_cnt) w[j] = load_frag_packed(L.wd, d_c, d_k0 + wave + j * kDecNW, kbf, lane);
-    const float* dl = L.dd ? L.dd + qg * 16 : reinterpret_cast<const float*>(L.wd);
+    const float* dsrc = L.dd ? L.dd + d_k0 * kFragK8 : L.sd;
+    const int lim = L.dd ? kcd * kFragK8 : d;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) qr.d[0][e] = reinterpret_cast<const float4*>(dl)[e];
+    for (int i = 0; i < kDecCols; ++i) dk[i] = dsrc[min((int)threadIdx.x + kDecThreads * i, lim - 1)];
   };
 
   // layer j's exchange buffers
@@ -351,6 +346,18 @@ __global__ __launch_bounds__(kDecThreads) void decode_ffn_kernel(DecParams P) {
         if (!(lane & 1))
           __hip_atomic_store(reinterpret_cast<uint32_t*>(hbuf(j) + g_item * 64 + lane),
                              hb | (hn << 16), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        // absmax of the item's smoothed values (the down input's quotients),
+        // over lanes 0..15, stored after the values in the item's line
+        float hm = bf16_bits_to_float(hb);
+        if (L.dd) hm = hm / sdd;
+        hm = fabsf(hm);
+        hm = fmaxf(hm, lane_xor<8>(hm));
+        hm = fmaxf(hm, lane_xor<4>(hm));
+        hm = fmaxf(hm, lane_xor<2>(hm));
+        hm = fmaxf(hm, lane_xor<1>(hm));
+        if (lane == 0)
+          __hip_atomic_store(reinterpret_cast<uint32_t*>(hbuf(j) + g_item * 64 + 16),
+                             __float_as_uint(hm), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
     grid_arrive(P.ctl, ++k);
@@ -358,12 +365,12 @@ __global__ __launch_bounds__(kDecThreads) void decode_ffn_kernel(DecParams P) {
     // ---------------- phase D
     if (!grid_wait(P.ctl, k, P.spin_limit)) return poison(P);
     if (d_item) {
-      {
-        const uint16_t* xr = hbuf(j) + qg * 64;
-        qr.x[0][0] = *reinterpret_cast<const uint4*>(xr);
-        qr.x[0][1] = *reinterpret_cast<const uint4*>(xr + 8);
-      }
-      dec_quant(qr, L.dd != nullptr, f, d_k0, kcd, lds_a, xs, s_row, j == last ? P.sh : sbuf(j));
+      const uint16_t* xr = hbuf(j) + qg * 64;
+      const uint4 h0 = *reinterpret_cast<const uint4*>(xr);
+      const uint4 h1 = *reinterpret_cast<const uint4*>(xr + 8);
+      const float pmax = *reinterpret_cast<const float*>(xr + 16);
+      dec_quant(h0, h1, pmax, dk, L.dd != nullptr, f, d_k0, kcd, lds_a,
+                reinterpret_cast<uint16_t*>(xs), s_row, j == last ? P.sh : sbuf(j));
       __syncthreads();
       v4i acc = {0, 0, 0, 0};
 #pragma unroll
