@@ -24,7 +24,7 @@
 // the epilogues use the same binary32 expressions), so the results are
 // bit-identical to it.
 //
-// Barriers: every workgroup adds one to its group's arrival counter (8
+// Barriers: every workgroup adds one to its group's arrival counter (4
 // groups, one 256-byte line each); the last arrival of a group adds one to a
 // top counter, which the waiting workgroups poll.  Every wait is bounded:
 // past the spin limit, or when another workgroup has given up, a workgroup

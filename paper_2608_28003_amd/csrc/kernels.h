@@ -140,7 +140,7 @@ hipError_t launch_glue(const GlueParams& g, hipStream_t st);
 constexpr int kDecMaxLayers = 32;  // layers per launch
 constexpr int kDecMaxFrags = 10;   // weight fragments a wave holds per phase
 constexpr int kDecMaxPanel = 64;   // activation fragments staged in LDS
-constexpr int kDecGroups = 8;      // barrier arrival groups (one counter each)
+constexpr int kDecGroups = 4;      // barrier arrival groups (one counter each)
 struct DecCtl {                    // cleared before every launch; 256-byte lines
   unsigned top[64];                // group completions (word 0)
   unsigned grp[kDecGroups][64];    // arrivals per group (word 0)
