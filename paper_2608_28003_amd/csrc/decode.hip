@@ -11,11 +11,13 @@
 //     -> dequant -> post-norm residual update of the token stream -> pre-norm
 //     -> smoothing by delta_gu -> per-token codes), then the gate/up
 //     products of this workgroup's 16-column items and the GeGLU epilogue,
-//     h = bf16(gelu_tanh(g) * u), written to global memory;
+//     h = bf16(gelu_tanh(g) * u), written to global memory with the item's
+//     absmax of h / delta_down;
 //   phase D (layer l): per-token quantisation of h (smoothed by delta_down,
-//     scale over the whole row) for this workgroup's K range, then the down
-//     products of its (column block, K split) item, written as int32 partial
-//     sums that the next layer's glue adds.
+//     scale over the whole row: the maximum of the item maxima) for this
+//     workgroup's K range, then the down products of its (column block,
+//     K split) item, written as int32 partial sums that the next layer's
+//     glue adds.
 //
 // Every weight fragment a workgroup needs in a phase is loaded into registers
 // before the barrier that opens the phase, so the weight stream overlaps the
