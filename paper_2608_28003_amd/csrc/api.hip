@@ -1263,9 +1263,38 @@ w8a8_status stack_run(const w8a8_stack_desc* desc, const uint8_t* prec, int lm_h
       CHECK(run_gemm_raw(p16, DT_BF16, h, f, m, L->wp_down, d, f, part, st));
     }
   }
-  CHECK(glue(desc->n_layers));
+  const int64_t V = desc->vocab, nl = desc->n_layers;
+  if (logits && lm_head_int8) {
+    // At one token the final glue (the last layer's residual update, the
+    // final RMSNorm and its quantisation) runs inside the INT8 lm_head's
+    // streaming GEMM, as the layer glue does inside a gate/up GEMM: every
+    // workgroup computes it for the row while its first weights arrive.
+    const Plan pl = plan_gemm(m, V, d, DT_I8, false);
+    const bool fuse_lm = m == 1 && !env_int("W8A8_NO_FUSED_GLUE", 0) && pl.stream &&
+                         pl.mb == 1 && pl.splits == 1 && d % 8 == 0 && d / 8 <= 64 * pl.nw &&
+                         (nl == 0 || splits_of(nl - 1) <= kGlueMaxSplits);
+    if (fuse_lm) {
+      QLoad ql;
+      ql.delta = desc->lm_head_int8.delta;
+      ql.g_x_in = xin;
+      ql.g_x_out = xbuf[nxt];
+      if (nl > 0) {
+        const bool i8 = prec[nl - 1] != 0;
+        ql.g_x_copy = hidden ? hidden + (nl - 1) * m * d : nullptr;
+        ql.g_part = part;
+        ql.g_splits = splits_of(nl - 1);
+        ql.g_part_f32 = !i8;
+        if (i8) {
+          ql.g_st = sh;
+          ql.g_si = desc->int8_ffn[nl - 1].s_down;
+        }
+      }
+      return run_gemm(pl, DT_I8, EPI_BF16, nullptr, 0, m, desc->lm_head_int8.wq, nullptr, V, d,
+                      nullptr, desc->lm_head_int8.s_w, nullptr, logits, V, base + w.lm, st, ql);
+    }
+  }
+  CHECK(glue(nl));
   if (!logits) return W8A8_OK;
-  const int64_t V = desc->vocab;
   if (lm_head_int8) {
     const Plan pl = plan_gemm(m, V, d, DT_I8, false);
     return run_gemm(pl, DT_I8, EPI_BF16, q, 0, m, desc->lm_head_int8.wq, nullptr, V, d, s,
