@@ -8,7 +8,8 @@ layer and for the logits, under mixed maps, runs longer than one launch takes,
 and the full Gemma-3-1B FFN shapes; the token streams also stay within the
 stack's rel-L2 bar of the oracle.  A wait that gives up (forced from the host
 with a spin limit of zero polls) must end the kernel and leave a NaN token
-stream.
+stream.  The final glue inside the INT8 lm_head's GEMM must equal the
+separate glue launch bit for bit at the full vocabulary.
 """
 
 import sys
@@ -148,3 +149,40 @@ def test_persistent_failed_wait_gives_nan(small, monkeypatch):
     monkeypatch.delenv("W8A8_DEC_SPIN_LIMIT")
     hid, logits = stack.trace(x, prec, lm_head_int8=False, logits=True)  # clean again
     assert torch.isfinite(hid.float()).all() and torch.isfinite(logits.float()).all()
+
+
+def test_full_vocab_fused_final_glue_bit_identical(monkeypatch):
+    """At one token the final glue (last layer's residual update, final
+    RMSNorm and its quantisation) runs inside the INT8 lm_head's streaming
+    GEMM; at the full 262144-wide vocabulary (every wave owning its column
+    blocks) the logits and the token streams must equal those of the separate
+    glue launch bit for bit, after the persistent kernel and after per-launch
+    layers alike."""
+    say("fused final glue, full vocab")
+    cfg = synth.stack_config(m=1, n_layers=2, vocab=512)
+    i8, bf = [], []
+    for L in cfg["layers"]:
+        qL = oracle.quantize_ffn(L["w_gate"], L["w_up"], L["w_down"], cfg["x_cal"])
+        i8.append(w8a8.FfnW8A8.from_weights(dev_bf16(L["w_gate"]), dev_bf16(L["w_up"]),
+                                            dev_bf16(L["w_down"]), dev_f32(qL["delta_gu"]),
+                                            dev_f32(qL["delta_down"])))
+        bf.append(w8a8.FfnBF16.from_weights(dev_bf16(L["w_gate"]), dev_bf16(L["w_up"]),
+                                            dev_bf16(L["w_down"])))
+    g = torch.Generator(device=DEV)
+    g.manual_seed(4003)
+    vocab = synth.VOCAB
+    w_lm = (torch.randn(vocab, synth.D_MODEL, device=DEV, generator=g) * synth.W_SIGMA).to(torch.bfloat16)
+    d_lm = (torch.rand(synth.D_MODEL, device=DEV, generator=g) + 0.5).contiguous()
+    stack = w8a8.Stack(i8, bf, w8a8.LinearW8A8.from_weight(w_lm, d_lm), w8a8.pack_bf16(w_lm), vocab)
+    x = dev_bf16(cfg["x"])
+    for persistent in ("0", "1"):
+        monkeypatch.setenv("W8A8_NO_PERSISTENT", "1" if persistent == "0" else "0")
+        for prec in (np.array([1, 1], np.uint8), np.array([1, 0], np.uint8), np.array([0, 0], np.uint8)):
+            outs = []
+            for flag in ("0", "1"):
+                monkeypatch.setenv("W8A8_NO_FUSED_GLUE", flag)
+                hid, logits = stack.trace(x, prec, lm_head_int8=True, logits=True)
+                outs.append((host_bf16(hid), host_bf16(logits), host_bf16(stack.run(x, prec, True))))
+            for a, b in zip(outs[0], outs[1]):
+                np.testing.assert_array_equal(a, b)
+            assert np.isfinite(oracle.bf16_to_f32(outs[0][1])).all()
