@@ -72,6 +72,7 @@ void tile_shape(int tile, int* bm, int* bn) {
     case TILE_GLU_64x64_K2: *bm = 64; *bn = 64; break;
     case TILE_GLU_256x64: *bm = 256; *bn = 64; break;
     case TILE_GLU_256x64_K2_W8: *bm = 256; *bn = 64; break;
+    case TILE_GLU_128x32_K3: *bm = 128; *bn = 32; break;
     default: *bm = 128; *bn = 128;
   }
 }
@@ -198,8 +199,8 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
   const bool i8 = dt == DT_I8;
   const bool long_k = i8 && !glu && k >= 4096 && n <= 4096;  // down-projection-like
   if (glu) {
-    if (m <= 128)
-      p.tile = TILE_GLU_128x32_K2;
+    if (m <= 128)  // int8: three fragment columns a stage (M = 128: 9.95 -> 9.01 us)
+      p.tile = i8 ? TILE_GLU_128x32_K3 : TILE_GLU_128x32_K2;
     else if (tiles_of(TILE_GLU_256x64, m, n) >= (i8 ? 384 : 512))  // two resident per CU
       p.tile = TILE_GLU_256x64;
     else if (i8)

@@ -793,6 +793,9 @@ static hipError_t tile_dispatch(int tile, const GemmParams& p, hipStream_t st) {
         case TILE_GLU_256x64:
           gemm_tile_kernel<DT, 256, 64, 2, 4, EPI, 3, 1><<<grid_for(256, 64), 256, 0, st>>>(p);
           return hipGetLastError();
+        case TILE_GLU_128x32_K3:  // 144 KiB of LDS: one workgroup per CU
+          gemm_tile_kernel<DT, 128, 32, 4, 4, EPI, 4, 3, 1><<<grid_for(128, 32), 256, 0, st>>>(p);
+          return hipGetLastError();
         default:
           break;
       }

@@ -84,6 +84,8 @@ enum TileCfg {
   TILE_GLU_256x64 = 13,    // gated: 4 waves of 128 x (32 + 32), 72 KiB LDS (2 per CU)
   TILE_GLU_256x64_K2_W8 = 14,  // gated: 8 waves of 64 x (32 + 32), two fragment columns
                                // per stage, 144 KiB LDS (1 per CU); FP8-capable
+  TILE_GLU_128x32_K3 = 15,     // as TILE_GLU_128x32, three fragment columns per stage,
+                               // four stages (1 per CU)
 };
 
 hipError_t launch_col_absmax(const void* x, bool bf16, int64_t rows, int64_t k, float* amax,
