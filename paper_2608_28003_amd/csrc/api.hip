@@ -73,6 +73,7 @@ void tile_shape(int tile, int* bm, int* bn) {
     case TILE_GLU_256x64: *bm = 256; *bn = 64; break;
     case TILE_GLU_256x64_K2_W8: *bm = 256; *bn = 64; break;
     case TILE_GLU_128x32_K3: *bm = 128; *bn = 32; break;
+    case TILE_64x64_K3: *bm = 64; *bn = 64; break;
     default: *bm = 128; *bn = 128;
   }
 }
@@ -208,7 +209,14 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
     else
       p.tile = tiles_of(TILE_GLU_128x64, m, n) >= 256 ? TILE_GLU_128x64 : TILE_GLU_64x64;
   } else if (long_k) {
-    p.tile = TILE_64x64_K2;  // with K split until ~512 workgroups are in flight
+    // with K split until ~512 workgroups are in flight (the split rule below);
+    // when the whole grid fits one workgroup per CU (the FFN down projection
+    // up to M = 128: 216 workgroups) stages of three fragment columns
+    // (26-layer stack at M = 128: 892 -> 844 us)
+    const int64_t t64 = tiles_of(TILE_64x64, m, n);
+    const int64_t sp = std::min<int64_t>(std::min<int64_t>(ceil_div(512, t64), 6),
+                                         std::max<int64_t>(1, kb / 8));
+    p.tile = t64 * sp <= 256 ? TILE_64x64_K3 : TILE_64x64_K2;
   } else {
     // measured on the lm_head (N = 262144): 256 x 256 from M = 256 (133.7 vs
     // 162.4 us at M = 256, 888 vs 924 us at M = 2048), 128 x 128 below

@@ -210,7 +210,7 @@ def test_gemm_split_k_is_bit_identical(m, n, k, splits, monkeypatch):
     A = torch.from_numpy(w8a8.rowmajor_to_frag(qa)).to(DEV)
     B = torch.from_numpy(w8a8.rowmajor_to_frag(qb)).to(DEV)
     monkeypatch.setenv("W8A8_GEMM_SPLITS", str(splits))
-    for tile in (0, 1, 2, 3, 7, 10, 11):
+    for tile in (0, 1, 2, 3, 7, 10, 11, 16):
         monkeypatch.setenv("W8A8_GEMM_TILE", str(tile))
         acc = w8a8.gemm_i8_i32(A, m, B, n, k)
         torch.cuda.synchronize()
