@@ -8,10 +8,11 @@
 //   unpack          packed layout -> row-major int8 (checks only)
 //   pack_bf16       row-major bf16 -> packed bf16 layout (bf16 path weights)
 //
-// Quantisation runs one workgroup per row: each thread owns a 16-column chunk
-// held in registers, a butterfly + LDS max gives the row absmax, and each chunk
-// becomes one 16-byte store into its fragment slot.  All arithmetic is IEEE binary32 (correctly rounded
-// division, v_rndne_f32 for round-half-to-even, no contraction).
+// Quantisation runs one workgroup per row: each thread owns a 16-column (or,
+// for few rows, 8-column) chunk held in registers, a butterfly + LDS max gives
+// the row absmax, and each chunk becomes one 16-byte (8-byte) store into its
+// fragment slot.  All arithmetic is IEEE binary32 (correctly rounded division,
+// v_rndne_f32 for round-half-to-even, no contraction).
 #include "device.h"
 #include "kernels.h"
 
@@ -45,6 +46,38 @@ __device__ __forceinline__ void load16<uint16_t>(const uint16_t* p, float (&v)[1
       v[8 * i + 2 * j + 1] = bf16_bits_to_float(w[j] >> 16);
     }
   }
+}
+
+template <typename T>
+__device__ __forceinline__ void load8(const T* p, float (&v)[8]);
+
+template <>
+__device__ __forceinline__ void load8<float>(const float* p, float (&v)[8]) {
+  const float4* q = reinterpret_cast<const float4*>(p);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    float4 t = q[i];
+    v[4 * i + 0] = t.x; v[4 * i + 1] = t.y; v[4 * i + 2] = t.z; v[4 * i + 3] = t.w;
+  }
+}
+
+template <>
+__device__ __forceinline__ void load8<uint16_t>(const uint16_t* p, float (&v)[8]) {
+  const uint4 t = *reinterpret_cast<const uint4*>(p);
+  const uint32_t w[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    v[2 * j + 0] = bf16_bits_to_float(w[j] & 0xffffu);
+    v[2 * j + 1] = bf16_bits_to_float(w[j] >> 16);
+  }
+}
+
+template <typename T, int CW>
+__device__ __forceinline__ void load_chunk(const T* p, float (&v)[CW]) {
+  if constexpr (CW == 16)
+    load16<T>(p, v);
+  else
+    load8<T>(p, v);
 }
 
 // ------------------------------------------------------------------ a1
@@ -96,65 +129,79 @@ __device__ __forceinline__ float block_max(float v) {
   return m;
 }
 
-template <typename T, bool MUL>
-__device__ __forceinline__ void smooth16(const T* __restrict__ xr, const float* __restrict__ delta,
-                                         int64_t c, float (&v)[16]) {
-  load16<T>(xr + c * 16, v);
+// Chunk c of CW (16 or 8) consecutive columns of row xr, smoothed.
+template <typename T, bool MUL, int CW>
+__device__ __forceinline__ void smooth_chunk(const T* __restrict__ xr,
+                                             const float* __restrict__ delta, int64_t c,
+                                             float (&v)[CW]) {
+  load_chunk<T, CW>(xr + c * CW, v);
   if (delta) {
-    float d[16];
-    load16<float>(delta + c * 16, d);
+    float d[CW];
+    load_chunk<float, CW>(delta + c * CW, d);
 #pragma unroll
-    for (int e = 0; e < 16; ++e) v[e] = MUL ? v[e] * d[e] : v[e] / d[e];
+    for (int e = 0; e < CW; ++e) v[e] = MUL ? v[e] * d[e] : v[e] / d[e];
   }
 }
 
+// The codes of chunk c (CW columns) of row r into their fragment slot: a
+// 16-column chunk is one 16-byte row segment, an 8-column chunk half of one.
+template <int CW>
 __device__ __forceinline__ void store_codes(int8_t* __restrict__ q, int64_t r, int64_t c,
-                                            int64_t kb_count, const int32_t (&packed)[4]) {
-  const int64_t kb = c >> 2;
-  const int g = (int)(c & 3);
+                                            int64_t kb_count, const int32_t (&packed)[CW / 4]) {
+  const int64_t c16 = c / (16 / CW);
+  const int64_t kb = c16 >> 2;
+  const int g = (int)(c16 & 3);
   const int64_t off = frag_offset(r >> 4, kb, kb_count) + (int64_t)((r & 15) + 16 * g) * 16;
-  *reinterpret_cast<int4*>(q + off) = make_int4(packed[0], packed[1], packed[2], packed[3]);
+  if constexpr (CW == 16)
+    *reinterpret_cast<int4*>(q + off) = make_int4(packed[0], packed[1], packed[2], packed[3]);
+  else
+    *reinterpret_cast<int2*>(q + off + 8 * (c & 1)) = make_int2(packed[0], packed[1]);
 }
 
 // One workgroup per row r of a rows x k matrix (k % 16 == 0); thread t owns the
-// 16-column chunk t (and t + blockDim, ... for very long rows), keeping its
+// CW-column chunk t (and t + blockDim, ... for very long rows), keeping its
 // smoothed values in registers between the absmax and the rounding pass.
+// CW = 16, or 8 for few rows, where halving each thread's serial divisions
+// shortens the one dependent chain a launch has.
 // Rows in [rows, rows_pad) and columns in [k, kp) of the packed output are
 // written as zeros.  MUL: v = x * delta (weights); else v = x / delta.
 // F8: OCP E4M3 codes instead of int8, s = amax / 448 and code = E4M3(v / s)
 // (binary32 quotient rounded to the nearest E4M3 value, ties to even).
-template <typename T, bool MUL, bool F8>
+template <typename T, bool MUL, bool F8, int CW>
 __global__ __launch_bounds__(1024) void quant_rows_kernel(const T* __restrict__ x, int64_t rows,
                                                           int64_t k, const float* __restrict__ delta,
                                                           int64_t rows_pad, int64_t kp,
                                                           int8_t* __restrict__ q,
                                                           float* __restrict__ s) {
+  static_assert(CW == 16 || CW == 8, "chunk width");
   const int64_t r = blockIdx.x;
   const int t = threadIdx.x;
   const int nt = blockDim.x;
   const int64_t kb_count = kp / kFragK8;
-  const int64_t chunks_pad = kp / 16;
-  const int64_t chunks = k / 16;
-  const int32_t zeros[4] = {0, 0, 0, 0};
+  const int64_t chunks_pad = kp / CW;
+  const int64_t chunks = k / CW;
+  int32_t zeros[CW / 4];
+#pragma unroll
+  for (int i = 0; i < CW / 4; ++i) zeros[i] = 0;
 
   if (r >= rows) {  // padding row: zeros
-    for (int64_t c = t; c < chunks_pad; c += nt) store_codes(q, r, c, kb_count, zeros);
+    for (int64_t c = t; c < chunks_pad; c += nt) store_codes<CW>(q, r, c, kb_count, zeros);
     return;
   }
 
   const T* xr = x + r * k;
-  float v[16];
+  float v[CW];
   float amax = 0.0f;
   if (t < chunks) {
-    smooth16<T, MUL>(xr, delta, t, v);
+    smooth_chunk<T, MUL, CW>(xr, delta, t, v);
 #pragma unroll
-    for (int e = 0; e < 16; ++e) amax = fmaxf(amax, fabsf(v[e]));
+    for (int e = 0; e < CW; ++e) amax = fmaxf(amax, fabsf(v[e]));
   }
-  for (int64_t c = t + nt; c < chunks; c += nt) {  // rows longer than 16 * blockDim
-    float w[16];
-    smooth16<T, MUL>(xr, delta, c, w);
+  for (int64_t c = t + nt; c < chunks; c += nt) {  // rows longer than CW * blockDim
+    float w[CW];
+    smooth_chunk<T, MUL, CW>(xr, delta, c, w);
 #pragma unroll
-    for (int e = 0; e < 16; ++e) amax = fmaxf(amax, fabsf(w[e]));
+    for (int e = 0; e < CW; ++e) amax = fmaxf(amax, fabsf(w[e]));
   }
   amax = block_max(amax);
   const float sr = amax / (F8 ? 448.0f : 127.0f);
@@ -163,18 +210,20 @@ __global__ __launch_bounds__(1024) void quant_rows_kernel(const T* __restrict__ 
   const bool fast = isfinite(inv);
 
   for (int64_t c = t; c < chunks_pad; c += nt) {
-    int32_t packed[4] = {0, 0, 0, 0};
+    int32_t packed[CW / 4];
+#pragma unroll
+    for (int i = 0; i < CW / 4; ++i) packed[i] = 0;
     if (c < chunks && sr != 0.0f) {
-      float w[16];
+      float w[CW];
       if (c == t) {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) w[e] = v[e];
+        for (int e = 0; e < CW; ++e) w[e] = v[e];
       } else {
-        smooth16<T, MUL>(xr, delta, c, w);
+        smooth_chunk<T, MUL, CW>(xr, delta, c, w);
       }
       if constexpr (F8) {
 #pragma unroll
-        for (int e = 0; e < 16; e += 2) {
+        for (int e = 0; e < CW; e += 2) {
           // the conversion gives NaN past the largest code; the quotient only
           // exceeds 448 when the scale itself lost precision (amax near the
           // binary32 subnormal range), and the nearest code is then 448
@@ -185,13 +234,13 @@ __global__ __launch_bounds__(1024) void quant_rows_kernel(const T* __restrict__ 
         }
       } else {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
+        for (int e = 0; e < CW; ++e) {
           int32_t iv = (int32_t)code_of(w[e], sr, inv, fast) & 0xff;
           packed[e >> 2] |= iv << (8 * (e & 3));
         }
       }
     }
-    store_codes(q, r, c, kb_count, packed);
+    store_codes<CW>(q, r, c, kb_count, packed);
   }
 }
 
@@ -243,23 +292,23 @@ hipError_t launch_smooth_delta(const float* a, const float* w, int64_t k, double
   return hipGetLastError();
 }
 
-template <bool F8>
+template <bool F8, int CW>
 static void quant_rows_launch(const void* x, bool bf16, bool mul, int64_t rows, int64_t k,
                               const float* delta, int64_t rows_pad, int64_t kp, int8_t* qpacked,
                               float* s, dim3 grid, dim3 block, hipStream_t st) {
   if (bf16) {
     if (mul)
-      quant_rows_kernel<uint16_t, true, F8><<<grid, block, 0, st>>>(
+      quant_rows_kernel<uint16_t, true, F8, CW><<<grid, block, 0, st>>>(
           (const uint16_t*)x, rows, k, delta, rows_pad, kp, qpacked, s);
     else
-      quant_rows_kernel<uint16_t, false, F8><<<grid, block, 0, st>>>(
+      quant_rows_kernel<uint16_t, false, F8, CW><<<grid, block, 0, st>>>(
           (const uint16_t*)x, rows, k, delta, rows_pad, kp, qpacked, s);
   } else {
     if (mul)
-      quant_rows_kernel<float, true, F8><<<grid, block, 0, st>>>(
+      quant_rows_kernel<float, true, F8, CW><<<grid, block, 0, st>>>(
           (const float*)x, rows, k, delta, rows_pad, kp, qpacked, s);
     else
-      quant_rows_kernel<float, false, F8><<<grid, block, 0, st>>>(
+      quant_rows_kernel<float, false, F8, CW><<<grid, block, 0, st>>>(
           (const float*)x, rows, k, delta, rows_pad, kp, qpacked, s);
   }
 }
@@ -269,14 +318,27 @@ hipError_t launch_quant_rows(const void* x, bool bf16, bool mul, int64_t rows, i
                              bool f8) {
   const int64_t rows_pad = (rows + 15) / 16 * 16;
   const int64_t kp = (k + kFragK8 - 1) / kFragK8 * kFragK8;
-  int64_t threads = (kp / 16 + 63) / 64 * 64;
+  // 8-column chunks while the rows leave CUs idle (one workgroup per row) and a
+  // row still fits one workgroup
+  const bool narrow = rows_pad <= 256 && kp / 8 <= 1024;
+  int64_t threads = (kp / (narrow ? 8 : 16) + 63) / 64 * 64;
   if (threads > 1024) threads = 1024;
   dim3 grid((unsigned)rows_pad), block((unsigned)threads);
-  if (f8)
-    quant_rows_launch<true>(x, bf16, mul, rows, k, delta, rows_pad, kp, qpacked, s, grid, block, st);
-  else
-    quant_rows_launch<false>(x, bf16, mul, rows, k, delta, rows_pad, kp, qpacked, s, grid, block,
-                             st);
+  if (f8) {
+    if (narrow)
+      quant_rows_launch<true, 8>(x, bf16, mul, rows, k, delta, rows_pad, kp, qpacked, s, grid,
+                                 block, st);
+    else
+      quant_rows_launch<true, 16>(x, bf16, mul, rows, k, delta, rows_pad, kp, qpacked, s, grid,
+                                  block, st);
+  } else {
+    if (narrow)
+      quant_rows_launch<false, 8>(x, bf16, mul, rows, k, delta, rows_pad, kp, qpacked, s, grid,
+                                  block, st);
+    else
+      quant_rows_launch<false, 16>(x, bf16, mul, rows, k, delta, rows_pad, kp, qpacked, s, grid,
+                                   block, st);
+  }
   return hipGetLastError();
 }
 
