@@ -211,8 +211,9 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
   } else if (long_k) {
     // with K split until ~512 workgroups are in flight (the split rule below);
     // when the whole grid fits one workgroup per CU (the FFN down projection
-    // up to M = 128: 216 workgroups) stages of three fragment columns
-    // (26-layer stack at M = 128: 892 -> 844 us)
+    // up to M = 128: 216 workgroups) 8 waves and stages of three fragment
+    // columns (26-layer stack at M = 128: 892 -> 844 us with 4 waves, 0.836 ->
+    // 0.825 ms with 8)
     const int64_t t64 = tiles_of(TILE_64x64, m, n);
     const int64_t sp = std::min<int64_t>(std::min<int64_t>(ceil_div(512, t64), 6),
                                          std::max<int64_t>(1, kb / 8));

@@ -829,7 +829,7 @@ static hipError_t tile_dispatch(int tile, const GemmParams& p, hipStream_t st) {
           gemm_tile_kernel<DT, 256, 256, 2, 8, EPI, 5, 1><<<grid_for(256, 256), 512, 0, st>>>(p);
           return hipGetLastError();
         case TILE_64x64_K3:  // 96 KiB of LDS: one workgroup per CU
-          gemm_tile_kernel<DT, 64, 64, 2, 4, EPI, 4, 3, 1><<<grid_for(64, 64), 256, 0, st>>>(p);
+          gemm_tile_kernel<DT, 64, 64, 2, 8, EPI, 4, 3, 1><<<grid_for(64, 64), 512, 0, st>>>(p);
           return hipGetLastError();
         default:
           break;

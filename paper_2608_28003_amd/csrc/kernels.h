@@ -86,8 +86,8 @@ enum TileCfg {
                                // per stage, 144 KiB LDS (1 per CU); FP8-capable
   TILE_GLU_128x32_K3 = 15,     // as TILE_GLU_128x32, three fragment columns per stage,
                                // four stages (1 per CU)
-  TILE_64x64_K3 = 16,          // as TILE_64x64, three fragment columns per stage, four
-                               // stages, 96 KiB of LDS (1 per CU)
+  TILE_64x64_K3 = 16,          // 8 waves of 32 x 16, three fragment columns per stage,
+                               // four stages, 96 KiB of LDS (1 per CU)
 };
 
 hipError_t launch_col_absmax(const void* x, bool bf16, int64_t rows, int64_t k, float* amax,
