@@ -313,8 +313,10 @@ w8a8_status w8a8_rmsnorm_residual(const void* x, const void* f, int64_t m, int64
 int w8a8_precision_map(const char* name, uint8_t* prec, int n_layers);
 
 /* The FFN stack under a precision map (host prec[n_layers], 0 = bf16, 1 = INT8):
-   for each layer x <- bf16(x + RMSNorm(FFN_l(RMSNorm(x)))), FFN_l INT8 or bf16 by
-   prec[l]; then the final RMSNorm and the lm_head, INT8 if lm_head_int8 != 0.
+   for each layer x <- bf16(x + bf16(RMSNorm(FFN_l(bf16(RMSNorm(x)))))) (both norm
+   outputs are bf16 activations, the residual sum is rounded again), FFN_l INT8 or
+   bf16 by prec[l]; then the final RMSNorm (rounded to bf16) and the lm_head, INT8
+   if lm_head_int8 != 0.
    x: bf16 m x d (not modified), logits: bf16 m x vocab.
    ws: w8a8_stack_workspace_bytes(m, d, f, vocab); calls that share a workspace
    must not overlap in time (the workspace holds the intermediates).

@@ -47,7 +47,7 @@ def build(force: bool = False) -> str:
     if force or not os.path.exists(_LIB_PATH) or (
             os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC)):
         tmp = _LIB_PATH + ".tmp%d" % os.getpid()
-        cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
+        cmd = ["gcc", "-O3", "-std=c11", "-fPIC", "-shared", "-fopenmp",
                "-ffp-contract=off", "-fno-fast-math", "-Wall", "-Wextra",
                "-o", tmp, _SRC, "-lm"]
         subprocess.run(cmd, check=True)
@@ -437,8 +437,10 @@ def residual_add(x, y) -> np.ndarray:
 
 def stack_hidden(x_bf16, layers, prec):
     """The token stream after every layer of the FFN stack under a precision
-    map (config glue, Sec. 3): x <- bf16(x + RMSNorm(FFN_l(RMSNorm(x)))), FFN_l
-    the INT8 block for layers in Q_FFN and the bf16 block otherwise."""
+    map (config glue, Sec. 3): x <- bf16(x + bf16(RMSNorm(FFN_l(bf16(RMSNorm(x)))))),
+    both norm outputs rounded to bf16 (every activation is a bf16 tensor) and
+    the residual sum rounded again; FFN_l the INT8 block for layers in Q_FFN
+    and the bf16 block otherwise."""
     x = _c(x_bf16, np.uint16)
     hidden = []
     for l, L in enumerate(layers):

@@ -1,0 +1,371 @@
+"""Pins of the oracle's bf16 reference path, its dequantisation orders and the
+stack composition (Sec. 3 FFN block and decoder-block structure; eq.
+gemm-final; eq. ffn55 / ffn1010 / ffnall26).
+
+Each pin checks the oracle against something other than itself: exact
+rational arithmetic, a hand-built case whose answer is fixed by where the
+roundings fall, or the same composition built from torch's library routines
+(``rms_norm``, ``gelu`` in binary64, ``matmul``).  Every pin also shows that a
+plausible mistake -- summing in binary32, rounding g before the activation,
+applying a scale in another order, dropping the post-norm or the residual --
+gives a different answer on the same input, so the pin has power.
+"""
+
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_28003_amd import synth
+
+
+# ------------------------------------------------------------------ helpers
+
+def rn(q: Fraction, p: int, emin: int) -> Fraction:
+    """Round a rational to the nearest binary floating-point number with p
+    significant bits and minimum normal exponent emin, ties to even (IEEE
+    round-to-nearest); no overflow handling (the pins stay in range)."""
+    if q == 0:
+        return Fraction(0)
+    s = -1 if q < 0 else 1
+    a = abs(q)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    if Fraction(2) ** e > a:
+        e -= 1
+    e = max(e, emin)                 # subnormals share the spacing of emin
+    ulp = Fraction(2) ** (e - p + 1)
+    n = a / ulp
+    fl = n.numerator // n.denominator
+    rem = n - fl
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and fl % 2 == 1):
+        fl += 1
+    return s * fl * ulp
+
+
+def rn32(q):
+    return rn(Fraction(q), 24, -126)
+
+
+def rnbf16(q):
+    return rn(Fraction(q), 8, -126)
+
+
+def bf16_bits_of(v: Fraction) -> int:
+    """bf16 pattern of a value that is exactly a bf16 number."""
+    f = np.array([float(v)], np.float32)
+    b = int(f.view(np.uint32)[0])
+    assert b & 0xFFFF == 0
+    return b >> 16
+
+
+def torch_bf16(t64: torch.Tensor) -> torch.Tensor:
+    """binary64 -> bf16 -> binary64 (torch's conversion, via binary32)."""
+    return t64.to(torch.float32).to(torch.bfloat16).to(torch.float64)
+
+
+def f64(bits):
+    return torch.from_numpy(oracle.bf16_to_f32(bits).astype(np.float64))
+
+
+def bf16_ulps(a_bits, b_bits):
+    a = a_bits.astype(np.int32)
+    b = b_bits.astype(np.int32)
+    sa = np.where(a & 0x8000, -(a & 0x7FFF), a & 0x7FFF)
+    sb = np.where(b & 0x8000, -(b & 0x7FFF), b & 0x7FFF)
+    return np.abs(sa - sb)
+
+
+def bounded_bf16(rng, shape, lo=-4, hi=4):
+    """bf16 values with exponents in [lo, hi): products of two of them need at
+    most 16 significant bits spread over 2 (hi - lo) + 16 bit positions, so a
+    binary64 sum of up to 2^20 of them is exact."""
+    mant = rng.integers(128, 256, size=shape)          # 8 significant bits
+    exp = rng.integers(lo, hi, size=shape) - 7
+    sign = rng.choice([-1.0, 1.0], size=shape)
+    v = (sign * mant * np.exp2(exp)).astype(np.float32)
+    return synth.to_bf16_bits(v)
+
+
+# ------------------------------------------------------------------ bf16 linear (binary64 sums)
+
+@pytest.mark.parametrize("m,n,k", [(1, 1, 1), (3, 5, 37), (2, 7, 64), (4, 3, 200)])
+def test_linear_f64_equals_exact_rational_sum(m, n, k):
+    """linear_f64 sums exact products in binary64: on inputs whose sums
+    binary64 holds exactly it must equal the rational sum, element by element
+    (a transposed operand, a dropped term or a binary32 sum would not)."""
+    rng = np.random.default_rng(100 + k)
+    x = bounded_bf16(rng, (m, k))
+    w = bounded_bf16(rng, (n, k))
+    xf, wf = oracle.bf16_to_f32(x), oracle.bf16_to_f32(w)
+    y = oracle.linear_f64(x, w)
+    b32_differs = False
+    for t in range(m):
+        for i in range(n):
+            exact = sum(Fraction(float(xf[t, j])) * Fraction(float(wf[i, j])) for j in range(k))
+            assert Fraction(float(y[t, i])) == exact, (t, i)
+            acc = np.float32(0)
+            for j in range(k):
+                acc = np.float32(acc + np.float32(xf[t, j] * wf[i, j]))
+            b32_differs |= Fraction(float(acc)) != exact
+    if k >= 37:
+        assert b32_differs   # the pin tells binary64 from binary32 sums
+
+
+def test_bf16_linear_rounds_the_exact_sum_once():
+    """bf16(sum) with one rounding: 1 + 2^-8 + 2^-30 lies just above the bf16
+    midpoint between 1 and 1 + 2^-7 and rounds up; rounding to binary32 first
+    loses the 2^-30 and the tie then goes to the even neighbour 1."""
+    x = synth.to_bf16_bits(np.array([[1.0, 1.0, 1.0]], np.float32))
+    w = synth.to_bf16_bits(np.array([[1.0, 2.0 ** -8, 2.0 ** -30]], np.float32))
+    y = oracle.bf16_linear(x, w)
+    assert int(y[0, 0]) == 0x3F81                  # 1 + 2^-7
+    assert bf16_bits_of(rnbf16(rn32(1 + Fraction(1, 256) + Fraction(1, 2 ** 30)))) == 0x3F80
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+def test_bf16_linear_is_nearest_to_exact_sum(seed):
+    rng = np.random.default_rng(seed)
+    x = bounded_bf16(rng, (3, 48))
+    w = bounded_bf16(rng, (6, 48))
+    xf, wf = oracle.bf16_to_f32(x), oracle.bf16_to_f32(w)
+    y = oracle.bf16_linear(x, w)
+    for t in range(3):
+        for i in range(6):
+            exact = sum(Fraction(float(xf[t, j])) * Fraction(float(wf[i, j])) for j in range(48))
+            assert int(y[t, i]) == bf16_bits_of(rnbf16(exact))
+
+
+# ------------------------------------------------------------------ bf16 FFN: where the roundings fall
+
+def _tiny_ffn(g_weights, u_weights):
+    """d = 2, f = 1 FFN on x = [1, 1] whose down projection copies h to the
+    first output: y[0] = bf16(h)."""
+    x = synth.to_bf16_bits(np.array([[1.0, 1.0]], np.float32))
+    wg = synth.to_bf16_bits(np.array([g_weights], np.float32))
+    wu = synth.to_bf16_bits(np.array([u_weights], np.float32))
+    wd = synth.to_bf16_bits(np.array([[1.0], [0.0]], np.float32))
+    return oracle.bf16_ffn(x, wg, wu, wd)
+
+
+def _gelu64(v):
+    return float(torch.nn.functional.gelu(torch.tensor([v], dtype=torch.float64),
+                                          approximate="tanh")[0])
+
+
+def test_bf16_ffn_keeps_g_in_binary32():
+    """g = 1 + 2^-9 is exact in binary32 but not in bf16.  With g kept,
+    h = gelu(1 + 2^-9) = 0.8433 rounds to 216/256; had g been rounded to bf16
+    (to 1) the block would return bf16(gelu(1)) = 215/256."""
+    y = _tiny_ffn([1.0, 2.0 ** -9], [1.0, 0.0])
+    h_kept = rnbf16(Fraction(_gelu64(1.0 + 2.0 ** -9)))
+    h_rounded_g = rnbf16(Fraction(_gelu64(1.0)))
+    assert h_kept == Fraction(216, 256) and h_rounded_g == Fraction(215, 256)
+    assert int(y[0, 0]) == bf16_bits_of(h_kept)
+    assert int(y[0, 1]) == 0
+
+
+def test_bf16_ffn_keeps_u_in_binary32():
+    """u = 1 + 2^-8 + 2^-10 is exact in binary32 but not in bf16: the block
+    must return bf16(gelu(1) u), which differs from bf16(gelu(1) bf16(u))."""
+    u = 1.0 + 2.0 ** -8 + 2.0 ** -10
+    y = _tiny_ffn([1.0, 0.0], [1.0, u - 1.0])
+    g1 = _gelu64(1.0)
+    want = rnbf16(Fraction(g1) * Fraction(u))
+    alt = rnbf16(Fraction(g1) * rnbf16(Fraction(u)))
+    assert want != alt
+    assert int(y[0, 0]) == bf16_bits_of(want)
+
+
+def test_bf16_ffn_rounds_h_before_the_down_projection():
+    """y = bf16(h W_down^T) with h already in bf16: a down row [1, -1] on
+    h1 = bf16(gelu(1 + 2^-9)) = 216/256 and h2 = bf16(gelu(1)) = 215/256
+    gives exactly 1/256; with h unrounded the difference would be 0.00212."""
+    x = synth.to_bf16_bits(np.array([[1.0, 1.0]], np.float32))
+    wg = synth.to_bf16_bits(np.array([[1.0, 2.0 ** -9], [1.0, 0.0]], np.float32))
+    wu = synth.to_bf16_bits(np.array([[1.0, 0.0], [1.0, 0.0]], np.float32))
+    wd = synth.to_bf16_bits(np.array([[1.0, -1.0], [0.0, 0.0]], np.float32))
+    y = oracle.bf16_ffn(x, wg, wu, wd)
+    assert int(y[0, 0]) == bf16_bits_of(Fraction(1, 256))
+    unrounded = rnbf16(Fraction(_gelu64(1.0 + 2.0 ** -9)) - Fraction(_gelu64(1.0)))
+    assert unrounded != Fraction(1, 256)
+
+
+# ------------------------------------------------------------------ dequantisation order
+
+def _order_cases():
+    # sums that binary32 does not hold (odd, above 2^24) and scales that are
+    # not powers of two, so every rounding step can move the result
+    rng = np.random.default_rng(21)
+    acc = rng.integers(2 ** 24, 2 ** 27, size=(6, 7)) | 1
+    s_t = (rng.uniform(0.3, 3.0, 6) / 127).astype(np.float32)
+    s_i = (rng.uniform(0.3, 3.0, 7) / 127).astype(np.float32)
+    return acc, s_t, s_i
+
+
+def test_int8_dequant_product_order():
+    """y = fl32(fl32(fl32(acc) * s_t) * s_i), token scale first (eq.
+    gemm-final with reading 6), checked with exact rationals."""
+    acc, s_t, s_i = _order_cases()
+    y = oracle.dequant(acc.astype(np.int32), s_t, s_i)
+    other = 0
+    for t in range(acc.shape[0]):
+        for i in range(acc.shape[1]):
+            a = Fraction(int(acc[t, i]))
+            st, si = Fraction(float(s_t[t])), Fraction(float(s_i[i]))
+            want = rn32(rn32(rn32(a) * st) * si)
+            assert Fraction(float(y[t, i])) == want, (t, i)
+            alts = (rn32(rn32(rn32(a) * si) * st), rn32(rn32(a) * rn32(st * si)),
+                    rn32(rn32(a * st) * si))
+            other += any(v != want for v in alts)
+    assert other > 0   # the inputs tell the orders apart
+
+
+def test_fp8_dequant_product_order():
+    """FP8 sums arrive in binary64: y = fl32(fl32(fl32(acc) * s_t) * s_i)."""
+    acc, s_t, s_i = _order_cases()
+    acc = acc.astype(np.float64) + 0.375      # binary64 sums with a fraction
+    y = oracle.dequant_fp8(acc, s_t, s_i)
+    other = 0
+    for t in range(acc.shape[0]):
+        for i in range(acc.shape[1]):
+            a = Fraction(float(acc[t, i]))
+            st, si = Fraction(float(s_t[t])), Fraction(float(s_i[i]))
+            want = rn32(rn32(rn32(a) * st) * si)
+            assert Fraction(float(y[t, i])) == want, (t, i)
+            alts = (rn32(rn32(a * st) * si), rn32(rn32(rn32(a) * si) * st),
+                    rn32(rn32(a) * rn32(st * si)))
+            other += any(v != want for v in alts)
+    assert other > 0
+
+
+# ------------------------------------------------------------------ stack composition
+
+D_S, F_S, L_S, M_S, V_S = 128, 256, 3, 6, 96
+
+
+@pytest.fixture(scope="module")
+def small_stack():
+    cfg = synth.stack_config(m=M_S, n_layers=L_S, d=D_S, f=F_S, vocab=V_S)
+    layers = [dict(L, int8=oracle.quantize_ffn(L["w_gate"], L["w_up"], L["w_down"],
+                                               cfg["x_cal"][:64]))
+              for L in cfg["layers"]]
+    d_lm = oracle.smooth_calibrate(cfg["x_cal"], [cfg["w_lm"]])
+    wq, sw = oracle.quantize_weights(cfg["w_lm"], d_lm)
+    lm = dict(w=cfg["w_lm"], wq=wq, s_w=sw, delta=d_lm)
+    return cfg, layers, lm
+
+
+def torch_rms(v64):
+    return torch.nn.functional.rms_norm(v64, (v64.shape[-1],), eps=oracle.RMS_EPS)
+
+
+def torch_bf16_ffn(a64, L):
+    """The bf16 FFN from torch routines: binary64 products, g and u rounded to
+    binary32, gelu(g) u rounded to bf16, down product rounded to bf16."""
+    g = (a64 @ f64(L["w_gate"]).T).to(torch.float32).to(torch.float64)
+    u = (a64 @ f64(L["w_up"]).T).to(torch.float32).to(torch.float64)
+    h = torch_bf16(torch.nn.functional.gelu(g, approximate="tanh") * u)
+    return torch_bf16(h @ f64(L["w_down"]).T)
+
+
+def torch_stack(x_bits, layers, prec, lm=None, lm_int8=False):
+    """Sandwich-norm stack from torch routines: x <- bf16(x + bf16(RMSNorm(
+    FFN(bf16(RMSNorm(x)))))); INT8 layers call the oracle's (separately
+    pinned) INT8 block on the bf16 pre-norm output."""
+    x = f64(x_bits)
+    hidden = []
+    for l, L in enumerate(layers):
+        a = torch_bf16(torch_rms(x))
+        if prec[l]:
+            a_bits = synth.to_bf16_bits(a.numpy().astype(np.float32))
+            f = f64(oracle.w8a8_ffn(a_bits, L["int8"]))
+        else:
+            f = torch_bf16_ffn(a, L)
+        x = torch_bf16(x + torch_bf16(torch_rms(f)))
+        hidden.append(synth.to_bf16_bits(x.numpy().astype(np.float32)))
+    if lm is None:
+        return hidden
+    xf = torch_bf16(torch_rms(x))
+    if lm_int8:
+        logits = oracle.w8a8_lm_head(synth.to_bf16_bits(xf.numpy().astype(np.float32)),
+                                     lm["wq"], lm["s_w"], lm["delta"])
+    else:
+        logits = synth.to_bf16_bits(torch_bf16(xf @ f64(lm["w"]).T).numpy().astype(np.float32))
+    return hidden, logits
+
+
+def _close(a_bits, b_bits):
+    u = bf16_ulps(a_bits, b_bits)
+    return u.max() <= 1 and float((u > 0).mean()) <= 0.01
+
+
+def test_stack_all_bf16_map_is_the_bf16_path(small_stack):
+    """prec = all bf16 with the bf16 lm_head: every layer and the logits equal
+    the torch composition (torch rounds binary64 to bf16 through binary32, so
+    an element may differ by one bf16 ulp where that double rounding bites)."""
+    cfg, layers, lm = small_stack
+    prec = np.zeros(L_S, np.uint8)
+    logits, hidden = oracle.stack(cfg["x"], layers, prec, lm, False, return_hidden=True)
+    t_hidden, t_logits = torch_stack(cfg["x"], layers, prec, lm, False)
+    for l in range(L_S):
+        assert _close(hidden[l], t_hidden[l]), l
+    assert _close(logits, t_logits)
+
+
+def test_stack_int8_layers_are_the_int8_block_on_the_prenorm(small_stack):
+    """Layer l of the all-INT8 map equals the INT8 FFN block on RMSNorm of its
+    input, post-normed and added to it; the INT8 lm_head runs on the final
+    RMSNorm."""
+    cfg, layers, lm = small_stack
+    for prec in (np.ones(L_S, np.uint8), np.array([1, 0, 1], np.uint8)):
+        logits, hidden = oracle.stack(cfg["x"], layers, prec, lm, True, return_hidden=True)
+        t_hidden, t_logits = torch_stack(cfg["x"], layers, prec, lm, True)
+        for l in range(L_S):
+            assert _close(hidden[l], t_hidden[l]), (prec, l)
+        assert _close(logits, t_logits)
+
+
+def test_stack_mistakes_are_caught(small_stack):
+    """The same comparison fails for a stack without the post-norm, without the
+    residual, or with the pre-norm output left unrounded."""
+    cfg, layers, lm = small_stack
+    prec = np.zeros(L_S, np.uint8)
+    hidden = oracle.stack_hidden(cfg["x"], layers, prec)
+    x = f64(cfg["x"])
+    a = torch_bf16(torch_rms(x))
+    f = torch_bf16_ffn(a, layers[0])
+    no_post = synth.to_bf16_bits(torch_bf16(x + f).numpy().astype(np.float32))
+    no_res = synth.to_bf16_bits(torch_bf16(torch_rms(f)).numpy().astype(np.float32))
+    assert not _close(hidden[0], no_post)
+    assert not _close(hidden[0], no_res)
+
+
+def test_zero_ffn_leaves_the_token_stream_unchanged():
+    """With every FFN weight 0 the FFN output is 0, RMSNorm(0) = 0 (the
+    epsilon keeps the root positive) and the residual returns x bit for bit."""
+    cfg = synth.stack_config(m=3, n_layers=2, d=64, f=128, vocab=16)
+    z = [dict(w_gate=np.zeros_like(L["w_gate"]), w_up=np.zeros_like(L["w_up"]),
+              w_down=np.zeros_like(L["w_down"])) for L in cfg["layers"]]
+    hidden = oracle.stack_hidden(cfg["x"], z, np.zeros(2, np.uint8))
+    for h in hidden:
+        np.testing.assert_array_equal(h, cfg["x"])
+
+
+def test_each_layer_adds_a_unit_rms_update(small_stack):
+    """Post-norm with unit gain: x_{l+1} - x_l = bf16(RMSNorm(f)) up to the
+    rounding of the add, so every row of the update has RMS 1 within bf16
+    accuracy."""
+    cfg, layers, lm = small_stack
+    prec = np.array([1, 0, 1], np.uint8)
+    hidden = oracle.stack_hidden(cfg["x"], layers, prec)
+    prev = oracle.bf16_to_f32(cfg["x"]).astype(np.float64)
+    for h in hidden:
+        cur = oracle.bf16_to_f32(h).astype(np.float64)
+        upd = cur - prev
+        rms = np.sqrt((upd ** 2).mean(1))
+        # each add rounds to bf16 relative to |x_{l+1}|: at most 2^-9 |x| per element
+        slack = np.sqrt(((2.0 ** -8 * np.abs(cur)) ** 2).mean(1))
+        assert np.all(np.abs(rms - 1.0) <= 2.0 ** -7 + slack)
+        prev = cur
