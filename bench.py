@@ -103,17 +103,16 @@ def main():
     for l, L in enumerate(w_layers):
         w8a8.rmsnorm(xc, out=a)
         a_amax = w8a8.col_absmax(a)
-        w_amax = w8a8.col_absmax(L["w_up"], w8a8.col_absmax(L["w_gate"]))
-        d_gu = w8a8.smooth_calibrate(a_amax, w_amax)
+        d_gu = w8a8.smooth_calibrate(a_amax, [L["w_gate"], L["w_up"]])
         h = w8a8.bf16_ffn_gate_up(bf16_layers[l], a)
-        d_dn = w8a8.smooth_calibrate(w8a8.col_absmax(h), w8a8.col_absmax(L["w_down"]))
+        d_dn = w8a8.smooth_calibrate(w8a8.col_absmax(h), [L["w_down"]])
         int8_layers.append(w8a8.FfnW8A8.from_weights(L["w_gate"], L["w_up"], L["w_down"], d_gu, d_dn))
         if not args.no_extras:   # the FP8 (E4M3) variant, same smoothing factors
             fp8_layers.append(w8a8.fp8_ffn_layer(L["w_gate"], L["w_up"], L["w_down"], d_gu, d_dn))
         w8a8.bf16_ffn(bf16_layers[l], a, out=fo, ws=ws_cal)
         w8a8.rmsnorm_residual(xc, fo, out=xc)
     w8a8.rmsnorm(xc, out=a)
-    d_lm = w8a8.smooth_calibrate(w8a8.col_absmax(a), w8a8.col_absmax(w_lm))
+    d_lm = w8a8.smooth_calibrate(w8a8.col_absmax(a), [w_lm])
     lm_int8 = w8a8.LinearW8A8.from_weight(w_lm, d_lm)
     lm_fp8 = None if args.no_extras else w8a8.fp8_linear_layer(w_lm, d_lm)
     lm_bf16 = w8a8.pack_bf16(w_lm)
@@ -373,11 +372,9 @@ def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all
     xo_all = torch.from_numpy(synth.to_bf16_bits(synth.activations(
         5007, 256, NQ, synth.outlier_channels(5009, NQ, synth.n_outliers_1pct(NQ)), 30.0))
         .view(np.int16)).view(torch.bfloat16).to(dev)
-    qkv8 = [w8a8.LinearW8A8.from_weight(wq_, w8a8.smooth_calibrate(w8a8.col_absmax(xa_all),
-                                                                   w8a8.col_absmax(wq_)))
+    qkv8 = [w8a8.LinearW8A8.from_weight(wq_, w8a8.smooth_calibrate(w8a8.col_absmax(xa_all), [wq_]))
             for wq_, _ in att]
-    o8 = [w8a8.LinearW8A8.from_weight(wo_, w8a8.smooth_calibrate(w8a8.col_absmax(xo_all),
-                                                                 w8a8.col_absmax(wo_)))
+    o8 = [w8a8.LinearW8A8.from_weight(wo_, w8a8.smooth_calibrate(w8a8.col_absmax(xo_all), [wo_]))
           for _, wo_ in att]
     qkv16 = [w8a8.pack_bf16(wq_) for wq_, _ in att]
     o16 = [w8a8.pack_bf16(wo_) for _, wo_ in att]

@@ -62,7 +62,8 @@ typedef enum {
     W8A8_EINVAL = 1,
     W8A8_EUNSUPPORTED = 2,
     W8A8_EHIP = 3,
-    W8A8_EWORKSPACE = 4
+    W8A8_EWORKSPACE = 4,
+    W8A8_ETIMEOUT = 5   /* w8a8_ffn_stack_status only: a persistent launch gave up */
 } w8a8_status;
 
 typedef enum { W8A8_F32 = 0, W8A8_BF16 = 1 } w8a8_dtype;
@@ -134,13 +135,30 @@ size_t w8a8_stack_workspace_bytes(int64_t m, int64_t d, int64_t f, int64_t vocab
 w8a8_status w8a8_col_absmax(const void* x, w8a8_dtype x_dtype, int64_t rows, int64_t k,
                             float* amax, w8a8_stream_t stream);
 
-/* SmoothQuant factor (Sec. 4 eq. delta-attn, Sec. 6 eq. delta-lmhead):
-   delta[j] = a_j^alpha / w_j^(1 - alpha) with a_j = max(act_amax[j], 1e-5) and
-   w_j = max(w_amax[j], 1e-5), evaluated in binary64 and rounded once to float
-   (square roots at alpha = 0.5).  All three arrays are device float[k].
-   EUNSUPPORTED if alpha is outside [0, 1]. */
-w8a8_status w8a8_smooth_calibrate(const float* act_amax, const float* w_amax, int64_t k,
+/* SmoothQuant factor from the weights (Sec. 4 eq. delta-attn, Sec. 6 eq.
+   delta-lmhead): delta[j] = a_j^alpha / w_j^(1 - alpha), where
+   a_j = max(act_amax[j], 1e-5) is the calibration activation statistic (from
+   w8a8_col_absmax over the calibration tokens) and w_j = max(max_i |W_ij|, 1e-5)
+   runs over the stacked rows of EVERY matrix that consumes this input (gate and
+   up for the FFN input; Wq, Wk and Wv for the attention input; the lm_head
+   alone for its input).  Evaluated in binary64 and rounded once to float
+   (square roots at alpha = 0.5).
+   w: HOST array of n_w DEVICE pointers, matrix i row-major n_rows[i] x k of
+   w_dtype (f32 or bf16); n_rows: HOST int64_t[n_w]; act_amax, delta: device
+   float[k] (delta is written; it also serves as the scratch of the weight
+   maximum, so it must not alias act_amax).  EUNSUPPORTED if alpha is outside
+   [0, 1] or w_dtype is neither f32 nor bf16. */
+w8a8_status w8a8_smooth_calibrate(const float* act_amax, const void* const* w,
+                                  const int64_t* n_rows, int n_w, w8a8_dtype w_dtype, int64_t k,
                                   float alpha, float* delta, w8a8_stream_t stream);
+
+/* The same factor from both statistics already gathered:
+   delta[j] = max(act_amax[j], 1e-5)^alpha / max(w_amax[j], 1e-5)^(1 - alpha),
+   with w_amax the running w8a8_col_absmax over every consumer's rows.  All three
+   arrays are device float[k]; delta may alias w_amax.  EUNSUPPORTED if alpha is
+   outside [0, 1]. */
+w8a8_status w8a8_smooth_delta(const float* act_amax, const float* w_amax, int64_t k,
+                              float alpha, float* delta, w8a8_stream_t stream);
 
 /* ---------------------------------------------------------------- a2: weights */
 
@@ -198,6 +216,19 @@ w8a8_status w8a8_linear(const w8a8_linear_desc* desc, const void* x, w8a8_dtype 
    qx: packed m x d codes, s_x: float[m], h: bf16 m x f row-major. */
 w8a8_status w8a8_ffn_gate_up(const w8a8_ffn_desc* desc, const void* qx, const float* s_x,
                              int64_t m, void* h, w8a8_stream_t stream);
+
+/* The stage between the FFN projections (Sec. 3, between Tab. 1 fused_fc and
+   proj) from dequantised sums given in memory: h = bf16(gelu_tanh(g) * u) with
+   the binary32 arithmetic of the gate/up epilogue above, then h / delta per
+   token quantised as w8a8_quantize_act does (the requantisation of the down
+   projection's input).  g, u: binary32 m x n row-major (n % 16 == 0); delta:
+   float[n] or NULL; q: w8a8_packed_bytes(m, n) bytes, fragment layout (zero
+   padded); s: float[m]; h: bf16 m x n row-major, written when not NULL (the
+   stage's intermediate, for checks).  The production FFN computes the same h
+   inside its gate/up GEMM and never stores g or u. */
+w8a8_status w8a8_geglu_requant(const float* g, const float* u, int64_t m, int64_t n,
+                               const float* delta, void* q, float* s, void* h,
+                               w8a8_stream_t stream);
 
 /* Whole INT8 FFN block (Sec. 3, Tab. 1 fused_fc + proj): quantise x / delta_gu,
    gate/up + GeGLU (above), requantise h / delta_down per token, down INT8 GEMM,
@@ -326,12 +357,20 @@ int w8a8_precision_map(const char* name, uint8_t* prec, int n_layers);
    identical to the per-layer launches.  It relies on all its workgroups being
    resident at once: the library checks that one fits per compute unit, and
    a barrier that is not reached within about a second (for instance because
-   other work keeps compute units busy that long) ends the launch and leaves
-   NaN in the token stream: the bf16 lm_head's logits are then NaN, the INT8
-   lm_head's all zero (its absmax skips NaN and the row quantises to zeros). */
+   other work keeps compute units busy that long) ends the launch, leaves NaN
+   in the token stream (so the logits, bf16 or INT8 lm_head, are NaN) and
+   records the failure in the workspace, where w8a8_ffn_stack_status finds it.
+   The call itself returns before the launch runs and cannot report it. */
 w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec,
                            int lm_head_int8, const void* x, int64_t m, void* logits,
                            void* ws, size_t ws_bytes, w8a8_stream_t stream);
+
+/* Outcome of the last w8a8_ffn_stack / w8a8_ffn_stack_trace call enqueued on
+   the workspace ws (every such call clears the record first): synchronises
+   `stream`, then returns W8A8_OK, or W8A8_ETIMEOUT when a device-wide wait of
+   the persistent decode kernel gave up in that call (its token stream and
+   logits are then NaN).  ws, ws_bytes: the workspace that call used. */
+w8a8_status w8a8_ffn_stack_status(const void* ws, size_t ws_bytes, w8a8_stream_t stream);
 
 /* ---------------------------------------------------------------- sensitivity and map selection */
 
@@ -391,6 +430,21 @@ int w8a8_rank_layers(const float* isolated_db, int n_layers, int* order);
 w8a8_status w8a8_select_precision_map(const w8a8_stack_desc* desc, const void* x, int64_t m,
                                       float budget_db, uint8_t* prec, float* final_db,
                                       void* ws, size_t ws_bytes, w8a8_stream_t stream);
+
+/* ---------------------------------------------------------------- planner overrides */
+
+/* The GEMM planner picks tile shapes, K splits, streaming plans and the decode
+   fusions by shape alone; the library never reads the environment.  For
+   experiments and for the tests that check every plan gives the same results,
+   these process-wide overrides replace a choice: "GLU_TILE", "GEMM_TILE",
+   "GEMM_SPLITS", "DOWN_TILE", "DOWN_SPLITS", "DOWN_WK", "WIDE_NW", "WIDE_WGS",
+   "STREAM_WK", "STREAM_SPLITS", "GROUP_M", "ROTATE", "NO_QLOAD",
+   "NO_FUSED_GLUE", "NO_PERSISTENT", "DEC_SPIN_LIMIT".  Returns 0, or -1 for an
+   unknown name.  Not for production use: an override applies to every later
+   call in the process, and changing one while another thread calls the library
+   races with it. */
+int w8a8_set_plan_override(const char* name, int value);
+void w8a8_clear_plan_overrides(void);
 
 /* ---------------------------------------------------------------- errors */
 

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
+#include <climits>
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
@@ -50,9 +52,33 @@ struct Plan {
   int nbpb = 1;         // streaming: column blocks per workgroup
 };
 
-int env_int(const char* name, int dflt) {
-  const char* v = std::getenv(name);
-  return v && *v ? std::atoi(v) : dflt;
+// Planner overrides (w8a8_set_plan_override): experiments and the tests that
+// check that every plan gives the same results set them explicitly; the
+// library never reads the environment.  Unset entries hold kUnset.
+constexpr int kUnset = INT32_MIN;
+const char* const kOverrideNames[] = {
+    "GLU_TILE", "GEMM_TILE", "GEMM_SPLITS", "DOWN_TILE", "DOWN_SPLITS", "DOWN_WK",
+    "WIDE_NW", "WIDE_WGS", "STREAM_WK", "STREAM_SPLITS", "GROUP_M", "ROTATE",
+    "NO_QLOAD", "NO_FUSED_GLUE", "NO_PERSISTENT", "DEC_SPIN_LIMIT"};
+constexpr int kNumOverrides = (int)(sizeof(kOverrideNames) / sizeof(kOverrideNames[0]));
+std::atomic<int> g_override[kNumOverrides];
+struct OverrideInit {
+  OverrideInit() {
+    for (auto& o : g_override) o.store(kUnset);
+  }
+} g_override_init;
+
+int override_index(const char* name) {
+  for (int i = 0; i < kNumOverrides; ++i)
+    if (std::strcmp(name, kOverrideNames[i]) == 0) return i;
+  return -1;
+}
+
+// The override named `name` (one of kOverrideNames), else dflt.
+int plan_override(const char* name, int dflt) {
+  const int i = override_index(name);
+  const int v = i < 0 ? kUnset : g_override[i].load(std::memory_order_relaxed);
+  return v == kUnset ? dflt : v;
 }
 
 void tile_shape(int tile, int* bm, int* bn) {
@@ -108,10 +134,10 @@ bool plan_stream(Plan& p, int64_t m, int64_t n, int64_t kb, bool glu, bool f8) {
   if (nbc >= 1024) {  // wide output (lm_head): every wave owns its column blocks
     if (p.mb * kb > 144) return false;
     p.wk = 1;
-    p.nw = env_int("W8A8_WIDE_NW", 4);
+    p.nw = plan_override("WIDE_NW", 4);
     p.splits = 1;
     p.kchunk = (int)kb;
-    const int64_t wgs = env_int("W8A8_WIDE_WGS", p.mb == 1 ? 1024 : 512);
+    const int64_t wgs = plan_override("WIDE_WGS", p.mb == 1 ? 1024 : 512);
     p.nbpb = p.nw == 1 ? (int)std::max<int64_t>(1, ceil_div(nbc, wgs))
                        : (int)round_up(std::max<int64_t>(4, ceil_div(nbc, wgs)), 4);
     return true;
@@ -121,8 +147,8 @@ bool plan_stream(Plan& p, int64_t m, int64_t n, int64_t kb, bool glu, bool f8) {
   // those that keep >= 768 waves busy
   bool found = false;
   int64_t best_pw = -1, best_waves = -1;
-  const int force_wk = env_int("W8A8_STREAM_WK", 0);
-  const int64_t min_splits = env_int("W8A8_STREAM_SPLITS", 1);
+  const int force_wk = plan_override("STREAM_WK", 0);
+  const int64_t min_splits = plan_override("STREAM_SPLITS", 1);
   for (int wk : {16, 4, 2}) {
     if (wk == 16 && p.mb > 1) continue;  // 16-wave workgroups only for MB = 1
     if (force_wk && wk != force_wk) continue;
@@ -180,7 +206,7 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
                                                                        : TILE_GLU_64x64_K2);
     else
       p.tile = tiles_of(TILE_128x128_K2, m, n) >= 256 ? TILE_128x128_K2 : TILE_64x64_K2;
-    const int want = glu ? env_int("W8A8_GLU_TILE", p.tile) : env_int("W8A8_GEMM_TILE", p.tile);
+    const int want = glu ? plan_override("GLU_TILE", p.tile) : plan_override("GEMM_TILE", p.tile);
     if (glu ? (want == TILE_GLU_128x32_K2 || want == TILE_GLU_64x64_K2 ||
                want == TILE_GLU_256x64_K2_W8)
             : (want == TILE_64x64_K2 || want == TILE_128x128_K2))
@@ -189,7 +215,7 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
     int64_t splits = 1;
     if (!glu && tiles < 200)
       splits = std::min<int64_t>(ceil_div(256, tiles), std::max<int64_t>(1, kb / 8));
-    splits = env_int("W8A8_GEMM_SPLITS", (int)splits);
+    splits = plan_override("GEMM_SPLITS", (int)splits);
     if (glu || splits < 1) splits = 1;
     p.kchunk = (int)round_up(ceil_div(kb, splits), 2);
     p.splits = (int)ceil_div(kb, p.kchunk);
@@ -231,7 +257,7 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
           // two-column stage is faster when K allows it
       p.tile = (i8 && kb % 2 == 0) ? TILE_64x64_K2 : TILE_64x64;
   }
-  p.tile = glu ? env_int("W8A8_GLU_TILE", p.tile) : env_int("W8A8_GEMM_TILE", p.tile);
+  p.tile = glu ? plan_override("GLU_TILE", p.tile) : plan_override("GEMM_TILE", p.tile);
   const int64_t tiles = tiles_of(p.tile, m, n);
   int splits = 1;
   if (long_k)
@@ -240,7 +266,7 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
   else if (!glu && tiles < 200)  // int8: at least 16 fragments per split (a split of a
                                  // 1152-deep K costs more than the parallelism it adds)
     splits = (int)std::min<int64_t>(ceil_div(256, tiles), std::max<int64_t>(1, kb / (i8 ? 16 : 4)));
-  splits = env_int("W8A8_GEMM_SPLITS", splits);
+  splits = plan_override("GEMM_SPLITS", splits);
   if (glu || splits < 1) splits = 1;
   p.kchunk = (int)ceil_div(kb, splits);
   p.splits = (int)ceil_div(kb, p.kchunk);
@@ -274,7 +300,7 @@ struct QLoad {
 // Streaming int8 / E4M3 plans over at most 16 rows quantise their bf16 input
 // themselves; every other plan reads codes produced by quant_rows_kernel.
 bool plan_qloads(const Plan& pl, int64_t m, int64_t k) {
-  if (env_int("W8A8_NO_QLOAD", 0) || (pl.dt != DT_I8 && pl.dt != DT_F8)) return false;
+  if (plan_override("NO_QLOAD", 0) || (pl.dt != DT_I8 && pl.dt != DT_F8)) return false;
   return pl.stream && pl.mb == 1 && m * (k / 16) <= qload_capacity(pl.nw);
 }
 
@@ -320,8 +346,8 @@ w8a8_status run_gemm(const Plan& pl, int dt, int epi, const void* A, int64_t lda
   p.out = out;
   p.ldo = ldo;
   p.part = pl.splits > 1 ? gemm_ws : nullptr;
-  p.group_m = env_int("W8A8_GROUP_M", 0);
-  p.rotate = env_int("W8A8_ROTATE", 1);
+  p.group_m = plan_override("GROUP_M", 0);
+  p.rotate = plan_override("ROTATE", 1);
   hipError_t e = pl.stream ? launch_gemm_stream(dt, epi, pl.mb, pl.nw, pl.wk, p, pl.nbpb, st)
                            : launch_gemm_tile(dt, epi, pl.tile, p, st);
   w8a8_status s = hip_check(e, pl.stream ? "gemm_stream" : "gemm_tile");
@@ -363,8 +389,8 @@ w8a8_status run_gemm_raw(const Plan& pl, int dt, const void* A, int64_t lda, int
   p.out = part;
   p.ldo = n;
   p.part = pl.splits > 1 ? part : nullptr;
-  p.group_m = env_int("W8A8_GROUP_M", 0);
-  p.rotate = env_int("W8A8_ROTATE", 1);
+  p.group_m = plan_override("GROUP_M", 0);
+  p.rotate = plan_override("ROTATE", 1);
   const int epi = dt == DT_BF16 ? EPI_F32 : EPI_I32;  // raw sums (fp32 for float types)
   hipError_t e = pl.stream ? launch_gemm_stream(dt, epi, pl.mb, pl.nw, pl.wk, p, pl.nbpb, st)
                            : launch_gemm_tile(dt, epi, pl.tile, p, st);
@@ -477,9 +503,9 @@ Plan stack_down_plan(int64_t m, int64_t d, int64_t f) {
     // and 72 busy CUs would cap the projection near 1.8 TB/s (measured best:
     // 2 splits of 16 waves; 4 splits leave too little work per wave).
     const int64_t kb = ceil_div(f, kFragK8), nbc = ceil_div(d, 16);
-    const int splits = env_int("W8A8_DOWN_SPLITS", (int)std::min<int64_t>(
+    const int splits = plan_override("DOWN_SPLITS", (int)std::min<int64_t>(
                                                        std::max<int64_t>(1, kb / 16), ceil_div(144, nbc)));
-    const int wk = env_int("W8A8_DOWN_WK", p.wk);
+    const int wk = plan_override("DOWN_WK", p.wk);
     if (splits > p.splits && (wk == 16 || wk == 4 || wk == 2) && !(wk == 16 && p.mb > 1)) {
       Plan q = p;
       q.nw = q.wk = wk;
@@ -501,9 +527,9 @@ Plan stack_down_plan(int64_t m, int64_t d, int64_t f) {
     p.tile = TILE_128x128;
     dflt_splits = 3;
   }
-  p.tile = env_int("W8A8_DOWN_TILE", p.tile);
+  p.tile = plan_override("DOWN_TILE", p.tile);
   const int64_t kb = ceil_div(f, kFragK8);
-  const int splits = std::max(1, env_int("W8A8_DOWN_SPLITS", dflt_splits));
+  const int splits = std::max(1, plan_override("DOWN_SPLITS", dflt_splits));
   p.kchunk = (int)ceil_div(kb, splits);
   p.splits = (int)ceil_div(kb, p.kchunk);
   return p;
@@ -520,7 +546,10 @@ StackWs stack_ws(int64_t m, int64_t d, int64_t f, int64_t vocab) {
   const size_t part = (size_t)planes * m * d * 4;
   const size_t lm = std::max(plan_ws_bytes(plan_gemm(m, vocab, d, DT_I8, false), m, vocab),
                              bf16_linear_ws(m, vocab, d));
-  w.x = 0;
+  // the persistent decode kernel's barrier counters and status first: the
+  // status query finds them at the start of the workspace
+  w.ctl = 0;
+  w.x = align256(sizeof(DecCtl));
   w.x2 = w.x + align256((size_t)m * d * 2);  // the token stream alternates between x and x2
   w.a = w.x2 + align256((size_t)m * d * 2);
   w.q = w.a + align256((size_t)m * d * 2);
@@ -530,9 +559,8 @@ StackWs stack_ws(int64_t m, int64_t d, int64_t f, int64_t vocab) {
   w.sh = w.qh + align256(w8a8_packed_bytes(m, f));
   w.part = w.sh + align256((size_t)m * 4);
   w.lm = w.part + align256(part);
-  // the persistent decode kernel's barrier counters and per-layer buffers
-  w.ctl = w.lm + align256(lm);
-  w.dec = w.ctl + align256(sizeof(DecCtl));
+  // the persistent decode kernel's per-layer buffers
+  w.dec = w.lm + align256(lm);
   const size_t dec = m == 1 ? (size_t)kDecMaxLayers * decode_layout(d, f, kGlueMaxSplits).layer_bytes : 0;
   w.total = w.dec + align256(dec);
   return w;
@@ -659,11 +687,24 @@ const char* w8a8_status_str(w8a8_status s) {
     case W8A8_EUNSUPPORTED: return "unsupported shape or dtype";
     case W8A8_EHIP: return "HIP error";
     case W8A8_EWORKSPACE: return "workspace too small";
+    case W8A8_ETIMEOUT: return "a device-wide wait of the persistent decode kernel gave up";
   }
   return "unknown status";
 }
 
 const char* w8a8_last_error(void) { return g_last_error.c_str(); }
+
+int w8a8_set_plan_override(const char* name, int value) {
+  if (!name) return -1;
+  const int i = override_index(name);
+  if (i < 0 || value == kUnset) return -1;
+  g_override[i].store(value);
+  return 0;
+}
+
+void w8a8_clear_plan_overrides(void) {
+  for (auto& o : g_override) o.store(kUnset);
+}
 
 // ---------------------------------------------------------------- a1
 
@@ -677,8 +718,8 @@ w8a8_status w8a8_col_absmax(const void* x, w8a8_dtype xt, int64_t rows, int64_t 
   return hip_check(launch_col_absmax(x, xt == W8A8_BF16, rows, k, amax, S(stream)), "col_absmax");
 }
 
-w8a8_status w8a8_smooth_calibrate(const float* act_amax, const float* w_amax, int64_t k,
-                                  float alpha, float* delta, w8a8_stream_t stream) {
+w8a8_status w8a8_smooth_delta(const float* act_amax, const float* w_amax, int64_t k,
+                              float alpha, float* delta, w8a8_stream_t stream) {
   g_last_error.clear();
   CHECK_PTR(act_amax);
   CHECK_PTR(w_amax);
@@ -686,6 +727,32 @@ w8a8_status w8a8_smooth_calibrate(const float* act_amax, const float* w_amax, in
   REQUIRE(k >= 1, W8A8_EINVAL, "k < 1");
   REQUIRE(alpha >= 0.0f && alpha <= 1.0f, W8A8_EUNSUPPORTED, "alpha outside [0, 1]");
   return hip_check(launch_smooth_delta(act_amax, w_amax, k, (double)alpha, delta, S(stream)),
+                   "smooth_delta");
+}
+
+w8a8_status w8a8_smooth_calibrate(const float* act_amax, const void* const* w,
+                                  const int64_t* n_rows, int n_w, w8a8_dtype w_dtype, int64_t k,
+                                  float alpha, float* delta, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(act_amax);
+  CHECK_PTR(delta);
+  REQUIRE(w != nullptr && n_rows != nullptr, W8A8_EINVAL, "w or n_rows is NULL");
+  REQUIRE(n_w >= 1, W8A8_EINVAL, "n_w < 1");
+  REQUIRE(k >= 1, W8A8_EINVAL, "k < 1");
+  REQUIRE(w_dtype == W8A8_F32 || w_dtype == W8A8_BF16, W8A8_EUNSUPPORTED, "w dtype");
+  REQUIRE(alpha >= 0.0f && alpha <= 1.0f, W8A8_EUNSUPPORTED, "alpha outside [0, 1]");
+  for (int i = 0; i < n_w; ++i) {
+    CHECK(check_ptr(w[i], "w[i]"));
+    REQUIRE(n_rows[i] >= 1, W8A8_EINVAL, "n_rows[i] < 1");
+  }
+  // delta holds the running weight maximum max_i |W_ij| over the stacked rows
+  // of every consumer, then the factor itself (elementwise, in place)
+  hipStream_t st = S(stream);
+  CHECK(hip_check(launch_fill_f32(delta, k, 0.0f, st), "fill"));
+  for (int i = 0; i < n_w; ++i)
+    CHECK(hip_check(launch_col_absmax(w[i], w_dtype == W8A8_BF16, n_rows[i], k, delta, st),
+                    "col_absmax"));
+  return hip_check(launch_smooth_delta(act_amax, delta, k, (double)alpha, delta, st),
                    "smooth_delta");
 }
 
@@ -805,6 +872,25 @@ w8a8_status w8a8_ffn_gate_up(const w8a8_ffn_desc* desc, const void* qx, const fl
   Plan pg = plan_gemm(m, desc->f, desc->d, DT_I8, true);
   return run_gemm(pg, DT_I8, EPI_GLU, qx, 0, m, desc->wq_gate, desc->wq_up, desc->f, desc->d, s_x,
                   desc->s_gate, desc->s_up, h, desc->f, nullptr, S(stream));
+}
+
+w8a8_status w8a8_geglu_requant(const float* g, const float* u, int64_t m, int64_t n,
+                               const float* delta, void* q, float* s, void* h,
+                               w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(g);
+  CHECK_PTR(u);
+  CHECK_PTR(q);
+  CHECK_PTR(s);
+  if (delta) CHECK_PTR(delta);
+  if (h) CHECK_PTR(h);
+  REQUIRE(m >= 1 && n >= 1, W8A8_EINVAL, "m or n < 1");
+  REQUIRE(n % 16 == 0, W8A8_EUNSUPPORTED, "n must be a multiple of 16");
+  CHECK(check_k(n));
+  REQUIRE(m <= INT32_MAX, W8A8_EUNSUPPORTED, "m too large");
+  return hip_check(launch_geglu_requant(g, u, m, n, delta, (int8_t*)q, s, (uint16_t*)h,
+                                        S(stream)),
+                   "geglu_requant");
 }
 
 w8a8_status w8a8_ffn(const w8a8_ffn_desc* desc, const void* x, int64_t m, void* y, void* ws,
@@ -1125,12 +1211,14 @@ w8a8_status stack_run(const w8a8_stack_desc* desc, const uint8_t* prec, int lm_h
   void* part = base + w.part;
   const Plan p8 = stack_down_plan(m, d, f), p16 = plan_gemm(m, d, f, DT_BF16, false);
   const Plan pg8 = plan_gemm(m, f, d, DT_I8, true), pg16 = plan_gemm(m, f, d, DT_BF16, true);
+  // every call starts with a clear failure word (w8a8_ffn_stack_status)
+  CHECK(hip_check(launch_dec_status_clear((DecCtl*)(base + w.ctl), st), "status clear"));
 
   // At one token, runs of consecutive INT8 layers go to the persistent decode
   // kernel (one launch per run of up to kDecMaxLayers layers) when the device
   // holds one of its workgroups per CU and the shape fits it.
   int dec_grid = 0, dec_splits = 0;
-  if (m == 1 && !env_int("W8A8_NO_PERSISTENT", 0)) {
+  if (m == 1 && !plan_override("NO_PERSISTENT", 0)) {
     int dev = 0;
     CHECK(hip_check(hipGetDevice(&dev), "hipGetDevice"));
     dec_grid = decode_grid(dev);
@@ -1181,7 +1269,7 @@ w8a8_status stack_run(const w8a8_stack_desc* desc, const uint8_t* prec, int lm_h
   // gate/up GEMM (every workgroup computes it for the row while its weights
   // arrive; workgroup 0 writes the token stream), one launch and one memory
   // round trip less per layer.
-  const bool fuse_ok = m == 1 && !env_int("W8A8_NO_FUSED_GLUE", 0) && pg8.stream &&
+  const bool fuse_ok = m == 1 && !plan_override("NO_FUSED_GLUE", 0) && pg8.stream &&
                        pg8.mb == 1 && d % 8 == 0 && d / 8 <= 64 * pg8.nw;
   auto fused = [&](int64_t l) {
     if (!fuse_ok || !prec[l]) return false;
@@ -1221,7 +1309,7 @@ w8a8_status stack_run(const w8a8_stack_desc* desc, const uint8_t* prec, int lm_h
       P.layout = decode_layout(d, f, dec_splits);
       P.splits = dec_splits;
       P.ctl = (DecCtl*)(base + w.ctl);
-      P.spin_limit = env_int("W8A8_DEC_SPIN_LIMIT", P.spin_limit);  // failure-path tests
+      P.spin_limit = plan_override("DEC_SPIN_LIMIT", P.spin_limit);  // failure-path tests
       CHECK(hip_check(launch_decode_ffn(P, dec_grid, st), "decode_ffn"));
       xin = xbuf[nxt];  // the token stream after layer l1 - 2
       nxt ^= 1;
@@ -1280,7 +1368,7 @@ w8a8_status stack_run(const w8a8_stack_desc* desc, const uint8_t* prec, int lm_h
     // streaming GEMM, as the layer glue does inside a gate/up GEMM: every
     // workgroup computes it for the row while its first weights arrive.
     const Plan pl = plan_gemm(m, V, d, DT_I8, false);
-    const bool fuse_lm = m == 1 && !env_int("W8A8_NO_FUSED_GLUE", 0) && pl.stream &&
+    const bool fuse_lm = m == 1 && !plan_override("NO_FUSED_GLUE", 0) && pl.stream &&
                          pl.mb == 1 && pl.splits == 1 && d % 8 == 0 && d / 8 <= 64 * pl.nw &&
                          (nl == 0 || splits_of(nl - 1) <= kGlueMaxSplits);
     if (fuse_lm) {
@@ -1389,6 +1477,21 @@ w8a8_status w8a8_ffn_stack(const w8a8_stack_desc* desc, const uint8_t* prec, int
   REQUIRE(ws_bytes >= w8a8_stack_workspace_bytes(m, desc->d, desc->f, desc->vocab),
           W8A8_EWORKSPACE, "workspace too small");
   return stack_run(desc, prec, lm_head_int8, x, m, logits, nullptr, ws, S(stream));
+}
+
+w8a8_status w8a8_ffn_stack_status(const void* ws, size_t ws_bytes, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(ws);
+  REQUIRE(ws_bytes >= sizeof(DecCtl), W8A8_EWORKSPACE, "workspace smaller than its status block");
+  unsigned word = 0;
+  const DecCtl* ctl = (const DecCtl*)ws;  // at the start of the stack workspace
+  CHECK(hip_check(hipStreamSynchronize(S(stream)), "hipStreamSynchronize"));
+  CHECK(hip_check(hipMemcpy(&word, &ctl->fail[0], sizeof(word), hipMemcpyDeviceToHost),
+                  "hipMemcpy"));
+  if (word != 0)
+    return fail(W8A8_ETIMEOUT, "the persistent decode kernel gave up waiting at a grid barrier; "
+                               "that call's token stream and logits are NaN");
+  return W8A8_OK;
 }
 
 w8a8_status w8a8_ffn_stack_trace(const w8a8_stack_desc* desc, const uint8_t* prec,

@@ -63,6 +63,10 @@ __global__ void dec_clear_kernel(DecCtl* ctl) {
   }
 }
 
+__global__ void dec_status_clear_kernel(DecCtl* ctl) {
+  if (threadIdx.x == 0) ctl->fail[0] = 0u;
+}
+
 // Arrival at barrier k (1, 2, ...): every wave waits until its own stores are
 // complete, then one thread adds one to the group counter; the group's last
 // arrival (the counter reaching k times the group size) adds one to the top.
@@ -93,6 +97,7 @@ __device__ __forceinline__ bool grid_wait(DecCtl* ctl, unsigned k, int spin_limi
       if (it >= spin_limit ||
           __hip_atomic_load(&ctl->err[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u) {
         __hip_atomic_store(&ctl->err[0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&ctl->fail[0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         ok = 0;
         break;
       }
@@ -465,6 +470,11 @@ hipError_t launch_decode_ffn(const DecParams& P, int grid, hipStream_t st) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   decode_ffn_kernel<<<grid, kDecThreads, 0, st>>>(P);
+  return hipGetLastError();
+}
+
+hipError_t launch_dec_status_clear(DecCtl* ctl, hipStream_t st) {
+  dec_status_clear_kernel<<<1, 64, 0, st>>>(ctl);
   return hipGetLastError();
 }
 

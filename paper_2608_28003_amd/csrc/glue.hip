@@ -241,7 +241,10 @@ __global__ __launch_bounds__(NT) void glue_kernel(GlueParams g) {
     }
   }
   amax = block_max_in(amax, red_q);
-  const float sr = amax / 127.0f;
+  // a NaN in the row (a failed persistent decode run poisons the token
+  // stream) reaches the norm's sum of squares; the max above would skip it,
+  // so the scale takes the NaN and everything dequantised from it is NaN
+  const float sr = ss == ss ? amax / 127.0f : ss;
   if (t == 0) g.s[r] = sr;
   const float sinv = 1.0f / sr;
   const bool fast = isfinite(sinv);

@@ -92,11 +92,18 @@ enum TileCfg {
 
 hipError_t launch_col_absmax(const void* x, bool bf16, int64_t rows, int64_t k, float* amax,
                              hipStream_t st);
+// p[0 .. n) = v (a kernel, not a memset: callers may capture it in a graph)
+hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t st);
 hipError_t launch_smooth_delta(const float* a, const float* w, int64_t k, double alpha,
                                float* delta, hipStream_t st);
 hipError_t launch_quant_rows(const void* x, bool bf16, bool mul, int64_t rows, int64_t k,
                              const float* delta, int8_t* qpacked, float* s, hipStream_t st,
                              bool f8 = false);
+// h = bf16(gelu_tanh(g) * u) of binary32 m x n rows g, u (h written if set),
+// then the per-row quantisation of h / delta as launch_quant_rows.
+hipError_t launch_geglu_requant(const float* g, const float* u, int64_t m, int64_t n,
+                                const float* delta, int8_t* qpacked, float* s, uint16_t* h,
+                                hipStream_t st);
 hipError_t launch_unpack(const void* qp, int64_t n, int64_t k, int8_t* q, hipStream_t st);
 hipError_t launch_pack_bf16(const void* w, int64_t n, int64_t k, void* wp, hipStream_t st);
 
@@ -145,10 +152,13 @@ constexpr int kDecMaxLayers = 32;  // layers per launch
 constexpr int kDecMaxFrags = 10;   // weight fragments a wave holds per phase
 constexpr int kDecMaxPanel = 64;   // activation fragments staged in LDS
 constexpr int kDecGroups = 4;      // barrier arrival groups (one counter each)
-struct DecCtl {                    // cleared before every launch; 256-byte lines
-  unsigned top[64];                // group completions (word 0)
-  unsigned grp[kDecGroups][64];    // arrivals per group (word 0)
-  unsigned err[64];                // word 0 nonzero: a wait gave up; the outputs are NaN
+struct DecCtl {                    // 256-byte lines
+  unsigned top[64];                // group completions (word 0)     } cleared before
+  unsigned grp[kDecGroups][64];    // arrivals per group (word 0)    } every launch
+  unsigned err[64];                // word 0 nonzero: a wait of this launch gave up
+  unsigned fail[64];               // word 0 nonzero: a wait gave up in some launch since
+                                   // the last launch_dec_status_clear (the run's outputs
+                                   // are NaN); read by w8a8_ffn_stack_status
 };
 struct DecLayer {
   const void* wg;      // packed gate weights (f x d)
@@ -203,6 +213,8 @@ int decode_grid(int device);
 // shape does not fit the kernel.
 int decode_splits(int64_t d, int64_t f, int grid);
 hipError_t launch_decode_ffn(const DecParams& P, int grid, hipStream_t st);
+// Clears ctl->fail (start of every stack call).
+hipError_t launch_dec_status_clear(DecCtl* ctl, hipStream_t st);
 
 // SQNR of test against ref over n elements (bf16 or f32): part holds
 // 2 * sqnr_groups(n) doubles of scratch, out receives {sum ref^2,

@@ -129,12 +129,38 @@ __device__ __forceinline__ float block_max(float v) {
   return m;
 }
 
-// Chunk c of CW (16 or 8) consecutive columns of row xr, smoothed.
-template <typename T, bool MUL, int CW>
+// Chunk c of CW (16 or 8) consecutive columns of row xr, smoothed.  GLU: the
+// row's values are the gated activation h = bf16(gelu_tanh(g) * u) of the
+// binary32 rows g (xr) and u (ur) -- the arithmetic of the gate/up GEMM's
+// epilogue on sums given in memory -- and h is also stored to hr (if set).
+template <typename T, bool MUL, int CW, bool GLU = false>
 __device__ __forceinline__ void smooth_chunk(const T* __restrict__ xr,
                                              const float* __restrict__ delta, int64_t c,
-                                             float (&v)[CW]) {
-  load_chunk<T, CW>(xr + c * CW, v);
+                                             float (&v)[CW], const float* __restrict__ ur = nullptr,
+                                             uint16_t* __restrict__ hr = nullptr) {
+  if constexpr (GLU) {
+    static_assert(sizeof(T) == 4, "g and u are binary32");
+    float g[CW], u[CW];
+    load_chunk<float, CW>(reinterpret_cast<const float*>(xr) + c * CW, g);
+    load_chunk<float, CW>(ur + c * CW, u);
+    uint32_t hb[CW / 2];
+#pragma unroll
+    for (int e = 0; e < CW; e += 2) {
+      const uint16_t b0 = float_to_bf16_bits(gelu_tanh(g[e]) * u[e]);
+      const uint16_t b1 = float_to_bf16_bits(gelu_tanh(g[e + 1]) * u[e + 1]);
+      v[e] = bf16_bits_to_float(b0);
+      v[e + 1] = bf16_bits_to_float(b1);
+      hb[e / 2] = (uint32_t)b0 | ((uint32_t)b1 << 16);
+    }
+    if (hr) {
+#pragma unroll
+      for (int i = 0; i < CW / 8; ++i)
+        reinterpret_cast<uint4*>(hr + c * CW)[i] =
+            make_uint4(hb[4 * i], hb[4 * i + 1], hb[4 * i + 2], hb[4 * i + 3]);
+    }
+  } else {
+    load_chunk<T, CW>(xr + c * CW, v);
+  }
   if (delta) {
     float d[CW];
     load_chunk<float, CW>(delta + c * CW, d);
@@ -167,12 +193,16 @@ __device__ __forceinline__ void store_codes(int8_t* __restrict__ q, int64_t r, i
 // written as zeros.  MUL: v = x * delta (weights); else v = x / delta.
 // F8: OCP E4M3 codes instead of int8, s = amax / 448 and code = E4M3(v / s)
 // (binary32 quotient rounded to the nearest E4M3 value, ties to even).
-template <typename T, bool MUL, bool F8, int CW>
+// GLU: the rows are the gated activation of the binary32 rows x (g) and u (see
+// smooth_chunk), written to h_out (if set) as bf16 m x k.
+template <typename T, bool MUL, bool F8, int CW, bool GLU = false>
 __global__ __launch_bounds__(1024) void quant_rows_kernel(const T* __restrict__ x, int64_t rows,
                                                           int64_t k, const float* __restrict__ delta,
                                                           int64_t rows_pad, int64_t kp,
                                                           int8_t* __restrict__ q,
-                                                          float* __restrict__ s) {
+                                                          float* __restrict__ s,
+                                                          const float* __restrict__ u = nullptr,
+                                                          uint16_t* __restrict__ h_out = nullptr) {
   static_assert(CW == 16 || CW == 8, "chunk width");
   const int64_t r = blockIdx.x;
   const int t = threadIdx.x;
@@ -190,16 +220,18 @@ __global__ __launch_bounds__(1024) void quant_rows_kernel(const T* __restrict__ 
   }
 
   const T* xr = x + r * k;
+  const float* ur = GLU ? u + r * k : nullptr;
+  uint16_t* hr = GLU && h_out ? h_out + r * k : nullptr;
   float v[CW];
   float amax = 0.0f;
   if (t < chunks) {
-    smooth_chunk<T, MUL, CW>(xr, delta, t, v);
+    smooth_chunk<T, MUL, CW, GLU>(xr, delta, t, v, ur, hr);
 #pragma unroll
     for (int e = 0; e < CW; ++e) amax = fmaxf(amax, fabsf(v[e]));
   }
   for (int64_t c = t + nt; c < chunks; c += nt) {  // rows longer than CW * blockDim
     float w[CW];
-    smooth_chunk<T, MUL, CW>(xr, delta, c, w);
+    smooth_chunk<T, MUL, CW, GLU>(xr, delta, c, w, ur, hr);
 #pragma unroll
     for (int e = 0; e < CW; ++e) amax = fmaxf(amax, fabsf(w[e]));
   }
@@ -219,7 +251,7 @@ __global__ __launch_bounds__(1024) void quant_rows_kernel(const T* __restrict__ 
 #pragma unroll
         for (int e = 0; e < CW; ++e) w[e] = v[e];
       } else {
-        smooth_chunk<T, MUL, CW>(xr, delta, c, w);
+        smooth_chunk<T, MUL, CW, GLU>(xr, delta, c, w, ur, nullptr);
       }
       if constexpr (F8) {
 #pragma unroll
@@ -286,6 +318,16 @@ hipError_t launch_col_absmax(const void* x, bool bf16, int64_t rows, int64_t k, 
   return hipGetLastError();
 }
 
+__global__ void fill_f32_kernel(float* __restrict__ p, int64_t n, float v) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t st) {
+  fill_f32_kernel<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(p, n, v);
+  return hipGetLastError();
+}
+
 hipError_t launch_smooth_delta(const float* a, const float* w, int64_t k, double alpha,
                                float* delta, hipStream_t st) {
   smooth_delta_kernel<<<(unsigned)((k + 255) / 256), 256, 0, st>>>(a, w, k, alpha, delta);
@@ -339,6 +381,24 @@ hipError_t launch_quant_rows(const void* x, bool bf16, bool mul, int64_t rows, i
       quant_rows_launch<false, 16>(x, bf16, mul, rows, k, delta, rows_pad, kp, qpacked, s, grid,
                                    block, st);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_geglu_requant(const float* g, const float* u, int64_t m, int64_t n,
+                                const float* delta, int8_t* qpacked, float* s, uint16_t* h,
+                                hipStream_t st) {
+  const int64_t rows_pad = (m + 15) / 16 * 16;
+  const int64_t kp = (n + kFragK8 - 1) / kFragK8 * kFragK8;
+  const bool narrow = rows_pad <= 256 && kp / 8 <= 1024;  // as launch_quant_rows
+  int64_t threads = (kp / (narrow ? 8 : 16) + 63) / 64 * 64;
+  if (threads > 1024) threads = 1024;
+  dim3 grid((unsigned)rows_pad), block((unsigned)threads);
+  if (narrow)
+    quant_rows_kernel<float, false, false, 8, true><<<grid, block, 0, st>>>(
+        g, m, n, delta, rows_pad, kp, qpacked, s, u, h);
+  else
+    quant_rows_kernel<float, false, false, 16, true><<<grid, block, 0, st>>>(
+        g, m, n, delta, rows_pad, kp, qpacked, s, u, h);
   return hipGetLastError();
 }
 

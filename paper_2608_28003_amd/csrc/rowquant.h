@@ -310,7 +310,7 @@ __device__ __forceinline__ void glue_panel(const GemmParams& p, int kb0, int kc,
     if (own) amax = fmaxf(amax, fabsf(a[e]));
   }
   amax = block_max_in(amax, red_q);
-  const float sr = amax / 127.0f;
+  const float sr = ss == ss ? amax / 127.0f : ss;  // a NaN in the row: NaN scale
   if (t == 0) {
     s_row[0] = sr;
     if (p.a_s_out && blockIdx.x == 0 && blockIdx.y == 0) p.a_s_out[0] = sr;

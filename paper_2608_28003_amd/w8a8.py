@@ -18,7 +18,7 @@ import torch
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libw8a8.so")
 
-OK, EINVAL, EUNSUPPORTED, EHIP, EWORKSPACE = 0, 1, 2, 3, 4
+OK, EINVAL, EUNSUPPORTED, EHIP, EWORKSPACE, ETIMEOUT = 0, 1, 2, 3, 4, 5
 F32, BF16 = 0, 1
 MAX_K = 133144
 
@@ -65,7 +65,13 @@ _SIGS = {
     "w8a8_bf16_linear_workspace_bytes": (SZ, [I64, I64, I64]),
     "w8a8_stack_workspace_bytes": (SZ, [I64, I64, I64, I64]),
     "w8a8_col_absmax": (INT, [P, INT, I64, I64, P, P]),
-    "w8a8_smooth_calibrate": (INT, [P, P, I64, ctypes.c_float, P, P]),
+    "w8a8_smooth_calibrate": (INT, [P, ctypes.POINTER(P), ctypes.POINTER(I64), INT, INT, I64,
+                                    ctypes.c_float, P, P]),
+    "w8a8_smooth_delta": (INT, [P, P, I64, ctypes.c_float, P, P]),
+    "w8a8_geglu_requant": (INT, [P, P, I64, I64, P, P, P, P, P]),
+    "w8a8_ffn_stack_status": (INT, [P, SZ, P]),
+    "w8a8_set_plan_override": (INT, [ctypes.c_char_p, INT]),
+    "w8a8_clear_plan_overrides": (None, []),
     "w8a8_quantize_weights": (INT, [P, INT, I64, I64, P, P, P, P]),
     "w8a8_unpack_weights": (INT, [P, I64, I64, P, P]),
     "w8a8_pack_bf16": (INT, [P, I64, I64, P, P]),
@@ -208,12 +214,53 @@ def col_absmax(x, amax=None, stream=None):
     return amax
 
 
-def smooth_calibrate(act_amax, w_amax, alpha=0.5, stream=None):
+def smooth_calibrate(act_amax, weights, alpha=0.5, stream=None):
+    """delta from the calibration statistic and every weight matrix (k columns,
+    one dtype) that consumes the input; the weight maximum runs over all their
+    rows stacked."""
     k = act_amax.numel()
+    weights = [_dev(w) for w in weights]
+    dt = _dt(weights[0])
+    if any(_dt(w) != dt or w.shape[1] != k for w in weights):
+        raise ValueError("weights must share dtype and have k columns")
     delta = torch.empty(k, dtype=torch.float32, device=act_amax.device)
-    _check(lib().w8a8_smooth_calibrate(_ptr(_dev(act_amax)), _ptr(_dev(w_amax)), k,
+    ptrs = (P * len(weights))(*[w.data_ptr() for w in weights])
+    rows = (I64 * len(weights))(*[w.shape[0] for w in weights])
+    _check(lib().w8a8_smooth_calibrate(_ptr(_dev(act_amax)), ptrs, rows, len(weights), dt, k,
                                        float(alpha), _ptr(delta), _stream(stream)))
     return delta
+
+
+def smooth_delta(act_amax, w_amax, alpha=0.5, stream=None):
+    """delta from both statistics already gathered (w8a8_col_absmax)."""
+    k = act_amax.numel()
+    delta = torch.empty(k, dtype=torch.float32, device=act_amax.device)
+    _check(lib().w8a8_smooth_delta(_ptr(_dev(act_amax)), _ptr(_dev(w_amax)), k,
+                                   float(alpha), _ptr(delta), _stream(stream)))
+    return delta
+
+
+def geglu_requant(g, u, delta=None, want_h=True, stream=None):
+    """(packed codes of h / delta, per-row scales, h or None) with
+    h = bf16(gelu_tanh(g) u) from binary32 g, u."""
+    _dev(g)
+    _dev(u)
+    m, n = g.shape
+    q = _empty(packed_bytes(m, n), g.device)
+    s = torch.empty(m, dtype=torch.float32, device=g.device)
+    h = torch.empty((m, n), dtype=torch.bfloat16, device=g.device) if want_h else None
+    _check(lib().w8a8_geglu_requant(_ptr(g), _ptr(u), m, n, _ptr(delta), _ptr(q), _ptr(s),
+                                    _ptr(h), _stream(stream)))
+    return q, s, h
+
+
+def set_plan_override(name, value):
+    if lib().w8a8_set_plan_override(name.encode(), int(value)) != 0:
+        raise ValueError("unknown planner override %r" % name)
+
+
+def clear_plan_overrides():
+    lib().w8a8_clear_plan_overrides()
 
 
 def quantize_weights(w, delta=None, stream=None):
@@ -558,6 +605,12 @@ class Stack:
                                     int(lm_head_int8), _ptr(_dev(x)), m, _ptr(out), _ptr(ws),
                                     ws.numel(), _stream(stream)))
         return out
+
+    @staticmethod
+    def status(ws, stream=None):
+        """Synchronises the stream; raises W8A8Error (status ETIMEOUT) when the
+        last run on workspace ws had a persistent decode launch give up."""
+        _check(lib().w8a8_ffn_stack_status(_ptr(ws), ws.numel(), _stream(stream)))
 
     def trace(self, x, prec: np.ndarray, lm_head_int8: bool = False, logits: bool = False,
               ws=None, stream=None):

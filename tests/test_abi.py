@@ -37,8 +37,8 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings():
     L = w8a8.lib()
-    for code in range(5):
-        assert L.w8a8_status_str(code)
+    for code in range(6):
+        assert L.w8a8_status_str(code) != b"unknown status"
     assert L.w8a8_status_str(99) == b"unknown status"
 
 
@@ -91,8 +91,20 @@ def test_quantize_weights_and_calibration_validation():
     assert L.w8a8_quantize_weights(FAKE, w8a8.F32, 16, 24, None, FAKE, FAKE, None) == w8a8.EUNSUPPORTED
     assert L.w8a8_quantize_weights(FAKE, w8a8.F32, 0, 64, None, FAKE, FAKE, None) == w8a8.EINVAL
     assert L.w8a8_quantize_weights(FAKE, w8a8.F32, 16, 64, MISALIGNED, FAKE, FAKE, None) == w8a8.EINVAL
-    assert L.w8a8_smooth_calibrate(FAKE, FAKE, 64, 1.5, FAKE, None) == w8a8.EUNSUPPORTED
-    assert L.w8a8_smooth_calibrate(FAKE, None, 64, 0.5, FAKE, None) == w8a8.EINVAL
+    assert L.w8a8_smooth_delta(FAKE, FAKE, 64, 1.5, FAKE, None) == w8a8.EUNSUPPORTED
+    assert L.w8a8_smooth_delta(FAKE, None, 64, 0.5, FAKE, None) == w8a8.EINVAL
+    ws = (P * 2)(FAKE.value, FAKE.value)
+    rows = (ctypes.c_int64 * 2)(6912, 6912)
+    sc = L.w8a8_smooth_calibrate
+    assert sc(FAKE, ws, rows, 2, w8a8.BF16, 1152, 1.5, FAKE, None) == w8a8.EUNSUPPORTED
+    assert sc(FAKE, ws, rows, 2, 9, 1152, 0.5, FAKE, None) == w8a8.EUNSUPPORTED
+    assert sc(FAKE, ws, rows, 0, w8a8.BF16, 1152, 0.5, FAKE, None) == w8a8.EINVAL
+    assert sc(FAKE, None, rows, 2, w8a8.BF16, 1152, 0.5, FAKE, None) == w8a8.EINVAL
+    assert sc(None, ws, rows, 2, w8a8.BF16, 1152, 0.5, FAKE, None) == w8a8.EINVAL
+    bad = (P * 2)(FAKE.value, None)
+    assert sc(FAKE, bad, rows, 2, w8a8.BF16, 1152, 0.5, FAKE, None) == w8a8.EINVAL
+    zero = (ctypes.c_int64 * 2)(6912, 0)
+    assert sc(FAKE, ws, zero, 2, w8a8.BF16, 1152, 0.5, FAKE, None) == w8a8.EINVAL
     assert L.w8a8_col_absmax(FAKE, w8a8.BF16, 0, 64, FAKE, None) == w8a8.EINVAL
     assert L.w8a8_pack_bf16(FAKE, 16, 48, FAKE, None) == w8a8.EUNSUPPORTED
 
@@ -116,6 +128,38 @@ def test_linear_and_ffn_validation():
     assert L.w8a8_lm_head(ctypes.byref(d), FAKE, 0, FAKE, FAKE, 1 << 30, None) == w8a8.EINVAL
     assert L.w8a8_gemm_i8_i32(FAKE, 4, FAKE, 16, 1000, FAKE, FAKE, 1 << 20, None) == w8a8.EUNSUPPORTED
     assert L.w8a8_bf16_linear(FAKE, 4, FAKE, 16, 48, FAKE, None, 0, None) == w8a8.EUNSUPPORTED
+
+
+def test_geglu_requant_validation():
+    L = w8a8.lib()
+    g = L.w8a8_geglu_requant
+    assert g(None, FAKE, 4, 6912, None, FAKE, FAKE, None, None) == w8a8.EINVAL
+    assert g(FAKE, FAKE, 0, 6912, None, FAKE, FAKE, None, None) == w8a8.EINVAL
+    assert g(FAKE, FAKE, 4, 6904, None, FAKE, FAKE, None, None) == w8a8.EUNSUPPORTED
+    assert g(FAKE, FAKE, 4, w8a8.MAX_K + 16, None, FAKE, FAKE, None, None) == w8a8.EUNSUPPORTED
+    assert g(FAKE, FAKE, 4, 6912, MISALIGNED, FAKE, FAKE, None, None) == w8a8.EINVAL
+    assert g(FAKE, FAKE, 4, 6912, None, FAKE, FAKE, MISALIGNED, None) == w8a8.EINVAL
+
+
+def test_stack_status_validation_and_codes():
+    L = w8a8.lib()
+    assert L.w8a8_ffn_stack_status(None, 1 << 20, None) == w8a8.EINVAL
+    assert L.w8a8_ffn_stack_status(FAKE, 16, None) == w8a8.EWORKSPACE
+    assert b"persistent" in L.w8a8_status_str(w8a8.ETIMEOUT)
+
+
+def test_plan_overrides_are_explicit():
+    """The planner reads overrides set through the ABI, never the environment."""
+    L = w8a8.lib()
+    assert L.w8a8_set_plan_override(b"NOT_A_KNOB", 1) == -1
+    assert L.w8a8_set_plan_override(None, 1) == -1
+    for name in (b"GLU_TILE", b"GEMM_SPLITS", b"NO_PERSISTENT", b"DEC_SPIN_LIMIT"):
+        assert L.w8a8_set_plan_override(name, 1) == 0
+    L.w8a8_clear_plan_overrides()
+    with pytest.raises(ValueError):
+        w8a8.set_plan_override("W8A8_GLU_TILE", 3)
+    src = open(os.path.join(ROOT, "paper_2608_28003_amd", "csrc", "api.hip")).read()
+    assert "getenv" not in src
 
 
 def test_stack_validation():

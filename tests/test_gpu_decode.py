@@ -69,7 +69,7 @@ def _both_paths(stack, x, prec, monkeypatch, lm_head_int8=True):
     """(hidden, logits) from the persistent kernel and from the per-launch path."""
     outs = []
     for flag in ("0", "1"):
-        monkeypatch.setenv("W8A8_NO_PERSISTENT", flag)
+        w8a8.set_plan_override("NO_PERSISTENT", int(flag))
         hid, logits = stack.trace(x, prec, lm_head_int8=lm_head_int8, logits=True)
         run = stack.run(x, prec, lm_head_int8)
         outs.append((host_bf16(hid), host_bf16(logits), host_bf16(run)))
@@ -108,7 +108,7 @@ def test_persistent_bit_identical_to_per_launch(small, name, monkeypatch):
 
 def test_persistent_matches_oracle(small, monkeypatch):
     cfg, layers_o, stack = small
-    monkeypatch.setenv("W8A8_NO_PERSISTENT", "0")
+    w8a8.set_plan_override("NO_PERSISTENT", 0)
     x = dev_bf16(cfg["x"])
     for name in ("all", "mixed"):
         prec = MAPS_34[name]
@@ -132,22 +132,32 @@ def test_persistent_full_size_bit_identical(name, monkeypatch):
     np.testing.assert_array_equal(r0, r1)
 
 
-def test_persistent_failed_wait_gives_nan(small, monkeypatch):
+def test_persistent_failed_wait_gives_nan(small):
     """Force every barrier wait to give up at its first poll: the kernel must
-    still end (every wait is bounded) and poison its outputs: the token stream
-    after the last layer is NaN, and so are the bf16 lm_head's logits (the
-    INT8 lm_head's quantiser, like every absmax here, skips NaN and leaves a
-    zero row)."""
+    still end (every wait is bounded), poison its outputs -- the token stream
+    after the last layer and the logits of either lm_head are NaN -- and leave
+    a record that w8a8_ffn_stack_status reports as ETIMEOUT; the next clean
+    call on the same workspace clears it."""
     cfg, _, stack = small
     x = dev_bf16(cfg["x"])
-    prec = MAPS_34["all"]
-    monkeypatch.setenv("W8A8_NO_PERSISTENT", "0")
-    monkeypatch.setenv("W8A8_DEC_SPIN_LIMIT", "0")
-    hid, logits = stack.trace(x, prec, lm_head_int8=False, logits=True)
-    assert torch.isnan(hid[-1].float()).all()
-    assert torch.isnan(logits.float()).all()
-    monkeypatch.delenv("W8A8_DEC_SPIN_LIMIT")
-    hid, logits = stack.trace(x, prec, lm_head_int8=False, logits=True)  # clean again
+    ws = torch.empty(w8a8.stack_workspace_bytes(1, stack.d, stack.f, stack.vocab),
+                     dtype=torch.uint8, device=DEV)
+    w8a8.set_plan_override("NO_PERSISTENT", 0)
+    w8a8.set_plan_override("DEC_SPIN_LIMIT", 0)
+    for name in ("all", "mixed"):
+        prec = MAPS_34[name]
+        for lm8 in (False, True):
+            say("failed wait", name, "lm_head int8" if lm8 else "lm_head bf16")
+            hid, logits = stack.trace(x, prec, lm_head_int8=lm8, logits=True, ws=ws)
+            assert torch.isnan(hid[-1].float()).all()
+            assert torch.isnan(logits.float()).all()
+            with pytest.raises(w8a8.W8A8Error) as e:
+                w8a8.Stack.status(ws)
+            assert e.value.status == w8a8.ETIMEOUT
+    w8a8.clear_plan_overrides()
+    w8a8.set_plan_override("NO_PERSISTENT", 0)
+    hid, logits = stack.trace(x, MAPS_34["all"], lm_head_int8=True, logits=True, ws=ws)
+    w8a8.Stack.status(ws)   # clean again
     assert torch.isfinite(hid.float()).all() and torch.isfinite(logits.float()).all()
 
 
@@ -176,11 +186,11 @@ def test_full_vocab_fused_final_glue_bit_identical(monkeypatch):
     stack = w8a8.Stack(i8, bf, w8a8.LinearW8A8.from_weight(w_lm, d_lm), w8a8.pack_bf16(w_lm), vocab)
     x = dev_bf16(cfg["x"])
     for persistent in ("0", "1"):
-        monkeypatch.setenv("W8A8_NO_PERSISTENT", "1" if persistent == "0" else "0")
+        w8a8.set_plan_override("NO_PERSISTENT", int("1" if persistent == "0" else "0"))
         for prec in (np.array([1, 1], np.uint8), np.array([1, 0], np.uint8), np.array([0, 0], np.uint8)):
             outs = []
             for flag in ("0", "1"):
-                monkeypatch.setenv("W8A8_NO_FUSED_GLUE", flag)
+                w8a8.set_plan_override("NO_FUSED_GLUE", int(flag))
                 hid, logits = stack.trace(x, prec, lm_head_int8=True, logits=True)
                 outs.append((host_bf16(hid), host_bf16(logits), host_bf16(stack.run(x, prec, True))))
             for a, b in zip(outs[0], outs[1]):

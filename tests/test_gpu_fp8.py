@@ -206,9 +206,9 @@ def test_fp8_gemm_tiles_and_splits(m, n, k, splits, monkeypatch):
     qa = random_codes(rng, (m, k))
     qb = random_codes(rng, (n, k))
     A, B = pack_codes(qa), pack_codes(qb)
-    monkeypatch.setenv("W8A8_GEMM_SPLITS", str(splits))
+    w8a8.set_plan_override("GEMM_SPLITS", splits)
     for tile in (10, 11):
-        monkeypatch.setenv("W8A8_GEMM_TILE", str(tile))
+        w8a8.set_plan_override("GEMM_TILE", tile)
         acc = host(w8a8.fp8_gemm_f32(A, m, B, n, k))
         check_sums(acc, qa, qb, k, "tile %d" % tile)
 
@@ -304,7 +304,7 @@ def test_fp8_gate_up_tiles_agree(m, monkeypatch):
     qx, sx = pack_codes(qx_o), dev_f32(sx_o)
     outs = []
     for tile in (9, 12, 14):
-        monkeypatch.setenv("W8A8_GLU_TILE", str(tile))
+        w8a8.set_plan_override("GLU_TILE", tile)
         outs.append(oracle.bf16_to_f32(host_bf16(w8a8.fp8_ffn_gate_up(layer, qx, sx, m))))
     for o in outs[1:]:
         assert rel_l2(o, outs[0]) <= 1e-4
@@ -370,7 +370,7 @@ def test_fp8_quantise_on_load_equals_separate_quantisation(m, monkeypatch):
     xl = dev_bf16(lm_cfg["x"])
     outs = []
     for flag in ("0", "1"):
-        monkeypatch.setenv("W8A8_NO_QLOAD", flag)
+        w8a8.set_plan_override("NO_QLOAD", int(flag))
         outs.append((host_bf16(w8a8.fp8_ffn(layer, x)), host_bf16(w8a8.fp8_lm_head(lm, xl))))
     np.testing.assert_array_equal(outs[0][0], outs[1][0])
     np.testing.assert_array_equal(outs[0][1], outs[1][1])

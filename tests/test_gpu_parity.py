@@ -134,15 +134,37 @@ def test_calibration_matches_oracle(alpha):
     a_g = w8a8.col_absmax(dev_bf16(x_cal))
     w_g = w8a8.col_absmax(dev_bf16(cfg["w_gate"]))
     w_g = w8a8.col_absmax(dev_bf16(cfg["w_up"]), w_g)
-    d_g = w8a8.smooth_calibrate(a_g, w_g, alpha)
+    d_g = w8a8.smooth_delta(a_g, w_g, alpha)
+    # the boundary's form: the consumer weights themselves, stacked inside
+    d_w = w8a8.smooth_calibrate(a_g, [dev_bf16(cfg["w_gate"]), dev_bf16(cfg["w_up"])], alpha)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(host(a_g), a_o)
     np.testing.assert_array_equal(host(w_g), w_o)
+    np.testing.assert_array_equal(host(d_w), host(d_g))
     if alpha == 0.5:
         np.testing.assert_array_equal(host(d_g), d_o)
+        np.testing.assert_array_equal(
+            host(d_w), oracle.smooth_calibrate(x_cal, [cfg["w_gate"], cfg["w_up"]], alpha))
     else:   # pow in binary64 on both sides, then one rounding to binary32
         ulps = np.abs(host(d_g).view(np.int32) - d_o.view(np.int32))
         assert ulps.max() <= 1
+
+
+@pytest.mark.parametrize("n_w,dtype", [(1, "f32"), (3, "bf16")])
+def test_smooth_calibrate_stacks_every_consumer(n_w, dtype):
+    """Consumers of one input (e.g. Wq, Wk, Wv of different heights): the
+    weight maximum runs over all their rows; a dead channel takes the floor."""
+    say("smooth_calibrate", n_w, dtype)
+    k = 1152
+    x_cal = act_input(512, k, 4400, dtype=dtype)
+    ws = [synth.normal(4410 + i, (n, k), 0.02) for i, n in enumerate((1024, 256, 256)[:n_w])]
+    ws[0][:, 7] = 0.0
+    if dtype == "bf16":
+        ws = [synth.to_bf16_bits(w) for w in ws]
+    d_o = oracle.smooth_calibrate(x_cal, ws)
+    d_g = w8a8.smooth_calibrate(w8a8.col_absmax(to_dev(x_cal)), [to_dev(w) for w in ws])
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(d_g), d_o)
 
 
 @pytest.mark.parametrize("n,k,dtype", [(6912, 1152, "f32"), (1152, 6912, "bf16"),
@@ -209,9 +231,9 @@ def test_gemm_split_k_is_bit_identical(m, n, k, splits, monkeypatch):
     acc_o = oracle.gemm_i32(qa, qb)
     A = torch.from_numpy(w8a8.rowmajor_to_frag(qa)).to(DEV)
     B = torch.from_numpy(w8a8.rowmajor_to_frag(qb)).to(DEV)
-    monkeypatch.setenv("W8A8_GEMM_SPLITS", str(splits))
+    w8a8.set_plan_override("GEMM_SPLITS", splits)
     for tile in (0, 1, 2, 3, 7, 10, 11, 16):
-        monkeypatch.setenv("W8A8_GEMM_TILE", str(tile))
+        w8a8.set_plan_override("GEMM_TILE", tile)
         acc = w8a8.gemm_i8_i32(A, m, B, n, k)
         torch.cuda.synchronize()
         np.testing.assert_array_equal(host(acc), acc_o, err_msg="tile %d" % tile)
@@ -263,6 +285,26 @@ def _ffn_setup(m, d=1152, f=6912, seed_base=2000):
     return cfg, q, layer
 
 
+def geglu_mismatch_ok(ulps):
+    """At most 1 bf16 ulp everywhere, and differing elements at most a 1e-4
+    fraction (measured about 2e-5); at one row (6912 values) the fraction's
+    resolution is 1.4e-4, so a single differing element is allowed."""
+    n_diff = int((ulps > 0).sum())
+    return ulps.max() <= 1 and n_diff <= max(1, 1e-4 * ulps.size)
+
+
+def tail_codes_agree(h_gpu, st, delta_down, m):
+    """Elements geglu_ulp_diff leaves out (the far negative tail, where the
+    kernel's binary32 activation may flush to 0): the requantised codes there
+    must be the same on both sides (0: they are far below half a step)."""
+    d = bf16_ulp_diff(h_gpu, st["h"])
+    tail = (d > 0) & (geglu_ulp_diff(h_gpu, st["h"], st["g"], st["u"]) == 0)
+    qh, _ = w8a8.quantize_act(dev_bf16(h_gpu), dev_f32(delta_down))
+    codes = w8a8.frag_to_rowmajor(host(qh), m, h_gpu.shape[1])
+    assert np.array_equal(codes[tail], st["qh"][tail])
+    return int(tail.sum())
+
+
 @pytest.mark.parametrize("m", [1, 5, 64, 128, 300])
 def test_ffn_gate_up_geglu_stage(m):
     say("ffn gate/up + GeGLU", m)
@@ -273,10 +315,48 @@ def test_ffn_gate_up_geglu_stage(m):
     torch.cuda.synchronize()
     hg = host_bf16(h)
     ulps = geglu_ulp_diff(hg, st["h"], st["g"], st["u"])
-    assert ulps.max() <= 1, ulps.max()
-    frac = float((ulps > 0).mean())
-    say("  h mismatch fraction", frac)
-    assert frac <= 1e-3
+    say("  h mismatches %d of %d" % (int((ulps > 0).sum()), ulps.size))
+    assert geglu_mismatch_ok(ulps)
+    n_tail = tail_codes_agree(hg, st, q["delta_down"], m)
+    say("  far-tail elements with equal codes", n_tail)
+
+
+@pytest.mark.parametrize("m", [1, 7, 128, 300])
+def test_geglu_requant_matches_oracle(m):
+    """The boundary's GeGLU + requant stage from the oracle's binary32 g, u:
+    h within one bf16 ulp of the oracle's (same bar as the fused epilogue, and
+    equal to that epilogue's h bit for bit); codes and scales bit-exact on
+    every row whose h equals the oracle's, and on the other rows wherever the
+    row maximum and the element agree."""
+    say("geglu_requant", m)
+    cfg, q, layer = _ffn_setup(m)
+    _, st = oracle.w8a8_ffn(cfg["x"], q, stages=True)
+    qh, sh, h = w8a8.geglu_requant(dev_f32(st["g"]), dev_f32(st["u"]), dev_f32(q["delta_down"]))
+    h_epi = w8a8.ffn_gate_up(layer, torch.from_numpy(w8a8.rowmajor_to_frag(st["qx"])).to(DEV),
+                             dev_f32(st["sx"]), m)
+    torch.cuda.synchronize()
+    hg, shg = host_bf16(h), host(sh)
+    np.testing.assert_array_equal(hg, host_bf16(h_epi))   # same arithmetic as the epilogue
+    assert geglu_mismatch_ok(geglu_ulp_diff(hg, st["h"], st["g"], st["u"]))
+    codes = w8a8.frag_to_rowmajor(host(qh), m, hg.shape[1])
+    full = packed_full(qh, m, hg.shape[1])
+    assert not full[m:].any(), "padding rows must be zero"
+    # the requant applied by the GPU to the oracle's h is bit-exact (tested
+    # below); here the GPU's h is used, so compare where the inputs agree
+    same_rows = np.all(hg == st["h"], axis=1)
+    np.testing.assert_array_equal(codes[same_rows], st["qh"][same_rows])
+    np.testing.assert_array_equal(shg[same_rows], st["sh"][same_rows])
+    eq_elem = (hg == st["h"]) & (shg == st["sh"])[:, None]
+    np.testing.assert_array_equal(codes[eq_elem], st["qh"][eq_elem])
+    say("  rows with identical h: %d of %d" % (int(same_rows.sum()), m))
+    if m >= 7:
+        assert same_rows.mean() >= 0.5
+    # no debug output requested: the same codes
+    qh2, sh2, h2 = w8a8.geglu_requant(dev_f32(st["g"]), dev_f32(st["u"]),
+                                      dev_f32(q["delta_down"]), want_h=False)
+    assert h2 is None
+    np.testing.assert_array_equal(host(qh2), host(qh))
+    np.testing.assert_array_equal(host(sh2), shg)
 
 
 @pytest.mark.parametrize("m", [300, 2048])
@@ -290,7 +370,7 @@ def test_gate_up_tiles_bit_identical(m, monkeypatch):
     sx = dev_f32(sx_o)
     ref = None
     for tile in (4, 5, 6, 8, 9, 12, 13, 14, 15):
-        monkeypatch.setenv("W8A8_GLU_TILE", str(tile))
+        w8a8.set_plan_override("GLU_TILE", tile)
         h = host_bf16(w8a8.ffn_gate_up(layer, qx, sx, m))
         if ref is None:
             ref = h
@@ -299,8 +379,7 @@ def test_gate_up_tiles_bit_identical(m, monkeypatch):
     if m == 300:   # small enough for the oracle's gate/up stage
         g = oracle.dequant(oracle.gemm_i32(qx_o, q["wq_gate"]), sx_o, q["s_gate"])
         u = oracle.dequant(oracle.gemm_i32(qx_o, q["wq_up"]), sx_o, q["s_up"])
-        ulps = geglu_ulp_diff(ref, oracle.f64_to_bf16(oracle.geglu(g, u)), g, u)
-        assert ulps.max() <= 1 and float((ulps > 0).mean()) <= 1e-3
+        assert geglu_mismatch_ok(geglu_ulp_diff(ref, oracle.f64_to_bf16(oracle.geglu(g, u)), g, u))
 
 
 @pytest.mark.parametrize("m", [1, 8, 64, 128, 512])
@@ -475,7 +554,8 @@ def test_stack_precision_map_matches_oracle():
         torch.cuda.synchronize()
         err = rel_l2(oracle.bf16_to_f32(host_bf16(y)), oracle.bf16_to_f32(y_o))
         say("  map", prec, "lm_head int8", lm8, "rel-L2 %.3g" % err)
-        assert err <= 1e-2
+        # bf16 layers: fp32 sums on the matrix cores against exact sums
+        assert err <= (1e-3 if prec.all() else 1e-2)
 
 
 @pytest.mark.parametrize("m", [1, 2, 5])
@@ -492,7 +572,7 @@ def test_quantise_on_load_equals_separate_quantisation(m, monkeypatch):
     xl = dev_bf16(lm_cfg["x"])
     outs = []
     for flag in ("0", "1"):
-        monkeypatch.setenv("W8A8_NO_QLOAD", flag)
+        w8a8.set_plan_override("NO_QLOAD", int(flag))
         outs.append((host_bf16(w8a8.ffn(layer, x)), host_bf16(w8a8.lm_head(lm, xl))))
     np.testing.assert_array_equal(outs[0][0], outs[1][0])
     np.testing.assert_array_equal(outs[0][1], outs[1][1])
@@ -525,8 +605,8 @@ def test_decode_down_stream_plans_bit_identical(wk, splits, monkeypatch):
     cfg, q, layer = _ffn_setup(1)
     x = dev_bf16(cfg["x"])
     ref = host_bf16(w8a8.ffn(layer, x))
-    monkeypatch.setenv("W8A8_STREAM_WK", str(wk))
-    monkeypatch.setenv("W8A8_STREAM_SPLITS", str(splits))
+    w8a8.set_plan_override("STREAM_WK", wk)
+    w8a8.set_plan_override("STREAM_SPLITS", splits)
     np.testing.assert_array_equal(host_bf16(w8a8.ffn(layer, x)), ref)
 
 
@@ -558,9 +638,9 @@ def test_decode_fused_layer_glue_bit_identical(prec, monkeypatch):
     x = dev_bf16(cfg["x"])
     prec = np.array(prec, np.uint8)
     outs = []
-    monkeypatch.setenv("W8A8_NO_PERSISTENT", "1")  # the per-launch decode path
+    w8a8.set_plan_override("NO_PERSISTENT", 1)  # the per-launch decode path
     for flag in ("0", "1"):
-        monkeypatch.setenv("W8A8_NO_FUSED_GLUE", flag)
+        w8a8.set_plan_override("NO_FUSED_GLUE", int(flag))
         hid, logits = stack.trace(x, prec, lm_head_int8=True, logits=True)
         outs.append((host_bf16(hid), host_bf16(logits), host_bf16(stack.run(x, prec, False))))
     for a, b in zip(outs[0], outs[1]):
@@ -575,9 +655,9 @@ def test_decode_fused_layer_glue_full_size(name, monkeypatch):
     x = dev_bf16(cfg["x"])
     prec = w8a8.precision_map(name)
     outs = []
-    monkeypatch.setenv("W8A8_NO_PERSISTENT", "1")
+    w8a8.set_plan_override("NO_PERSISTENT", 1)
     for flag in ("0", "1"):
-        monkeypatch.setenv("W8A8_NO_FUSED_GLUE", flag)
+        w8a8.set_plan_override("NO_FUSED_GLUE", int(flag))
         hid, logits = stack.trace(x, prec, lm_head_int8=True, logits=True)
         outs.append((host_bf16(hid), host_bf16(logits)))
     np.testing.assert_array_equal(outs[0][0], outs[1][0])
