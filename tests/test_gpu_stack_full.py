@@ -5,14 +5,14 @@ CPU oracle: every layer's token stream, and the logits on sampled vocabulary
 columns (lm_head rows are independent, so the oracle quantises and multiplies
 only the sampled rows).
 
-Bars:
-* all-INT8 map (all26): rel-L2 <= 1e-3 on every layer's token stream and on
-  the logits;
-* maps with bf16 layers (5+5, 10+10): rel-L2 <= 1e-2 -- the bf16 layers sum
-  in fp32 on the matrix cores while the oracle sums exactly (reading 10), so
-  only tolerance applies to them;
-* the persistent one-token kernel at the full shape: every layer's token
-  stream against the oracle at 1e-3.
+Bars (the oracle's arithmetic is binary64 with one rounding per bf16
+activation, the kernels' binary32; a pin on the CPU shows that this alone
+moves the 26-layer result by more than 1e-3, see tests/norm_variant.py):
+* every layer on its own, from the oracle's token stream: rel-L2 <= 1e-3
+  (INT8 and bf16 layers);
+* end to end, the token stream after every layer and the logits: rel-L2 <=
+  1e-3 + 2 x the drift of the binary32 variant of the oracle at that point;
+* the persistent one-token kernel at the full shape: the same two checks.
 
 The weights' smoothing factors come from the oracle (64 calibration tokens
 per layer, on the layer's own synthetic calibration draw); the GPU quantises
@@ -27,6 +27,7 @@ import pytest
 import torch
 
 import oracle
+from norm_variant import rel_l2, stack_bars
 from paper_2608_28003_amd import synth, w8a8
 
 pytestmark = [pytest.mark.gpu,
@@ -50,12 +51,6 @@ def dev_f32(a):
 
 def host_bf16(t):
     return t.detach().cpu().view(torch.int16).numpy().view(np.uint16)
-
-
-def rel_l2(a_bits, b_bits):
-    a = oracle.bf16_to_f32(a_bits).astype(np.float64)
-    b = oracle.bf16_to_f32(b_bits).astype(np.float64)
-    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
 
 
 @pytest.fixture(scope="module")
@@ -89,7 +84,13 @@ def _oracle_logits(hidden_last, lm_c):
     return oracle.w8a8_lm_head(oracle.rmsnorm(hidden_last), lm_c["wq"], lm_c["s_w"], lm_c["delta"])
 
 
-def _check_map(full, name, m, bar):
+def _one_layer_stacks(full):
+    cfg, layers_o, stack, cols, lm_c = full
+    return [w8a8.Stack([stack.int8_layers[l]], [stack.bf16_layers[l]], stack.lm_int8,
+                       stack.lm_bf16, stack.vocab) for l in range(len(layers_o))]
+
+
+def _check_map(full, name, m, local=True):
     cfg, layers_o, stack, cols, lm_c = full
     x = np.ascontiguousarray(cfg["x"][:m])
     prec = w8a8.precision_map(name)
@@ -99,36 +100,45 @@ def _check_map(full, name, m, bar):
     hid = host_bf16(hid)
     lg = host_bf16(logits[:, torch.from_numpy(cols).to(DEV)])
     del logits
-    say("stack %s, M=%d: oracle" % (name, m))
+    say("stack %s, M=%d: oracle and its binary32 variant" % (name, m))
     hid_o = oracle.stack_hidden(x, layers_o, prec)
-    worst = 0.0
-    for l in range(len(prec)):
-        err = rel_l2(hid[l], hid_o[l])
-        worst = max(worst, err)
-        assert err <= bar, (name, m, l, err)
+    bars, var_last = stack_bars(x, layers_o, prec, hid_o)
     lg_o = _oracle_logits(hid_o[-1], lm_c)
+    lg_bar = 1e-3 + 2.0 * rel_l2(_oracle_logits(var_last, lm_c), lg_o)
+    if local:
+        # every layer from the oracle's own input: no drift to allow for
+        one = _one_layer_stacks(full)
+        worst_local = 0.0
+        for l in range(len(prec)):
+            x_l = x if l == 0 else hid_o[l - 1]
+            y = host_bf16(one[l].trace(dev_bf16(x_l), prec[l:l + 1])[0])
+            err = rel_l2(y, hid_o[l])
+            worst_local = max(worst_local, err)
+            assert err <= 1e-3, ("local", name, m, l, int(prec[l]), err)
+        say("  worst single-layer rel-L2 %.3g" % worst_local)
+    errs = [rel_l2(hid[l], hid_o[l]) for l in range(len(prec))]
+    for l in range(len(prec)):
+        assert errs[l] <= bars[l], (name, m, l, errs[l], bars[l])
     err = rel_l2(lg, lg_o)
-    same = float((lg == lg_o).mean())
-    say("  worst layer rel-L2 %.3g, last layer bit-identical %.6f; logits rel-L2 %.3g, "
-        "bit-identical %.6f" % (worst, float((hid[-1] == hid_o[-1]).mean()), err, same))
-    assert err <= bar
-    return worst, err
+    say("  end to end: layer rel-L2 %s" % " ".join("%.2g/%.2g" % (e, b) for e, b in zip(errs, bars)))
+    say("  logits rel-L2 %.3g (bar %.3g), bit-identical %.6f" % (err, lg_bar, float((lg == lg_o).mean())))
+    assert err <= lg_bar
 
 
 @pytest.mark.timeout(600)
 def test_all26_int8_lm_head_m512(full):
-    _check_map(full, "all26", 512, 1e-3)
+    _check_map(full, "all26", 512)
 
 
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("name", ["5+5", "10+10"])
 def test_mixed_maps_int8_lm_head_m512(full, name):
-    _check_map(full, name, 512, 1e-2)
+    _check_map(full, name, 512)
 
 
 @pytest.mark.timeout(900)
 def test_all26_int8_lm_head_m2048(full):
-    _check_map(full, "all26", 2048, 1e-3)
+    _check_map(full, "all26", 2048, local=False)
 
 
 @pytest.mark.timeout(600)
@@ -148,7 +158,8 @@ def test_ffn_block_m2048_matches_oracle(full):
 @pytest.mark.parametrize("name", ["all26", "10+10"])
 def test_persistent_decode_full_shape_matches_oracle(full, name):
     """One token through 26 layers (runs of INT8 layers in the persistent
-    kernel) against the oracle at d = 1152, f = 6912."""
+    kernel) against the oracle at d = 1152, f = 6912: each layer from the
+    oracle's input, and end to end."""
     cfg, layers_o, stack, cols, lm_c = full
     x = np.ascontiguousarray(cfg["x"][:1])
     prec = w8a8.precision_map(name)
@@ -157,11 +168,17 @@ def test_persistent_decode_full_shape_matches_oracle(full, name):
     hid = host_bf16(hid)
     lg = host_bf16(logits[:, torch.from_numpy(cols).to(DEV)])
     hid_o = oracle.stack_hidden(x, layers_o, prec)
-    bar = 1e-3 if name == "all26" else 1e-2
+    one = _one_layer_stacks(full)
     for l in range(len(prec)):
-        err = rel_l2(hid[l], hid_o[l])
-        assert err <= bar, (l, err)
-    err = rel_l2(lg, _oracle_logits(hid_o[-1], lm_c))
-    say("  persistent %s: last layer rel-L2 %.3g, logits rel-L2 %.3g"
-        % (name, rel_l2(hid[-1], hid_o[-1]), err))
-    assert err <= bar
+        x_l = x if l == 0 else hid_o[l - 1]
+        y = host_bf16(one[l].trace(dev_bf16(x_l), prec[l:l + 1])[0])
+        assert rel_l2(y, hid_o[l]) <= 1e-3, ("local", l)
+    bars, var_last = stack_bars(x, layers_o, prec, hid_o)
+    for l in range(len(prec)):
+        assert rel_l2(hid[l], hid_o[l]) <= bars[l], (l, rel_l2(hid[l], hid_o[l]), bars[l])
+    lg_o = _oracle_logits(hid_o[-1], lm_c)
+    lg_bar = 1e-3 + 2.0 * rel_l2(_oracle_logits(var_last, lm_c), lg_o)
+    err = rel_l2(lg, lg_o)
+    say("  persistent %s: last layer rel-L2 %.3g (bar %.3g), logits rel-L2 %.3g (bar %.3g)"
+        % (name, rel_l2(hid[-1], hid_o[-1]), bars[-1], err, lg_bar))
+    assert err <= lg_bar

@@ -369,3 +369,28 @@ def test_each_layer_adds_a_unit_rms_update(small_stack):
         slack = np.sqrt(((2.0 ** -8 * np.abs(cur)) ** 2).mean(1))
         assert np.all(np.abs(rms - 1.0) <= 2.0 ** -7 + slack)
         prev = cur
+
+
+# ------------------------------------------------------------------ depth sensitivity
+
+def test_stack_sensitivity_to_binary32_rounding():
+    """Why the 26-layer stack is compared layer by layer at 1e-3 and end to end
+    against a bar scaled by this sensitivity: the same stack with binary32
+    norms and sums (tests/norm_variant.py) agrees with the oracle to < 1e-4
+    after one layer but drifts past 1e-3 within the 26 layers, on the
+    all-INT8 and on the all-bf16 map -- a property of the arithmetic (each
+    flipped bf16 rounding rescales its row through the next norm), not of an
+    implementation."""
+    from norm_variant import rel_l2, stack_hidden32
+    cfg = synth.stack_config(m=32, n_layers=26, d=256, f=512, vocab=16)
+    layers = [dict(L, int8=oracle.quantize_ffn(L["w_gate"], L["w_up"], L["w_down"],
+                                               cfg["x_cal"][:64]))
+              for L in cfg["layers"]]
+    for name, first_max, last_min in (("bf16", 1e-4, 3e-3), ("all26", 1e-4, 1e-3)):
+        prec = oracle.precision_map(name)
+        ref = oracle.stack_hidden(cfg["x"], layers, prec)
+        var = stack_hidden32(cfg["x"], layers, prec)
+        errs = [rel_l2(var[l], ref[l]) for l in range(26)]
+        assert errs[0] <= first_max, (name, errs[0])
+        assert errs[-1] >= last_min, (name, errs[-1])
+        assert max(errs) < 0.05
