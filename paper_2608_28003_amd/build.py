@@ -47,20 +47,30 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = True) -> str:
-    """Compile every ``csrc/*.hip`` and link the shared library (always rebuilds)."""
-    os.makedirs(BUILD_DIR, exist_ok=True)
-    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
-    with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
-        objs = list(ex.map(_compile, srcs))
-    tmp = LIB_PATH + ".tmp%d" % os.getpid()
+PEAK_LIB_PATH = os.path.join(HERE, "libw8a8_peak.so")
+
+
+def _link(objs, path):
+    tmp = path + ".tmp%d" % os.getpid()
     cmd = [_hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n%s\n%s" % (r.stdout, r.stderr))
-    os.replace(tmp, LIB_PATH)
+    os.replace(tmp, path)
+
+
+def build(verbose: bool = True) -> str:
+    """Compile every ``csrc/*.hip`` into ``libw8a8.so`` and ``csrc/peak/*.hip``
+    (the benchmark's ceiling probes) into ``libw8a8_peak.so`` (always rebuilds)."""
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+    peak_srcs = sorted(glob.glob(os.path.join(CSRC, "peak", "*.hip")))
+    with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs) + len(peak_srcs))) as ex:
+        objs = list(ex.map(_compile, srcs + peak_srcs))
+    _link(objs[:len(srcs)], LIB_PATH)
+    _link(objs[len(srcs):], PEAK_LIB_PATH)
     if verbose:
-        print("built", LIB_PATH, file=sys.stderr)
+        print("built", LIB_PATH, "and", PEAK_LIB_PATH, file=sys.stderr)
     return LIB_PATH
 
 
