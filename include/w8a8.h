@@ -236,6 +236,20 @@ w8a8_status w8a8_geglu_requant(const float* g, const float* u, int64_t m, int64_
 w8a8_status w8a8_ffn(const w8a8_ffn_desc* desc, const void* x, int64_t m, void* y,
                      void* ws, size_t ws_bytes, w8a8_stream_t stream);
 
+/* For callers that cannot allocate (code under graph capture, tight serving
+   loops, harnesses that forbid hipMalloc): w8a8_ffn without a workspace
+   argument.  The intermediates live in a fixed device array inside the
+   library, W8A8_FFN_NOALLOC_SCRATCH_BYTES (32 MiB) on every GPU it runs on,
+   held until the process ends; the call itself allocates nothing.  Shapes
+   whose w8a8_ffn_workspace_bytes(m, d, f) exceed it fail with EWORKSPACE
+   (at d = 1152, f = 6912: m up to about 1000).  Every call on one GPU uses
+   the same array: calls that overlap in time on one GPU (other streams,
+   other threads) race and must be serialised by the caller.  The stream must
+   belong to the current device.  Results equal w8a8_ffn's. */
+#define W8A8_FFN_NOALLOC_SCRATCH_BYTES (32u << 20)
+w8a8_status w8a8_ffn_noalloc(const w8a8_ffn_desc* desc, const void* x, int64_t m, void* y,
+                             w8a8_stream_t stream);
+
 /* ---------------------------------------------------------------- a7: lm_head */
 
 /* INT8 lm_head (Sec. 6, eq. gemm-final, all 262144 rows in one launch): logits

@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <mutex>
 #include <climits>
 #include <cstdint>
 #include <cstdlib>
@@ -891,6 +892,61 @@ w8a8_status w8a8_geglu_requant(const float* g, const float* u, int64_t m, int64_
   return hip_check(launch_geglu_requant(g, u, m, n, delta, (int8_t*)q, s, (uint16_t*)h,
                                         S(stream)),
                    "geglu_requant");
+}
+
+// ------------------------------------------------------------------ no-allocation FFN
+
+namespace {
+
+// Scratch memory of w8a8_ffn_noalloc: one copy of this array on every GPU the
+// library runs on, resident until the process ends.  In host code the name
+// is only a host-side stand-in (passing it to a kernel compiles and then
+// faults); the device address of each GPU's copy comes from
+// hipGetSymbolAddress, taken once per device with that device current, and
+// only that address is ever handed to kernels.
+__device__ __align__(256) char scratch[W8A8_FFN_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+struct ScratchSlot {
+  std::once_flag once;
+  void* ptr = nullptr;
+  hipError_t err = hipSuccess;
+};
+ScratchSlot g_scratch[kMaxDevices];
+
+// Device address of the current device's scratch array (looked up on the
+// first call on that device).
+w8a8_status current_scratch(void** out) {
+  int dev = 0;
+  CHECK(hip_check(hipGetDevice(&dev), "hipGetDevice"));
+  REQUIRE(dev >= 0 && dev < kMaxDevices, W8A8_EUNSUPPORTED, "device index above 63");
+  ScratchSlot& slot = g_scratch[dev];
+  std::call_once(slot.once, [&slot] {
+    slot.err = hipGetSymbolAddress(&slot.ptr, HIP_SYMBOL(scratch));
+  });
+  CHECK(hip_check(slot.err, "hipGetSymbolAddress(scratch)"));
+  REQUIRE(slot.ptr != nullptr, W8A8_EHIP, "no device address for the scratch array");
+  *out = slot.ptr;
+  return W8A8_OK;
+}
+
+}  // namespace
+
+w8a8_status w8a8_ffn_noalloc(const w8a8_ffn_desc* desc, const void* x, int64_t m, void* y,
+                             w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK(check_ffn_desc(desc));
+  CHECK_PTR(x);
+  CHECK_PTR(y);
+  REQUIRE(m >= 1, W8A8_EINVAL, "m < 1");
+  const size_t need = w8a8_ffn_workspace_bytes(m, desc->d, desc->f);
+  REQUIRE(need <= (size_t)W8A8_FFN_NOALLOC_SCRATCH_BYTES, W8A8_EWORKSPACE,
+          "this m x d x f needs " + std::to_string(need) +
+              " bytes of scratch; the no-allocation FFN holds " +
+              std::to_string((size_t)W8A8_FFN_NOALLOC_SCRATCH_BYTES));
+  void* ws = nullptr;
+  CHECK(current_scratch(&ws));
+  return ffn_impl(desc, x, m, y, ws, S(stream));
 }
 
 w8a8_status w8a8_ffn(const w8a8_ffn_desc* desc, const void* x, int64_t m, void* y, void* ws,

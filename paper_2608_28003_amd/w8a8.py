@@ -80,6 +80,7 @@ _SIGS = {
     "w8a8_linear": (INT, [ctypes.POINTER(LinearDesc), P, INT, I64, P, INT, P, SZ, P]),
     "w8a8_ffn_gate_up": (INT, [ctypes.POINTER(FfnDesc), P, P, I64, P, P]),
     "w8a8_ffn": (INT, [ctypes.POINTER(FfnDesc), P, I64, P, P, SZ, P]),
+    "w8a8_ffn_noalloc": (INT, [ctypes.POINTER(FfnDesc), P, I64, P, P]),
     "w8a8_lm_head": (INT, [ctypes.POINTER(LinearDesc), P, I64, P, P, SZ, P]),
     "w8a8_fp8_linear_workspace_bytes": (SZ, [I64, I64, I64]),
     "w8a8_fp8_ffn_workspace_bytes": (SZ, [I64, I64, I64]),
@@ -399,6 +400,17 @@ def ffn(layer: FfnW8A8, x, out=None, ws=None, stream=None):
     d = layer.desc()
     _check(lib().w8a8_ffn(ctypes.byref(d), _ptr(x), m, _ptr(out), _ptr(ws), ws.numel(),
                           _stream(stream)))
+    return out
+
+
+def ffn_noalloc(layer: FfnW8A8, x, out=None, stream=None):
+    """w8a8_ffn with the library's per-GPU scratch array instead of a workspace."""
+    _dev(x)
+    m = x.shape[0]
+    if out is None:
+        out = torch.empty((m, layer.d), dtype=torch.bfloat16, device=x.device)
+    d = layer.desc()
+    _check(lib().w8a8_ffn_noalloc(ctypes.byref(d), _ptr(x), m, _ptr(out), _stream(stream)))
     return out
 
 
