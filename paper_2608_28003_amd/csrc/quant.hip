@@ -276,6 +276,123 @@ __global__ __launch_bounds__(1024) void quant_rows_kernel(const T* __restrict__ 
   }
 }
 
+// ------------------------------------------------------------------ many rows of bf16
+
+// Correctly rounded binary32 quotient a / b for binary32 a and a reciprocal
+// rb = RN64(1 / b) formed once: RN32(RN64(a * rb)).  The exact quotient of two
+// binary32 numbers is never a binary32 rounding midpoint and lies more than
+// 2^-49 (relative) away from every midpoint of the normal range (write a = A 2^x,
+// b = B 2^y, a midpoint (2K + 1) 2^(z - 1) with A, B, K < 2^24: a - midpoint * b
+// is a nonzero multiple of 2^(z - 1 + y)); the two binary64 roundings err by at
+// most 2^-52, so the final rounding lands on the same binary32 value as a / b
+// rounded once.  Quotients below the normal range (|result| < 2^-126, a != 0)
+// are not covered; callers take the IEEE division for them.
+__device__ __forceinline__ float div_via_f64(float a, double rb) {
+  return (float)((double)a * rb);
+}
+
+// Per-token quantisation of R rows of a bf16 matrix per workgroup (the large-M
+// activation and requantisation path): thread t owns the 16-column chunk t of
+// each row, the smoothing factors' reciprocals are formed once per workgroup,
+// all R rows' loads are in flight together, and one block reduction gives
+// the R row maxima.  Same results as quant_rows_kernel (x / delta and v / s
+// correctly rounded, see div_via_f64; the maximum does not depend on order).
+template <int R>
+__global__ __launch_bounds__(1024) void quant_rows_bf16_kernel(
+    const uint16_t* __restrict__ x, int64_t rows, int64_t k, const float* __restrict__ delta,
+    int64_t rows_pad, int64_t kp, int8_t* __restrict__ q, float* __restrict__ s) {
+  __shared__ float red[R][16];
+  const int t = threadIdx.x;
+  const int nw = blockDim.x >> 6;
+  const int64_t r0 = (int64_t)blockIdx.x * R;
+  const int64_t kb_count = kp / kFragK8;
+  const int64_t chunks = k / 16, chunks_pad = kp / 16;
+  const bool own = t < chunks;
+
+  double rd[16];
+  if (own && delta) {
+    float d[16];
+    load16<float>(delta + (int64_t)t * 16, d);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) rd[e] = 1.0 / (double)d[e];
+  }
+  uint4 raw[R][2];
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    if (own && r0 + i < rows) {
+      const uint4* p = reinterpret_cast<const uint4*>(x + (r0 + i) * k + (int64_t)t * 16);
+      raw[i][0] = p[0];
+      raw[i][1] = p[1];
+    } else {
+      raw[i][0] = raw[i][1] = make_uint4(0u, 0u, 0u, 0u);
+    }
+  }
+  float v[R][16];
+  float mx[R];
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const uint32_t w[8] = {raw[i][0].x, raw[i][0].y, raw[i][0].z, raw[i][0].w,
+                           raw[i][1].x, raw[i][1].y, raw[i][1].z, raw[i][1].w};
+    bool tiny = false;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const float xv = bf16_bits_to_float((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xffffu));
+      float vv = xv;
+      if (delta) {
+        vv = div_via_f64(xv, rd[e]);
+        tiny |= (fabsf(vv) < 1.17549435e-38f) && (xv != 0.0f);
+      }
+      v[i][e] = vv;
+    }
+    if (tiny) {  // quotient below the normal range: the IEEE division
+      float d[16];
+      load16<float>(delta + (int64_t)t * 16, d);
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        v[i][e] = bf16_bits_to_float((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xffffu)) / d[e];
+    }
+    float m = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) m = fmaxf(m, fabsf(v[i][e]));
+    mx[i] = wave_max(m);
+  }
+  if ((t & 63) == 0) {
+#pragma unroll
+    for (int i = 0; i < R; ++i) red[i][t >> 6] = mx[i];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    float m = red[i][0];
+    for (int w = 1; w < nw; ++w) m = fmaxf(m, red[i][w]);
+    mx[i] = m;
+  }
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const int64_t r = r0 + i;
+    if (r >= rows_pad) break;
+    int32_t packed[4] = {0, 0, 0, 0};
+    if (r < rows) {
+      const float sr = mx[i] / 127.0f;
+      if (t == 0) s[r] = sr;
+      if (own && sr != 0.0f) {
+        const double rs = 1.0 / (double)sr;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          // |v / s| <= 127 (1 + 2^-23) except for a subnormal scale; the clamp
+          // keeps the codes of that case, as in code_of
+          float c = rintf(div_via_f64(v[i][e], rs));
+          c = fminf(fmaxf(c, -127.0f), 127.0f);
+          packed[e >> 2] |= ((int32_t)(int)c & 0xff) << (8 * (e & 3));
+        }
+      }
+    }
+    // blockDim covers chunks_pad: one chunk per thread (padding columns and
+    // padding rows get zero codes)
+    if (t < chunks_pad) store_codes<16>(q, r, t, kb_count, packed);
+  }
+}
+
 // packed int8 -> row-major int8 (n x k)
 __global__ void unpack_kernel(const int8_t* __restrict__ qp, int64_t n, int64_t k, int64_t kp,
                               int8_t* __restrict__ q) {
@@ -363,6 +480,14 @@ hipError_t launch_quant_rows(const void* x, bool bf16, bool mul, int64_t rows, i
   // 8-column chunks while the rows leave CUs idle (one workgroup per row) and a
   // row still fits one workgroup
   const bool narrow = rows_pad <= 256 && kp / 8 <= 1024;
+  if (bf16 && !mul && !f8 && !narrow && kp / 16 <= 1024) {
+    // many bf16 rows (activations): several rows per workgroup
+    constexpr int R = 4;
+    const int64_t threads = (kp / 16 + 63) / 64 * 64;
+    quant_rows_bf16_kernel<R><<<(unsigned)((rows_pad + R - 1) / R), (unsigned)threads, 0, st>>>(
+        (const uint16_t*)x, rows, k, delta, rows_pad, kp, qpacked, s);
+    return hipGetLastError();
+  }
   int64_t threads = (kp / (narrow ? 8 : 16) + 63) / 64 * 64;
   if (threads > 1024) threads = 1024;
   dim3 grid((unsigned)rows_pad), block((unsigned)threads);

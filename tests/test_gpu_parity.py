@@ -121,6 +121,37 @@ def test_quantize_act_bit_exact(m, k, dtype, smooth):
     np.testing.assert_array_equal(host(sx), s_o)
 
 
+def test_quantize_act_many_rows_division_edge_cases():
+    """The many-row bf16 quantiser forms x / delta and v / s through binary64
+    (correctly rounded in the normal range, IEEE division below it): every
+    bf16 value of magnitude below 2^64, both signs, against smoothing factors
+    from 2^-60 to 2^60, near powers of two, with all mantissa bits set, and
+    quotients deep in the subnormal range, against the oracle's binary32
+    divisions, bit for bit."""
+    k = 6912
+    pats = np.arange(0, 0x5F80, dtype=np.uint32)        # every bf16 value below 2^64
+    vals = np.concatenate([pats, pats | 0x8000]).astype(np.uint16)
+    m = 320                                # more than 256 rows: the many-row kernel
+    n_pat = -(-vals.size // k)
+    rng = np.random.default_rng(77)
+    x = synth.to_bf16_bits(rng.standard_normal((m, k)).astype(np.float32))
+    flat = np.zeros(n_pat * k, np.uint16)
+    flat[:vals.size] = vals
+    x[:n_pat] = flat.reshape(n_pat, k)
+    # ordinary rows with tiny values mixed in (subnormal quotients)
+    x[-4:, ::5] = synth.to_bf16_bits(np.full((4, (k + 4) // 5), 3e-38, np.float32))
+    x[-8:-4] = synth.to_bf16_bits((rng.standard_normal((4, k)) * 1e-36).astype(np.float32))
+    # 2^-60 .. 2^60: the quotients stay finite (non-finite ones are outside the contract)
+    delta = np.exp2(rng.uniform(-60, 60, k)).astype(np.float32)
+    delta[:64] = np.float32([1.0, 3.0, 1 / 3, 0.1, 1.9999999, 1.0000001, 127.0, 2.0 ** 20] * 8)
+    delta[64:128] = (np.arange(64, dtype=np.uint32) | 0x3FFFFFC0).view(np.float32)
+    q_o, s_o = oracle.quantize_act(x, delta)
+    qx, sx = w8a8.quantize_act(dev_bf16(x), dev_f32(delta))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(sx), s_o)
+    np.testing.assert_array_equal(w8a8.frag_to_rowmajor(host(qx), m, k), q_o)
+
+
 # ------------------------------------------------------------------ a1 / a2
 
 @pytest.mark.parametrize("alpha", [0.5, 0.3])
