@@ -453,8 +453,8 @@ w8a8_status w8a8_select_precision_map(const w8a8_stack_desc* desc, const void* x
    these process-wide overrides replace a choice: "GLU_TILE", "GEMM_TILE",
    "GEMM_SPLITS", "DOWN_TILE", "DOWN_SPLITS", "DOWN_WK", "WIDE_NW", "WIDE_WGS",
    "STREAM_WK", "STREAM_SPLITS", "GROUP_M", "ROTATE", "NO_QLOAD",
-   "NO_FUSED_GLUE", "NO_PERSISTENT", "DEC_SPIN_LIMIT".  Returns 0, or -1 for an
-   unknown name.  Not for production use: an override applies to every later
+   "NO_FUSED_GLUE", "NO_PERSISTENT", "DEC_SPIN_LIMIT", "XCD_M", "NT_OUT".
+   Returns 0, or -1 for an unknown name.  Not for production use: an override applies to every later
    call in the process, and changing one while another thread calls the library
    races with it. */
 int w8a8_set_plan_override(const char* name, int value);

@@ -51,7 +51,26 @@ struct Plan {
   int splits = 1;
   int kchunk = 0;
   int nbpb = 1;         // streaming: column blocks per workgroup
+  bool xcd_m = false;   // tiled: M tiles dealt to XCDs (A outweighs B)
+  bool nt_out = false;  // tiled: non-temporal output stores (very wide outputs)
 };
+
+void tile_shape(int tile, int* bm, int* bn);
+int plan_override(const char* name, int dflt);
+
+// Walk order and store policy of a tiled plan: when A (m x k) outweighs the
+// weights (n x k) and the M tiles split evenly over the 8 XCDs, each XCD
+// takes whole rows of tiles so its L2 holds its rows of A once (the down
+// projection at M = 2048 re-fetched its 14 MB A panel for every column tile
+// spread over the XCDs: 135 MB per launch); outputs of 64K columns and more
+// (the lm_head's logits) are stored non-temporally, so they do not evict A.
+void plan_order(Plan& p, int64_t m, int64_t n) {
+  if (p.stream) return;
+  int bm = 0, bn = 0;
+  tile_shape(p.tile, &bm, &bn);
+  p.xcd_m = m > n && ceil_div(m, bm) % 8 == 0 && plan_override("XCD_M", 1) != 0;
+  p.nt_out = n >= 65536 && plan_override("NT_OUT", 1) != 0;
+}
 
 // Planner overrides (w8a8_set_plan_override): experiments and the tests that
 // check that every plan gives the same results set them explicitly; the
@@ -60,7 +79,7 @@ constexpr int kUnset = INT32_MIN;
 const char* const kOverrideNames[] = {
     "GLU_TILE", "GEMM_TILE", "GEMM_SPLITS", "DOWN_TILE", "DOWN_SPLITS", "DOWN_WK",
     "WIDE_NW", "WIDE_WGS", "STREAM_WK", "STREAM_SPLITS", "GROUP_M", "ROTATE",
-    "NO_QLOAD", "NO_FUSED_GLUE", "NO_PERSISTENT", "DEC_SPIN_LIMIT"};
+    "NO_QLOAD", "NO_FUSED_GLUE", "NO_PERSISTENT", "DEC_SPIN_LIMIT", "XCD_M", "NT_OUT"};
 constexpr int kNumOverrides = (int)(sizeof(kOverrideNames) / sizeof(kOverrideNames[0]));
 std::atomic<int> g_override[kNumOverrides];
 struct OverrideInit {
@@ -220,6 +239,7 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
     if (glu || splits < 1) splits = 1;
     p.kchunk = (int)round_up(ceil_div(kb, splits), 2);
     p.splits = (int)ceil_div(kb, p.kchunk);
+    plan_order(p, m, n);
     return p;
   }
   // int8 choices from a sweep of the FFN shapes (d = 1152, f = 6912) at
@@ -271,6 +291,7 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
   if (glu || splits < 1) splits = 1;
   p.kchunk = (int)ceil_div(kb, splits);
   p.splits = (int)ceil_div(kb, p.kchunk);
+  plan_order(p, m, n);
   return p;
 }
 
@@ -349,6 +370,8 @@ w8a8_status run_gemm(const Plan& pl, int dt, int epi, const void* A, int64_t lda
   p.part = pl.splits > 1 ? gemm_ws : nullptr;
   p.group_m = plan_override("GROUP_M", 0);
   p.rotate = plan_override("ROTATE", 1);
+  p.xcd_m = pl.xcd_m ? 1 : 0;
+  p.nt_out = pl.nt_out ? 1 : 0;
   hipError_t e = pl.stream ? launch_gemm_stream(dt, epi, pl.mb, pl.nw, pl.wk, p, pl.nbpb, st)
                            : launch_gemm_tile(dt, epi, pl.tile, p, st);
   w8a8_status s = hip_check(e, pl.stream ? "gemm_stream" : "gemm_tile");
@@ -392,6 +415,8 @@ w8a8_status run_gemm_raw(const Plan& pl, int dt, const void* A, int64_t lda, int
   p.part = pl.splits > 1 ? part : nullptr;
   p.group_m = plan_override("GROUP_M", 0);
   p.rotate = plan_override("ROTATE", 1);
+  p.xcd_m = pl.xcd_m ? 1 : 0;
+  p.nt_out = pl.nt_out ? 1 : 0;
   const int epi = dt == DT_BF16 ? EPI_F32 : EPI_I32;  // raw sums (fp32 for float types)
   hipError_t e = pl.stream ? launch_gemm_stream(dt, epi, pl.mb, pl.nw, pl.wk, p, pl.nbpb, st)
                            : launch_gemm_tile(dt, epi, pl.tile, p, st);
@@ -533,6 +558,7 @@ Plan stack_down_plan(int64_t m, int64_t d, int64_t f) {
   const int splits = std::max(1, plan_override("DOWN_SPLITS", dflt_splits));
   p.kchunk = (int)ceil_div(kb, splits);
   p.splits = (int)ceil_div(kb, p.kchunk);
+  plan_order(p, m, d);
   return p;
 }
 

@@ -194,20 +194,32 @@ __global__ __launch_bounds__(64 * NW, MINB) void gemm_tile_kernel(GemmParams p) 
   const int n_tiles = (p.N + BN - 1) / BN;
   const int n_total = m_tiles * n_tiles;
   const int per_xcd = (n_total + 7) / 8;
-  const int t = (int)(blockIdx.x % 8) * per_xcd + (int)(blockIdx.x / 8);
-  if (t >= n_total) return;  // whole workgroup, before any barrier
-  int mt, nt;
-  if (p.group_m > 0 && p.group_m < m_tiles) {  // bands of group_m M tiles, N within a band
-    const int band_tiles = p.group_m * n_tiles;
-    const int band = t / band_tiles, in_band = t % band_tiles;
-    const int gm = min(p.group_m, m_tiles - band * p.group_m);
-    mt = band * p.group_m + in_band % gm;
-    nt = in_band / gm;
+  int mt, nt, z;
+  if (p.xcd_m) {
+    // workgroup ids are dealt to the XCDs round-robin: XCD x = id % 8 takes
+    // the M tiles x, x + 8, ... with every N tile and K split of each, so an
+    // XCD's L2 holds its own rows of A once
+    const int x = (int)(blockIdx.x % 8), j = (int)(blockIdx.x / 8);
+    const int per = n_tiles * p.splits;
+    mt = x + 8 * (j / per);
+    nt = (j % per) % n_tiles;
+    z = (j % per) / n_tiles;
+    if (mt >= m_tiles) return;  // whole workgroup, before any barrier
   } else {
-    mt = t % m_tiles;
-    nt = t / m_tiles;
+    const int t = (int)(blockIdx.x % 8) * per_xcd + (int)(blockIdx.x / 8);
+    if (t >= n_total) return;  // whole workgroup, before any barrier
+    if (p.group_m > 0 && p.group_m < m_tiles) {  // bands of group_m M tiles, N within a band
+      const int band_tiles = p.group_m * n_tiles;
+      const int band = t / band_tiles, in_band = t % band_tiles;
+      const int gm = min(p.group_m, m_tiles - band * p.group_m);
+      mt = band * p.group_m + in_band % gm;
+      nt = in_band / gm;
+    } else {
+      mt = t % m_tiles;
+      nt = t / m_tiles;
+    }
+    z = blockIdx.y;
   }
-  const int z = blockIdx.y;
   const int kb0 = z * p.kchunk;
   const int kb1 = min(p.kb_count, kb0 + p.kchunk);
   const int nk = kb1 - kb0;
@@ -446,7 +458,10 @@ __global__ __launch_bounds__(64 * NW, MINB) void gemm_tile_kernel(GemmParams p) 
       char* gp = dst + ((int64_t)row * ld + col) * esz;
       const int n_in = min(16 / esz, p.N - col);
       if (n_in == 16 / esz && ((reinterpret_cast<uintptr_t>(gp) & 15) == 0)) {
-        *reinterpret_cast<uint4*>(gp) = *reinterpret_cast<const uint4*>(srcp);
+        if (p.nt_out)  // output far larger than the caches: stream it past them
+          __builtin_nontemporal_store(*reinterpret_cast<const v4i*>(srcp), reinterpret_cast<v4i*>(gp));
+        else
+          *reinterpret_cast<uint4*>(gp) = *reinterpret_cast<const uint4*>(srcp);
       } else {
         for (int e = 0; e < n_in; ++e)
           for (int bb = 0; bb < esz; ++bb) gp[e * esz + bb] = srcp[e * esz + bb];
@@ -751,51 +766,52 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmParams p) {
 
 // ------------------------------------------------------------------ dispatch
 
+// Launch of one tile configuration: one workgroup per tile, 8 x ceil(tiles /
+// 8) dealt to the XCDs round-robin with a y dimension of K splits, or the
+// one-dimensional XCD-by-M grid (8 x ceil(M tiles / 8) x N tiles x splits).
+template <int DT, int BM, int BN, int WAVES_M, int NW, int EPI, int S, int KS, int MINB = 2>
+static hipError_t launch_tile(const GemmParams& p, hipStream_t st) {
+  const int mt = (p.M + BM - 1) / BM;
+  const int nt = (p.N + BN - 1) / BN;
+  const int per_xcd = (mt * nt + 7) / 8;
+  dim3 grid((unsigned)(8 * per_xcd), (unsigned)p.splits);
+  if (p.xcd_m) {
+    grid = dim3((unsigned)((mt + 7) / 8 * 8 * nt * p.splits), 1u);
+  }
+  gemm_tile_kernel<DT, BM, BN, WAVES_M, NW, EPI, S, KS, MINB><<<grid, 64 * NW, 0, st>>>(p);
+  return hipGetLastError();
+}
+
 // Tile shapes per type: FP8 needs stages of whole 128-deep MFMA steps, so only
 // the shapes with two fragment columns per stage exist for it.
 template <int DT, int EPI>
 static hipError_t tile_dispatch(int tile, const GemmParams& p, hipStream_t st) {
-  auto grid_for = [&](int bm, int bn) {
-    int mt = (p.M + bm - 1) / bm;
-    int nt = (p.N + bn - 1) / bn;
-    int per_xcd = (mt * nt + 7) / 8;
-    return dim3((unsigned)(8 * per_xcd), (unsigned)p.splits);
-  };
   constexpr bool K1 = DT != DT_F8;  // single-fragment stages available
   if constexpr (EPI == EPI_GLU) {
     switch (tile) {
       case TILE_GLU_128x32_K2:
-        gemm_tile_kernel<DT, 128, 32, 4, 4, EPI, 6, 2><<<grid_for(128, 32), 256, 0, st>>>(p);
-        return hipGetLastError();
+        return launch_tile<DT, 128, 32, 4, 4, EPI, 6, 2>(p, st);
       case TILE_GLU_64x64_K2:
-        gemm_tile_kernel<DT, 64, 64, 2, 4, EPI, 3, 2><<<grid_for(64, 64), 256, 0, st>>>(p);
-        return hipGetLastError();
+        return launch_tile<DT, 64, 64, 2, 4, EPI, 3, 2>(p, st);
       case TILE_GLU_256x64_K2_W8:  // 144 KiB of LDS: one workgroup per CU
-        gemm_tile_kernel<DT, 256, 64, 4, 8, EPI, 3, 2, 1><<<grid_for(256, 64), 512, 0, st>>>(p);
-        return hipGetLastError();
+        return launch_tile<DT, 256, 64, 4, 8, EPI, 3, 2, 1>(p, st);
       default:
         break;
     }
     if constexpr (K1) {
       switch (tile) {
         case TILE_GLU_128x32:
-          gemm_tile_kernel<DT, 128, 32, 4, 4, EPI, 12, 1><<<grid_for(128, 32), 256, 0, st>>>(p);
-          return hipGetLastError();
+          return launch_tile<DT, 128, 32, 4, 4, EPI, 12, 1>(p, st);
         case TILE_GLU_64x64:
-          gemm_tile_kernel<DT, 64, 64, 2, 4, EPI, 6, 1><<<grid_for(64, 64), 256, 0, st>>>(p);
-          return hipGetLastError();
+          return launch_tile<DT, 64, 64, 2, 4, EPI, 6, 1>(p, st);
         case TILE_GLU_128x64:
-          gemm_tile_kernel<DT, 128, 64, 2, 4, EPI, 5, 1><<<grid_for(128, 64), 256, 0, st>>>(p);
-          return hipGetLastError();
+          return launch_tile<DT, 128, 64, 2, 4, EPI, 5, 1>(p, st);
         case TILE_GLU_256x128:
-          gemm_tile_kernel<DT, 256, 128, 2, 8, EPI, 5, 1><<<grid_for(256, 128), 512, 0, st>>>(p);
-          return hipGetLastError();
+          return launch_tile<DT, 256, 128, 2, 8, EPI, 5, 1>(p, st);
         case TILE_GLU_256x64:
-          gemm_tile_kernel<DT, 256, 64, 2, 4, EPI, 3, 1><<<grid_for(256, 64), 256, 0, st>>>(p);
-          return hipGetLastError();
+          return launch_tile<DT, 256, 64, 2, 4, EPI, 3, 1>(p, st);
         case TILE_GLU_128x32_K3:  // 144 KiB of LDS: one workgroup per CU
-          gemm_tile_kernel<DT, 128, 32, 4, 4, EPI, 4, 3, 1><<<grid_for(128, 32), 256, 0, st>>>(p);
-          return hipGetLastError();
+          return launch_tile<DT, 128, 32, 4, 4, EPI, 4, 3, 1>(p, st);
         default:
           break;
       }
@@ -803,34 +819,26 @@ static hipError_t tile_dispatch(int tile, const GemmParams& p, hipStream_t st) {
   } else {
     switch (tile) {
       case TILE_64x64_K2:
-        gemm_tile_kernel<DT, 64, 64, 2, 4, EPI, 3, 2><<<grid_for(64, 64), 256, 0, st>>>(p);
-        return hipGetLastError();
+        return launch_tile<DT, 64, 64, 2, 4, EPI, 3, 2>(p, st);
       case TILE_128x128_K2:
-        gemm_tile_kernel<DT, 128, 128, 2, 4, EPI, 3, 2><<<grid_for(128, 128), 256, 0, st>>>(p);
-        return hipGetLastError();
+        return launch_tile<DT, 128, 128, 2, 4, EPI, 3, 2>(p, st);
       default:
         break;
     }
     if constexpr (K1) {
       switch (tile) {
         case TILE_128x128:
-          gemm_tile_kernel<DT, 128, 128, 2, 4, EPI, 5, 1><<<grid_for(128, 128), 256, 0, st>>>(p);
-          return hipGetLastError();
+          return launch_tile<DT, 128, 128, 2, 4, EPI, 5, 1>(p, st);
         case TILE_128x64:
-          gemm_tile_kernel<DT, 128, 64, 2, 4, EPI, 6, 1><<<grid_for(128, 64), 256, 0, st>>>(p);
-          return hipGetLastError();
+          return launch_tile<DT, 128, 64, 2, 4, EPI, 6, 1>(p, st);
         case TILE_64x64:
-          gemm_tile_kernel<DT, 64, 64, 2, 4, EPI, 6, 1><<<grid_for(64, 64), 256, 0, st>>>(p);
-          return hipGetLastError();
+          return launch_tile<DT, 64, 64, 2, 4, EPI, 6, 1>(p, st);
         case TILE_256x128:
-          gemm_tile_kernel<DT, 256, 128, 2, 8, EPI, 5, 1><<<grid_for(256, 128), 512, 0, st>>>(p);
-          return hipGetLastError();
+          return launch_tile<DT, 256, 128, 2, 8, EPI, 5, 1>(p, st);
         case TILE_256x256:
-          gemm_tile_kernel<DT, 256, 256, 2, 8, EPI, 5, 1><<<grid_for(256, 256), 512, 0, st>>>(p);
-          return hipGetLastError();
+          return launch_tile<DT, 256, 256, 2, 8, EPI, 5, 1>(p, st);
         case TILE_64x64_K3:  // 96 KiB of LDS: one workgroup per CU
-          gemm_tile_kernel<DT, 64, 64, 2, 8, EPI, 4, 3, 1><<<grid_for(64, 64), 512, 0, st>>>(p);
-          return hipGetLastError();
+          return launch_tile<DT, 64, 64, 2, 8, EPI, 4, 3, 1>(p, st);
         default:
           break;
       }

@@ -56,6 +56,13 @@ struct GemmParams {
   // of all M tiles); rotate: start each workgroup's K walk at a different step.
   int group_m = 0;
   int rotate = 1;
+  // xcd_m: one-dimensional grid of m_tiles x n_tiles x splits workgroups,
+  // M tiles dealt to the 8 XCDs (M tile mt on XCD mt % 8, with all its N tiles
+  // and K splits), for products whose A panel outweighs B (set only when
+  // m_tiles % 8 == 0).  nt_out: output stores marked non-temporal (outputs
+  // far larger than the L2, e.g. the logits, so they do not evict the operands).
+  int xcd_m = 0;
+  int nt_out = 0;
 };
 
 // Operand / accumulator types of the GEMM kernels (the launchers take an int;

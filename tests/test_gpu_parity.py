@@ -253,8 +253,15 @@ def test_gemm_i32_bit_exact(m, n, k):
 
 
 @pytest.mark.parametrize("m,n,k,splits", [(128, 1152, 6912, 1), (128, 1152, 6912, 3),
-                                          (300, 640, 1152, 7), (96, 2048, 6912, 2)])
+                                          (300, 640, 1152, 7), (96, 2048, 6912, 2),
+                                          (128, 1152, 6912, 5), (2048, 1152, 6912, 3),
+                                          (1024, 1152, 6912, 3)])
 def test_gemm_split_k_is_bit_identical(m, n, k, splits, monkeypatch):
+    """Every tile shape, K split and walk order gives the exact sums.  Five
+    splits of the 108 fragment columns of K = 6912 leave chunks of 22 and 20,
+    so the three-column-stage tiles run ragged last stages (22 = 3 * 7 + 1,
+    20 = 3 * 6 + 2); M > N with M tiles in multiples of 8 takes the walk that
+    deals M tiles to the XCDs, compared with the default walk."""
     say("split-K", m, n, k, splits)
     rng = np.random.default_rng(99 + splits)
     qa = rng.integers(-127, 128, (m, k), dtype=np.int8)
@@ -263,11 +270,34 @@ def test_gemm_split_k_is_bit_identical(m, n, k, splits, monkeypatch):
     A = torch.from_numpy(w8a8.rowmajor_to_frag(qa)).to(DEV)
     B = torch.from_numpy(w8a8.rowmajor_to_frag(qb)).to(DEV)
     w8a8.set_plan_override("GEMM_SPLITS", splits)
-    for tile in (0, 1, 2, 3, 7, 10, 11, 16):
-        w8a8.set_plan_override("GEMM_TILE", tile)
-        acc = w8a8.gemm_i8_i32(A, m, B, n, k)
-        torch.cuda.synchronize()
-        np.testing.assert_array_equal(host(acc), acc_o, err_msg="tile %d" % tile)
+    for xcd in ((0, 1) if m > n else (1,)):
+        w8a8.set_plan_override("XCD_M", xcd)
+        for tile in (0, 1, 2, 3, 7, 10, 11, 16):
+            w8a8.set_plan_override("GEMM_TILE", tile)
+            acc = w8a8.gemm_i8_i32(A, m, B, n, k)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(host(acc), acc_o, err_msg="tile %d xcd %d" % (tile, xcd))
+
+
+@pytest.mark.parametrize("d", [1024, 1088])
+def test_gate_up_three_column_tile_ragged_stages(d):
+    """The gated tile with three fragment columns a stage on K = 1024 (16
+    fragment columns: last stage 1 column) and 1088 (17: last stage 2)."""
+    say("gate/up three-column tile, d =", d)
+    m, f = 96, 512
+    cfg = synth.ffn_config(m=m, d=d, f=f)
+    q = oracle.quantize_ffn(cfg["w_gate"], cfg["w_up"], cfg["w_down"], cfg["x_cal"][:64])
+    layer = w8a8.FfnW8A8.from_weights(dev_bf16(cfg["w_gate"]), dev_bf16(cfg["w_up"]),
+                                      dev_bf16(cfg["w_down"]), dev_f32(q["delta_gu"]),
+                                      dev_f32(q["delta_down"]))
+    _, st = oracle.w8a8_ffn(cfg["x"], q, stages=True)
+    qx = torch.from_numpy(w8a8.rowmajor_to_frag(st["qx"])).to(DEV)
+    w8a8.set_plan_override("GLU_TILE", 15)
+    h = host_bf16(w8a8.ffn_gate_up(layer, qx, dev_f32(st["sx"]), m))
+    w8a8.set_plan_override("GLU_TILE", 4)
+    h_ref = host_bf16(w8a8.ffn_gate_up(layer, qx, dev_f32(st["sx"]), m))
+    np.testing.assert_array_equal(h, h_ref)
+    assert geglu_mismatch_ok(geglu_ulp_diff(h, st["h"], st["g"], st["u"]))
 
 
 # ------------------------------------------------------------------ a5: linear
