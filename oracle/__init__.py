@@ -15,7 +15,10 @@ those functions in the order the paper states:
 * dynamic per-token activation quantisation, eq. ``stx`` / ``xint8`` (Sec. 6);
 * the INT8 product and its two-scale dequantisation, eq. ``gemm-final``;
 * the gated FFN between the projections (Sec. 3, Tab. 1 ``fused_fc``/``proj``);
-* the FFN layer subsets, eq. ``ffn55`` / ``ffn1010`` / ``ffnall26``.
+* the FFN layer subsets, eq. ``ffn55`` / ``ffn1010`` / ``ffnall26``;
+* the attention-projection layer subsets and the INT8 key/value cache with the
+  one-token attention that reads it (Sec. 4, further speed-ups; Sec. 5, eq.
+  ``attnffn55`` / ``attnffn1010``).
 
 bf16 tensors are passed as ``numpy.uint16`` bit patterns.
 """
@@ -82,6 +85,7 @@ def _L():
             "orc_quant_rows_fp8": [P, I64, I64, P, ctypes.c_int, P, P],
             "orc_gemm_fp8": [P, P, I64, I64, I64, P],
             "orc_dequant_fp8": [P, P, P, I64, I64, P],
+            "orc_attn_decode_f64": [P, I64, I64, P, P, I64, D, P],
         }
         for name, args in sigs.items():
             fn = getattr(lib, name)
@@ -535,3 +539,114 @@ def select_map(x_bf16, layers, budget_db, return_trace=False):
     if return_trace:
         return prec, best, iso, trace
     return prec, best
+
+
+# ---------------------------------------------------------------- f4: attention decode with a KV cache
+
+HEAD_DIM = 256      # Sec. 2: four query heads and one key/value head of 256
+N_Q_HEADS = 4
+ATTN_SCALE = 1.0 / 16.0   # 1 / sqrt(head dim)
+GLOBAL_LAYERS = (0, 6, 12, 18)   # Sec. 2: the layers that attend the whole context
+LOCAL_WINDOW = 1024              # Sec. 2: sliding window of the other layers
+
+
+def kv_quantize(kv_bf16):
+    """INT8 key/value cache rows: the per-token rule of eq. stx / xint8 with no
+    smoothing (delta = 1): s_t = max_d |k_td| / 127, codes rne(k / s_t)
+    clamped to [-127, 127]; an all-zero row stores s = 0 and zero codes."""
+    return quant_rows(kv_bf16, None, MODE_DIV)
+
+
+def kv_dequant(codes, scales) -> np.ndarray:
+    """k = s_t * code, exact in binary64."""
+    return _c(codes, np.int8).astype(np.float64) * _c(scales, np.float32).astype(np.float64)[:, None]
+
+
+def attn_decode(q, k, v, scale=ATTN_SCALE) -> np.ndarray:
+    """One query token with h heads (rows of q) against t cached rows of one
+    shared key/value head: softmax(scale q k^T) v per head, binary64."""
+    q = np.ascontiguousarray(q, dtype=np.float64)
+    k = np.ascontiguousarray(k, dtype=np.float64)
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    h, dh = q.shape
+    t = k.shape[0]
+    assert k.shape == (t, dh) and v.shape == (t, dh) and t >= 1
+    out = np.empty((h, dh), np.float64)
+    _L().orc_attn_decode_f64(_p(q), h, dh, _p(k), _p(v), t, float(scale), _p(out))
+    return out
+
+
+def kv_cache(t_max, int8=True, head_dim=HEAD_DIM):
+    """An empty key/value cache of t_max rows: INT8 codes with per-row scales,
+    or bf16 rows."""
+    if int8:
+        return dict(int8=True, k=np.zeros((t_max, head_dim), np.int8), sk=np.zeros(t_max, np.float32),
+                    v=np.zeros((t_max, head_dim), np.int8), sv=np.zeros(t_max, np.float32))
+    return dict(int8=False, k=np.zeros((t_max, head_dim), np.uint16),
+                v=np.zeros((t_max, head_dim), np.uint16))
+
+
+def kv_fill(cache, t0, k_bf16, v_bf16):
+    """Write rows t0 .. t0 + n - 1 of the cache from bf16 keys and values."""
+    n = k_bf16.shape[0]
+    if cache["int8"]:
+        cache["k"][t0:t0 + n], cache["sk"][t0:t0 + n] = kv_quantize(k_bf16)
+        cache["v"][t0:t0 + n], cache["sv"][t0:t0 + n] = kv_quantize(v_bf16)
+    else:
+        cache["k"][t0:t0 + n] = k_bf16
+        cache["v"][t0:t0 + n] = v_bf16
+
+
+def kv_rows(cache, t0, t1):
+    """Cached keys and values of rows t0 .. t1 - 1 as binary64."""
+    if cache["int8"]:
+        return (kv_dequant(cache["k"][t0:t1], cache["sk"][t0:t1]),
+                kv_dequant(cache["v"][t0:t1], cache["sv"][t0:t1]))
+    return (bf16_to_f32(cache["k"][t0:t1]).astype(np.float64),
+            bf16_to_f32(cache["v"][t0:t1]).astype(np.float64))
+
+
+def attn_block_decode(qkv_bf16, cache, pos, window, n_heads=N_Q_HEADS, head_dim=HEAD_DIM):
+    """The attention of one decode step: the projection output row [q heads |
+    k | v] (bf16) appends its key and value at row pos of the cache, then the
+    query heads attend rows max(0, pos + 1 - window) .. pos.  Returns the
+    attention output (n_heads x head_dim, concatenated) rounded once to bf16,
+    the input of the O projection."""
+    qkv = _c(qkv_bf16, np.uint16).reshape(-1)
+    nq = n_heads * head_dim
+    assert qkv.size == nq + 2 * head_dim
+    kv_fill(cache, pos, qkv[nq:nq + head_dim][None, :], qkv[nq + head_dim:][None, :])
+    t0 = max(0, pos + 1 - window)
+    k, v = kv_rows(cache, t0, pos + 1)
+    q = bf16_to_f32(qkv[:nq]).astype(np.float64).reshape(n_heads, head_dim)
+    return f64_to_bf16(attn_decode(q, k, v).reshape(-1))
+
+
+def attn_window(layer: int, context: int) -> int:
+    """Rows a layer attends (Sec. 2): the whole context in the global layers,
+    the sliding window in the others."""
+    return context if layer in GLOBAL_LAYERS else LOCAL_WINDOW
+
+
+def attn_precision_map(name: str, n_layers: int = N_LAYERS) -> np.ndarray:
+    """Q_ATT: the layers whose QKV and O projections run in INT8.  The paper's
+    Attn+FFN configurations take Q_ATT = L (eq. attnffn55 / attnffn1010) and
+    name blockwise attention subsets by analogy with the FFN ones as a further
+    direction (Sec. 4), so the FFN sets of eq. ffn55 / ffn1010 / ffnall26 serve
+    for Q_ATT too; "none" keeps every projection in bf16."""
+    return precision_map("bf16" if name == "none" else name, n_layers)
+
+
+def attn_block_proj_decode(x_bf16, xo_bf16, L, int8):
+    """The two projections of one attention block at one token: the fused QKV
+    projection of the block input and the O projection of the attention
+    output, INT8 (eq. gemm-final, one shared quantisation of x for Q, K and V)
+    or bf16.  L holds w_qkv, w_o (bf16) and, for INT8, their codes, scales and
+    smoothing vectors."""
+    if int8:
+        qkv = w8a8_linear(x_bf16, L["wq_qkv"], L["s_qkv"], L["delta_qkv"], "bf16")
+        o = w8a8_linear(xo_bf16, L["wq_o"], L["s_o"], L["delta_o"], "bf16")
+    else:
+        qkv = bf16_linear(x_bf16, L["w_qkv"])
+        o = bf16_linear(xo_bf16, L["w_o"])
+    return qkv, o

@@ -358,3 +358,41 @@ void orc_rmsnorm_f64(const float* x, int64_t m, int64_t d, double eps, double* y
         for (int64_t j = 0; j < d; ++j) y[t * d + j] = (double)x[t * d + j] * inv;
     }
 }
+
+/* ------------------------------------------------------------------ */
+/* f4  One-token attention over a key/value cache (Sec. 4 lists an     */
+/* INT8 key/value cache among the further speed-ups; Sec. 2 gives the   */
+/* grouped-query layout: several query heads share one key/value head)  */
+/* ------------------------------------------------------------------ */
+
+/* q is h x dh (the query heads of one token), k and v are t x dh (the rows of
+   the one shared key/value head), all binary64.  For every head i:
+     score_t = scale * sum_d q[i][d] * k[t][d]
+     p_t     = exp(score_t - max_u score_u) / sum_u exp(score_u - max_u score_u)
+     out[i][d] = sum_t p_t * v[t][d]
+   Subtracting the maximum leaves p unchanged and keeps every exp finite. */
+void orc_attn_decode_f64(const double* q, int64_t h, int64_t dh, const double* k,
+                         const double* v, int64_t t, double scale, double* out) {
+    for (int64_t i = 0; i < h; ++i) {
+        const double* qi = q + i * dh;
+        double* oi = out + i * dh;
+        double mx = -INFINITY;
+        for (int64_t u = 0; u < t; ++u) {
+            double sc = 0.0;
+            for (int64_t d = 0; d < dh; ++d) sc += qi[d] * k[u * dh + d];
+            sc *= scale;
+            if (sc > mx) mx = sc;
+        }
+        double den = 0.0;
+        for (int64_t d = 0; d < dh; ++d) oi[d] = 0.0;
+        for (int64_t u = 0; u < t; ++u) {
+            double sc = 0.0;
+            for (int64_t d = 0; d < dh; ++d) sc += qi[d] * k[u * dh + d];
+            sc *= scale;
+            double p = exp(sc - mx);
+            den += p;
+            for (int64_t d = 0; d < dh; ++d) oi[d] += p * v[u * dh + d];
+        }
+        for (int64_t d = 0; d < dh; ++d) oi[d] /= den;
+    }
+}
