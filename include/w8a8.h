@@ -69,6 +69,7 @@ typedef enum {
 typedef enum { W8A8_F32 = 0, W8A8_BF16 = 1 } w8a8_dtype;
 
 #define W8A8_MAX_K 133144
+#define W8A8_HEAD_DIM 256   /* attention head width (Sec. 2, Tab. 2) */
 
 /* One INT8 linear layer y = x W^T (Sec. 6): packed codes of W_hat = W diag(delta)
    (n x k, fragment layout), their per-output-channel scales s_w[n], and the
@@ -444,6 +445,55 @@ int w8a8_rank_layers(const float* isolated_db, int n_layers, int* order);
 w8a8_status w8a8_select_precision_map(const w8a8_stack_desc* desc, const void* x, int64_t m,
                                       float budget_db, uint8_t* prec, float* final_db,
                                       void* ws, size_t ws_bytes, w8a8_stream_t stream);
+
+/* ---------------------------------------------------------------- f4: key/value cache, attention decode */
+
+/* Sec. 4 lists an INT8 key/value cache among the further speed-ups, and Sec. 2
+   gives the attention layout: four query heads share one key/value head of
+   256 (grouped-query attention).  The cache of one layer is t_max rows of 256:
+   either INT8 codes (row-major, 256 B a row) with one binary32 scale per row,
+   or bf16 rows (512 B).  A row is quantised by the per-token rule of eq. stx /
+   xint8 without smoothing: s = max_d |k_d| / 127, codes rne(k / s) clamped to
+   [-127, 127] (an all-zero row stores s = 0 and zero codes), the same rule and
+   results as w8a8_quantize_act with delta = NULL.  The caller owns the cache
+   and every buffer below; the library keeps no state. */
+
+/* Rows of 256 bf16 values (row r at kv + r * ld elements, ld >= 256 and a
+   multiple of 8; e.g. the key part of a fused QKV projection output) ->
+   codes[rows][256] and scales[rows] (kv and codes 16-byte aligned, scales
+   4-byte aligned, so row slices of a cache can be filled).  EINVAL for NULL
+   or unaligned pointers, rows < 1 or a bad ld. */
+w8a8_status w8a8_kv_quantize(const void* kv, int64_t rows, int64_t ld, int8_t* codes,
+                             float* scales, w8a8_stream_t stream);
+
+/* Workspace of one attention decode call on a cache of t_max rows (any pos and
+   window); 0 when one workgroup covers the rows. */
+size_t w8a8_attn_decode_workspace_bytes(int64_t t_max);
+
+/* One decode step of attention (Sec. 2 layout, Sec. 4 INT8 cache): qkv is the
+   current token's projection output in bf16, [n_heads x 256 query | 256 key |
+   256 value] (the fused QKV projection's row).  The key and value are
+   quantised as above and stored at row pos of the cache, then every query
+   head attends rows t0 .. pos, t0 = max(0, pos + 1 - window) (window = the
+   context for the global layers, the sliding window for the others):
+     out[h] = sum_t softmax_t(q_h . k_t / 16) v_t,   k_t = s_t * code (INT8 cache),
+   scores and sums in binary32, out (n_heads x 256, bf16, the O projection's
+   input) rounded once.  n_heads in {1, 2, 4, 8}; 0 <= pos < t_max; rows
+   t0 .. pos - 1 must hold earlier tokens.  ws: w8a8_attn_decode_workspace_bytes
+   (t_max) bytes (may be NULL when that is 0).  EUNSUPPORTED for other head
+   counts, EINVAL for a bad pos, window or pointer, EWORKSPACE if ws is short.
+   Two calls on one cache must be ordered (the second may read the first's
+   row). */
+w8a8_status w8a8_attn_decode(const void* qkv, int n_heads, int64_t pos, int64_t window,
+                             int8_t* k_codes, float* k_scales, int8_t* v_codes, float* v_scales,
+                             int64_t t_max, void* out, void* ws, size_t ws_bytes,
+                             w8a8_stream_t stream);
+
+/* The same step on a bf16 cache (k_rows, v_rows: bf16 [t_max][256]): the
+   baseline the INT8 cache is measured against. */
+w8a8_status w8a8_attn_decode_bf16(const void* qkv, int n_heads, int64_t pos, int64_t window,
+                                  void* k_rows, void* v_rows, int64_t t_max, void* out, void* ws,
+                                  size_t ws_bytes, w8a8_stream_t stream);
 
 /* ---------------------------------------------------------------- planner overrides */
 

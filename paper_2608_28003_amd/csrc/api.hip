@@ -1710,4 +1710,77 @@ int w8a8_rank_layers(const float* isolated_db, int n_layers, int* order) {
   return 0;
 }
 
+// ---------------------------------------------------------------- f4: key/value cache and attention decode
+
+size_t w8a8_attn_decode_workspace_bytes(int64_t t_max) {
+  return t_max >= 1 ? attn_ws_bytes_max(t_max) : 0;
+}
+
+w8a8_status w8a8_kv_quantize(const void* kv, int64_t rows, int64_t ld, int8_t* codes,
+                             float* scales, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(kv);
+  CHECK_PTR(codes);
+  // one binary32 store per row: a slice of a scale array need only be 4-byte aligned
+  REQUIRE(scales && ((uintptr_t)scales & 3) == 0, W8A8_EINVAL, "scales is NULL or not 4-byte aligned");
+  REQUIRE(rows >= 1, W8A8_EINVAL, "rows < 1");
+  REQUIRE(ld >= W8A8_HEAD_DIM && ld % 8 == 0, W8A8_EINVAL, "ld must be >= 256 and a multiple of 8");
+  return hip_check(launch_kv_quant((const uint16_t*)kv, rows, ld, codes, scales, S(stream)),
+                   "kv_quant");
+}
+
+namespace {
+w8a8_status attn_common(const void* qkv, int n_heads, int64_t pos, int64_t window, int64_t t_max,
+                        void* out, void* ws, size_t ws_bytes, AttnParams* p) {
+  CHECK_PTR(qkv);
+  CHECK_PTR(out);
+  REQUIRE(n_heads == 1 || n_heads == 2 || n_heads == 4 || n_heads == 8, W8A8_EUNSUPPORTED,
+          "n_heads must be 1, 2, 4 or 8");
+  REQUIRE(t_max >= 1 && pos >= 0 && pos < t_max, W8A8_EINVAL, "pos outside [0, t_max)");
+  REQUIRE(window >= 1, W8A8_EINVAL, "window < 1");
+  p->qkv = (const uint16_t*)qkv;
+  p->out = (uint16_t*)out;
+  p->pos = pos;
+  p->t0 = std::max<int64_t>(0, pos + 1 - window);
+  const size_t need = attn_ws_bytes(pos + 1 - p->t0);
+  if (need) {
+    CHECK_PTR(ws);
+    REQUIRE(ws_bytes >= need, W8A8_EWORKSPACE, "workspace too small");
+  }
+  p->part = (float*)ws;
+  return W8A8_OK;
+}
+}  // namespace
+
+w8a8_status w8a8_attn_decode(const void* qkv, int n_heads, int64_t pos, int64_t window,
+                             int8_t* k_codes, float* k_scales, int8_t* v_codes, float* v_scales,
+                             int64_t t_max, void* out, void* ws, size_t ws_bytes,
+                             w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(k_codes);
+  CHECK_PTR(v_codes);
+  CHECK_PTR(k_scales);
+  CHECK_PTR(v_scales);
+  AttnParams p;
+  CHECK(attn_common(qkv, n_heads, pos, window, t_max, out, ws, ws_bytes, &p));
+  p.k = k_codes;
+  p.v = v_codes;
+  p.sk = k_scales;
+  p.sv = v_scales;
+  return hip_check(launch_attn_decode(p, n_heads, true, S(stream)), "attn_decode");
+}
+
+w8a8_status w8a8_attn_decode_bf16(const void* qkv, int n_heads, int64_t pos, int64_t window,
+                                  void* k_rows, void* v_rows, int64_t t_max, void* out, void* ws,
+                                  size_t ws_bytes, w8a8_stream_t stream) {
+  g_last_error.clear();
+  CHECK_PTR(k_rows);
+  CHECK_PTR(v_rows);
+  AttnParams p;
+  CHECK(attn_common(qkv, n_heads, pos, window, t_max, out, ws, ws_bytes, &p));
+  p.k = k_rows;
+  p.v = v_rows;
+  return hip_check(launch_attn_decode(p, n_heads, false, S(stream)), "attn_decode_bf16");
+}
+
 }  // extern "C"

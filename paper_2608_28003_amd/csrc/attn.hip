@@ -1,0 +1,373 @@
+// One-token attention over a key/value cache, with the cache held as INT8
+// codes and per-row scales or as bf16 rows (Sec. 4 names the INT8 key/value
+// cache among the further speed-ups; Sec. 2: four query heads share one
+// key/value head of 256, grouped-query attention).
+//
+// The cache of one layer is a row-major array of t_max rows of 256: INT8
+// codes (256 B a row) with one binary32 scale per row, or bf16 (512 B a row).
+// A decode step appends the current token's key and value at row pos and
+// attends rows t0 .. pos with every query head.  The work is split over the
+// rows: each workgroup walks its range in passes of 64 rows with a running
+// maximum and sum per head (the softmax is formed exactly as one pass would
+// form it, up to binary32 rounding), and a second launch merges the
+// workgroups' partial results.  The workgroup whose range holds row pos
+// quantises (or copies) the new key and value, stores them in the cache and
+// uses them from LDS, so no other workgroup reads the row being written.
+#include <algorithm>
+
+#include "device.h"
+#include "kernels.h"
+
+namespace w8a8 {
+
+namespace {
+
+constexpr int kHd = 256;       // head dimension
+constexpr int kPass = 64;      // cached rows per pass of a workgroup (16 per wave)
+constexpr int kMaxHeads = 8;
+
+// Codes of one 256-wide row held 4 per lane by one wave: the per-token rule
+// (s = max |x| / 127, codes rne(x / s) clamped to +-127, zero row -> s = 0).
+__device__ __forceinline__ uint32_t quant_row4(const float (&v)[4], float* s_out) {
+  float a = fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3])));
+  const float amax = wave_max(a);
+  const float s = amax / 127.0f;
+  uint32_t packed = 0;
+  if (s != 0.0f) {
+    const float inv = 1.0f / s;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      packed |= (uint32_t)(uint8_t)code_of(v[e], s, inv, true) << (8 * e);
+  }
+  *s_out = s;
+  return packed;
+}
+
+__device__ __forceinline__ void load_bf16x4(const uint16_t* p, float (&v)[4]) {
+  const uint2 raw = *reinterpret_cast<const uint2*>(p);
+  v[0] = bf16_bits_to_float(raw.x & 0xffffu);
+  v[1] = bf16_bits_to_float(raw.x >> 16);
+  v[2] = bf16_bits_to_float(raw.y & 0xffffu);
+  v[3] = bf16_bits_to_float(raw.y >> 16);
+}
+
+__device__ __forceinline__ float byte_f(uint32_t w, int e) {
+  return (float)(int8_t)(uint8_t)(w >> (8 * e));
+}
+
+}  // namespace
+
+// One wave per row of 256 bf16 values (stride ld elements): INT8 codes
+// (row-major, 256 a row) and the row's scale.
+__global__ __launch_bounds__(256) void kv_quant_kernel(const uint16_t* __restrict__ src,
+                                                       int64_t rows, int64_t ld,
+                                                       int8_t* __restrict__ codes,
+                                                       float* __restrict__ scales) {
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= rows) return;  // whole wave
+  const int l = lane_id();
+  float v[4];
+  load_bf16x4(src + r * ld + 4 * l, v);
+  float s;
+  const uint32_t packed = quant_row4(v, &s);
+  *reinterpret_cast<uint32_t*>(codes + r * kHd + 4 * l) = packed;
+  if (l == 0) scales[r] = s;
+}
+
+// Partial results of one workgroup: per head the running maximum m and sum l
+// of exp(score - m), and the unnormalised output o (256 values).
+constexpr int kPartFloats = 2 * kMaxHeads + kMaxHeads * kHd;
+
+template <bool I8, int NH>
+__global__ __launch_bounds__(256) void attn_decode_kernel(AttnParams p) {
+  __shared__ float qs[NH][kHd];
+  __shared__ float sc[NH][kPass];     // scores, then weights p (x the row's value scale)
+  __shared__ float corr[NH];          // rescale of the running sums for this pass
+  __shared__ float run_m[NH], run_l[NH];
+  __shared__ float ored[4][NH][kHd];  // the four waves' partial outputs
+  __shared__ uint32_t knew[kHd / 2], vnew[kHd / 2];  // the new row (codes or bf16 bits)
+  __shared__ float knew_s, vnew_s;
+
+  const int tid = threadIdx.x, w = tid >> 6, l = lane_id();
+  const int64_t r_begin = p.t0 + (int64_t)blockIdx.x * p.rows_per_wg;
+  const int64_t r_end = min(r_begin + p.rows_per_wg, p.pos + 1);  // exclusive
+
+  for (int i = tid; i < NH * kHd; i += 256) qs[i / kHd][i % kHd] = bf16_bits_to_float(p.qkv[i]);
+  if (tid < NH) {
+    run_m[tid] = -INFINITY;
+    run_l[tid] = 0.0f;
+  }
+  const bool has_new = r_end == p.pos + 1;
+  if (has_new && w < 2) {  // wave 0: the key, wave 1: the value
+    const uint16_t* src = p.qkv + NH * kHd + w * kHd + 4 * l;
+    if constexpr (I8) {
+      float v[4], s;
+      load_bf16x4(src, v);
+      const uint32_t packed = quant_row4(v, &s);
+      int8_t* dst = reinterpret_cast<int8_t*>(w == 0 ? p.k : p.v) + p.pos * kHd;
+      *reinterpret_cast<uint32_t*>(dst + 4 * l) = packed;
+      (w == 0 ? knew : vnew)[l] = packed;
+      if (l == 0) {
+        (w == 0 ? p.sk : p.sv)[p.pos] = s;
+        if (w == 0) knew_s = s; else vnew_s = s;
+      }
+    } else {
+      const uint2 raw = *reinterpret_cast<const uint2*>(src);
+      uint16_t* dst = reinterpret_cast<uint16_t*>(w == 0 ? p.k : p.v) + p.pos * kHd;
+      *reinterpret_cast<uint2*>(dst + 4 * l) = raw;
+      (w == 0 ? knew : vnew)[2 * l] = raw.x;
+      (w == 0 ? knew : vnew)[2 * l + 1] = raw.y;
+    }
+  }
+  __syncthreads();
+
+  // per lane: 4 output dimensions (4l .. 4l + 3) of every head, summed over
+  // the rows this wave handles
+  float o[NH][4];
+#pragma unroll
+  for (int h = 0; h < NH; ++h)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[h][e] = 0.0f;
+
+  const int jr = l >> 2, qd = l & 3;  // score phase: row 16w + jr, dimensions 64 qd ..
+  for (int64_t r0 = r_begin; r0 < r_end; r0 += kPass) {
+    // ---- values of this wave's 16 rows (loaded first, used after the softmax)
+    uint32_t vv[16][I8 ? 1 : 2];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int64_t row = r0 + 16 * w + i;
+      if (row < r_end && row != p.pos) {
+        if constexpr (I8) {
+          vv[i][0] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const int8_t*>(p.v) +
+                                                       row * kHd + 4 * l);
+        } else {
+          const uint2 raw = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(p.v) +
+                                                           row * kHd + 4 * l);
+          vv[i][0] = raw.x;
+          vv[i][1] = raw.y;
+        }
+      } else if (row == p.pos) {
+        vv[i][0] = I8 ? vnew[l] : vnew[2 * l];
+        if constexpr (!I8) vv[i][1] = vnew[2 * l + 1];
+      } else {
+        vv[i][0] = 0;
+        if constexpr (!I8) vv[i][1] = 0;
+      }
+    }
+    // ---- scores: four lanes per row, 64 dimensions each
+    {
+      const int64_t row = r0 + 16 * w + jr;
+      const bool valid = row < r_end;
+      float acc[NH];
+#pragma unroll
+      for (int h = 0; h < NH; ++h) acc[h] = 0.0f;
+      if (valid) {
+        if constexpr (I8) {
+          uint4 kc[4];
+          if (row != p.pos) {
+            const uint4* src = reinterpret_cast<const uint4*>(reinterpret_cast<const int8_t*>(p.k) +
+                                                              row * kHd + 64 * qd);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) kc[c] = src[c];
+          } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+              kc[c] = make_uint4(knew[16 * qd + 4 * c], knew[16 * qd + 4 * c + 1],
+                                 knew[16 * qd + 4 * c + 2], knew[16 * qd + 4 * c + 3]);
+          }
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const uint32_t wd[4] = {kc[c].x, kc[c].y, kc[c].z, kc[c].w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const int d = 64 * qd + 16 * c + 4 * i + e;
+                const float kv = byte_f(wd[i], e);
+                // q (bf16) times an integer code below 128 is exact in binary32
+#pragma unroll
+                for (int h = 0; h < NH; ++h) acc[h] = __builtin_fmaf(qs[h][d], kv, acc[h]);
+              }
+          }
+        } else {
+          uint4 kc[8];
+          if (row != p.pos) {
+            const uint4* src = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p.k) +
+                                                              row * kHd + 64 * qd);
+#pragma unroll
+            for (int c = 0; c < 8; ++c) kc[c] = src[c];
+          } else {
+#pragma unroll
+            for (int c = 0; c < 8; ++c)
+              kc[c] = make_uint4(knew[32 * qd + 4 * c], knew[32 * qd + 4 * c + 1],
+                                 knew[32 * qd + 4 * c + 2], knew[32 * qd + 4 * c + 3]);
+          }
+#pragma unroll
+          for (int c = 0; c < 8; ++c) {
+            const uint32_t wd[4] = {kc[c].x, kc[c].y, kc[c].z, kc[c].w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+              for (int e = 0; e < 2; ++e) {
+                const int d = 64 * qd + 8 * c + 2 * i + e;
+                const float kv = bf16_bits_to_float(e ? wd[i] >> 16 : wd[i] & 0xffffu);
+                // a product of two bf16 values is exact in binary32
+#pragma unroll
+                for (int h = 0; h < NH; ++h) acc[h] = __builtin_fmaf(qs[h][d], kv, acc[h]);
+              }
+          }
+        }
+      }
+#pragma unroll
+      for (int h = 0; h < NH; ++h) {
+        acc[h] += lane_xor<1>(acc[h]);
+        acc[h] += lane_xor<2>(acc[h]);
+      }
+      if (qd == 0) {
+        float ks = 1.0f;
+        if constexpr (I8) ks = valid ? (row == p.pos ? knew_s : p.sk[row]) : 0.0f;
+#pragma unroll
+        for (int h = 0; h < NH; ++h)
+          sc[h][16 * w + jr] = valid ? (acc[h] * ks) * 0.0625f : -INFINITY;
+      }
+    }
+    __syncthreads();
+    // ---- running softmax: wave w takes heads w, w + 4
+#pragma unroll
+    for (int h = w; h < NH; h += 4) {
+      const float s = sc[h][l];
+      const float m_old = run_m[h];
+      const float m_new = fmaxf(m_old, wave_max(s));
+      const float e = expf(s - m_new);  // 0 for rows past the end (score -inf)
+      const float sum = wave_sum(e);
+      float wgt = e;
+      if constexpr (I8) {
+        const int64_t row = r0 + l;
+        wgt = row < r_end ? e * (row == p.pos ? vnew_s : p.sv[row]) : 0.0f;
+      }
+      sc[h][l] = wgt;
+      if (l == 0) {
+        const float c = expf(m_old - m_new);  // 0 on the first pass
+        corr[h] = c;
+        run_l[h] = run_l[h] * c + sum;
+        run_m[h] = m_new;
+      }
+    }
+    __syncthreads();
+    // ---- weighted values: this wave's 16 rows into its 4 dimensions per lane
+#pragma unroll
+    for (int h = 0; h < NH; ++h) {
+      const float c = corr[h];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[h][e] *= c;
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      float vf[4];
+      if constexpr (I8) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) vf[e] = byte_f(vv[i][0], e);
+      } else {
+        vf[0] = bf16_bits_to_float(vv[i][0] & 0xffffu);
+        vf[1] = bf16_bits_to_float(vv[i][0] >> 16);
+        vf[2] = bf16_bits_to_float(vv[i][1] & 0xffffu);
+        vf[3] = bf16_bits_to_float(vv[i][1] >> 16);
+      }
+#pragma unroll
+      for (int h = 0; h < NH; ++h) {
+        const float wt = sc[h][16 * w + i];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[h][e] = __builtin_fmaf(wt, vf[e], o[h][e]);
+      }
+    }
+    __syncthreads();  // sc and corr are rewritten by the next pass
+  }
+
+  // ---- the four waves' sums, then the result or this workgroup's partial
+#pragma unroll
+  for (int h = 0; h < NH; ++h)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) ored[w][h][4 * l + e] = o[h][e];
+  __syncthreads();
+  for (int i = tid; i < NH * kHd; i += 256) {
+    const int h = i / kHd, d = i % kHd;
+    const float od = ((ored[0][h][d] + ored[1][h][d]) + ored[2][h][d]) + ored[3][h][d];
+    if (p.n_wg == 1) {
+      p.out[i] = float_to_bf16_bits(od / run_l[h]);
+    } else {
+      float* part = p.part + (int64_t)blockIdx.x * kPartFloats;
+      part[2 * kMaxHeads + h * kHd + d] = od;
+      if (d == 0) {
+        part[h] = run_m[h];
+        part[kMaxHeads + h] = run_l[h];
+      }
+    }
+  }
+}
+
+// Merge of the workgroups' partial results: one workgroup per head, one
+// thread per dimension.
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
+  const int h = blockIdx.x, d = threadIdx.x;
+  float m = -INFINITY;
+  for (int c = 0; c < p.n_wg; ++c) m = fmaxf(m, p.part[(int64_t)c * kPartFloats + h]);
+  float den = 0.0f, num = 0.0f;
+  for (int c = 0; c < p.n_wg; ++c) {
+    const float* part = p.part + (int64_t)c * kPartFloats;
+    const float f = expf(part[h] - m);
+    den += part[kMaxHeads + h] * f;
+    num += part[2 * kMaxHeads + h * kHd + d] * f;
+  }
+  p.out[h * kHd + d] = float_to_bf16_bits(num / den);
+}
+
+hipError_t launch_kv_quant(const uint16_t* src, int64_t rows, int64_t ld, int8_t* codes,
+                           float* scales, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  kv_quant_kernel<<<dim3((unsigned)((rows + 3) / 4)), 256, 0, st>>>(src, rows, ld, codes, scales);
+  return hipGetLastError();
+}
+
+void attn_plan(int64_t rows, int* rows_per_wg, int* n_wg) {
+  const int64_t passes = (rows + kPass - 1) / kPass;
+  const int64_t per = (passes + kAttnMaxWgs - 1) / kAttnMaxWgs;  // passes per workgroup
+  *rows_per_wg = (int)(per * kPass);
+  *n_wg = (int)((passes + per - 1) / per);
+}
+
+size_t attn_ws_bytes(int64_t rows) {
+  int rpw = 0, n = 0;
+  attn_plan(rows, &rpw, &n);
+  return n > 1 ? (size_t)n * kPartFloats * sizeof(float) : 0;
+}
+
+// Enough for every row count up to t_max: a launch uses min(passes, 1024)
+// workgroups or fewer, and more rows never mean fewer passes.
+size_t attn_ws_bytes_max(int64_t t_max) {
+  const int64_t passes = (t_max + kPass - 1) / kPass;
+  const int64_t n = std::min<int64_t>(passes, kAttnMaxWgs);
+  return n > 1 ? (size_t)n * kPartFloats * sizeof(float) : 0;
+}
+
+template <bool I8>
+static hipError_t attn_launch(const AttnParams& p, int nh, hipStream_t st) {
+  const dim3 grid((unsigned)p.n_wg);
+  switch (nh) {
+    case 1: attn_decode_kernel<I8, 1><<<grid, 256, 0, st>>>(p); break;
+    case 2: attn_decode_kernel<I8, 2><<<grid, 256, 0, st>>>(p); break;
+    case 4: attn_decode_kernel<I8, 4><<<grid, 256, 0, st>>>(p); break;
+    case 8: attn_decode_kernel<I8, 8><<<grid, 256, 0, st>>>(p); break;
+    default: return hipErrorInvalidValue;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.n_wg == 1) return e;
+  attn_merge_kernel<<<dim3((unsigned)nh), 256, 0, st>>>(p);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_decode(AttnParams p, int nh, bool i8, hipStream_t st) {
+  attn_plan(p.pos + 1 - p.t0, &p.rows_per_wg, &p.n_wg);
+  return i8 ? attn_launch<true>(p, nh, st) : attn_launch<false>(p, nh, st);
+}
+
+}  // namespace w8a8

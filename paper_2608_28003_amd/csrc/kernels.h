@@ -231,4 +231,29 @@ int sqnr_groups(int64_t n);
 hipError_t launch_sqnr(const void* ref, const void* test, bool bf16, int64_t n, double* part,
                        double* out, hipStream_t st);
 
+// ------------------------------------------------------------------ attention decode (attn.hip)
+
+// One token's query heads against a key/value cache of rows of 256 (INT8
+// codes with per-row scales, or bf16), the new row appended at pos.
+constexpr int kAttnMaxWgs = 1024;  // workgroups a launch splits the rows over, at most
+struct AttnParams {
+  const uint16_t* qkv = nullptr;  // [n_heads x 256 query | 256 key | 256 value] bf16
+  void* k = nullptr;              // cache rows: int8 [t_max][256] or bf16 [t_max][256]
+  void* v = nullptr;
+  float* sk = nullptr;            // INT8 cache: per-row scales
+  float* sv = nullptr;
+  int64_t pos = 0;                // row of the new token
+  int64_t t0 = 0;                 // first attended row (pos + 1 - window, at least 0)
+  int rows_per_wg = 0;            // set by the launcher
+  int n_wg = 0;
+  float* part = nullptr;          // workspace: per-workgroup partial results
+  uint16_t* out = nullptr;        // n_heads x 256 bf16
+};
+// rows of 256 bf16 (stride ld elements) -> row-major INT8 codes and row scales
+hipError_t launch_kv_quant(const uint16_t* src, int64_t rows, int64_t ld, int8_t* codes,
+                           float* scales, hipStream_t st);
+hipError_t launch_attn_decode(AttnParams p, int nh, bool i8, hipStream_t st);
+size_t attn_ws_bytes(int64_t rows);  // workspace of one launch over `rows` attended rows
+size_t attn_ws_bytes_max(int64_t t_max);  // ... of any launch over at most t_max rows
+
 }  // namespace w8a8

@@ -141,3 +141,30 @@ def attn_config(m: int = 32, d: int = D_MODEL, seed_base: int = 5000,
     return dict(x=x, x_o=x_o, x_cal=x_cal,
                 w_qkv=to_bf16_bits(np.concatenate([wq, wk, wv], 0)),
                 w_o=to_bf16_bits(wo))
+
+
+HEAD_DIM = 256
+KV_SIGMA = 2.0
+
+
+def kv_decode_inputs(seed: int, t: int, n_heads: int = 4):
+    """Cached keys and values of t earlier tokens and the fused QKV row of the
+    current token ([n_heads x 256 query | 256 key | 256 value]), bf16.
+
+    Scale: a projection with N(0, 0.02^2) weights of a 1152-wide activation
+    whose 12 outlier channels carry 30x has outputs of standard deviation near
+    0.02 * sqrt(1140 + 12 * 900) ~ 2.2, so keys, values and queries are drawn
+    N(0, 2^2); keys also carry 8 outlier dimensions (x 8, on their own seed),
+    the per-channel structure key projections show, which makes the per-token
+    INT8 scale of a key row larger than its typical entry.  With this scale
+    the scores q.k / 16 have a standard deviation near 7, a peaked softmax."""
+    ch = outlier_channels(seed + 1, HEAD_DIM, 8)
+    k = normal(seed + 2, (t, HEAD_DIM), KV_SIGMA)
+    k[:, ch] *= np.float32(8.0)
+    v = normal(seed + 3, (t, HEAD_DIM), KV_SIGMA)
+    q = normal(seed + 4, (n_heads * HEAD_DIM,), KV_SIGMA)
+    kn = normal(seed + 5, (HEAD_DIM,), KV_SIGMA)
+    kn[ch] *= np.float32(8.0)
+    vn = normal(seed + 6, (HEAD_DIM,), KV_SIGMA)
+    return dict(k=to_bf16_bits(k), v=to_bf16_bits(v),
+                qkv=to_bf16_bits(np.concatenate([q, kn, vn])), channels=ch)

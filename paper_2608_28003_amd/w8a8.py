@@ -106,6 +106,10 @@ _SIGS = {
     "w8a8_rank_layers": (INT, [P, INT, P]),
     "w8a8_select_precision_map": (INT, [ctypes.POINTER(StackDesc), P, I64, ctypes.c_float, P, P,
                                         P, SZ, P]),
+    "w8a8_kv_quantize": (INT, [P, I64, I64, P, P, P]),
+    "w8a8_attn_decode_workspace_bytes": (SZ, [I64]),
+    "w8a8_attn_decode": (INT, [P, INT, I64, I64, P, P, P, P, I64, P, P, SZ, P]),
+    "w8a8_attn_decode_bf16": (INT, [P, INT, I64, I64, P, P, I64, P, P, SZ, P]),
     "w8a8_status_str": (ctypes.c_char_p, [INT]),
     "w8a8_last_error": (ctypes.c_char_p, []),
 }
@@ -693,6 +697,78 @@ def rank_layers(isolated_db) -> np.ndarray:
 
 
 # ----------------------------------------------------------------- layout helpers
+
+# ---------------------------------------------------------------- key/value cache, attention decode
+
+HEAD_DIM = 256
+
+
+class KVCache:
+    """One layer's key/value cache of t_max rows of 256: INT8 codes with
+    per-row scales, or bf16 rows."""
+
+    def __init__(self, t_max, int8=True, device="cuda"):
+        self.t_max, self.int8 = t_max, int8
+        if int8:
+            self.k = torch.zeros((t_max, HEAD_DIM), dtype=torch.int8, device=device)
+            self.v = torch.zeros((t_max, HEAD_DIM), dtype=torch.int8, device=device)
+            self.sk = torch.zeros(t_max, dtype=torch.float32, device=device)
+            self.sv = torch.zeros(t_max, dtype=torch.float32, device=device)
+        else:
+            self.k = torch.zeros((t_max, HEAD_DIM), dtype=torch.bfloat16, device=device)
+            self.v = torch.zeros((t_max, HEAD_DIM), dtype=torch.bfloat16, device=device)
+
+    def fill(self, t0, k, v, stream=None):
+        """Rows t0 .. t0 + n - 1 from bf16 keys and values (n x 256 views with
+        unit column stride, e.g. column slices of a fused QKV output)."""
+        n = k.shape[0]
+        if self.int8:
+            kv_quantize(k, self.k[t0:t0 + n], self.sk[t0:t0 + n], stream)
+            kv_quantize(v, self.v[t0:t0 + n], self.sv[t0:t0 + n], stream)
+        else:
+            self.k[t0:t0 + n].copy_(k)
+            self.v[t0:t0 + n].copy_(v)
+
+
+def kv_quantize(kv, codes=None, scales=None, stream=None):
+    """Rows of 256 bf16 values (row stride kv.stride(0)) -> (INT8 codes
+    [rows, 256], scales [rows])."""
+    if not kv.is_cuda or kv.dim() != 2 or kv.shape[1] != HEAD_DIM or kv.stride(1) != 1 \
+            or kv.dtype != torch.bfloat16:
+        raise ValueError("kv must be a bf16 GPU tensor of rows of 256 with unit column stride")
+    rows = kv.shape[0]
+    if codes is None:
+        codes = torch.empty((rows, HEAD_DIM), dtype=torch.int8, device=kv.device)
+    if scales is None:
+        scales = torch.empty(rows, dtype=torch.float32, device=kv.device)
+    _check(lib().w8a8_kv_quantize(_ptr(kv), rows, kv.stride(0), _ptr(codes), _ptr(scales),
+                                  _stream(stream)))
+    return codes, scales
+
+
+def attn_decode_workspace_bytes(t_max):
+    return lib().w8a8_attn_decode_workspace_bytes(t_max)
+
+
+def attn_decode(qkv, cache: KVCache, pos, window, n_heads=4, out=None, ws=None, stream=None):
+    """Append the token's key and value (from its fused QKV row, bf16) at row
+    pos of the cache and attend rows max(0, pos + 1 - window) .. pos; returns
+    the bf16 attention output (n_heads * 256)."""
+    _dev(qkv)
+    if out is None:
+        out = torch.empty(n_heads * HEAD_DIM, dtype=torch.bfloat16, device=qkv.device)
+    if ws is None:
+        ws = _empty(max(1, attn_decode_workspace_bytes(cache.t_max)), qkv.device)
+    if cache.int8:
+        _check(lib().w8a8_attn_decode(_ptr(qkv), n_heads, pos, window, _ptr(cache.k), _ptr(cache.sk),
+                                      _ptr(cache.v), _ptr(cache.sv), cache.t_max, _ptr(out),
+                                      _ptr(ws), ws.numel(), _stream(stream)))
+    else:
+        _check(lib().w8a8_attn_decode_bf16(_ptr(qkv), n_heads, pos, window, _ptr(cache.k),
+                                           _ptr(cache.v), cache.t_max, _ptr(out), _ptr(ws),
+                                           ws.numel(), _stream(stream)))
+    return out
+
 
 def frag_to_rowmajor(packed: np.ndarray, rows: int, k: int) -> np.ndarray:
     """Packed int8 fragment layout (include/w8a8.h) -> row-major rows x k."""

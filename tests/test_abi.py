@@ -141,6 +141,33 @@ def test_geglu_requant_validation():
     assert g(FAKE, FAKE, 4, 6912, None, FAKE, FAKE, MISALIGNED, None) == w8a8.EINVAL
 
 
+def test_kv_cache_and_attention_validation():
+    L = w8a8.lib()
+    q = L.w8a8_kv_quantize
+    assert q(None, 4, 256, FAKE, FAKE, None) == w8a8.EINVAL
+    assert q(FAKE, 0, 256, FAKE, FAKE, None) == w8a8.EINVAL
+    assert q(FAKE, 4, 255, FAKE, FAKE, None) == w8a8.EINVAL
+    assert q(FAKE, 4, 260, FAKE, FAKE, None) == w8a8.EINVAL
+    assert q(FAKE, 4, 256, MISALIGNED, FAKE, None) == w8a8.EINVAL
+    assert L.w8a8_attn_decode_workspace_bytes(64) == 0
+    assert L.w8a8_attn_decode_workspace_bytes(32768) > 0
+    a = L.w8a8_attn_decode
+    ok = (FAKE, 4, 10, 1024, FAKE, FAKE, FAKE, FAKE, 64, FAKE, None, 0, None)
+    for i, bad, code in ((0, None, w8a8.EINVAL), (1, 3, w8a8.EUNSUPPORTED), (1, 16, w8a8.EUNSUPPORTED),
+                         (2, 64, w8a8.EINVAL), (2, -1, w8a8.EINVAL), (3, 0, w8a8.EINVAL),
+                         (4, None, w8a8.EINVAL), (5, MISALIGNED, w8a8.EINVAL),
+                         (8, 0, w8a8.EINVAL), (9, None, w8a8.EINVAL)):
+        args = list(ok)
+        args[i] = bad
+        assert a(*args) == code, (i, bad)
+    # a long context needs the workspace
+    assert a(FAKE, 4, 32767, 32768, FAKE, FAKE, FAKE, FAKE, 32768, FAKE, None, 0, None) == w8a8.EINVAL
+    assert a(FAKE, 4, 32767, 32768, FAKE, FAKE, FAKE, FAKE, 32768, FAKE, FAKE, 64, None) == w8a8.EWORKSPACE
+    b = L.w8a8_attn_decode_bf16
+    assert b(FAKE, 4, 10, 1024, None, FAKE, 64, FAKE, None, 0, None) == w8a8.EINVAL
+    assert b(FAKE, 5, 10, 1024, FAKE, FAKE, 64, FAKE, None, 0, None) == w8a8.EUNSUPPORTED
+
+
 def test_stack_status_validation_and_codes():
     L = w8a8.lib()
     assert L.w8a8_ffn_stack_status(None, 1 << 20, None) == w8a8.EINVAL
