@@ -504,6 +504,90 @@ def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all
             groups["attn_proj_m%d" % m]["o"]["int8_us"],
             min(groups["attn_proj_m%d" % m]["o"]["bf16_us"], groups["attn_proj_m%d" % m]["o"]["torch_bf16_us"]))
         for m in (1, 32, 256)))
+
+    # --- decode attention with a key/value cache (Sec. 2 layout: 4 query heads,
+    # one key/value head of 256; Sec. 4: INT8 cache).  The kernel alone at a
+    # few context lengths, INT8 cache vs bf16 cache, then 26 attention blocks
+    # at one token (fused QKV projection, append-and-attend over the layer's
+    # cache, O projection) under the attention layer sets Q_ATT, with the
+    # global layers (0, 6, 12, 18) attending the whole context and the others
+    # the last 1024 rows.
+    HD = w8a8.HEAD_DIM
+    attn_kernel = {}
+    for T in (1024, 4096, 32768):
+        kvd = synth.kv_decode_inputs(5800, T - 1)
+        kt = torch.from_numpy(kvd["k"].view(np.int16)).view(torch.bfloat16).to(dev)
+        vt = torch.from_numpy(kvd["v"].view(np.int16)).view(torch.bfloat16).to(dev)
+        qkv1 = torch.from_numpy(kvd["qkv"].view(np.int16)).view(torch.bfloat16).to(dev)
+        wsa = torch.empty(max(1, w8a8.attn_decode_workspace_bytes(T)), dtype=torch.uint8, device=dev)
+        outa = torch.empty(NQ, dtype=torch.bfloat16, device=dev)
+        ent = {}
+        for kind in ("int8", "bf16"):
+            cache = w8a8.KVCache(T, kind == "int8", dev)
+            cache.fill(0, kt, vt)
+            # 26 calls per replay (one per layer of a step), so the graph's own
+            # launch is not charged to one call
+            g = make_graph(lambda: [w8a8.attn_decode(qkv1, cache, T - 1, T, out=outa, ws=wsa)
+                                    for _ in range(NL)])
+            t = time_graph(g) / NL
+            del g, cache
+            row = 2 * HD + 8 if kind == "int8" else 4 * HD   # key + value codes and scales, or bf16
+            ent[kind + "_us"] = round(t * 1e6, 2)
+            ent[kind + "_GBs"] = round(T * row / t / 1e9, 1)
+        ent["speedup_int8_cache"] = round(ent["bf16_us"] / ent["int8_us"], 3)
+        attn_kernel["t%d" % T] = ent
+        del kt, vt, wsa
+    groups["attn_decode_kernel"] = attn_kernel
+    log("attention decode kernel: " + ", ".join("T=%s int8 %.2f us (%.0f GB/s) bf16 %.2f us" % (
+        k[1:], v["int8_us"], v["int8_GBs"], v["bf16_us"]) for k, v in attn_kernel.items()))
+
+    CTX = 4096
+    kvd = synth.kv_decode_inputs(5900, CTX - 1)
+    kt = torch.from_numpy(kvd["k"].view(np.int16)).view(torch.bfloat16).to(dev)
+    vt = torch.from_numpy(kvd["v"].view(np.int16)).view(torch.bfloat16).to(dev)
+    caches = {}
+    for kind in ("int8", "bf16"):
+        caches[kind] = [w8a8.KVCache(CTX, kind == "int8", dev) for _ in range(NL)]
+        for c in caches[kind]:
+            c.fill(0, kt, vt)
+    del kt, vt
+    x1a = xa_all[:1].contiguous()
+    qkv_b = torch.empty((1, NQKV), dtype=torch.bfloat16, device=dev)
+    att_b = torch.empty((1, NQ), dtype=torch.bfloat16, device=dev)
+    o_b = torch.empty((1, D), dtype=torch.bfloat16, device=dev)
+    wsa = torch.empty(max(1, w8a8.attn_decode_workspace_bytes(CTX)), dtype=torch.uint8, device=dev)
+    nb = max(w8a8.linear_workspace_bytes(1, NQKV, D), w8a8.linear_workspace_bytes(1, D, NQ),
+             w8a8.bf16_linear_workspace_bytes(1, NQKV, D), w8a8.bf16_linear_workspace_bytes(1, D, NQ))
+    wsl = torch.empty(max(1, nb), dtype=torch.uint8, device=dev)
+    windows = [CTX if l in (0, 6, 12, 18) else 1024 for l in range(NL)]
+
+    def blocks(prec, kind):
+        for l in range(NL):
+            if prec[l]:
+                w8a8.linear(qkv8[l], x1a, out_dtype=torch.bfloat16, out=qkv_b, ws=wsl)
+            else:
+                w8a8.bf16_linear(x1a, qkv16[l], NQKV, D, out=qkv_b, ws=wsl)
+            w8a8.attn_decode(qkv_b.view(-1), caches[kind][l], CTX - 1, windows[l], out=att_b.view(-1),
+                             ws=wsa)
+            if prec[l]:
+                w8a8.linear(o8[l], att_b, out_dtype=torch.bfloat16, out=o_b, ws=wsl)
+            else:
+                w8a8.bf16_linear(att_b, o16[l], D, NQ, out=o_b, ws=wsl)
+
+    att_maps = {}
+    for name in ("none", "5+5", "10+10", "all26"):
+        prec = w8a8.precision_map("bf16" if name == "none" else name)
+        for kind in ("bf16", "int8"):
+            g = make_graph(lambda: blocks(prec, kind))
+            att_maps["Q_ATT %s, %s cache" % (name, kind)] = round(time_graph(g) * 1e6, 1)
+            del g
+    groups["attn_blocks_m1_ctx%d" % CTX] = {
+        "us_per_step_26_blocks": att_maps,
+        "note": "one token; per layer QKV projection + append-and-attend + O projection; "
+                "global layers 0, 6, 12, 18 attend %d rows, the others 1024" % CTX}
+    log("attention blocks at one token, context %d: " % CTX
+        + ", ".join("%s %.1f us" % kv for kv in att_maps.items()))
+    del caches, wsa, wsl
     del att, qkv8, o8, qkv16, o16, qkv_t, o_t
 
     # --- lm_head decode: INT8 vs our bf16 kernel vs torch.mm (hipBLASLt) bf16.
@@ -608,6 +692,23 @@ def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all
         "us": round(ts * 1e6, 1), "speedup_vs_bf16": round(base1 / ts, 3),
         "weight_GBs": round(weight_bytes(prec, True) / ts / 1e9, 1)}
     groups["stack_maps_m1"] = maps1
+    # one decode step composed of separately timed parts: the FFN stack with
+    # its lm_head (above) and the 26 attention blocks (projections + cache)
+    att = groups["attn_blocks_m1_ctx4096"]["us_per_step_26_blocks"]
+    composed = {}
+    for name, ffn_key, att_key in [
+            ("bf16", "bf16", "Q_ATT none, bf16 cache"),
+            ("FFN 5+5 + lm_head", "FFN 5+5 + lm_head", "Q_ATT none, bf16 cache"),
+            ("FFN all26 + lm_head", "FFN all26 + lm_head", "Q_ATT none, bf16 cache"),
+            ("Attn+FFN 5+5 (Q_ATT all26) + lm_head", "FFN 5+5 + lm_head", "Q_ATT all26, bf16 cache"),
+            ("Attn+FFN all26 + lm_head", "FFN all26 + lm_head", "Q_ATT all26, bf16 cache"),
+            ("Attn+FFN all26 + lm_head + INT8 cache", "FFN all26 + lm_head", "Q_ATT all26, int8 cache"),
+            ("Attn 5+5 + FFN 5+5 + lm_head + INT8 cache", "FFN 5+5 + lm_head", "Q_ATT 5+5, int8 cache")]:
+        composed[name] = round(maps1[ffn_key]["us"] + att[att_key], 1)
+    base_c = composed["bf16"]
+    groups["decode_step_composed_ctx4096"] = {
+        k: {"us": v, "speedup_vs_bf16": round(base_c / v, 3)} for k, v in composed.items()}
+    log("composed decode step (context 4096): " + ", ".join("%s %.1f us" % kv for kv in composed.items()))
     # layer sensitivity (SQNR, dB) on 64 tokens and automatically chosen maps,
     # timed at the step's M against its all-bf16 step
     xm = x_all[:M].contiguous()

@@ -25,6 +25,11 @@ namespace {
 constexpr int kHd = 256;       // head dimension
 constexpr int kPass = 64;      // cached rows per pass of a workgroup (16 per wave)
 constexpr int kMaxHeads = 8;
+// q in LDS with 4 floats of padding after every 64: the four lanes of a row
+// read 64 apart, and the padding puts their 16-byte reads in distinct banks
+constexpr int kQStride = kHd + 16;
+
+__device__ __forceinline__ int qidx(int d) { return d + ((d >> 6) << 2); }
 
 // Codes of one 256-wide row held 4 per lane by one wave: the per-token rule
 // (s = max |x| / 127, codes rne(x / s) clamped to +-127, zero row -> s = 0).
@@ -80,7 +85,7 @@ constexpr int kPartFloats = 2 * kMaxHeads + kMaxHeads * kHd;
 
 template <bool I8, int NH>
 __global__ __launch_bounds__(256) void attn_decode_kernel(AttnParams p) {
-  __shared__ float qs[NH][kHd];
+  __shared__ float qs[NH][kQStride];
   __shared__ float sc[NH][kPass];     // scores, then weights p (x the row's value scale)
   __shared__ float corr[NH];          // rescale of the running sums for this pass
   __shared__ float run_m[NH], run_l[NH];
@@ -92,7 +97,55 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(AttnParams p) {
   const int64_t r_begin = p.t0 + (int64_t)blockIdx.x * p.rows_per_wg;
   const int64_t r_end = min(r_begin + p.rows_per_wg, p.pos + 1);  // exclusive
 
-  for (int i = tid; i < NH * kHd; i += 256) qs[i / kHd][i % kHd] = bf16_bits_to_float(p.qkv[i]);
+  const int jr = l >> 2, qd = l & 3;  // score phase: row 16w + jr, dimensions 64 qd ..
+  // The keys and values of a pass are loaded one pass ahead: pass i + 1's
+  // loads are issued before pass i's arithmetic and barriers.
+  struct PassRegs {
+    uint4 kc[I8 ? 4 : 8];          // key row 16 w + jr, dimensions 64 qd .. 64 qd + 63
+    uint32_t vv[16][I8 ? 1 : 2];   // value rows 16 w .. 16 w + 15, dimensions 4 l .. 4 l + 3
+  };
+  // loads of a pass; the new row (pos) comes from LDS, where its codes are
+  // staged behind the first barrier
+  auto load_pass = [&](int64_t r0, PassRegs& R) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int64_t row = r0 + 16 * w + i;
+      if (row == p.pos) {
+        R.vv[i][0] = I8 ? vnew[l] : vnew[2 * l];
+        if constexpr (!I8) R.vv[i][1] = vnew[2 * l + 1];
+      } else if (row < r_end && row != p.pos) {
+        if constexpr (I8) {
+          R.vv[i][0] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const int8_t*>(p.v) +
+                                                         row * kHd + 4 * l);
+        } else {
+          const uint2 raw = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(p.v) +
+                                                           row * kHd + 4 * l);
+          R.vv[i][0] = raw.x;
+          R.vv[i][1] = raw.y;
+        }
+      } else {
+        R.vv[i][0] = 0;
+        if constexpr (!I8) R.vv[i][1] = 0;
+      }
+    }
+    constexpr int NK = I8 ? 4 : 8;  // 16-byte words of 64 dimensions
+    const int64_t row = r0 + 16 * w + jr;
+    if (row == p.pos) {
+#pragma unroll
+      for (int c = 0; c < NK; ++c)
+        R.kc[c] = make_uint4(knew[4 * NK * qd + 4 * c], knew[4 * NK * qd + 4 * c + 1],
+                             knew[4 * NK * qd + 4 * c + 2], knew[4 * NK * qd + 4 * c + 3]);
+    } else if (row < r_end && row != p.pos) {
+      const uint4* src = reinterpret_cast<const uint4*>(
+          reinterpret_cast<const int8_t*>(p.k) + (row * kHd + 64 * qd) * (I8 ? 1 : 2));
+#pragma unroll
+      for (int c = 0; c < NK; ++c) R.kc[c] = src[c];
+    } else {
+#pragma unroll
+      for (int c = 0; c < NK; ++c) R.kc[c] = make_uint4(0, 0, 0, 0);
+    }
+  };
+  for (int i = tid; i < NH * kHd; i += 256) qs[i / kHd][qidx(i % kHd)] = bf16_bits_to_float(p.qkv[i]);
   if (tid < NH) {
     run_m[tid] = -INFINITY;
     run_l[tid] = 0.0f;
@@ -121,6 +174,9 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(AttnParams p) {
   }
   __syncthreads();
 
+  PassRegs cur, nxt;
+  if (r_begin < r_end) load_pass(r_begin, cur);
+
   // per lane: 4 output dimensions (4l .. 4l + 3) of every head, summed over
   // the rows this wave handles
   float o[NH][4];
@@ -129,31 +185,8 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(AttnParams p) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) o[h][e] = 0.0f;
 
-  const int jr = l >> 2, qd = l & 3;  // score phase: row 16w + jr, dimensions 64 qd ..
   for (int64_t r0 = r_begin; r0 < r_end; r0 += kPass) {
-    // ---- values of this wave's 16 rows (loaded first, used after the softmax)
-    uint32_t vv[16][I8 ? 1 : 2];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int64_t row = r0 + 16 * w + i;
-      if (row < r_end && row != p.pos) {
-        if constexpr (I8) {
-          vv[i][0] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const int8_t*>(p.v) +
-                                                       row * kHd + 4 * l);
-        } else {
-          const uint2 raw = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(p.v) +
-                                                           row * kHd + 4 * l);
-          vv[i][0] = raw.x;
-          vv[i][1] = raw.y;
-        }
-      } else if (row == p.pos) {
-        vv[i][0] = I8 ? vnew[l] : vnew[2 * l];
-        if constexpr (!I8) vv[i][1] = vnew[2 * l + 1];
-      } else {
-        vv[i][0] = 0;
-        if constexpr (!I8) vv[i][1] = 0;
-      }
-    }
+    if (r0 + kPass < r_end) load_pass(r0 + kPass, nxt);
     // ---- scores: four lanes per row, 64 dimensions each
     {
       const int64_t row = r0 + 16 * w + jr;
@@ -161,60 +194,40 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(AttnParams p) {
       float acc[NH];
 #pragma unroll
       for (int h = 0; h < NH; ++h) acc[h] = 0.0f;
-      if (valid) {
-        if constexpr (I8) {
-          uint4 kc[4];
-          if (row != p.pos) {
-            const uint4* src = reinterpret_cast<const uint4*>(reinterpret_cast<const int8_t*>(p.k) +
-                                                              row * kHd + 64 * qd);
+      if constexpr (I8) {
 #pragma unroll
-            for (int c = 0; c < 4; ++c) kc[c] = src[c];
-          } else {
+        for (int c = 0; c < 4; ++c) {
+          const uint32_t wd[4] = {cur.kc[c].x, cur.kc[c].y, cur.kc[c].z, cur.kc[c].w};
 #pragma unroll
-            for (int c = 0; c < 4; ++c)
-              kc[c] = make_uint4(knew[16 * qd + 4 * c], knew[16 * qd + 4 * c + 1],
-                                 knew[16 * qd + 4 * c + 2], knew[16 * qd + 4 * c + 3]);
+          for (int i = 0; i < 4; ++i) {
+            const int d0 = 64 * qd + 16 * c + 4 * i;
+#pragma unroll
+            for (int h = 0; h < NH; ++h) {
+              const float4 qv = *reinterpret_cast<const float4*>(&qs[h][qidx(d0)]);
+              // q (bf16) times an integer code below 128 is exact in binary32
+              acc[h] = __builtin_fmaf(qv.x, byte_f(wd[i], 0), acc[h]);
+              acc[h] = __builtin_fmaf(qv.y, byte_f(wd[i], 1), acc[h]);
+              acc[h] = __builtin_fmaf(qv.z, byte_f(wd[i], 2), acc[h]);
+              acc[h] = __builtin_fmaf(qv.w, byte_f(wd[i], 3), acc[h]);
+            }
           }
+        }
+      } else {
 #pragma unroll
-          for (int c = 0; c < 4; ++c) {
-            const uint32_t wd[4] = {kc[c].x, kc[c].y, kc[c].z, kc[c].w};
+        for (int c = 0; c < 8; ++c) {
+          const uint32_t wd[4] = {cur.kc[c].x, cur.kc[c].y, cur.kc[c].z, cur.kc[c].w};
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+          for (int i = 0; i < 4; i += 2) {
+            const int d0 = 64 * qd + 8 * c + 2 * i;
 #pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                const int d = 64 * qd + 16 * c + 4 * i + e;
-                const float kv = byte_f(wd[i], e);
-                // q (bf16) times an integer code below 128 is exact in binary32
-#pragma unroll
-                for (int h = 0; h < NH; ++h) acc[h] = __builtin_fmaf(qs[h][d], kv, acc[h]);
-              }
-          }
-        } else {
-          uint4 kc[8];
-          if (row != p.pos) {
-            const uint4* src = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p.k) +
-                                                              row * kHd + 64 * qd);
-#pragma unroll
-            for (int c = 0; c < 8; ++c) kc[c] = src[c];
-          } else {
-#pragma unroll
-            for (int c = 0; c < 8; ++c)
-              kc[c] = make_uint4(knew[32 * qd + 4 * c], knew[32 * qd + 4 * c + 1],
-                                 knew[32 * qd + 4 * c + 2], knew[32 * qd + 4 * c + 3]);
-          }
-#pragma unroll
-          for (int c = 0; c < 8; ++c) {
-            const uint32_t wd[4] = {kc[c].x, kc[c].y, kc[c].z, kc[c].w};
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-              for (int e = 0; e < 2; ++e) {
-                const int d = 64 * qd + 8 * c + 2 * i + e;
-                const float kv = bf16_bits_to_float(e ? wd[i] >> 16 : wd[i] & 0xffffu);
-                // a product of two bf16 values is exact in binary32
-#pragma unroll
-                for (int h = 0; h < NH; ++h) acc[h] = __builtin_fmaf(qs[h][d], kv, acc[h]);
-              }
+            for (int h = 0; h < NH; ++h) {
+              const float4 qv = *reinterpret_cast<const float4*>(&qs[h][qidx(d0)]);
+              // a product of two bf16 values is exact in binary32
+              acc[h] = __builtin_fmaf(qv.x, bf16_bits_to_float(wd[i] & 0xffffu), acc[h]);
+              acc[h] = __builtin_fmaf(qv.y, bf16_bits_to_float(wd[i] >> 16), acc[h]);
+              acc[h] = __builtin_fmaf(qv.z, bf16_bits_to_float(wd[i + 1] & 0xffffu), acc[h]);
+              acc[h] = __builtin_fmaf(qv.w, bf16_bits_to_float(wd[i + 1] >> 16), acc[h]);
+            }
           }
         }
       }
@@ -266,12 +279,12 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(AttnParams p) {
       float vf[4];
       if constexpr (I8) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) vf[e] = byte_f(vv[i][0], e);
+        for (int e = 0; e < 4; ++e) vf[e] = byte_f(cur.vv[i][0], e);
       } else {
-        vf[0] = bf16_bits_to_float(vv[i][0] & 0xffffu);
-        vf[1] = bf16_bits_to_float(vv[i][0] >> 16);
-        vf[2] = bf16_bits_to_float(vv[i][1] & 0xffffu);
-        vf[3] = bf16_bits_to_float(vv[i][1] >> 16);
+        vf[0] = bf16_bits_to_float(cur.vv[i][0] & 0xffffu);
+        vf[1] = bf16_bits_to_float(cur.vv[i][0] >> 16);
+        vf[2] = bf16_bits_to_float(cur.vv[i][1] & 0xffffu);
+        vf[3] = bf16_bits_to_float(cur.vv[i][1] >> 16);
       }
 #pragma unroll
       for (int h = 0; h < NH; ++h) {
@@ -281,6 +294,7 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(AttnParams p) {
       }
     }
     __syncthreads();  // sc and corr are rewritten by the next pass
+    cur = nxt;
   }
 
   // ---- the four waves' sums, then the result or this workgroup's partial
@@ -305,20 +319,48 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(AttnParams p) {
   }
 }
 
-// Merge of the workgroups' partial results: one workgroup per head, one
-// thread per dimension.
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
-  const int h = blockIdx.x, d = threadIdx.x;
+// Merge of the workgroups' partial results.  Four workgroups per head, each
+// over 64 output dimensions with 16 waves: the maximum over the chunks, then
+// every chunk's factor exp(m_c - M) and the denominator, then each thread
+// sums the chunks c = wave, wave + 16, ... of one dimension (16 loads in
+// flight per dimension instead of one chain over all chunks).
+__global__ __launch_bounds__(1024) void attn_merge_kernel(AttnParams p) {
+  __shared__ float fc[kAttnWgTarget];  // exp(m_c - M)
+  __shared__ float red[16][64];
+  __shared__ float wred[16];
+  const int h = blockIdx.x >> 2, d = (blockIdx.x & 3) * 64 + (threadIdx.x & 63);
+  const int tid = threadIdx.x, g = tid >> 6, n = p.n_wg;
   float m = -INFINITY;
-  for (int c = 0; c < p.n_wg; ++c) m = fmaxf(m, p.part[(int64_t)c * kPartFloats + h]);
-  float den = 0.0f, num = 0.0f;
-  for (int c = 0; c < p.n_wg; ++c) {
+  for (int c = tid; c < n; c += 1024) m = fmaxf(m, p.part[(int64_t)c * kPartFloats + h]);
+  m = wave_max(m);
+  if ((tid & 63) == 0) wred[g] = m;
+  __syncthreads();
+  m = wred[0];
+  for (int i = 1; i < 16; ++i) m = fmaxf(m, wred[i]);
+  __syncthreads();
+  float den = 0.0f;
+  for (int c = tid; c < n; c += 1024) {
     const float* part = p.part + (int64_t)c * kPartFloats;
     const float f = expf(part[h] - m);
+    fc[c] = f;
     den += part[kMaxHeads + h] * f;
-    num += part[2 * kMaxHeads + h * kHd + d] * f;
   }
-  p.out[h * kHd + d] = float_to_bf16_bits(num / den);
+  den = wave_sum(den);
+  if ((tid & 63) == 0) wred[g] = den;
+  __syncthreads();
+  den = 0.0f;
+  for (int i = 0; i < 16; ++i) den += wred[i];
+  float num = 0.0f;
+  const float* col = p.part + 2 * kMaxHeads + h * kHd + d;
+#pragma unroll 4
+  for (int c = g; c < n; c += 16) num += col[(int64_t)c * kPartFloats] * fc[c];
+  red[g][tid & 63] = num;
+  __syncthreads();
+  if (g == 0) {
+    float t = 0.0f;
+    for (int i = 0; i < 16; ++i) t += red[i][tid & 63];
+    p.out[h * kHd + d] = float_to_bf16_bits(t / den);
+  }
 }
 
 hipError_t launch_kv_quant(const uint16_t* src, int64_t rows, int64_t ld, int8_t* codes,
@@ -328,24 +370,27 @@ hipError_t launch_kv_quant(const uint16_t* src, int64_t rows, int64_t ld, int8_t
   return hipGetLastError();
 }
 
-void attn_plan(int64_t rows, int* rows_per_wg, int* n_wg) {
+// Rows per workgroup: whole passes of 64, at most kAttnWgTarget workgroups
+// (about one per CU: more would only add partial results to merge).
+void attn_plan(int64_t rows, int target, int* rows_per_wg, int* n_wg) {
+  target = std::max(1, std::min(target, kAttnWgTarget));
   const int64_t passes = (rows + kPass - 1) / kPass;
-  const int64_t per = (passes + kAttnMaxWgs - 1) / kAttnMaxWgs;  // passes per workgroup
+  const int64_t per = (passes + target - 1) / target;  // passes per workgroup
   *rows_per_wg = (int)(per * kPass);
   *n_wg = (int)((passes + per - 1) / per);
 }
 
-size_t attn_ws_bytes(int64_t rows) {
+size_t attn_ws_bytes(int64_t rows, int target) {
   int rpw = 0, n = 0;
-  attn_plan(rows, &rpw, &n);
+  attn_plan(rows, target, &rpw, &n);
   return n > 1 ? (size_t)n * kPartFloats * sizeof(float) : 0;
 }
 
-// Enough for every row count up to t_max: a launch uses min(passes, 1024)
-// workgroups or fewer, and more rows never mean fewer passes.
+// Enough for every row count up to t_max: a launch uses min(passes,
+// kAttnWgTarget) workgroups or fewer, and more rows never mean fewer passes.
 size_t attn_ws_bytes_max(int64_t t_max) {
   const int64_t passes = (t_max + kPass - 1) / kPass;
-  const int64_t n = std::min<int64_t>(passes, kAttnMaxWgs);
+  const int64_t n = std::min<int64_t>(passes, kAttnWgTarget);
   return n > 1 ? (size_t)n * kPartFloats * sizeof(float) : 0;
 }
 
@@ -361,12 +406,12 @@ static hipError_t attn_launch(const AttnParams& p, int nh, hipStream_t st) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_wg == 1) return e;
-  attn_merge_kernel<<<dim3((unsigned)nh), 256, 0, st>>>(p);
+  attn_merge_kernel<<<dim3((unsigned)(4 * nh)), 1024, 0, st>>>(p);
   return hipGetLastError();
 }
 
-hipError_t launch_attn_decode(AttnParams p, int nh, bool i8, hipStream_t st) {
-  attn_plan(p.pos + 1 - p.t0, &p.rows_per_wg, &p.n_wg);
+hipError_t launch_attn_decode(AttnParams p, int nh, bool i8, int target, hipStream_t st) {
+  attn_plan(p.pos + 1 - p.t0, target, &p.rows_per_wg, &p.n_wg);
   return i8 ? attn_launch<true>(p, nh, st) : attn_launch<false>(p, nh, st);
 }
 

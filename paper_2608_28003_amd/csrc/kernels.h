@@ -235,7 +235,6 @@ hipError_t launch_sqnr(const void* ref, const void* test, bool bf16, int64_t n, 
 
 // One token's query heads against a key/value cache of rows of 256 (INT8
 // codes with per-row scales, or bf16), the new row appended at pos.
-constexpr int kAttnMaxWgs = 1024;  // workgroups a launch splits the rows over, at most
 struct AttnParams {
   const uint16_t* qkv = nullptr;  // [n_heads x 256 query | 256 key | 256 value] bf16
   void* k = nullptr;              // cache rows: int8 [t_max][256] or bf16 [t_max][256]
@@ -252,8 +251,10 @@ struct AttnParams {
 // rows of 256 bf16 (stride ld elements) -> row-major INT8 codes and row scales
 hipError_t launch_kv_quant(const uint16_t* src, int64_t rows, int64_t ld, int8_t* codes,
                            float* scales, hipStream_t st);
-hipError_t launch_attn_decode(AttnParams p, int nh, bool i8, hipStream_t st);
-size_t attn_ws_bytes(int64_t rows);  // workspace of one launch over `rows` attended rows
+// target: workgroups to split the rows over (at most kAttnWgTarget)
+constexpr int kAttnWgTarget = 1024;
+hipError_t launch_attn_decode(AttnParams p, int nh, bool i8, int target, hipStream_t st);
+size_t attn_ws_bytes(int64_t rows, int target);  // workspace of one launch over `rows` rows
 size_t attn_ws_bytes_max(int64_t t_max);  // ... of any launch over at most t_max rows
 
 }  // namespace w8a8

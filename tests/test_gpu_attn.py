@@ -154,8 +154,8 @@ def test_attn_decode_head_counts(n_heads):
 
 @pytest.mark.timeout(300)
 def test_attn_decode_long_context_several_passes_per_workgroup():
-    """131072 rows: 2048 passes of 64 over 1024 workgroups, so every workgroup
-    carries its running maximum and sum across two passes."""
+    """131072 rows: 2048 passes of 64 over 256 workgroups, so every workgroup
+    carries its running maximum and sum across eight passes."""
     t_max = pos = 131071
     inp = synth.kv_decode_inputs(5300, pos, n_heads=4)
     oc, gc = make_caches(inp, pos, t_max + 1, True)
