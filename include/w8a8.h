@@ -512,7 +512,8 @@ void w8a8_clear_plan_overrides(void);
 
 /* ---------------------------------------------------------------- errors */
 
-const char* w8a8_status_str(w8a8_status s);
+/* Text of a status (any int: values outside w8a8_status give "unknown status"). */
+const char* w8a8_status_str(int status);
 /* Detail of the last error on the calling thread ("" if none). */
 const char* w8a8_last_error(void);
 

@@ -34,6 +34,9 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "w8a8_oracle.c")
 _LIB_PATH = os.path.join(_HERE, "liborc.so")
+# a prebuilt oracle library to load instead (the sanitizer test's instrumented
+# build); when set, build() compiles nothing
+_LIB_OVERRIDE = os.environ.get("W8A8_ORACLE_LIB")
 
 MODE_DIV = 0  # activations: x / delta
 MODE_MUL = 1  # weights:     W * delta
@@ -47,6 +50,8 @@ ALPHA = 0.5  # SmoothQuant migration strength used throughout the paper
 
 def build(force: bool = False) -> str:
     """Compile ``w8a8_oracle.c`` into ``liborc.so`` with gcc."""
+    if _LIB_OVERRIDE:
+        return _LIB_OVERRIDE
     if force or not os.path.exists(_LIB_PATH) or (
             os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC)):
         tmp = _LIB_PATH + ".tmp%d" % os.getpid()
@@ -64,8 +69,7 @@ _lib = None
 def _L():
     global _lib
     if _lib is None:
-        build()
-        lib = ctypes.CDLL(_LIB_PATH)
+        lib = ctypes.CDLL(build())
         P = ctypes.c_void_p
         I64 = ctypes.c_int64
         D = ctypes.c_double

@@ -708,7 +708,7 @@ size_t w8a8_stack_workspace_bytes(int64_t m, int64_t d, int64_t f, int64_t vocab
   return stack_ws(m, d, f, vocab).total;
 }
 
-const char* w8a8_status_str(w8a8_status s) {
+const char* w8a8_status_str(int s) {
   switch (s) {
     case W8A8_OK: return "ok";
     case W8A8_EINVAL: return "invalid argument";
