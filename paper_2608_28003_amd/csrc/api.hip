@@ -203,8 +203,8 @@ bool plan_stream(Plan& p, int64_t m, int64_t n, int64_t kb, bool glu, bool f8) {
 }
 
 // Deterministic in (m, n, k, path); the workspace queries use the same plan.
-// Tuning hooks for the tiled path: W8A8_GEMM_TILE / W8A8_GEMM_SPLITS (plain
-// epilogues) and W8A8_GLU_TILE (gated epilogue).
+// Planner overrides for the tiled path: GEMM_TILE / GEMM_SPLITS (plain
+// epilogues) and GLU_TILE (gated epilogue).
 Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
   Plan p;
   p.dt = dt;
@@ -520,7 +520,7 @@ size_t bf16_linear_ws(int64_t m, int64_t n, int64_t k) {
 // workspace.
 // INT8 down projection inside the stack: its split-K sums are reduced by the
 // glue launch, so the plan may split K more freely than a standalone call.
-// Experiment hooks: W8A8_DOWN_TILE, W8A8_DOWN_SPLITS.
+// Planner overrides: DOWN_TILE, DOWN_SPLITS.
 Plan stack_down_plan(int64_t m, int64_t d, int64_t f) {
   Plan p = plan_gemm(m, d, f, DT_I8, false);
   if (p.stream) {

@@ -645,7 +645,7 @@ def test_stack_precision_map_matches_oracle():
 def test_quantise_on_load_equals_separate_quantisation(m, monkeypatch):
     """At decode sizes the streaming GEMM quantises its bf16 input itself; its
     codes and scales, hence every output, must equal those of the separate
-    quantisation launch (the tuning switch W8A8_NO_QLOAD forces the latter)."""
+    quantisation launch (the planner override NO_QLOAD forces the latter)."""
     say("quantise-on-load", m)
     cfg, q, layer = _ffn_setup(m)
     x = dev_bf16(cfg["x"])
