@@ -56,6 +56,12 @@ def _link(objs, path):
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n%s\n%s" % (r.stdout, r.stderr))
+    # a shared library links with unresolved symbols; none of ours may be
+    nm = subprocess.run(["nm", "-D", "-C", "--undefined-only", tmp], capture_output=True, text=True)
+    missing = [l.split()[-1] for l in nm.stdout.splitlines() if "w8a8" in l]
+    if nm.returncode == 0 and missing:
+        os.remove(tmp)
+        raise RuntimeError("unresolved library symbols: %s" % ", ".join(missing))
     os.replace(tmp, path)
 
 

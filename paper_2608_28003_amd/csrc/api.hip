@@ -80,7 +80,7 @@ const char* const kOverrideNames[] = {
     "GLU_TILE", "GEMM_TILE", "GEMM_SPLITS", "DOWN_TILE", "DOWN_SPLITS", "DOWN_WK",
     "WIDE_NW", "WIDE_WGS", "STREAM_WK", "STREAM_SPLITS", "GROUP_M", "ROTATE",
     "NO_QLOAD", "NO_FUSED_GLUE", "NO_PERSISTENT", "DEC_SPIN_LIMIT", "XCD_M", "NT_OUT",
-    "ATTN_WGS"};
+    "ATTN_WGS", "QROWS_R"};
 constexpr int kNumOverrides = (int)(sizeof(kOverrideNames) / sizeof(kOverrideNames[0]));
 std::atomic<int> g_override[kNumOverrides];
 struct OverrideInit {
@@ -1790,3 +1790,6 @@ w8a8_status w8a8_attn_decode_bf16(const void* qkv, int n_heads, int64_t pos, int
 }
 
 }  // extern "C"
+
+// rows per workgroup of the many-row bf16 quantiser (declared in kernels.h)
+int w8a8::quant_rows_per_workgroup(int dflt) { return plan_override("QROWS_R", dflt); }

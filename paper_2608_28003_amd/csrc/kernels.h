@@ -103,6 +103,8 @@ hipError_t launch_col_absmax(const void* x, bool bf16, int64_t rows, int64_t k, 
 hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t st);
 hipError_t launch_smooth_delta(const float* a, const float* w, int64_t k, double alpha,
                                float* delta, hipStream_t st);
+// rows per workgroup of the many-row bf16 quantiser: dflt unless overridden
+int quant_rows_per_workgroup(int dflt);
 hipError_t launch_quant_rows(const void* x, bool bf16, bool mul, int64_t rows, int64_t k,
                              const float* delta, int8_t* qpacked, float* s, hipStream_t st,
                              bool f8 = false);

@@ -482,10 +482,20 @@ hipError_t launch_quant_rows(const void* x, bool bf16, bool mul, int64_t rows, i
   const bool narrow = rows_pad <= 256 && kp / 8 <= 1024;
   if (bf16 && !mul && !f8 && !narrow && kp / 16 <= 1024) {
     // many bf16 rows (activations): several rows per workgroup
-    constexpr int R = 4;
     const int64_t threads = (kp / 16 + 63) / 64 * 64;
-    quant_rows_bf16_kernel<R><<<(unsigned)((rows_pad + R - 1) / R), (unsigned)threads, 0, st>>>(
-        (const uint16_t*)x, rows, k, delta, rows_pad, kp, qpacked, s);
+    // rows per workgroup, measured at k = 6912 (requantisation of h): 4 from
+    // 2048 rows (17.9 against 19.8 us with 2), 2 below (512 rows: 8.3 against
+    // 11.2 us; 1024 rows: 11.7 against 12.5 us); at k = 1152, 2048 rows: 7.4
+    // against 10.0 us
+    const int r = quant_rows_per_workgroup(rows_pad >= 2048 && kp >= 4096 ? 4 : 2);
+#define W8A8_QROWS(R)                                                                      \
+  quant_rows_bf16_kernel<R><<<(unsigned)((rows_pad + R - 1) / R), (unsigned)threads, 0, st>>>( \
+      (const uint16_t*)x, rows, k, delta, rows_pad, kp, qpacked, s)
+    if (r == 1) W8A8_QROWS(1);
+    else if (r == 2) W8A8_QROWS(2);
+    else if (r == 8) W8A8_QROWS(8);
+    else W8A8_QROWS(4);
+#undef W8A8_QROWS
     return hipGetLastError();
   }
   int64_t threads = (kp / (narrow ? 8 : 16) + 63) / 64 * 64;

@@ -838,3 +838,22 @@ def test_bf16_gate_up_stage_matches_oracle():
     say("  rel-L2", err)
     assert err <= 2e-3
     assert float((hg == h_o).mean()) >= 0.95
+
+
+@pytest.mark.parametrize("m,k", [(300, 6912), (2048, 1152)])
+def test_quantize_act_rows_per_workgroup_bit_exact(m, k):
+    """The many-row quantiser gives the oracle's codes and scales whatever
+    number of rows a workgroup takes (1, 2, 4, 8; the planner picks 2 or 4),
+    including ragged row counts."""
+    say("quantiser rows per workgroup", m, k)
+    rng = np.random.default_rng(77 + m)
+    x = synth.to_bf16_bits((rng.standard_normal((m, k)) * np.exp(rng.standard_normal((m, 1)))).astype(np.float32))
+    x[3] = 0
+    delta = (rng.random(k) + 0.25).astype(np.float32)
+    q_o, s_o = oracle.quantize_act(x, delta)
+    xd, dd = dev_bf16(x), dev_f32(delta)
+    for r in (1, 2, 4, 8):
+        w8a8.set_plan_override("QROWS_R", r)
+        q, s = w8a8.quantize_act(xd, dd)
+        np.testing.assert_array_equal(w8a8.frag_to_rowmajor(host(q), m, k), q_o, err_msg="R=%d" % r)
+        np.testing.assert_array_equal(host(s), s_o, err_msg="R=%d" % r)
