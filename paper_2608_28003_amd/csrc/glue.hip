@@ -83,7 +83,10 @@ __global__ __launch_bounds__(1024) void rmsnorm_kernel(const uint16_t* x,
 // NT: the workgroup size it is compiled for (the row's threads rounded up to
 // whole waves); at 1152 columns 192 threads, whose registers then hold every
 // partial sum without spilling.
-template <int NT>
+// MAXZ: split-K partial sums held in registers (more splits stream from
+// memory); 4 for the stack's plans keeps the kernel at ~80 registers, so
+// every row of a 2048-token batch is resident at once.
+template <int NT, int MAXZ>
 __global__ __launch_bounds__(NT) void glue_kernel(GlueParams g) {
   __shared__ float red_y[16], red_x[16], red_q[16];
   const int64_t r = blockIdx.x;
@@ -110,7 +113,6 @@ __global__ __launch_bounds__(NT) void glue_kernel(GlueParams g) {
   float4 d0 = make_float4(1.f, 1.f, 1.f, 1.f), d1 = d0;
   float4 si0 = make_float4(0.f, 0.f, 0.f, 0.f), si1 = si0;
   float st = 0.0f;
-  constexpr int MAXZ = 8;  // partial sums held in registers; more splits stream
   int4 pr[MAXZ][2];  // int32 partial sums, or the bits of fp32 ones
   const int64_t plane = g.m * d;
   if (own) {
@@ -265,10 +267,18 @@ hipError_t launch_glue(const GlueParams& g, hipStream_t st) {
   const int64_t rows = g.q ? g.rows_pad : g.m;
   const int64_t per_row = std::max(g.d / 8, g.q ? g.kp / 8 : 0);
   const int64_t threads = std::min<int64_t>((per_row + 63) / 64 * 64, 1024);
-  if (threads <= 256)
-    glue_kernel<256><<<(unsigned)rows, (unsigned)threads, 0, st>>>(g);
-  else
-    glue_kernel<1024><<<(unsigned)rows, (unsigned)threads, 0, st>>>(g);
+  const bool few = !g.part || g.splits <= 4;
+  if (threads <= 256) {
+    if (few)
+      glue_kernel<256, 4><<<(unsigned)rows, (unsigned)threads, 0, st>>>(g);
+    else
+      glue_kernel<256, 8><<<(unsigned)rows, (unsigned)threads, 0, st>>>(g);
+  } else {
+    if (few)
+      glue_kernel<1024, 4><<<(unsigned)rows, (unsigned)threads, 0, st>>>(g);
+    else
+      glue_kernel<1024, 8><<<(unsigned)rows, (unsigned)threads, 0, st>>>(g);
+  }
   return hipGetLastError();
 }
 
