@@ -235,3 +235,29 @@ def test_attention_projection_map_with_int8_cache(name):
         else:
             o = w8a8.bf16_linear(dev_bf16(att_o[None, :]), w8a8.pack_bf16(dev_bf16(L["w_o"])), n_o, 1024)
             assert rel_l2(host_bf16(o), o_o) <= 1e-2, l
+
+
+@pytest.mark.parametrize("int8", [True, False])
+@pytest.mark.parametrize("t_max,pos,window", [(200, 150, 1), (200, 150, 2), (5000, 100, 4096), (4097, 4096, 4097)])
+def test_attn_decode_edge_windows(int8, t_max, pos, window):
+    """A window of one row (the output is the new value alone), of two, a
+    cache far longer than the rows written, and a pass boundary right before
+    the new row with many workgroups."""
+    say("attn edge int8=%d t_max=%d pos=%d window=%d" % (int8, t_max, pos, window))
+    inp = synth.kv_decode_inputs(6100 + pos + window, pos, n_heads=4)
+    oc, gc = make_caches(inp, pos, t_max, int8)
+    out_o = oracle.attn_block_decode(inp["qkv"], oc, pos, window)
+    out = w8a8.attn_decode(dev_bf16(inp["qkv"]), gc, pos, window)
+    check_out(host_bf16(out), out_o, "edge")
+    if window == 1:  # softmax over one row: the value itself, for every head
+        v = oracle.kv_rows(oc, pos, pos + 1)[1][0]
+        np.testing.assert_array_equal(out_o, oracle.f64_to_bf16(np.tile(v, 4)))
+
+
+def test_attn_decode_eight_heads_bf16_cache():
+    t_max, pos, window = 3000, 2999, 3000
+    inp = synth.kv_decode_inputs(6200, pos, n_heads=8)
+    oc, gc = make_caches(inp, pos, t_max, False)
+    out_o = oracle.attn_block_decode(inp["qkv"], oc, pos, window, n_heads=8)
+    out = w8a8.attn_decode(dev_bf16(inp["qkv"]), gc, pos, window, n_heads=8)
+    check_out(host_bf16(out), out_o, "8 heads bf16")
