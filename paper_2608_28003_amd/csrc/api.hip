@@ -121,6 +121,7 @@ void tile_shape(int tile, int* bm, int* bn) {
     case TILE_GLU_256x64_K2_W8: *bm = 256; *bn = 64; break;
     case TILE_GLU_128x32_K3: *bm = 128; *bn = 32; break;
     case TILE_64x64_K3: *bm = 64; *bn = 64; break;
+    case TILE_256x128_W4: *bm = 256; *bn = 128; break;
     default: *bm = 128; *bn = 128;
   }
 }
@@ -270,8 +271,14 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
     p.tile = t64 * sp <= 256 ? TILE_64x64_K3 : TILE_64x64_K2;
   } else {
     // measured on the lm_head (N = 262144): 256 x 256 from M = 256 (133.7 vs
-    // 162.4 us at M = 256, 888 vs 924 us at M = 2048), 128 x 128 below
-    if (i8 && m >= 256 && tiles_of(TILE_256x256, m, n) >= 512)
+    // 162.4 us at M = 256, 888 vs 924 us at M = 2048), 128 x 128 below; from
+    // M = 512 and ~400 tiles the 4-wave 256 x 128 tile, two per CU (lm_head
+    // M = 2048 856 -> 827 us, M = 512 242 -> 237 us; N = 13824 at M = 1024
+    // 47.5 -> 40.9 us; N = 6912 at M = 2048 50.4 -> 42.9 us; with fewer tiles
+    // it loses: N = 6912 at M = 1024 36.9 vs 33.2 us)
+    if (i8 && m >= 512 && tiles_of(TILE_256x128_W4, m, n) >= 400)
+      p.tile = TILE_256x128_W4;
+    else if (i8 && m >= 256 && tiles_of(TILE_256x256, m, n) >= 512)
       p.tile = TILE_256x256;
     else if (i8 && m <= 64 && kb % 2 == 0 && tiles_of(TILE_64x64, m, n) >= 1024)
       p.tile = TILE_64x64_K2;  // very wide outputs at up to 64 rows (lm_head)

@@ -839,6 +839,8 @@ static hipError_t tile_dispatch(int tile, const GemmParams& p, hipStream_t st) {
           return launch_tile<DT, 256, 256, 2, 8, EPI, 5, 1>(p, st);
         case TILE_64x64_K3:  // 96 KiB of LDS: one workgroup per CU
           return launch_tile<DT, 64, 64, 2, 8, EPI, 4, 3, 1>(p, st);
+        case TILE_256x128_W4:  // 72 KiB of LDS: two workgroups per CU
+          return launch_tile<DT, 256, 128, 2, 4, EPI, 3, 1>(p, st);
         default:
           break;
       }

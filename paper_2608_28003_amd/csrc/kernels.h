@@ -95,6 +95,8 @@ enum TileCfg {
                                // four stages (1 per CU)
   TILE_64x64_K3 = 16,          // 8 waves of 32 x 16, three fragment columns per stage,
                                // four stages, 96 KiB of LDS (1 per CU)
+  TILE_256x128_W4 = 17,        // 4 waves of 128 x 64, three stages, 72 KiB of LDS
+                               // (2 per CU)
 };
 
 hipError_t launch_col_absmax(const void* x, bool bf16, int64_t rows, int64_t k, float* amax,

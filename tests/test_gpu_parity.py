@@ -272,7 +272,7 @@ def test_gemm_split_k_is_bit_identical(m, n, k, splits, monkeypatch):
     w8a8.set_plan_override("GEMM_SPLITS", splits)
     for xcd in ((0, 1) if m > n else (1,)):
         w8a8.set_plan_override("XCD_M", xcd)
-        for tile in (0, 1, 2, 3, 7, 10, 11, 16):
+        for tile in (0, 1, 2, 3, 7, 10, 11, 16, 17):
             w8a8.set_plan_override("GEMM_TILE", tile)
             acc = w8a8.gemm_i8_i32(A, m, B, n, k)
             torch.cuda.synchronize()
@@ -333,6 +333,27 @@ def test_linear_attention_shapes_bit_exact(m, n, k):
     y = w8a8.linear(layer, dev_bf16(x), torch.bfloat16)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(host_bf16(y), y_o)
+
+
+@pytest.mark.parametrize("out_dtype", ["f32", "bf16"])
+def test_linear_wide_tile_both_epilogues_bit_exact(out_dtype):
+    """The 4-wave 256 x 128 tile (the plan from M = 512 on wide outputs) with
+    both dequantising epilogues, ragged in M (600 = 2 * 256 + 88) and N
+    (1000 = 7 * 128 + 104); the planner's own choice at M = 1024, N = 13824
+    is the same tile."""
+    say("linear 4-wave 256 x 128 tile", out_dtype)
+    m, n, k = 600, 1000, 1152
+    x = act_input(m, k, 4242)
+    w = synth.to_bf16_bits(synth.normal(4343, (n, k), 0.02))
+    delta = oracle.smooth_calibrate(act_input(512, k, 4444), [w])
+    wq_o, sw_o = oracle.quantize_weights(w, delta)
+    y_o = oracle.w8a8_linear(x, wq_o, sw_o, delta, out_dtype)
+    layer = w8a8.LinearW8A8.from_weight(dev_bf16(w), dev_f32(delta))
+    w8a8.set_plan_override("GEMM_TILE", 17)
+    w8a8.set_plan_override("GEMM_SPLITS", 1)
+    y = w8a8.linear(layer, dev_bf16(x), torch.float32 if out_dtype == "f32" else torch.bfloat16)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(y) if out_dtype == "f32" else host_bf16(y), y_o)
 
 
 # ------------------------------------------------------------------ a6: FFN
@@ -509,16 +530,18 @@ def lm_full():
     return cfg, delta, layer
 
 
-@pytest.mark.parametrize("m", [1, 8, 64, 256])
+@pytest.mark.parametrize("m", [1, 8, 64, 256, 600])
 def test_lm_head_full_vocab_sampled_columns(m, lm_full):
-    """M = 256 takes the 256 x 256 tile (rows beyond the fixture's 64 are
+    """M = 256 takes the 256 x 256 tile, M = 600 the 4-wave 256 x 128 tile
+    with a ragged last row block of 88 (rows beyond the fixture's 64 are
     scaled and negated copies, so every row block holds distinct rows)."""
     say("lm_head full vocab, sampled columns", m)
     cfg, delta, layer = lm_full
     x = cfg["x"]
     if m > x.shape[0]:
         xf = oracle.bf16_to_f32(x)
-        x = np.concatenate([x] + [synth.to_bf16_bits(xf * c) for c in (1.5, 0.75, -1.0)])
+        x = np.concatenate([x] + [synth.to_bf16_bits(xf * c)
+                                  for c in (1.5, 0.75, -1.0, 2.0, -0.5, 3.0, 0.25, -1.5, 1.25)])
     x = np.ascontiguousarray(x[:m])
     y = w8a8.lm_head(layer, dev_bf16(x))
     torch.cuda.synchronize()
