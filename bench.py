@@ -595,6 +595,20 @@ def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all
     # 2 x 604 MB bf16; the memory-side cache holds 256 MB), so every call
     # reads its weights from HBM.
     n8, nb = 3, 2
+    import ctypes
+    from paper_2608_28003_amd import build as hip_build
+    PL = ctypes.CDLL(hip_build.PEAK_LIB_PATH)
+    PL.w8a8_peak_read_write.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
+                                        ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def rw_floor(wq, lg, m):
+        rc = PL.w8a8_peak_read_write(ctypes.c_void_p(wq.data_ptr()), V, D, ctypes.c_void_p(lg.data_ptr()),
+                                     m, 1024, ctypes.c_void_p(sink.data_ptr()),
+                                     ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        if rc != 0:
+            raise RuntimeError("read/write probe failed: %d" % rc)
+
     lm8s = [lm_int8] + [w8a8.LinearW8A8(lm_int8.n, lm_int8.k, lm_int8.wq.clone(), lm_int8.s_w.clone(),
                                         lm_int8.delta) for _ in range(n8 - 1)]
     lmfs = [lm_fp8] + [w8a8.LinearW8A8(lm_fp8.n, lm_fp8.k, lm_fp8.wq.clone(), lm_fp8.s_w.clone(),
@@ -613,6 +627,10 @@ def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all
                                  for wp in lmbs])
         gt = make_graph(lambda: [torch.mm(xm, wt, out=lg) for wt in w_lm_ts])
         gf = make_graph(lambda: [w8a8.fp8_lm_head(L, xm, out=lg, ws=wsf) for L in lmfs])
+        # the same weight bytes read and the same logits written by a kernel
+        # that does no arithmetic: the practical floor of this call
+        gp = make_graph(lambda: [rw_floor(L.wq, lg, m) for L in lm8s])
+        tp = time_graph(gp) / n8
         t8 = time_graph(g8) / n8
         tb = time_graph(gb) / nb
         tt = time_graph(gt) / nb
@@ -624,12 +642,14 @@ def extras(torch, w8a8, stack, int8_layers, bf16_layers, lm_int8, lm_bf16, x_all
             "bf16_torch_us": round(tt * 1e6, 2), "speedup": round(min(tb, tt) / t8, 3),
             "int8_GBs": round(b8 / t8 / 1e9, 1), "int8_hbm_frac": round(b8 / t8 / 1e9 / HBM_PEAK_GBS, 3),
             "int8_frac_of_measured_read": round(b8 / t8 / 1e9 / peaks["hbm_read_GBs"], 3),
+            "read_write_floor_us": round(tp * 1e6, 2),
+            "int8_frac_of_read_write_floor": round(tp / t8, 3),
             "bf16_best_GBs": round(bb / min(tb, tt) / 1e9, 1),
             "fp8_us": round(tf * 1e6, 2), "fp8_GBs": round(b8 / tf / 1e9, 1),
             "note": "median of 15; each replay rotates over %d INT8 / %d bf16 weight copies" % (n8, nb)}
-        del g8, gb, gt, gf
-        log("lm_head m=%d: int8 %.2f us, bf16 ours %.2f us, torch %.2f us, fp8 %.2f us"
-            % (m, t8 * 1e6, tb * 1e6, tt * 1e6, tf * 1e6))
+        del g8, gb, gt, gf, gp
+        log("lm_head m=%d: int8 %.2f us, bf16 ours %.2f us, torch %.2f us, fp8 %.2f us, "
+            "read+write floor %.2f us" % (m, t8 * 1e6, tb * 1e6, tt * 1e6, tf * 1e6, tp * 1e6))
     del w_lm_ts, lm8s, lmfs, lmbs
 
     # --- the paper's precision maps on the whole step: at the step's M and at

@@ -54,6 +54,40 @@ __global__ __launch_bounds__(256) void read_stream_kernel(const v4u* __restrict_
   if (s == 0x9e3779b9u) sink[0] = s;
 }
 
+// The lm_head's memory traffic without its arithmetic: runs of 64 weight rows
+// (64 x k bytes, contiguous) are read with 16-byte loads, all of a thread's
+// loads in flight at once, and after each run the run's 64 columns of `rows`
+// bf16 output rows are written as 128-byte row segments.  Workgroups take
+// runs grid-stride.  k is a multiple of 64 and at most 64 * kRwMaxLoads.
+constexpr int kRwMaxLoads = 24;
+__global__ __launch_bounds__(256) void read_write_kernel(const v4u* __restrict__ w, int64_t n,
+                                                         int k, v4u* __restrict__ out, int rows,
+                                                         unsigned* sink) {
+  const int t = (int)threadIdx.x;
+  const int per_t = k / 64;                  // 16-byte loads per thread and run
+  const int64_t run_words = (int64_t)k * 4;  // 64 rows of k bytes, in 16-byte words
+  const int64_t runs = n / 64;
+  const int64_t ld_row = n / 8;              // output row stride in 16-byte words
+  v4u acc = {0u, 0u, 0u, 0u};
+  for (int64_t r = blockIdx.x; r < runs; r += gridDim.x) {
+    const v4u* src = w + r * run_words;
+    v4u v[kRwMaxLoads];
+#pragma unroll
+    for (int u = 0; u < kRwMaxLoads; ++u)
+      if (u < per_t) v[u] = __builtin_nontemporal_load(src + u * 256 + t);
+#pragma unroll
+    for (int u = 0; u < kRwMaxLoads; ++u)
+      if (u < per_t) acc ^= v[u];
+    for (int i = t; i < rows * 8; i += 256) {
+      const int row = i >> 3, ch = i & 7;
+      const v4u val = {acc.x, (unsigned)row, (unsigned)ch, (unsigned)r};
+      __builtin_nontemporal_store(val, out + row * ld_row + r * 8 + ch);
+    }
+  }
+  const unsigned s = acc.x ^ acc.y ^ acc.z ^ acc.w;
+  if (s == 0x9e3779b9u) sink[0] = s;
+}
+
 }  // namespace
 
 extern "C" {
@@ -73,6 +107,17 @@ int w8a8_peak_read(const void* buf, size_t bytes, int blocks, unsigned* sink, vo
     return 1;
   read_stream_kernel<<<blocks, 256, 0, reinterpret_cast<hipStream_t>(stream)>>>(
       reinterpret_cast<const v4u*>(buf), (int64_t)(bytes / 16), sink);
+  return hipGetLastError() == hipSuccess ? 0 : 3;
+}
+
+int w8a8_peak_read_write(const void* w, int64_t n, int k, void* out, int rows, int blocks,
+                         unsigned* sink, void* stream) {
+  if (!w || !out || !sink || n < 64 || n % 64 || k < 64 || k % 64 || k > 64 * kRwMaxLoads ||
+      rows < 0 || blocks < 1 || (reinterpret_cast<uintptr_t>(w) & 15) ||
+      (reinterpret_cast<uintptr_t>(out) & 15))
+    return 1;
+  read_write_kernel<<<blocks, 256, 0, reinterpret_cast<hipStream_t>(stream)>>>(
+      reinterpret_cast<const v4u*>(w), n, k, reinterpret_cast<v4u*>(out), rows, sink);
   return hipGetLastError() == hipSuccess ? 0 : 3;
 }
 

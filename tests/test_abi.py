@@ -20,8 +20,8 @@ FAKE = P(0x1000)          # aligned, never dereferenced: validation fails first
 MISALIGNED = P(0x1004)
 
 
-def _declared():
-    text = open(HEADER).read()
+def _declared(header=HEADER):
+    text = open(header).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(w8a8_[a-z0-9_]+)\s*\(", text)))
 
@@ -33,6 +33,26 @@ def test_library_exports_every_declared_symbol():
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(w8a8.exported_names())
+
+
+def test_peak_library_exports_its_header_and_rejects_bad_arguments():
+    """The benchmark's ceiling probes (include/w8a8_peak.h): every declared
+    symbol is exported, and bad arguments return 1 before any launch."""
+    from paper_2608_28003_amd import build as hip_build
+    L = ctypes.CDLL(hip_build.PEAK_LIB_PATH)
+    names = _declared(os.path.join(ROOT, "include", "w8a8_peak.h"))
+    assert len(names) == 4
+    for n in names:
+        assert hasattr(L, n), n
+    L.w8a8_peak_read_write.argtypes = [P, ctypes.c_int64, ctypes.c_int, P, ctypes.c_int,
+                                       ctypes.c_int, P, P]
+    L.w8a8_peak_read.argtypes = [P, ctypes.c_size_t, ctypes.c_int, P, P]
+    assert L.w8a8_peak_read_write(FAKE, 262144, 1100, FAKE, 64, 1024, FAKE, None) == 1  # k % 64
+    assert L.w8a8_peak_read_write(FAKE, 262144, 1600, FAKE, 64, 1024, FAKE, None) == 1  # k > 1536
+    assert L.w8a8_peak_read_write(FAKE, 100, 1152, FAKE, 64, 1024, FAKE, None) == 1     # n % 64
+    assert L.w8a8_peak_read_write(MISALIGNED, 262144, 1152, FAKE, 64, 1024, FAKE, None) == 1
+    assert L.w8a8_peak_read_write(FAKE, 262144, 1152, None, 64, 1024, FAKE, None) == 1
+    assert L.w8a8_peak_read(FAKE, 8, 16, FAKE, None) == 1
 
 
 def test_status_strings():
