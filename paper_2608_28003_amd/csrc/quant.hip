@@ -297,11 +297,19 @@ __device__ __forceinline__ float div_via_f64(float a, double rb) {
 // all R rows' loads are in flight together, and one block reduction gives
 // the R row maxima.  Same results as quant_rows_kernel (x / delta and v / s
 // correctly rounded, see div_via_f64; the maximum does not depend on order).
+//
+// Quotients x / delta below the normal range are the one case div_via_f64
+// does not cover, and they are settled per row, not per element: if the row's
+// maximum is at least 2^-118, such an element is not the maximum (its value is
+// below 2^-126 on either route) and its code is 0 on either route (|v / s| <=
+// 127 * 2^-126 / 2^-118 < 1/2); a row below 2^-118 is redone with IEEE
+// divisions.
 template <int R>
 __global__ __launch_bounds__(1024) void quant_rows_bf16_kernel(
     const uint16_t* __restrict__ x, int64_t rows, int64_t k, const float* __restrict__ delta,
     int64_t rows_pad, int64_t kp, int8_t* __restrict__ q, float* __restrict__ s) {
   __shared__ float red[R][16];
+  __shared__ float red_ieee[16];
   const int t = threadIdx.x;
   const int nw = blockDim.x >> 6;
   const int64_t r0 = (int64_t)blockIdx.x * R;
@@ -327,33 +335,21 @@ __global__ __launch_bounds__(1024) void quant_rows_bf16_kernel(
       raw[i][0] = raw[i][1] = make_uint4(0u, 0u, 0u, 0u);
     }
   }
+  auto x_of = [&](int i, int e) {
+    const uint32_t w = (e >> 1) < 4 ? (&raw[i][0].x)[e >> 1] : (&raw[i][1].x)[(e >> 1) - 4];
+    return bf16_bits_to_float((e & 1) ? (w >> 16) : (w & 0xffffu));
+  };
   float v[R][16];
   float mx[R];
 #pragma unroll
   for (int i = 0; i < R; ++i) {
-    const uint32_t w[8] = {raw[i][0].x, raw[i][0].y, raw[i][0].z, raw[i][0].w,
-                           raw[i][1].x, raw[i][1].y, raw[i][1].z, raw[i][1].w};
-    bool tiny = false;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const float xv = bf16_bits_to_float((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xffffu));
-      float vv = xv;
-      if (delta) {
-        vv = div_via_f64(xv, rd[e]);
-        tiny |= (fabsf(vv) < 1.17549435e-38f) && (xv != 0.0f);
-      }
-      v[i][e] = vv;
-    }
-    if (tiny) {  // quotient below the normal range: the IEEE division
-      float d[16];
-      load16<float>(delta + (int64_t)t * 16, d);
-#pragma unroll
-      for (int e = 0; e < 16; ++e)
-        v[i][e] = bf16_bits_to_float((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xffffu)) / d[e];
-    }
     float m = 0.0f;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) m = fmaxf(m, fabsf(v[i][e]));
+    for (int e = 0; e < 16; ++e) {
+      const float xv = x_of(i, e);
+      v[i][e] = delta ? div_via_f64(xv, rd[e]) : xv;
+      m = fmaxf(m, fabsf(v[i][e]));
+    }
     mx[i] = wave_max(m);
   }
   if ((t & 63) == 0) {
@@ -367,6 +363,31 @@ __global__ __launch_bounds__(1024) void quant_rows_bf16_kernel(
     for (int w = 1; w < nw; ++w) m = fmaxf(m, red[i][w]);
     mx[i] = m;
   }
+  // rows below 2^-118 (every thread holds the same maximum: a uniform branch)
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    if (!delta || r0 + i >= rows || !(mx[i] < 0x1p-118f)) continue;
+    float m = 0.0f;
+    if (own) {  // the row is read again (the registers holding it are free by now)
+      float d[16];
+      load16<float>(delta + (int64_t)t * 16, d);
+      const uint4* p = reinterpret_cast<const uint4*>(x + (r0 + i) * k + (int64_t)t * 16);
+      const uint4 w0 = p[0], w1 = p[1];
+      const uint32_t w[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        v[i][e] = bf16_bits_to_float((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xffffu)) / d[e];
+        m = fmaxf(m, fabsf(v[i][e]));
+      }
+    }
+    m = wave_max(m);
+    __syncthreads();  // an earlier row's maxima have been read
+    if ((t & 63) == 0) red_ieee[t >> 6] = m;
+    __syncthreads();
+    m = red_ieee[0];
+    for (int w = 1; w < nw; ++w) m = fmaxf(m, red_ieee[w]);
+    mx[i] = m;
+  }
 #pragma unroll
   for (int i = 0; i < R; ++i) {
     const int64_t r = r0 + i;
@@ -377,14 +398,20 @@ __global__ __launch_bounds__(1024) void quant_rows_bf16_kernel(
       if (t == 0) s[r] = sr;
       if (own && sr != 0.0f) {
         const double rs = 1.0 / (double)sr;
+        uint32_t b[16];
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          // |v / s| <= 127 (1 + 2^-23) except for a subnormal scale; the clamp
-          // keeps the codes of that case, as in code_of
-          float c = rintf(div_via_f64(v[i][e], rs));
-          c = fminf(fmaxf(c, -127.0f), 127.0f);
-          packed[e >> 2] |= ((int32_t)(int)c & 0xff) << (8 * (e & 3));
+          // |v / s| <= 127 (1 + 2^-23) except for a subnormal scale; clamping
+          // before rounding gives the codes of rounding first, as in code_of.
+          // c + 1.5 * 2^23 rounds c to an integer, ties to even (the offset is
+          // even), and its low byte is that integer in two's complement.
+          const float c = fminf(fmaxf(div_via_f64(v[i][e], rs), -127.0f), 127.0f);
+          b[e] = __float_as_uint(c + 12582912.0f);
         }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          packed[j] = (int32_t)((b[4 * j] & 0xffu) | ((b[4 * j + 1] & 0xffu) << 8) |
+                                ((b[4 * j + 2] & 0xffu) << 16) | (b[4 * j + 3] << 24));
       }
     }
     // blockDim covers chunks_pad: one chunk per thread (padding columns and
