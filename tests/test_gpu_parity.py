@@ -152,6 +152,40 @@ def test_quantize_act_many_rows_division_edge_cases():
     np.testing.assert_array_equal(w8a8.frag_to_rowmajor(host(qx), m, k), q_o)
 
 
+@pytest.mark.parametrize("k", [6912, 1152])
+@pytest.mark.parametrize("r", [1, 2, 4])
+def test_quantize_act_many_rows_tiny_rows(k, r):
+    """Rows whose every quotient x / delta lies below 2^-118 take the IEEE
+    divisions in the many-row quantiser; rows with a larger maximum keep the
+    binary64 route even where some quotients are subnormal (their codes are
+    0 either way).  Rows on both sides of the threshold, subnormal and
+    underflowing quotients, all-zero rows; bit for bit against the oracle."""
+    say("quantize_act tiny rows", k, r)
+    m = 320
+    rng = np.random.default_rng(k + r)
+    delta = np.exp2(rng.uniform(20, 40, k)).astype(np.float32)
+    target = np.exp2(rng.uniform(-150, -100, (m, k)))              # quotients to aim for
+    target[0::4] = np.exp2(rng.uniform(-150, -119, (m // 4, k)))   # whole row below 2^-118
+    target[1::4] = np.exp2(rng.uniform(-160, -127, (m // 4, k)))   # subnormal ...
+    target[1::4, 7] = 2.0 ** -117                                  # ... under a maximum above
+    target[2::4] = np.exp2(rng.uniform(-140, -118.5, (m // 4, k)))
+    target[2::8, 3] = 2.0 ** -118 * (1 - 2.0 ** -6)                # maxima just below and
+    target[6::8, 3] = 2.0 ** -118 * (1 + 2.0 ** -6)                # just above the threshold
+    sign = np.where(rng.random((m, k)) < 0.5, -1.0, 1.0)
+    x = synth.to_bf16_bits((sign * target * delta).astype(np.float32))
+    x[4] = 0                                                       # all-zero rows
+    x[m - 1] = 0
+    w8a8.set_plan_override("QROWS_R", r)
+    q_o, s_o = oracle.quantize_act(x, delta)
+    qx, sx = w8a8.quantize_act(dev_bf16(x), dev_f32(delta))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(sx), s_o)
+    np.testing.assert_array_equal(w8a8.frag_to_rowmajor(host(qx), m, k), q_o)
+    thr = np.float32(2.0 ** -118 / 127)
+    assert (s_o[0::4] < thr).sum() > 40 and (s_o[1::4] > thr).all()
+    assert (s_o[2::8] < thr).all() and (s_o[6::8] > thr).all()
+
+
 # ------------------------------------------------------------------ a1 / a2
 
 @pytest.mark.parametrize("alpha", [0.5, 0.3])
