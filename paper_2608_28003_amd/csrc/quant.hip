@@ -335,18 +335,16 @@ __global__ __launch_bounds__(1024) void quant_rows_bf16_kernel(
       raw[i][0] = raw[i][1] = make_uint4(0u, 0u, 0u, 0u);
     }
   }
-  auto x_of = [&](int i, int e) {
-    const uint32_t w = (e >> 1) < 4 ? (&raw[i][0].x)[e >> 1] : (&raw[i][1].x)[(e >> 1) - 4];
-    return bf16_bits_to_float((e & 1) ? (w >> 16) : (w & 0xffffu));
-  };
   float v[R][16];
   float mx[R];
 #pragma unroll
   for (int i = 0; i < R; ++i) {
+    const uint32_t w[8] = {raw[i][0].x, raw[i][0].y, raw[i][0].z, raw[i][0].w,
+                           raw[i][1].x, raw[i][1].y, raw[i][1].z, raw[i][1].w};
     float m = 0.0f;
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      const float xv = x_of(i, e);
+      const float xv = bf16_bits_to_float((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xffffu));
       v[i][e] = delta ? div_via_f64(xv, rd[e]) : xv;
       m = fmaxf(m, fabsf(v[i][e]));
     }
