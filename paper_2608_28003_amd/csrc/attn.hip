@@ -394,6 +394,59 @@ size_t attn_ws_bytes_max(int64_t t_max) {
   return n > 1 ? (size_t)n * kPartFloats * sizeof(float) : 0;
 }
 
+// Merge of at most 16 * CPT partial results: every partial's maximum, sum
+// and output dimension loaded at once (one memory round trip), then the
+// maximum over the chunks, each thread's factors exp(m_c - M) for its chunks
+// c = wave, wave + 16, ..., and the sums over the 16 waves in wave order.
+template <int CPT>
+__global__ __launch_bounds__(1024) void attn_merge_few_kernel(AttnParams p) {
+  __shared__ float wmax[16], wden[16];
+  __shared__ float red[16][64];
+  const int h = blockIdx.x >> 2, d = (blockIdx.x & 3) * 64 + (threadIdx.x & 63);
+  const int tid = threadIdx.x, g = tid >> 6, lane = tid & 63, n = p.n_wg;
+  float mc[CPT], lc[CPT], oc[CPT];
+#pragma unroll
+  for (int j = 0; j < CPT; ++j) {
+    const int c = g + 16 * j;
+    mc[j] = -INFINITY;
+    lc[j] = 0.0f;
+    oc[j] = 0.0f;
+    if (c < n) {
+      const float* part = p.part + (int64_t)c * kPartFloats;
+      mc[j] = part[h];
+      lc[j] = part[kMaxHeads + h];
+      oc[j] = part[2 * kMaxHeads + h * kHd + d];
+    }
+  }
+  float m = mc[0];
+#pragma unroll
+  for (int j = 1; j < CPT; ++j) m = fmaxf(m, mc[j]);
+  if (lane == 0) wmax[g] = m;  // the same in every lane of the wave
+  __syncthreads();
+  m = wmax[0];
+  for (int i = 1; i < 16; ++i) m = fmaxf(m, wmax[i]);
+  float den = 0.0f, num = 0.0f;
+#pragma unroll
+  for (int j = 0; j < CPT; ++j) {
+    if (g + 16 * j < n) {
+      const float f = expf(mc[j] - m);
+      den += lc[j] * f;
+      num += oc[j] * f;
+    }
+  }
+  if (lane == 0) wden[g] = den;
+  red[g][lane] = num;
+  __syncthreads();
+  if (g == 0) {
+    float t = 0.0f, dn = 0.0f;
+    for (int i = 0; i < 16; ++i) {
+      t += red[i][lane];
+      dn += wden[i];
+    }
+    p.out[h * kHd + d] = float_to_bf16_bits(t / dn);
+  }
+}
+
 template <bool I8>
 static hipError_t attn_launch(const AttnParams& p, int nh, hipStream_t st) {
   const dim3 grid((unsigned)p.n_wg);
@@ -406,7 +459,10 @@ static hipError_t attn_launch(const AttnParams& p, int nh, hipStream_t st) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_wg == 1) return e;
-  attn_merge_kernel<<<dim3((unsigned)(4 * nh)), 1024, 0, st>>>(p);
+  if (p.n_wg <= 64)  // up to 4096 rows: one round trip for every partial
+    attn_merge_few_kernel<4><<<dim3((unsigned)(4 * nh)), 1024, 0, st>>>(p);
+  else
+    attn_merge_kernel<<<dim3((unsigned)(4 * nh)), 1024, 0, st>>>(p);
   return hipGetLastError();
 }
 
