@@ -98,11 +98,15 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(AttnParams p) {
   const int64_t r_end = min(r_begin + p.rows_per_wg, p.pos + 1);  // exclusive
 
   const int jr = l >> 2, qd = l & 3;  // score phase: row 16w + jr, dimensions 64 qd ..
-  // The keys and values of a pass are loaded one pass ahead: pass i + 1's
-  // loads are issued before pass i's arithmetic and barriers.
+  // The keys, values and (INT8) their scales of a pass are loaded one pass
+  // ahead: pass i + 1's loads are issued before pass i's arithmetic and
+  // barriers; the first pass's before the staging of the query and the new
+  // row, unless that pass holds the new row.
   struct PassRegs {
     uint4 kc[I8 ? 4 : 8];          // key row 16 w + jr, dimensions 64 qd .. 64 qd + 63
     uint32_t vv[16][I8 ? 1 : 2];   // value rows 16 w .. 16 w + 15, dimensions 4 l .. 4 l + 3
+    float ks, vs;                  // INT8: scale of key row 16 w + jr, of value row l (the
+                                   // new row's come from LDS where they are used)
   };
   // loads of a pass; the new row (pos) comes from LDS, where its codes are
   // staged behind the first barrier
@@ -144,7 +148,18 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(AttnParams p) {
 #pragma unroll
       for (int c = 0; c < NK; ++c) R.kc[c] = make_uint4(0, 0, 0, 0);
     }
+    R.ks = 0.0f;
+    R.vs = 0.0f;
+    if constexpr (I8) {
+      if (row < r_end && row != p.pos) R.ks = p.sk[row];
+      const int64_t rv = r0 + l;
+      if (rv < r_end && rv != p.pos) R.vs = p.sv[rv];
+    }
   };
+  PassRegs cur, nxt;
+  // the first pass's loads ahead of the staging when they need nothing staged
+  const bool early = r_begin < r_end && !(p.pos >= r_begin && p.pos < r_begin + kPass);
+  if (early) load_pass(r_begin, cur);
   for (int i = tid; i < NH * kHd; i += 256) qs[i / kHd][qidx(i % kHd)] = bf16_bits_to_float(p.qkv[i]);
   if (tid < NH) {
     run_m[tid] = -INFINITY;
@@ -173,9 +188,7 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(AttnParams p) {
     }
   }
   __syncthreads();
-
-  PassRegs cur, nxt;
-  if (r_begin < r_end) load_pass(r_begin, cur);
+  if (r_begin < r_end && !early) load_pass(r_begin, cur);
 
   // per lane: 4 output dimensions (4l .. 4l + 3) of every head, summed over
   // the rows this wave handles
@@ -238,7 +251,7 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(AttnParams p) {
       }
       if (qd == 0) {
         float ks = 1.0f;
-        if constexpr (I8) ks = valid ? (row == p.pos ? knew_s : p.sk[row]) : 0.0f;
+        if constexpr (I8) ks = valid ? (row == p.pos ? knew_s : cur.ks) : 0.0f;
 #pragma unroll
         for (int h = 0; h < NH; ++h)
           sc[h][16 * w + jr] = valid ? (acc[h] * ks) * 0.0625f : -INFINITY;
@@ -256,7 +269,7 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(AttnParams p) {
       float wgt = e;
       if constexpr (I8) {
         const int64_t row = r0 + l;
-        wgt = row < r_end ? e * (row == p.pos ? vnew_s : p.sv[row]) : 0.0f;
+        wgt = row < r_end ? e * (row == p.pos ? vnew_s : cur.vs) : 0.0f;
       }
       sc[h][l] = wgt;
       if (l == 0) {
