@@ -264,7 +264,7 @@ def main():
 def measured_traffic(m):
     """HBM bytes per launch of the gate/up kernel at M = m from the committed
     counter summary, or None when there is none for this M or it was taken on
-    other kernel sources than the ones built here."""
+    other kernel or planner sources than the ones built here."""
     import hashlib
     import re
     path = os.path.join(ROOT, "profiles", "gate_up_geglu_m%d_hbm_traffic.md" % m)
@@ -274,7 +274,7 @@ def measured_traffic(m):
     except (OSError, AttributeError, ValueError):
         return None
     h = hashlib.sha256()
-    for f in ("gemm.hip", "device.h", "kernels.h"):
+    for f in ("gemm.hip", "device.h", "kernels.h", "api.hip"):  # kernels and their plans
         with open(os.path.join(ROOT, "paper_2608_28003_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     if rec.get("m") != m or rec.get("source_sha256") != h.hexdigest():

@@ -1,7 +1,7 @@
 """Host-side pieces of the benchmark that need no GPU: the refusal of a
 multi-GPU run, and the rule that the roofline's HBM traffic is read from a
-committed counter summary only while the kernel sources still hash to the
-value recorded with it."""
+committed counter summary only while the kernel and planner sources still
+hash to the value recorded with it."""
 
 import hashlib
 import json
@@ -26,14 +26,14 @@ def test_more_than_one_gpu_is_refused_with_a_message():
 def _fake_tree(tmp_path, m, sha, traffic=12345):
     csrc = tmp_path / "paper_2608_28003_amd" / "csrc"
     csrc.mkdir(parents=True)
-    for name in ("gemm.hip", "device.h", "kernels.h"):
+    for name in ("gemm.hip", "device.h", "kernels.h", "api.hip"):
         (csrc / name).write_text("// %s\n" % name)
     (tmp_path / "profiles").mkdir()
     rec = {"kernel": "k", "m": m, "traffic_bytes": traffic, "source_sha256": sha}
     (tmp_path / "profiles" / ("gate_up_geglu_m%d_hbm_traffic.md" % m)).write_text(
         "# summary\n\n```json\n%s\n```\n" % json.dumps(rec))
     h = hashlib.sha256()
-    for name in ("gemm.hip", "device.h", "kernels.h"):
+    for name in ("gemm.hip", "device.h", "kernels.h", "api.hip"):
         h.update((csrc / name).read_bytes())
     return h.hexdigest()
 

@@ -313,6 +313,32 @@ def test_gemm_split_k_is_bit_identical(m, n, k, splits, monkeypatch):
             np.testing.assert_array_equal(host(acc), acc_o, err_msg="tile %d xcd %d" % (tile, xcd))
 
 
+@pytest.mark.parametrize("glu_tile", [13, 6, 15])
+def test_nontemporal_output_stores_are_bit_identical(glu_tile):
+    """The store policy changes no value: gated outputs (h) and dequantised
+    linear outputs with and without non-temporal stores, on tiles with ragged
+    rows and columns (m = 300, 1008 columns)."""
+    say("non-temporal stores, gated tile", glu_tile)
+    m, d, f = 300, 1152, 1008
+    cfg = synth.ffn_config(m=m, d=d, f=f)
+    q = oracle.quantize_ffn(cfg["w_gate"], cfg["w_up"], cfg["w_down"], cfg["x_cal"][:64])
+    layer = w8a8.FfnW8A8.from_weights(dev_bf16(cfg["w_gate"]), dev_bf16(cfg["w_up"]),
+                                      dev_bf16(cfg["w_down"]), dev_f32(q["delta_gu"]),
+                                      dev_f32(q["delta_down"]))
+    _, st = oracle.w8a8_ffn(cfg["x"], q, stages=True)
+    qx = torch.from_numpy(w8a8.rowmajor_to_frag(st["qx"])).to(DEV)
+    w8a8.set_plan_override("GLU_TILE", glu_tile)
+    outs = []
+    for nt in (0, 1):
+        w8a8.set_plan_override("NT_OUT", nt)
+        h = host_bf16(w8a8.ffn_gate_up(layer, qx, dev_f32(st["sx"]), m))
+        y = host_bf16(w8a8.linear(layer.up, dev_bf16(cfg["x"]), torch.bfloat16))
+        outs.append((h, y))
+    np.testing.assert_array_equal(outs[0][0], outs[1][0])
+    np.testing.assert_array_equal(outs[0][1], outs[1][1])
+    assert geglu_mismatch_ok(geglu_ulp_diff(outs[1][0], st["h"], st["g"], st["u"]))
+
+
 @pytest.mark.parametrize("d", [1024, 1088])
 def test_gate_up_three_column_tile_ragged_stages(d):
     """The gated tile with three fragment columns a stage on K = 1024 (16
