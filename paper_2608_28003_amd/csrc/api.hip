@@ -246,6 +246,8 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
     p.kchunk = (int)round_up(ceil_div(kb, splits), 2);
     p.splits = (int)ceil_div(kb, p.kchunk);
     plan_order(p, m, n);
+    if (glu && plan_override("NT_OUT", -1) < 0)  // as the int8 gated plans below
+      p.nt_out = plan_override("NT_GLU", m * n * 2 >= (16 << 20) ? 1 : 0) != 0;
     return p;
   }
   // int8 choices from a sweep of the FFN shapes (d = 1152, f = 6912) at

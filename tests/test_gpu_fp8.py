@@ -274,8 +274,8 @@ def test_fp8_lm_head_full_vocab_sampled_columns(m):
 
 # ------------------------------------------------------------------ FFN
 
-def _ffn_fp8(m, seed_base=2200):
-    cfg = synth.ffn_config(m=m, d=1152, f=6912, seed_base=seed_base)
+def _ffn_fp8(m, seed_base=2200, f=6912):
+    cfg = synth.ffn_config(m=m, d=1152, f=f, seed_base=seed_base)
     q = oracle.quantize_ffn_fp8(cfg["w_gate"], cfg["w_up"], cfg["w_down"], cfg["x_cal"])
     layer = w8a8.fp8_ffn_layer(dev_bf16(cfg["w_gate"]), dev_bf16(cfg["w_up"]),
                                dev_bf16(cfg["w_down"]), dev_f32(q["delta_gu"]),
@@ -308,6 +308,25 @@ def test_fp8_gate_up_tiles_agree(m, monkeypatch):
         outs.append(oracle.bf16_to_f32(host_bf16(w8a8.fp8_ffn_gate_up(layer, qx, sx, m))))
     for o in outs[1:]:
         assert rel_l2(o, outs[0]) <= 1e-4
+
+
+@pytest.mark.parametrize("glu_tile", [9, 12, 14])
+def test_fp8_nontemporal_gated_stores_are_bit_identical(glu_tile):
+    """The store policy of the gated output changes no value on the FP8 tiles
+    (m = 300: ragged rows; f = 1152, since the FP8 down projection takes K in
+    steps of 128)."""
+    say("fp8 non-temporal stores, gated tile", glu_tile)
+    m = 300
+    cfg, q, layer = _ffn_fp8(m, f=1152)
+    _, st = oracle.fp8_ffn(cfg["x"], q, stages=True)
+    qx, sx = pack_codes(st["qx"]), dev_f32(st["sx"])
+    w8a8.set_plan_override("GLU_TILE", glu_tile)
+    outs = []
+    for nt in (0, 1):
+        w8a8.set_plan_override("NT_OUT", nt)
+        outs.append(host_bf16(w8a8.fp8_ffn_gate_up(layer, qx, sx, m)))
+    np.testing.assert_array_equal(outs[0], outs[1])
+    assert rel_l2(oracle.bf16_to_f32(outs[1]), oracle.bf16_to_f32(st["h"])) <= 1e-3
 
 
 @pytest.mark.parametrize("m", [1, 64, 300])
