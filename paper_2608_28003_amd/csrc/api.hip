@@ -247,7 +247,7 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
     p.splits = (int)ceil_div(kb, p.kchunk);
     plan_order(p, m, n);
     if (glu && plan_override("NT_OUT", -1) < 0)  // as the int8 gated plans below
-      p.nt_out = plan_override("NT_GLU", m * n * 2 >= (16 << 20) ? 1 : 0) != 0;
+      p.nt_out = plan_override("NT_GLU", m * n * 2 >= (2 << 20) ? 1 : 0) != 0;
     return p;
   }
   // int8 choices from a sweep of the FFN shapes (d = 1152, f = 6912) at
@@ -308,10 +308,11 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
   p.kchunk = (int)ceil_div(kb, splits);
   p.splits = (int)ceil_div(kb, p.kchunk);
   plan_order(p, m, n);
-  // the gated output h of a large batch streams past the caches too (M = 2048:
-  // 28 MB; gate/up 44.6 -> 42.6 us, its operand panels stay in L2)
+  // the gated output h streams past the caches too, so its operand panels stay
+  // in L2 (f = 6912: gate/up at M = 2048 44.6 -> 42.6 us, M = 1024 24.5 ->
+  // 23.0 us, M = 512 16.6 -> 16.0 us; M = 128 unchanged)
   if (glu && plan_override("NT_OUT", -1) < 0)
-    p.nt_out = plan_override("NT_GLU", m * n * 2 >= (16 << 20) ? 1 : 0) != 0;
+    p.nt_out = plan_override("NT_GLU", m * n * 2 >= (2 << 20) ? 1 : 0) != 0;
   return p;
 }
 
