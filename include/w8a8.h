@@ -504,7 +504,7 @@ w8a8_status w8a8_attn_decode_bf16(const void* qkv, int n_heads, int64_t pos, int
    "GEMM_SPLITS", "DOWN_TILE", "DOWN_SPLITS", "DOWN_WK", "WIDE_NW", "WIDE_WGS",
    "STREAM_WK", "STREAM_SPLITS", "GROUP_M", "ROTATE", "NO_QLOAD",
    "NO_FUSED_GLUE", "NO_PERSISTENT", "DEC_SPIN_LIMIT", "XCD_M", "NT_OUT",
-   "ATTN_WGS", "QROWS_R", "NO_STREAM", "NT_GLU".
+   "ATTN_WGS", "QROWS_R", "NO_STREAM", "NT_GLU", "NT_DOWN".
    Returns 0, or -1 for an unknown name.  Not for production use: an override applies to every later
    call in the process, and changing one while another thread calls the library
    races with it. */
