@@ -254,15 +254,31 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
   // M = 128 ... 2048; the bf16 path keeps the older rule
   const bool i8 = dt == DT_I8;
   const bool long_k = i8 && !glu && k >= 4096 && n <= 4096;  // down-projection-like
+  // bf16 (FFN shapes d = 1152, f = 6912; the FFN block, gate/up then down):
+  // the 8-wave 256 x 128 gated tile from ~200 tiles (M = 2048 242 -> 208 us,
+  // M = 1024 134 -> 119 us), the 128 x 64 gated tile from 200 tiles (M = 256
+  // 54.4 -> 50.0 us); the long-K down projection on 256 x 128 or 128 x 128
+  // tiles with three K splits from 64 tiles (M = 2048 242 -> 178 us, M = 1024
+  // 134 -> 103 us), as the int8 stack's down projection
+  const bool long_k16 = dt == DT_BF16 && !glu && k >= 4096 && n <= 4096;
+  int dflt_splits = 0;
   if (glu) {
     if (m <= 128)  // int8: three fragment columns a stage (M = 128: 9.95 -> 9.01 us)
       p.tile = i8 ? TILE_GLU_128x32_K3 : TILE_GLU_128x32_K2;
+    else if (!i8 && tiles_of(TILE_GLU_256x128, m, n) >= 200)
+      p.tile = TILE_GLU_256x128;
     else if (tiles_of(TILE_GLU_256x64, m, n) >= (i8 ? 384 : 512))  // two resident per CU
       p.tile = TILE_GLU_256x64;
     else if (i8)
       p.tile = tiles_of(TILE_GLU_128x64, m, n) >= 400 ? TILE_GLU_128x64 : TILE_GLU_64x64_K2;
     else
-      p.tile = tiles_of(TILE_GLU_128x64, m, n) >= 256 ? TILE_GLU_128x64 : TILE_GLU_64x64;
+      p.tile = tiles_of(TILE_GLU_128x64, m, n) >= 200 ? TILE_GLU_128x64 : TILE_GLU_64x64;
+  } else if (long_k16 && tiles_of(TILE_256x128, m, n) >= 64) {
+    p.tile = TILE_256x128;
+    dflt_splits = 3;
+  } else if (long_k16 && tiles_of(TILE_128x128, m, n) >= 64) {
+    p.tile = TILE_128x128;
+    dflt_splits = 3;
   } else if (long_k) {
     // with K split until ~512 workgroups are in flight (the split rule below);
     // when the whole grid fits one workgroup per CU (the FFN down projection
@@ -297,7 +313,9 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int dt, bool glu) {
   p.tile = glu ? plan_override("GLU_TILE", p.tile) : plan_override("GEMM_TILE", p.tile);
   const int64_t tiles = tiles_of(p.tile, m, n);
   int splits = 1;
-  if (long_k)
+  if (dflt_splits > 0)
+    splits = dflt_splits;
+  else if (long_k)
     splits = (int)std::min<int64_t>(std::min<int64_t>(ceil_div(512, tiles), 6),
                                     std::max<int64_t>(1, kb / 8));
   else if (!glu && tiles < 200)  // int8: at least 16 fragments per split (a split of a
