@@ -617,8 +617,12 @@ def test_lm_head_full_vocab_sampled_columns(m, lm_full):
 # ------------------------------------------------------------------ bf16 path and glue
 
 @pytest.mark.parametrize("m,n,k", [(1, 6912, 1152), (128, 1152, 6912), (64, 4096, 1152),
-                                   (300, 1000, 1152), (2048, 1152, 1152)])
+                                   (300, 1000, 1152), (2048, 1152, 1152), (512, 65536, 1152),
+                                   (1024, 1152, 6912)])
 def test_bf16_linear_matches_oracle(m, n, k):
+    """Includes the planner's wide 256 x 256 tiles (512 x 65536) and the long-K
+    tiles with three K splits whose fp32 partial sums are added in split order
+    (1024 x 1152 x 6912)."""
     say("bf16 linear", m, n, k)
     x = act_input(m, k, 800 + m, factor=4.0)
     w = synth.to_bf16_bits(synth.normal(900 + n, (n, k), 0.02))
@@ -642,8 +646,10 @@ def test_bf16_linear_matches_oracle(m, n, k):
     assert float((yg == y_o).mean()) >= 0.99
 
 
-@pytest.mark.parametrize("m", [1, 128])
+@pytest.mark.parametrize("m", [1, 128, 1024, 2048])
 def test_bf16_ffn_matches_oracle(m):
+    """M = 1024 and 2048 take the 8-wave 256 x 128 gated tile and the down
+    projection on 128 x 128 / 256 x 128 tiles with three K splits."""
     say("bf16 ffn", m)
     cfg = synth.ffn_config(m=m)
     y_o = oracle.bf16_ffn(cfg["x"], cfg["w_gate"], cfg["w_up"], cfg["w_down"])
