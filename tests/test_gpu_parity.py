@@ -339,6 +339,35 @@ def test_nontemporal_output_stores_are_bit_identical(glu_tile):
     assert geglu_mismatch_ok(geglu_ulp_diff(outs[1][0], st["h"], st["g"], st["u"]))
 
 
+def test_stack_store_policy_is_bit_identical():
+    """The stack stores h and the down projection's split-K partial sums
+    non-temporally from 2 MiB; token streams and logits are the same bits
+    with either store policy (m = 300: partial sums of 6 K splits, 8.3 MB)."""
+    say("stack store policy")
+    m, n_layers, vocab = 300, 3, 4096
+    cfg = synth.stack_config(m=m, n_layers=n_layers, vocab=vocab)
+    torch.manual_seed(13)
+    i8, bf = [], []
+    for L in cfg["layers"]:
+        wg, wu, wd = dev_bf16(L["w_gate"]), dev_bf16(L["w_up"]), dev_bf16(L["w_down"])
+        i8.append(w8a8.FfnW8A8.from_weights(wg, wu, wd, (torch.rand(1152, device=DEV) + 0.5).contiguous(),
+                                            (torch.rand(6912, device=DEV) + 0.5).contiguous()))
+        bf.append(w8a8.FfnBF16.from_weights(wg, wu, wd))
+    w_lm = dev_bf16(cfg["w_lm"])
+    lm8 = w8a8.LinearW8A8.from_weight(w_lm, (torch.rand(1152, device=DEV) + 0.5).contiguous())
+    stack = w8a8.Stack(i8, bf, lm8, w8a8.pack_bf16(w_lm), vocab)
+    x = dev_bf16(cfg["x"])
+    prec = np.array([1, 0, 1], np.uint8)
+    outs = []
+    for nt in (0, 1):
+        w8a8.set_plan_override("NT_DOWN", nt)
+        w8a8.set_plan_override("NT_GLU", nt)
+        hid, logits = stack.trace(x, prec, lm_head_int8=True, logits=True)
+        outs.append((host_bf16(hid), host_bf16(logits)))
+    np.testing.assert_array_equal(outs[0][0], outs[1][0])
+    np.testing.assert_array_equal(outs[0][1], outs[1][1])
+
+
 @pytest.mark.parametrize("d", [1024, 1088])
 def test_gate_up_three_column_tile_ragged_stages(d):
     """The gated tile with three fragment columns a stage on K = 1024 (16
